@@ -1,0 +1,196 @@
+/*
+ * luffy.h - C ABI of the token-condensation MoE layer on one MI355X (gfx950).
+ *
+ * The layer is the single-GPU data-parallel path of the token condensation of
+ * Luffy (arXiv 2411.15419): route tokens to experts (Sec. 2.1), inside every
+ * expert's bucket find tokens whose cosine similarity clears a threshold and
+ * keep one representative per group (Sec. 5.1 steps 1 and 3, Sec. 5.2), run
+ * the expert FFN on the representatives only (Sec. 3), and give every
+ * condensed token its representative's expert output when combining
+ * (Sec. 6, the token_to_token table; Sec. 2.1 combine).
+ *
+ * Conventions for every call
+ *  - Pointers named as device pointers point to device memory owned by the
+ *    caller; the library allocates nothing.  Scratch memory is passed in
+ *    through a workspace pointer whose minimum size the matching
+ *    *_workspace_size function returns (256-byte alignment required).
+ *  - Matrices are row-major.  Weights use the [out, in] layout, so the
+ *    contraction index is contiguous in every operand.
+ *  - dtype (luffy_dtype) selects the element type of activations and
+ *    weights: LUFFY_F32 (float) or LUFFY_BF16 (bfloat16 bit patterns,
+ *    uint16).  Gates, norms and accumulations are float32.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream) and never synchronises the device.  Counts that depend on the
+ *    data (bucket sizes, representative counts) stay on the device; grids are
+ *    sized from upper bounds and kernels read the counts they need.
+ *  - Arguments are checked on the host before anything is enqueued; a
+ *    rejected call enqueues nothing and returns a negative status.  Launch
+ *    failures return LUFFY_E_HIP.  luffy_last_error() gives a message for the
+ *    most recent failure on the calling thread.  No C++ exception crosses the
+ *    ABI.
+ *  - Outputs must not alias inputs.  Integer outputs are deterministic: the
+ *    same inputs give bit-identical indices on every run.
+ *  - Supported sizes: d and d_ff multiples of 64, 1 <= E <= 64,
+ *    k in {1, 2}, T*k < 2^31.  Other sizes return LUFFY_E_UNSUPPORTED.
+ */
+#ifndef LUFFY_H
+#define LUFFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LUFFY_ABI_VERSION 1
+
+typedef enum {
+  LUFFY_OK = 0,
+  LUFFY_E_INVALID = -1,     /* null pointer, bad size, k > E, k not 1 or 2 */
+  LUFFY_E_UNSUPPORTED = -2, /* a size this build does not handle           */
+  LUFFY_E_WORKSPACE = -3,   /* workspace missing, too small or misaligned  */
+  LUFFY_E_HIP = -4          /* a HIP runtime call or launch failed         */
+} luffy_status;
+
+typedef enum { LUFFY_F32 = 0, LUFFY_BF16 = 1 } luffy_dtype;
+
+/* Expert activation (Sec. 2.1: an expert is an FFN).
+ * GELU is the exact form 0.5 z (1 + erf(z / sqrt 2)); SiLU is z / (1 + e^-z). */
+typedef enum { LUFFY_ACT_GELU = 0, LUFFY_ACT_SILU = 1 } luffy_act;
+
+int luffy_abi_version(void);
+const char* luffy_status_string(int status);
+const char* luffy_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * luffy_route - gate, top-k and the stable dispatch order (Sec. 2.1: the gate
+ * network selects experts for every token and tokens are grouped by expert).
+ *
+ *   x          [T, d] dtype, device          token embeddings
+ *   w_gate     [E, d] dtype, device          gate weights
+ *   b_gate     [E] float, device, or NULL    gate bias
+ *   capacity_factor  > 0: each expert keeps at most C = ceil(cf*k*T/E)
+ *                    slots; <= 0: no limit
+ * Outputs (device):
+ *   topk_idx   [T, k] int32   experts by descending logit, ties to the lower
+ *                             id; logits are float32 sums, and a choice
+ *                             whose float32 margin is small is re-decided on
+ *                             float64 logits
+ *   topk_gate  [T, k] float   softmax probability of the expert (k = 1), or
+ *                             the two probabilities renormalised to sum to 1
+ *                             (k = 2)
+ *   slot_pos   [T, k] int32   bucket position of slot (t, j), -1 if dropped
+ *   perm_token [T*k]  int32   token of every bucket position; only the first
+ *                             offsets[E] entries are written
+ *   offsets    [E+1]  int32   bucket e holds positions offsets[e] ..
+ *                             offsets[e+1]-1
+ * A slot is (token t, choice j) with id s = j*T + t.  Buckets are stable in
+ * s (all first choices in token order, then all second choices); with a
+ * capacity the first C slots of a bucket stay and later ones are dropped.
+ * ---------------------------------------------------------------------- */
+size_t luffy_route_workspace_size(int T, int E, int k);
+int luffy_route(const void* x, int T, int d, int dtype,
+                const void* w_gate, const float* b_gate, int E, int k,
+                float capacity_factor,
+                int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
+                int32_t* perm_token, int32_t* offsets,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * luffy_condense - per-bucket similarity, representative selection and
+ * compaction (Sec. 5.1 steps 1 and 3, Sec. 5.2, Sec. 6).
+ *
+ * Inside each bucket, positions a != b are joined when the cosine of their
+ * embeddings is >= threshold (pairs in different buckets are never
+ * compared).  A token with a zero embedding joins nothing.  The degree of a
+ * position is its number of edges.  Positions are then visited by
+ * descending degree (lower position first on ties): a position not yet
+ * decided becomes a representative and absorbs every undecided direct
+ * neighbour.  Each absorbed position maps to the first representative
+ * visited among its neighbours.
+ *
+ *   x            [T, d] dtype, device     embeddings (same as luffy_route)
+ *   perm_token, offsets                   as written by luffy_route
+ *   max_bucket   upper bound on any bucket size (min(T, C) for outputs of
+ *                luffy_route); sizes the workspace.  Buckets larger than it
+ *                make the call write nothing past the workspace and leave the
+ *                outputs undefined.
+ *   threshold    cosine threshold h (a value > 1 disables condensation)
+ * Outputs (device):
+ *   rep_of_pos   [T*k] int32  position of the representative of every
+ *                             position (representatives map to themselves)
+ *   rep_row      [T*k] int32  row of that representative in the compacted
+ *                             list (representatives in position order)
+ *   rep_offsets  [E+1] int32  representatives of expert e are rows
+ *                             rep_offsets[e] .. rep_offsets[e+1]-1
+ *   rep_token    [T*k] int32  token of every representative row
+ *   x_rep        [T*k, d] dtype or NULL   gathered representative rows
+ *   degree       [T*k] int32 or NULL      degree of every position
+ * Only the first offsets[E] (positions) or rep_offsets[E] (rows) entries are
+ * written.
+ * ---------------------------------------------------------------------- */
+size_t luffy_condense_workspace_size(int T, int d, int E, int k, int max_bucket);
+int luffy_condense(const void* x, int T, int d, int dtype,
+                   const int32_t* perm_token, const int32_t* offsets,
+                   int E, int k, int max_bucket, float threshold,
+                   int32_t* rep_of_pos, int32_t* rep_row,
+                   int32_t* rep_offsets, int32_t* rep_token,
+                   void* x_rep, int32_t* degree,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * luffy_expert_ffn - expert FFN on the representatives only (Sec. 2.1: an
+ * expert is an FFN; Sec. 3: only one token of a similar group goes through
+ * the expert).
+ *
+ *   y_rep[r] = W2_e act(W1_e x_r)   for the rows r of expert e, no biases
+ *
+ *   x            [*, d] dtype, device   input rows
+ *   row_index    [max_rows] int32, device, or NULL: row r of the FFN reads
+ *                x[row_index[r]] (pass rep_token and the embeddings to skip
+ *                the gathered copy); NULL reads x[r] (e.g. x_rep)
+ *   rep_offsets  [E+1] int32, device    rows of expert e
+ *   w1           [E, d_ff, d] dtype, device
+ *   w2           [E, d, d_ff] dtype, device
+ *   max_rows     upper bound on rep_offsets[E] (T*k)
+ *   y_rep        [max_rows, d] dtype, device (first rep_offsets[E] rows written)
+ * The hidden activations are rounded to dtype between the two products.
+ * ---------------------------------------------------------------------- */
+size_t luffy_expert_ffn_workspace_size(int max_rows, int E, int d_ff, int dtype);
+int luffy_expert_ffn(const void* x, const int32_t* row_index,
+                     const int32_t* rep_offsets, int E, int d, int d_ff,
+                     int dtype, const void* w1, const void* w2, int act,
+                     int max_rows, void* y_rep,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * luffy_combine - give every slot its representative's expert output and
+ * un-permute with the gates (Sec. 2.1 combine; Sec. 6 token_to_token).
+ *
+ *   y[t] = sum over kept slots j of topk_gate[t,j] * y_rep[rep_row[slot_pos[t,j]]]
+ * A token with no kept slot gets zeros.  Sums are float32, stored as dtype.
+ *   y_rep [*, d] dtype; rep_row [T*k]; slot_pos, topk_gate [T, k];
+ *   y [T, d] dtype, device.
+ * ---------------------------------------------------------------------- */
+int luffy_combine(const void* y_rep, const int32_t* rep_row,
+                  const int32_t* slot_pos, const float* topk_gate,
+                  int T, int k, int d, int dtype, void* y, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Measurement hook (not part of the layer).  luffy_profile_kernel(name)
+ * makes every later launch of the named kernel record a pair of HIP events
+ * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
+ * waits for the recorded events and returns the summed kernel time in
+ * milliseconds and the number of launches since the previous read.
+ * Kernel names: gate, slot_hist, slot_scan, slot_scatter, norm, gram_prep,
+ * gram, degree, greedy_round, greedy_finish, assign, rep_scan, rep_row,
+ * gather, ffn1, ffn2, combine.
+ * ---------------------------------------------------------------------- */
+int luffy_profile_kernel(const char* name);
+int luffy_profile_read(double* total_ms, int* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LUFFY_H */

@@ -1,0 +1,286 @@
+"""Token-condensation MoE layer (Luffy, arXiv 2411.15419) on one MI355X.
+
+Thin ctypes binding of ``libluffy.so`` (the HIP kernels behind the C ABI in
+``include/luffy.h``).  Every function passes device pointers, sizes and the
+current HIP stream through; every step of the layer runs in the library's
+kernels.  torch supplies device memory and streams only.  There is no
+fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+__all__ = [
+    "LuffyError", "load_library", "LUFFY_F32", "LUFFY_BF16", "LUFFY_ACT_GELU",
+    "LUFFY_ACT_SILU", "luffy_route", "luffy_condense", "luffy_expert_ffn",
+    "luffy_combine", "route_workspace_size", "condense_workspace_size",
+    "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
+    "profile_read", "KERNELS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
+
+LUFFY_F32, LUFFY_BF16 = 0, 1
+LUFFY_ACT_GELU, LUFFY_ACT_SILU = 0, 1
+_ACTS = {"gelu": LUFFY_ACT_GELU, "silu": LUFFY_ACT_SILU}
+
+_c_int, _c_float, _c_size, _vp = ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_void_p
+
+_SIGS = {
+    "luffy_abi_version": (_c_int, []),
+    "luffy_status_string": (ctypes.c_char_p, [_c_int]),
+    "luffy_last_error": (ctypes.c_char_p, []),
+    "luffy_route_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
+    "luffy_route": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_float,
+                             _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
+    "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
+                                _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "luffy_expert_ffn_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
+    "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
+                                  _c_int, _c_int, _vp, _vp, _c_size, _vp]),
+    "luffy_combine": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
+    "luffy_profile_kernel": (_c_int, [ctypes.c_char_p]),
+    "luffy_profile_read": (_c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_c_int)]),
+}
+
+_LIB = None
+
+
+class LuffyError(RuntimeError):
+    pass
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libluffy.so once and declares the C signatures."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise LuffyError(f"{path} is not built; run `python -m paper_2411_15419_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        lib = load_library()
+        msg = lib.luffy_last_error().decode()
+        raise LuffyError(f"{what}: {lib.luffy_status_string(status).decode()} ({status}): {msg}")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return LUFFY_F32
+    if t.dtype == torch.bfloat16:
+        return LUFFY_BF16
+    raise LuffyError(f"unsupported dtype {t.dtype}")
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise LuffyError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise LuffyError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def capacity(T: int, k: int, E: int, cf: float) -> int:
+    """Per-expert capacity ceil(cf*k*T/E) (0 = unlimited)."""
+    if cf <= 0:
+        return 0
+    return int(math.ceil(cf * k * T / E - 1e-9))
+
+
+def route_workspace_size(T: int, E: int, k: int) -> int:
+    return load_library().luffy_route_workspace_size(T, E, k)
+
+
+def condense_workspace_size(T: int, d: int, E: int, k: int, max_bucket: int) -> int:
+    return load_library().luffy_condense_workspace_size(T, d, E, k, max_bucket)
+
+
+def expert_ffn_workspace_size(max_rows: int, E: int, d_ff: int, dtype: int) -> int:
+    return load_library().luffy_expert_ffn_workspace_size(max_rows, E, d_ff, dtype)
+
+
+def luffy_route(x, w_gate, b_gate, k, capacity_factor, topk_idx, topk_gate, slot_pos,
+                perm_token, offsets, workspace, stream=None):
+    T, d = x.shape
+    E = w_gate.shape[0]
+    lib = load_library()
+    _check(lib.luffy_route(_p(x), T, d, _dtype_code(x), _p(w_gate), _p(b_gate), E, k,
+                           float(capacity_factor), _p(topk_idx), _p(topk_gate), _p(slot_pos),
+                           _p(perm_token), _p(offsets), _p(workspace), workspace.numel(),
+                           _stream(stream)), "luffy_route")
+
+
+def luffy_condense(x, perm_token, offsets, k, max_bucket, threshold, rep_of_pos, rep_row,
+                   rep_offsets, rep_token, x_rep, degree, workspace, stream=None):
+    T, d = x.shape
+    E = offsets.numel() - 1
+    lib = load_library()
+    _check(lib.luffy_condense(_p(x), T, d, _dtype_code(x), _p(perm_token), _p(offsets), E, k,
+                              max_bucket, float(threshold), _p(rep_of_pos), _p(rep_row),
+                              _p(rep_offsets), _p(rep_token), _p(x_rep), _p(degree),
+                              _p(workspace), workspace.numel(), _stream(stream)), "luffy_condense")
+
+
+def luffy_expert_ffn(x, row_index, rep_offsets, w1, w2, act, max_rows, y_rep, workspace,
+                     stream=None):
+    E, d_ff, d = w1.shape
+    lib = load_library()
+    act_code = _ACTS[act] if isinstance(act, str) else int(act)
+    _check(lib.luffy_expert_ffn(_p(x), _p(row_index), _p(rep_offsets), E, d, d_ff,
+                                _dtype_code(x), _p(w1), _p(w2), act_code, max_rows, _p(y_rep),
+                                _p(workspace), workspace.numel(), _stream(stream)),
+           "luffy_expert_ffn")
+
+
+def luffy_combine(y_rep, rep_row, slot_pos, topk_gate, y, stream=None):
+    T, k = slot_pos.shape
+    d = y.shape[1]
+    lib = load_library()
+    _check(lib.luffy_combine(_p(y_rep), _p(rep_row), _p(slot_pos), _p(topk_gate), T, k, d,
+                             _dtype_code(y), _p(y), _stream(stream)), "luffy_combine")
+
+
+def profile_kernel(name: Optional[str]) -> None:
+    """Selects the kernel whose launches are bracketed by HIP events (None: off)."""
+    _check(load_library().luffy_profile_kernel(name.encode() if name else None),
+           "luffy_profile_kernel")
+
+
+def profile_read():
+    """(summed milliseconds, launches) of the selected kernel since the last read."""
+    ms, n = ctypes.c_double(), _c_int()
+    _check(load_library().luffy_profile_read(ctypes.byref(ms), ctypes.byref(n)),
+           "luffy_profile_read")
+    return ms.value, n.value
+
+
+KERNELS = ("gate", "slot_hist", "slot_scan", "slot_scatter", "norm", "gram_prep", "gram",
+           "degree", "greedy_round", "greedy_finish", "assign", "rep_scan", "rep_row",
+           "gather", "ffn1", "ffn2", "combine")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator hands out 512-byte aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class LayerBuffers:
+    topk_idx: torch.Tensor
+    topk_gate: torch.Tensor
+    slot_pos: torch.Tensor
+    perm_token: torch.Tensor
+    offsets: torch.Tensor
+    rep_of_pos: torch.Tensor
+    rep_row: torch.Tensor
+    rep_offsets: torch.Tensor
+    rep_token: torch.Tensor
+    degree: Optional[torch.Tensor]
+    x_rep: Optional[torch.Tensor]
+    y_rep: torch.Tensor
+    y: torch.Tensor
+    ws_route: torch.Tensor
+    ws_condense: torch.Tensor
+    ws_ffn: torch.Tensor
+
+
+class MoELayer:
+    """Holds the weights and every buffer of one condensed MoE layer and runs
+    the four library calls in order on the current stream.
+
+    gather_x_rep=False (default) lets the FFN read representative rows of x
+    through rep_token instead of materialising x_rep.
+    """
+
+    def __init__(self, w_gate, b_gate, w1, w2, *, k: int, act: str, threshold: float,
+                 capacity_factor: float = 0.0, T: int, keep_degree: bool = True,
+                 gather_x_rep: bool = False):
+        self.w_gate, self.b_gate, self.w1, self.w2 = w_gate, b_gate, w1, w2
+        self.k, self.act, self.h, self.cf = k, act, threshold, capacity_factor
+        self.E, self.d_ff, self.d = w1.shape
+        self.T = T
+        self.dtype = w1.dtype
+        dev = w1.device
+        S = T * k
+        C = capacity(T, k, self.E, capacity_factor)
+        self.max_bucket = min(T, C) if C > 0 else T
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.buf = LayerBuffers(
+            topk_idx=torch.empty(T, k, **i32),
+            topk_gate=torch.empty(T, k, dtype=torch.float32, device=dev),
+            slot_pos=torch.empty(T, k, **i32),
+            perm_token=torch.empty(S, **i32),
+            offsets=torch.empty(self.E + 1, **i32),
+            rep_of_pos=torch.empty(S, **i32),
+            rep_row=torch.empty(S, **i32),
+            rep_offsets=torch.empty(self.E + 1, **i32),
+            rep_token=torch.empty(S, **i32),
+            degree=torch.empty(S, **i32) if keep_degree else None,
+            x_rep=torch.empty(S, self.d, dtype=self.dtype, device=dev) if gather_x_rep else None,
+            y_rep=torch.empty(S, self.d, dtype=self.dtype, device=dev),
+            y=torch.empty(T, self.d, dtype=self.dtype, device=dev),
+            ws_route=_workspace(route_workspace_size(T, self.E, k), dev),
+            ws_condense=_workspace(condense_workspace_size(T, self.d, self.E, k,
+                                                           self.max_bucket), dev),
+            ws_ffn=_workspace(expert_ffn_workspace_size(
+                S, self.E, self.d_ff, LUFFY_BF16 if self.dtype == torch.bfloat16 else LUFFY_F32),
+                dev),
+        )
+
+    def route(self, x, stream=None):
+        b = self.buf
+        luffy_route(x, self.w_gate, self.b_gate, self.k, self.cf, b.topk_idx, b.topk_gate,
+                    b.slot_pos, b.perm_token, b.offsets, b.ws_route, stream)
+
+    def condense(self, x, stream=None, threshold=None):
+        b = self.buf
+        h = self.h if threshold is None else threshold
+        luffy_condense(x, b.perm_token, b.offsets, self.k, self.max_bucket, h, b.rep_of_pos,
+                       b.rep_row, b.rep_offsets, b.rep_token, b.x_rep, b.degree, b.ws_condense,
+                       stream)
+
+    def expert_ffn(self, x, stream=None):
+        b = self.buf
+        if b.x_rep is not None:
+            src, idx = b.x_rep, None
+        else:
+            src, idx = x, b.rep_token
+        luffy_expert_ffn(src, idx, b.rep_offsets, self.w1, self.w2, self.act, self.T * self.k,
+                         b.y_rep, b.ws_ffn, stream)
+
+    def combine(self, stream=None):
+        b = self.buf
+        luffy_combine(b.y_rep, b.rep_row, b.slot_pos, b.topk_gate, b.y, stream)
+
+    def __call__(self, x, stream=None, threshold=None):
+        if x.shape != (self.T, self.d) or x.dtype != self.dtype:
+            raise LuffyError(f"x must be [{self.T}, {self.d}] {self.dtype}")
+        self.route(x, stream)
+        self.condense(x, stream, threshold)
+        self.expert_ffn(x, stream)
+        self.combine(stream)
+        return self.buf.y

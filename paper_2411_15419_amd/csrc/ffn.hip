@@ -1,0 +1,234 @@
+// luffy_expert_ffn: grouped FFN over the representatives of every expert,
+//   H = act(X_rep W1_e^T)   (rounded to the element type)
+//   Y = H W2_e^T
+// Row counts per expert live on the device.  The grid is sized from the
+// upper bound ceil(max_rows/128) + E row tiles; each block finds its expert
+// and row range from rep_offsets and exits when it has none.
+//
+// bf16: 128 x 128 MFMA tiles.  The weight rows are the P operand and the
+// token rows the Q operand, so each lane ends with four consecutive output
+// columns of one row and stores them as one 8-byte word.
+// fp32: 64 x 64 tiles of plain FMA (4 x 4 per thread).
+#include "gemm_core.h"
+#include "luffy_common.h"
+
+namespace luffy {
+namespace {
+
+template <int ACT>
+__device__ __forceinline__ float act_fn(float z) {
+  if constexpr (ACT == LUFFY_ACT_GELU) {
+    return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  } else {
+    return z / (1.0f + expf(-z));
+  }
+}
+
+// Row tile q of the ragged row list: expert e, first row row0 and row count.
+// Wave-uniform; lane e handles expert e.  Returns false past the last tile.
+__device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_offsets, int E,
+                                                int BM, int q, int& e_out, int& row0, int& rows) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0, hi = 0, cnt = 0;
+  if (lane < E) {
+    lo = rep_offsets[lane];
+    hi = rep_offsets[lane + 1];
+    cnt = (hi - lo + BM - 1) / BM;
+  }
+  int incl = cnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const uint64_t before = __ballot(lane < E && incl <= q);
+  const int e = __popcll(before);
+  if (e >= E) return false;
+  const int excl = __shfl(incl - cnt, e, 64);
+  const int elo = __shfl(lo, e, 64);
+  const int ehi = __shfl(hi, e, 64);
+  e_out = e;
+  row0 = elo + (q - excl) * BM;
+  rows = min(BM, ehi - row0);
+  return true;
+}
+
+template <int ACT, bool FIRST>
+__global__ __launch_bounds__(256, 2) void ffn_kernel_bf16(
+    const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
+    const int32_t* __restrict__ rep_offsets, int E, int K, int N,
+    const uint16_t* __restrict__ W, uint16_t* __restrict__ out) {
+  __shared__ uint16_t lds[kTileLdsElems];
+  int e, row0, rows;
+  if (!locate_row_tile(rep_offsets, E, kTile, blockIdx.x, e, row0, rows)) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int n0 = blockIdx.y * kTile;
+  const uint16_t* We = W + static_cast<size_t>(e) * N * K;
+  const uint16_t* prow[4];
+  const uint16_t* qrow[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = (tid >> 3) + 32 * q;
+    const int n = min(n0 + r, N - 1);
+    prow[q] = We + static_cast<size_t>(n) * K;
+    const int m = row0 + min(r, rows - 1);
+    const int src = row_index ? row_index[m] : m;
+    qrow[q] = A + static_cast<size_t>(src) * K;
+  }
+  f32x4 acc[4][4];
+  zero_acc(acc);
+  gemm_tile_bf16(prow, qrow, K, lds, acc);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = n0 + 64 * wm + 16 * i + 4 * (lane >> 4);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int ml = 64 * wn + 16 * j + (lane & 15);
+      if (ml < rows && n < N) {
+        uint16_t v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float z = acc[i][j][r];
+          if constexpr (FIRST) z = act_fn<ACT>(z);
+          v[r] = f32_to_bf16(z);
+        }
+        uint2 pk;
+        pk.x = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 16);
+        pk.y = static_cast<uint32_t>(v[2]) | (static_cast<uint32_t>(v[3]) << 16);
+        *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n) = pk;
+      }
+    }
+  }
+}
+
+constexpr int kF32Tile = 64;
+
+template <int ACT, bool FIRST>
+__global__ __launch_bounds__(256) void ffn_kernel_f32(
+    const float* __restrict__ A, const int32_t* __restrict__ row_index,
+    const int32_t* __restrict__ rep_offsets, int E, int K, int N,
+    const float* __restrict__ W, float* __restrict__ out) {
+  constexpr int KC = 16;
+  __shared__ float As[kF32Tile][KC + 1];
+  __shared__ float Bs[kF32Tile][KC + 1];
+  int e, row0, rows;
+  if (!locate_row_tile(rep_offsets, E, kF32Tile, blockIdx.x, e, row0, rows)) return;
+  const int tid = threadIdx.x;
+  const int n0 = blockIdx.y * kF32Tile;
+  const float* We = W + static_cast<size_t>(e) * N * K;
+  const int rb = (tid >> 4) * 4, cb = (tid & 15) * 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += KC) {
+    __syncthreads();
+    for (int idx = tid; idx < kF32Tile * KC; idx += 256) {
+      const int r = idx / KC, kk = idx % KC;
+      const int m = row0 + min(r, rows - 1);
+      const int src = row_index ? row_index[m] : m;
+      As[r][kk] = A[static_cast<size_t>(src) * K + k0 + kk];
+      const int n = min(n0 + r, N - 1);
+      Bs[r][kk] = We[static_cast<size_t>(n) * K + k0 + kk];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KC; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[rb + i][kk];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[cb + j][kk];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (rb + i >= rows) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + cb + j;
+      if (n >= N) continue;
+      float z = acc[i][j];
+      if constexpr (FIRST) z = act_fn<ACT>(z);
+      out[static_cast<size_t>(row0 + rb + i) * N + n] = z;
+    }
+  }
+}
+
+template <int ACT>
+void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d,
+                int d_ff, int dtype, const void* w1, const void* w2, int max_rows, void* y_rep,
+                void* hidden, hipStream_t s) {
+  if (dtype == LUFFY_BF16) {
+    const int mt = (max_rows + kTile - 1) / kTile + E;
+    dim3 g1(mt, (d_ff + kTile - 1) / kTile), g2(mt, (d + kTile - 1) / kTile);
+    {
+      ProfileScope prof_("ffn1", s);
+      ffn_kernel_bf16<ACT, true><<<g1, 256, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
+                                                    d_ff, static_cast<const uint16_t*>(w1),
+                                                    static_cast<uint16_t*>(hidden));
+    }
+    {
+      ProfileScope prof_("ffn2", s);
+      ffn_kernel_bf16<ACT, false><<<g2, 256, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
+                                                     E, d_ff, d, static_cast<const uint16_t*>(w2),
+                                                     static_cast<uint16_t*>(y_rep));
+    }
+  } else {
+    const int mt = (max_rows + kF32Tile - 1) / kF32Tile + E;
+    dim3 g1(mt, (d_ff + kF32Tile - 1) / kF32Tile), g2(mt, (d + kF32Tile - 1) / kF32Tile);
+    {
+      ProfileScope prof_("ffn1", s);
+      ffn_kernel_f32<ACT, true><<<g1, 256, 0, s>>>(static_cast<const float*>(x), row_index, rep_offsets, E, d, d_ff,
+                                                   static_cast<const float*>(w1), static_cast<float*>(hidden));
+    }
+    {
+      ProfileScope prof_("ffn2", s);
+      ffn_kernel_f32<ACT, false><<<g2, 256, 0, s>>>(static_cast<const float*>(hidden), nullptr, rep_offsets, E,
+                                                    d_ff, d, static_cast<const float*>(w2),
+                                                    static_cast<float*>(y_rep));
+    }
+  }
+}
+
+}  // namespace
+}  // namespace luffy
+
+using namespace luffy;
+
+extern "C" size_t luffy_expert_ffn_workspace_size(int max_rows, int E, int d_ff, int dtype) {
+  (void)E;
+  if (max_rows <= 0 || d_ff <= 0) return 0;
+  Carver c(nullptr);
+  c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
+  return c.size();
+}
+
+extern "C" int luffy_expert_ffn(const void* x, const int32_t* row_index,
+                                const int32_t* rep_offsets, int E, int d, int d_ff,
+                                int dtype, const void* w1, const void* w2, int act,
+                                int max_rows, void* y_rep,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  if (!x || !rep_offsets || !w1 || !w2 || !y_rep)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn: null pointer argument");
+  if (E <= 0 || d <= 0 || d_ff <= 0 || max_rows <= 0)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn: E=%d d=%d d_ff=%d max_rows=%d", E, d, d_ff, max_rows);
+  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn: unknown dtype %d", dtype);
+  if (act != LUFFY_ACT_GELU && act != LUFFY_ACT_SILU)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn: unknown activation %d", act);
+  if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: E=%d > %d", E, kMaxExperts);
+  if (d % 64 != 0 || d_ff % 64 != 0)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: d=%d d_ff=%d must be multiples of 64", d, d_ff);
+  const size_t need = luffy_expert_ffn_workspace_size(max_rows, E, d_ff, dtype);
+  if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LUFFY_E_WORKSPACE, "luffy_expert_ffn: workspace needs %zu bytes, 256-aligned", need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (act == LUFFY_ACT_GELU)
+    launch_ffn<LUFFY_ACT_GELU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, workspace, s);
+  else
+    launch_ffn<LUFFY_ACT_SILU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, workspace, s);
+  return check_launch("luffy_expert_ffn");
+}

@@ -1,0 +1,136 @@
+// Status strings, error reporting and ABI version.
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <utility>
+#include <vector>
+
+#include "luffy_common.h"
+
+namespace luffy {
+
+static thread_local char g_last_error[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+}
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("%s: %s", what, hipGetErrorString(e));
+    return LUFFY_E_HIP;
+  }
+  return LUFFY_OK;
+}
+
+// ---------------------------------------------------------------- profiling
+namespace {
+std::atomic<bool> g_prof_on{false};
+std::mutex g_prof_mu;
+char g_prof_name[64] = "";
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_done;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t take_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+ProfileScope::ProfileScope(const char* name, hipStream_t s) : stream_(s) {
+  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (std::strcmp(name, g_prof_name) != 0) return;
+  start_ = take_event();
+  stop_ = take_event();
+  if (start_ && stop_) hipEventRecord(start_, stream_);
+}
+
+ProfileScope::~ProfileScope() {
+  if (!start_ || !stop_) return;
+  hipEventRecord(stop_, stream_);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_done.emplace_back(start_, stop_);
+}
+
+}  // namespace luffy
+
+extern "C" int luffy_profile_kernel(const char* name) {
+  using namespace luffy;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!name || !*name) {
+    g_prof_name[0] = 0;
+    g_prof_on.store(false);
+    return LUFFY_OK;
+  }
+  if (std::strlen(name) >= sizeof(g_prof_name))
+    return fail(LUFFY_E_INVALID, "luffy_profile_kernel: name too long");
+  std::strcpy(g_prof_name, name);
+  while (g_prof_pool.size() < 256) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return fail(LUFFY_E_HIP, "luffy_profile_kernel: hipEventCreate");
+    g_prof_pool.push_back(e);
+  }
+  g_prof_on.store(true);
+  return LUFFY_OK;
+}
+
+extern "C" int luffy_profile_read(double* total_ms, int* launches) {
+  using namespace luffy;
+  if (!total_ms || !launches) return fail(LUFFY_E_INVALID, "luffy_profile_read: null pointer");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  double sum = 0.0;
+  int n = 0;
+  int status = LUFFY_OK;
+  for (auto& pr : g_prof_done) {
+    float ms = 0.f;
+    if (hipEventSynchronize(pr.second) != hipSuccess ||
+        hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess) {
+      status = fail(LUFFY_E_HIP, "luffy_profile_read: event query failed");
+    } else {
+      sum += ms;
+      ++n;
+    }
+    g_prof_pool.push_back(pr.first);
+    g_prof_pool.push_back(pr.second);
+  }
+  g_prof_done.clear();
+  *total_ms = sum;
+  *launches = n;
+  return status;
+}
+
+extern "C" int luffy_abi_version(void) { return LUFFY_ABI_VERSION; }
+
+extern "C" const char* luffy_status_string(int status) {
+  switch (status) {
+    case LUFFY_OK: return "ok";
+    case LUFFY_E_INVALID: return "invalid argument";
+    case LUFFY_E_UNSUPPORTED: return "unsupported size";
+    case LUFFY_E_WORKSPACE: return "workspace too small or misaligned";
+    case LUFFY_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* luffy_last_error(void) { return luffy::g_last_error; }

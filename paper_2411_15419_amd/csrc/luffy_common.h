@@ -1,0 +1,93 @@
+// Shared device/host helpers of the HIP path (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "luffy.h"
+
+namespace luffy {
+
+// ---------------------------------------------------------------- types
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+union Pack16 {          // 16 bytes seen as 8 bf16 or raw words
+  uint4 u4;
+  uint16_t h[8];
+  bf16x8 v;
+};
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// float -> bf16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const unsigned lane = threadIdx.x & 63u;
+  return lane == 0 ? 0ull : (~0ull >> (64u - lane));
+}
+
+// Relaxed agent-scope accesses for flags other waves update in place.
+__device__ __forceinline__ int load_flag(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_flag(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------- host-side helpers
+void set_error(const char* fmt, ...);
+int fail(int status, const char* fmt, ...);
+int check_launch(const char* what);
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Carves a caller-provided workspace into aligned sub-buffers.  With a null
+// base it only measures, so size queries and the real carve share one
+// layout.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t n) {
+    off = align_up(off, 256);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+  size_t size() const { return align_up(off, 256); }
+};
+
+inline int elem_bytes(int dtype) { return dtype == LUFFY_BF16 ? 2 : 4; }
+
+// Brackets one kernel launch with HIP events on its stream when that kernel
+// is the one selected by luffy_profile_kernel(); otherwise does nothing.
+class ProfileScope {
+ public:
+  ProfileScope(const char* name, hipStream_t s);
+  ~ProfileScope();
+  ProfileScope(const ProfileScope&) = delete;
+  ProfileScope& operator=(const ProfileScope&) = delete;
+
+ private:
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr, stop_ = nullptr;
+};
+
+constexpr int kMaxExperts = 64;
+
+}  // namespace luffy

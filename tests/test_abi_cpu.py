@@ -1,0 +1,98 @@
+"""The C-ABI library loads without a GPU, exports every symbol the header
+declares, sizes workspaces, and rejects bad arguments on the host before
+enqueueing anything (CPU only; no compute call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "luffy.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2411_15419_amd as L
+    if not os.path.exists(L.LIB_PATH):
+        from paper_2411_15419_amd import build
+        build.build()
+    return L.load_library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(luffy_[a-z_]+)\s*\(", text)))
+
+
+def test_header_lists_the_four_calls():
+    names = header_functions()
+    for n in ("luffy_route", "luffy_condense", "luffy_expert_ffn", "luffy_combine"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_strings(lib):
+    assert lib.luffy_abi_version() == 1
+    assert lib.luffy_status_string(0) == b"ok"
+    assert lib.luffy_status_string(-3).startswith(b"workspace")
+
+
+def test_workspace_sizes(lib):
+    import paper_2411_15419_amd as L
+    assert L.route_workspace_size(8192, 16, 2) >= 16 * 16 * 4
+    # bitmask: T*k rows of ceil(max_bucket/64) words
+    c3 = L.condense_workspace_size(32768, 2048, 32, 2, 32768)
+    assert c3 >= 65536 * 512 * 8
+    assert L.condense_workspace_size(65536, 1024, 64, 1, 1024) < c3
+    assert L.expert_ffn_workspace_size(65536, 32, 8192, L.LUFFY_BF16) == 65536 * 8192 * 2
+    assert L.route_workspace_size(0, 16, 2) == 0
+
+
+def test_invalid_arguments_rejected_on_host(lib):
+    fake = ctypes.c_void_p(256)     # never dereferenced: validation fails first
+    # null pointers
+    assert lib.luffy_route(None, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
+                           fake, fake, 1 << 20, None) == -1
+    # k out of range, k > E
+    assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 3, 0.0, fake, fake, fake, fake,
+                           fake, fake, 1 << 20, None) == -1
+    assert lib.luffy_route(fake, 8, 64, 1, fake, None, 1, 2, 0.0, fake, fake, fake, fake,
+                           fake, fake, 1 << 20, None) == -1
+    # unsupported sizes
+    assert lib.luffy_route(fake, 8, 65, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
+                           fake, fake, 1 << 20, None) == -2
+    assert lib.luffy_route(fake, 8, 64, 1, fake, None, 65, 1, 0.0, fake, fake, fake, fake,
+                           fake, fake, 1 << 20, None) == -2
+    # workspace too small / misaligned
+    assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
+                           fake, fake, 0, None) == -3
+    assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
+                           fake, ctypes.c_void_p(260), 1 << 20, None) == -3
+    assert b"workspace" in lib.luffy_last_error()
+    # condense: NaN threshold, bad dtype
+    assert lib.luffy_condense(fake, 8, 64, 1, fake, fake, 4, 1, 8, float("nan"), fake, fake,
+                              fake, fake, None, None, fake, 1 << 30, None) == -1
+    assert lib.luffy_condense(fake, 8, 64, 7, fake, fake, 4, 1, 8, 0.9, fake, fake,
+                              fake, fake, None, None, fake, 1 << 30, None) == -1
+    # ffn: unknown activation, d_ff not a multiple of 64
+    assert lib.luffy_expert_ffn(fake, None, fake, 4, 64, 128, 1, fake, fake, 9, 8, fake,
+                                fake, 1 << 30, None) == -1
+    assert lib.luffy_expert_ffn(fake, None, fake, 4, 64, 100, 1, fake, fake, 0, 8, fake,
+                                fake, 1 << 30, None) == -2
+    # combine: k not 1/2
+    assert lib.luffy_combine(fake, fake, fake, fake, 8, 3, 64, 1, fake, None) == -1
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    import paper_2411_15419_amd as L
+    x = torch.zeros(8, 64, dtype=torch.bfloat16)
+    with pytest.raises(L.LuffyError):
+        L.luffy_combine(x, torch.zeros(8, dtype=torch.int32), torch.zeros(8, 1, dtype=torch.int32),
+                        torch.zeros(8, 1), x)
