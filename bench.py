@@ -57,8 +57,6 @@ def kernel_work(name, cfg, counts):
         return dict(flops=2.0 * S * d, bytes=float(R * d * b + 12 * T * k + T * d * b))
     if name == "gather":
         return dict(flops=0.0, bytes=float(2 * R * d * b + 8 * S))
-    if name == "degree":
-        return dict(flops=0.0, bytes=float(sum(x * ((x + 63) // 64) * 8 for x in counts["bucket_sizes"])))
     return dict(flops=0.0, bytes=0.0)
 
 

@@ -31,7 +31,8 @@
  *  - Outputs must not alias inputs.  Integer outputs are deterministic: the
  *    same inputs give bit-identical indices on every run.
  *  - Supported sizes: d and d_ff multiples of 64, 1 <= E <= 64,
- *    k in {1, 2}, T*k < 2^31.  Other sizes return LUFFY_E_UNSUPPORTED.
+ *    k in {1, 2}, T*k < 2^31 (luffy_condense: T*k <= 2^24).  Other sizes
+ *    return LUFFY_E_UNSUPPORTED.
  */
 #ifndef LUFFY_H
 #define LUFFY_H
@@ -183,9 +184,9 @@ int luffy_combine(const void* y_rep, const int32_t* rep_row,
  * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
- * Kernel names: gate, slot_hist, slot_scan, slot_scatter, norm, gram_prep,
- * gram, degree, greedy_round, greedy_finish, assign, rep_scan, rep_row,
- * gather, ffn1, ffn2, combine.
+ * Kernel names: gate, slot_scan, slot_scatter, norm, gram_prep, gram,
+ * greedy_round, greedy_finish, assign, rep_local, rep_finalize, gather,
+ * ffn1, ffn2, combine.
  * ---------------------------------------------------------------------- */
 int luffy_profile_kernel(const char* name);
 int luffy_profile_read(double* total_ms, int* launches);

@@ -178,9 +178,9 @@ def profile_read():
     return ms.value, n.value
 
 
-KERNELS = ("gate", "slot_hist", "slot_scan", "slot_scatter", "norm", "gram_prep", "gram",
-           "degree", "greedy_round", "greedy_finish", "assign", "rep_scan", "rep_row",
-           "gather", "ffn1", "ffn2", "combine")
+KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram_prep", "gram", "greedy_round",
+           "greedy_finish", "assign", "rep_local", "rep_finalize", "gather", "ffn1", "ffn2",
+           "combine")
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:

@@ -2,23 +2,26 @@
 // selection and compaction.
 //
 // Kernels, in launch order:
-//   norm_kernel          1/|x_t| per token (one wave per row).
+//   norm_kernel          1/|x_t| per token (one wave per row); clears the
+//                        degree counters and walk states.
 //   gram_prep_kernel     per-bucket tile counts and bitmask offsets.
-//   gram_kernel_{bf16,f32}  persistent loop over the upper-triangle 128x128
-//                        tiles of every bucket's Gram matrix.  The epilogue
-//                        turns cos >= h into adjacency bits and writes both
-//                        the tile and its transpose, so every bitmask word is
-//                        written exactly once.
-//   degree_kernel        popcount of every adjacency row.
+//   gram_kernel_{bf16,f32}  persistent loop over the upper-triangle tiles
+//                        (256 rows bf16, 128 rows fp32) of every bucket's Gram
+//                        matrix.  The epilogue turns cos >= h into adjacency
+//                        bits, writes both the tile and its transpose (every
+//                        bitmask word is written exactly once) and adds each
+//                        row's edge count to its degree.
 //   greedy_round_kernel  one round of the parallel form of the greedy walk
-//                        (run a fixed number of times over the whole grid).
+//                        (launched a fixed number of times; a round exits at
+//                        once when the previous one left nothing undecided).
 //   greedy_finish_kernel one workgroup per bucket repeats rounds until the
-//                        bucket is fully decided.
+//                        bucket is fully decided (exits at once if nothing is
+//                        left).
 //   assign_kernel        every absorbed position picks its first-visited
 //                        adjacent representative.
-//   rep_scan_kernel      one workgroup: exclusive scan of the representative
-//                        flags -> rows, rep_token, rep_offsets.
-//   rep_row_kernel, gather_kernel
+//   rep_local_kernel, rep_finalize_kernel  representative rows by a two-pass
+//                        scan: rep_row, rep_token, rep_offsets.
+//   gather_kernel        optional copy of the representative rows.
 //
 // The walk of Sec. 5.2 visits positions by priority (degree descending,
 // position ascending) and keeps a position iff no neighbour of higher
@@ -34,6 +37,8 @@ namespace luffy {
 namespace {
 
 constexpr int kGreedyGridRounds = 4;
+constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig)
+constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
@@ -60,7 +65,13 @@ __device__ __forceinline__ int bucket_of(const int32_t* __restrict__ offsets, in
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, int T, int d,
-                                                   float* __restrict__ inv_norm) {
+                                                   float* __restrict__ inv_norm, int S,
+                                                   int32_t* __restrict__ deg, int32_t* __restrict__ state) {
+  // also clears the degree counters and walk states of all S positions
+  for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
+    deg[p] = 0;
+    state[p] = 0;
+  }
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -94,15 +105,17 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
 // tile) when a bucket exceeds max_bucket or the bitmask exceeds the
 // workspace.
 __global__ void gram_prep_kernel(const int32_t* __restrict__ offsets, int E, int max_bucket,
-                                 long long cap_words, int32_t* __restrict__ tile_off,
-                                 long long* __restrict__ bm_off, int* __restrict__ err) {
+                                 int tile, long long cap_words, int32_t* __restrict__ tile_off,
+                                 long long* __restrict__ bm_off, int* __restrict__ err,
+                                 int* __restrict__ undecided) {
+  if (threadIdx.x <= kGreedyGridRounds) undecided[threadIdx.x] = 0;
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   long long words = 0;
   int tiles = 0, bad = 0;
   for (int e = 0; e < E; ++e) {
     const int n = offsets[e + 1] - offsets[e];
     if (n < 0 || n > max_bucket) bad = 1;
-    const int nt = (n + kTile - 1) / kTile;
+    const int nt = (n + tile - 1) / tile;
     tile_off[e] = tiles;
     bm_off[e] = words;
     tiles += nt * (nt + 1) / 2;
@@ -151,90 +164,149 @@ __device__ __forceinline__ void write_tile_words(const TileCoord& c, const uint1
            (static_cast<uint64_t>(g[2]) << 32) | (static_cast<uint64_t>(g[3]) << 48);
   };
   {
-    const int a = c.ti * kTile + rl;
+    const int a = c.ti * kTileF32 + rl;
     const int wd = 2 * c.tj + ww;
     if (a < c.n && wd < c.W)
       bitmask[base + static_cast<long long>(a) * c.W + wd] = pack(&dbits[rl][4 * ww]);
   }
   if (c.ti != c.tj) {
-    const int b = c.tj * kTile + rl;
+    const int b = c.tj * kTileF32 + rl;
     const int wd = 2 * c.ti + ww;
     if (b < c.n && wd < c.W)
       bitmask[base + static_cast<long long>(b) * c.W + wd] = pack(&tbits[rl][4 * ww]);
   }
 }
 
-__global__ __launch_bounds__(256, 2) void gram_kernel_bf16(
+// Tile order inside a bucket for the 256-row tiles: columns are taken in
+// groups of 4; inside a group the tiles go row by row (ti major), first the
+// full rows above the group's diagonal block, then its upper triangle.  Any
+// 32 consecutive tiles then cover about 8 row blocks x 4 column blocks, so
+// the blocks of one XCD that run them together share operand rows in L2.
+__device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t* __restrict__ tile_off,
+                                                         const int32_t* __restrict__ offsets, int E) {
+  TileCoord c;
+  int e = 0;
+  while (e + 1 < E && tile_off[e + 1] <= tile) ++e;
+  c.e = e;
+  c.lo = offsets[e];
+  c.n = offsets[e + 1] - c.lo;
+  c.W = (c.n + 63) / 64;
+  const int nt = (c.n + kTile - 1) / kTile;
+  const int q = tile - tile_off[e];
+  // tiles before column group g: 8g^2 + 2g
+  int g = static_cast<int>((sqrtf(4.0f + 32.0f * q) - 2.0f) / 16.0f);
+  while (g > 0 && 8 * g * g + 2 * g > q) --g;
+  while (8 * (g + 1) * (g + 1) + 2 * (g + 1) <= q) ++g;
+  const int r = q - (8 * g * g + 2 * g);
+  const int wdt = min(4, nt - 4 * g);
+  if (r < 4 * g * wdt) {
+    c.ti = r / wdt;
+    c.tj = 4 * g + r % wdt;
+  } else {
+    int r2 = r - 4 * g * wdt, i = 0;
+    while (r2 >= wdt - i) { r2 -= wdt - i; ++i; }
+    c.ti = 4 * g + i;
+    c.tj = 4 * g + i + r2;
+  }
+  return c;
+}
+
+__global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
     const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, uint64_t* __restrict__ bitmask) {
-  __shared__ uint16_t lds[kTileLdsElems];
-  __shared__ uint16_t dbits[kTile][8];
-  __shared__ uint16_t tbits[kTile][8];
+    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
+  using G = GemmBig;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   __shared__ float inv_a[kTile], inv_b[kTile];
+  // after the K loop the operand buffers hold the tile's adjacency pieces:
+  // dbits[row][32-column group], tbits[column][32-row group]
+  uint32_t (*dbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds);
+  uint32_t (*tbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kTile * kTile / 8);
   if (*err) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / G::WN, wn = w % G::WN;
   const int total = tile_off[E];
-  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
-    const TileCoord c = decode_tile(tile, tile_off, offsets, E);
+  for (int tile = xcd_virtual_block(); tile < total; tile += gridDim.x) {
+    const TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
     const int32_t* pt = perm_token + c.lo;
-    const uint16_t* prow[4];
-    const uint16_t* qrow[4];
+    uint32_t poff[G::LOADS / 2], qoff[G::LOADS / 2];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = (tid >> 3) + 32 * q;
-      const int a = min(c.ti * kTile + r, c.n - 1);
-      const int b = min(c.tj * kTile + r, c.n - 1);
-      prow[q] = X + static_cast<size_t>(pt[a]) * d;
-      qrow[q] = X + static_cast<size_t>(pt[b]) * d;
+    for (int j = 0; j < G::LOADS / 2; ++j) {
+      poff[j] = static_cast<uint32_t>(pt[min(c.ti * kTile + G::load_row(j), c.n - 1)]) * d;
+      qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(j + G::LOADS / 2) - G::BM, c.n - 1)]) * d;
     }
     if (tid < kTile) inv_a[tid] = inv_norm[pt[min(c.ti * kTile + tid, c.n - 1)]];
     else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
-    reinterpret_cast<uint32_t*>(&dbits[0][0])[tid] = 0u;
-    reinterpret_cast<uint32_t*>(&dbits[0][0])[tid + 256] = 0u;
-    reinterpret_cast<uint32_t*>(&tbits[0][0])[tid] = 0u;
-    reinterpret_cast<uint32_t*>(&tbits[0][0])[tid + 256] = 0u;
-    f32x4 acc[4][4];
-    zero_acc(acc);
-    gemm_tile_bf16(prow, qrow, d, lds, acc);  // ends with a barrier
+    G::Acc acc;
+    G::zero(acc);
+    G::run_single(X, poff, X, qoff, d, lds, acc);  // ends with a barrier
 
+    // Each (fm, fn) block is 32 x 32: ballot v covers rows
+    // abase + 8(v/4) + (v%4) (bits 0..31) and that row + 4 (bits 32..63),
+    // bit position within a half = column.  Lanes 0..31 store one 32-bit
+    // row piece and one 32-bit column piece each, so every piece of the tile
+    // is written exactly once.
+    const int vsel = (lane & 31) >> 1, half = lane & 1, l31 = lane & 31;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        uint64_t m[4];
-        const int bl = 64 * wn + 16 * j + (lane & 15);
+      for (int fn = 0; fn < G::FN; ++fn) {
+        const int bl = wn * G::WTN + 32 * fn + l31;
         const int b = c.tj * kTile + bl;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int al = 64 * wm + 16 * i + 4 * (lane >> 4) + r;
+        const float ib = inv_b[bl];
+        const int abase = wm * G::WTM + 32 * fm;
+        auto edge = [&](int v) {
+          const int al = abase + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
           const int a = c.ti * kTile + al;
-          const float cs = acc[i][j][r] * inv_a[al] * inv_b[bl];
-          m[r] = __ballot(a < c.n && b < c.n && a != b && cs >= h);
+          return a < c.n && b < c.n && a != b && acc[fm][fn][v] * inv_a[al] * ib >= h;
+        };
+        uint64_t any = 0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) any |= __ballot(edge(v));
+        uint32_t piece = 0, tv = 0;
+        if (any) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const uint64_t mv = __ballot(edge(v));
+            if (v == vsel) piece = static_cast<uint32_t>(mv >> (32 * half));
+            const int base = 8 * (v >> 2) + (v & 3);
+            tv |= static_cast<uint32_t>((mv >> l31) & 1ull) << base;
+            tv |= static_cast<uint32_t>((mv >> (32 + l31)) & 1ull) << (base + 4);
+          }
         }
-        if (m[0] | m[1] | m[2] | m[3]) {
-          if (lane < 4) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              dbits[64 * wm + 16 * i + 4 * lane + r][4 * wn + j] =
-                  static_cast<uint16_t>(m[r] >> (16 * lane));
-          }
-          if (lane < 16) {
-            uint32_t v = 0;
-#pragma unroll
-            for (int qd = 0; qd < 4; ++qd)
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                v |= static_cast<uint32_t>((m[r] >> (16 * qd + lane)) & 1ull) << (4 * qd + r);
-            tbits[64 * wn + 16 * j + lane][4 * wm + i] = static_cast<uint16_t>(v);
-          }
+        if (lane < 32) {
+          dbits[abase + 8 * (vsel >> 2) + 4 * half + (vsel & 3)][(wn * G::WTN + 32 * fn) >> 5] = piece;
+          tbits[bl][abase >> 5] = tv;
         }
       }
     }
     __syncthreads();
-    write_tile_words(c, dbits, tbits, bitmask, bm_off[c.e]);
+    // degree: edges of each tile row (and, off the diagonal, of each mirrored row)
+    {
+      const bool mirror = tid >= kTile;
+      const int rl = mirror ? tid - kTile : tid;
+      const uint32_t* pcs = mirror ? tbits[rl] : dbits[rl];
+      int cnt = 0;
+#pragma unroll
+      for (int g = 0; g < kTile / 32; ++g) cnt += __popc(pcs[g]);
+      const int r = (mirror ? c.tj : c.ti) * kTile + rl;
+      if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
+    }
+    // write the words: 4 per row of the tile, direct and (off-diagonal) mirrored
+    for (int i = tid; i < kTile * 4; i += G::THREADS) {
+      const int rl = i >> 2, ww = i & 3;
+      const uint64_t dv = static_cast<uint64_t>(dbits[rl][2 * ww]) |
+                          (static_cast<uint64_t>(dbits[rl][2 * ww + 1]) << 32);
+      const int a = c.ti * kTile + rl, wd = 4 * c.tj + ww;
+      if (a < c.n && wd < c.W) bitmask[bm_off[c.e] + static_cast<long long>(a) * c.W + wd] = dv;
+      if (c.ti != c.tj) {
+        const uint64_t tv = static_cast<uint64_t>(tbits[rl][2 * ww]) |
+                            (static_cast<uint64_t>(tbits[rl][2 * ww + 1]) << 32);
+        const int bb = c.tj * kTile + rl, wt = 4 * c.ti + ww;
+        if (bb < c.n && wt < c.W) bitmask[bm_off[c.e] + static_cast<long long>(bb) * c.W + wt] = tv;
+      }
+    }
     __syncthreads();
   }
 }
@@ -245,14 +317,14 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
     const float* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, uint64_t* __restrict__ bitmask) {
+    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
   constexpr int KC = 16;
-  __shared__ float Ps[kTile][KC + 1];
-  __shared__ float Qs[kTile][KC + 1];
-  __shared__ uint8_t edge[kTile][kTile];
-  __shared__ uint16_t dbits[kTile][8];
-  __shared__ uint16_t tbits[kTile][8];
-  __shared__ float inv_a[kTile], inv_b[kTile];
+  __shared__ float Ps[kTileF32][KC + 1];
+  __shared__ float Qs[kTileF32][KC + 1];
+  __shared__ uint8_t edge[kTileF32][kTileF32];
+  __shared__ uint16_t dbits[kTileF32][8];
+  __shared__ uint16_t tbits[kTileF32][8];
+  __shared__ float inv_a[kTileF32], inv_b[kTileF32];
   if (*err) return;
   const int tid = threadIdx.x;
   const int rb = (tid >> 4) * 8, cb = (tid & 15) * 8;
@@ -260,8 +332,8 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
   for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
     const TileCoord c = decode_tile(tile, tile_off, offsets, E);
     const int32_t* pt = perm_token + c.lo;
-    if (tid < kTile) inv_a[tid] = inv_norm[pt[min(c.ti * kTile + tid, c.n - 1)]];
-    else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
+    if (tid < kTileF32) inv_a[tid] = inv_norm[pt[min(c.ti * kTileF32 + tid, c.n - 1)]];
+    else inv_b[tid - kTileF32] = inv_norm[pt[min(c.tj * kTileF32 + tid - kTileF32, c.n - 1)]];
     float acc[8][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -269,10 +341,10 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
     for (int k0 = 0; k0 < d; k0 += KC) {
       __syncthreads();
-      for (int idx = tid; idx < kTile * KC; idx += 256) {
+      for (int idx = tid; idx < kTileF32 * KC; idx += 256) {
         const int r = idx / KC, kk = idx % KC;
-        const int a = min(c.ti * kTile + r, c.n - 1);
-        const int b = min(c.tj * kTile + r, c.n - 1);
+        const int a = min(c.ti * kTileF32 + r, c.n - 1);
+        const int b = min(c.tj * kTileF32 + r, c.n - 1);
         Ps[r][kk] = X[static_cast<size_t>(pt[a]) * d + k0 + kk];
         Qs[r][kk] = X[static_cast<size_t>(pt[b]) * d + k0 + kk];
       }
@@ -294,12 +366,12 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int a = c.ti * kTile + rb + i, b = c.tj * kTile + cb + j;
+        const int a = c.ti * kTileF32 + rb + i, b = c.tj * kTileF32 + cb + j;
         const float cs = acc[i][j] * inv_a[rb + i] * inv_b[cb + j];
         edge[rb + i][cb + j] = (a < c.n && b < c.n && a != b && cs >= h) ? 1 : 0;
       }
     __syncthreads();
-    for (int idx = tid; idx < kTile * 8; idx += 256) {
+    for (int idx = tid; idx < kTileF32 * 8; idx += 256) {
       const int r = idx >> 3, g = idx & 7;
       uint32_t dv = 0, tv = 0;
       for (int bit = 0; bit < 16; ++bit) {
@@ -310,28 +382,15 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       tbits[r][g] = static_cast<uint16_t>(tv);
     }
     __syncthreads();
+    {
+      const bool mirror = tid >= kTileF32;
+      const int rl = mirror ? tid - kTileF32 : tid;
+      int cnt = 0;
+      for (int g = 0; g < 8; ++g) cnt += __popc(mirror ? tbits[rl][g] : dbits[rl][g]);
+      const int r = (mirror ? c.tj : c.ti) * kTileF32 + rl;
+      if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
+    }
     write_tile_words(c, dbits, tbits, bitmask, bm_off[c.e]);
-  }
-}
-
-__global__ __launch_bounds__(256) void degree_kernel(
-    const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, const uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg,
-    int32_t* __restrict__ state, int32_t* __restrict__ degree_out) {
-  if (*err) return;
-  const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= offsets[E]) return;
-  const int e = bucket_of(offsets, E, p);
-  const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
-  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
-  int cnt = 0;
-  for (int wd = lane; wd < W; wd += 64) cnt += __popcll(row[wd]);
-  cnt = wave_sum_i32(cnt);
-  if (lane == 0) {
-    deg[p] = cnt;
-    state[p] = kStateUndecided;
-    if (degree_out) degree_out[p] = cnt;
   }
 }
 
@@ -371,17 +430,28 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
   return true;
 }
 
+// One round over all positions (one wave each).  Round r exits at once when
+// round r-1 left nothing undecided; a position still undecided after its
+// visit sets undecided[r].  Round 0 also publishes the degrees.
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state) {
+    const int32_t* __restrict__ deg, int32_t* state, int r, int* __restrict__ undecided,
+    int32_t* __restrict__ degree_out) {
   if (*err) return;
+  if (r > 0 && load_flag(&undecided[r - 1]) == 0) return;
+  const int lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (p >= offsets[E]) return;
+  if (r == 0 && degree_out && lane == 0) degree_out[p] = deg[p];
   if (load_flag(&state[p]) != kStateUndecided) return;
   const int e = bucket_of(offsets, E, p);
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
-  greedy_visit(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg, state);
+  // flag (not count) positions left undecided: a read before the store keeps
+  // the number of writes to the shared word small
+  if (greedy_visit(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg, state) &&
+      lane == 0 && load_flag(&undecided[r]) == 0)
+    store_flag(&undecided[r], 1);
 }
 
 // One workgroup per bucket: rounds until every position is decided.  Each
@@ -390,8 +460,9 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
 __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state) {
+    const int32_t* __restrict__ deg, int32_t* state, const int* __restrict__ undecided) {
   if (*err) return;
+  if (load_flag(&undecided[kGreedyGridRounds - 1]) == 0) return;
   const int e = blockIdx.x;
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   if (n == 0) return;
@@ -448,68 +519,82 @@ __global__ __launch_bounds__(256) void assign_kernel(
   if (lane == 0) rep_of_pos[p] = static_cast<int>(~static_cast<unsigned int>(best & 0xffffffffull));
 }
 
-// One workgroup: rep_index[p] = number of representatives before p,
-// rep_token[row] = token of that representative, rep_offsets per expert.
-__global__ __launch_bounds__(1024) void rep_scan_kernel(
+// Representative rows, in two passes over 1024-position blocks.
+// rep_local_kernel: rank of each representative inside its block (wave
+// ballots + LDS prefix of the 16 wave counts) and the block's count.
+__global__ __launch_bounds__(1024) void rep_local_kernel(const int32_t* __restrict__ offsets, int E,
+                                                        const int32_t* __restrict__ rep_of_pos,
+                                                        int32_t* __restrict__ local,
+                                                        int32_t* __restrict__ bsum) {
+  __shared__ int wcnt[16];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int S = offsets[E];
+  const int base = blockIdx.x * 1024;
+  if (base >= S) return;
+  const int p = base + tid;
+  const bool f = p < S && rep_of_pos[p] == p;
+  const uint64_t bal = __ballot(f);
+  if (lane == 0) wcnt[wv] = __popcll(bal);
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int i = 0; i < 16; ++i) {
+    const int v = wcnt[i];
+    before += i < wv ? v : 0;
+    total += v;
+  }
+  if (p < S) local[p] = before + __popcll(bal & lanemask_lt());
+  if (tid == 0) bsum[blockIdx.x] = total;
+}
+
+// rep_finalize_kernel: every block prefixes the block counts in LDS, then
+// writes rep_token, rep_row (through the representative's own block prefix)
+// and, in block 0, rep_offsets.
+__global__ __launch_bounds__(1024) void rep_finalize_kernel(
     const int32_t* __restrict__ offsets, int E, const int32_t* __restrict__ rep_of_pos,
-    const int32_t* __restrict__ perm_token, int32_t* rep_index, int32_t* __restrict__ rep_token,
-    int32_t* __restrict__ rep_offsets) {
-  constexpr int ITEMS = 16;
+    const int32_t* __restrict__ perm_token, const int32_t* __restrict__ local,
+    const int32_t* __restrict__ bsum, int32_t* __restrict__ rep_row, int32_t* __restrict__ rep_token,
+    int32_t* __restrict__ rep_offsets, int max_blocks) {
+  extern __shared__ int bpre[];   // max_blocks + 1 entries
   __shared__ int wsum[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int S = offsets[E];
+  const int nb = (S + 1023) / 1024;
+  // exclusive prefix of bsum[0..nb) into bpre, 1024 at a time
   int carry = 0;
-  for (int base = 0; base < S; base += 1024 * ITEMS) {
-    int f[ITEMS];
-    int local = 0;
-#pragma unroll
-    for (int i = 0; i < ITEMS; ++i) {
-      const int p = base + tid * ITEMS + i;
-      f[i] = (p < S && rep_of_pos[p] == p) ? 1 : 0;
-      local += f[i];
-    }
-    int incl = local;
+  for (int c0 = 0; c0 < nb; c0 += 1024) {
+    const int i = c0 + tid;
+    const int v = i < nb ? bsum[i] : 0;
+    int incl = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += v;
+      const int u = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += u;
     }
     if (lane == 63) wsum[wv] = incl;
     __syncthreads();
-    int wbase = 0, chunk_total = 0;
-    for (int i = 0; i < 16; ++i) {
-      const int v = wsum[i];
-      if (i < wv) wbase += v;
-      chunk_total += v;
+    int wb = 0, tot = 0;
+    for (int k = 0; k < 16; ++k) {
+      wb += k < wv ? wsum[k] : 0;
+      tot += wsum[k];
     }
-    int r = carry + wbase + incl - local;
-#pragma unroll
-    for (int i = 0; i < ITEMS; ++i) {
-      const int p = base + tid * ITEMS + i;
-      if (p < S) {
-        rep_index[p] = r;
-        if (f[i]) rep_token[r] = perm_token[p];
-        r += f[i];
-      }
-    }
-    carry += chunk_total;
+    if (i < nb) bpre[i] = carry + wb + incl - v;
+    carry += tot;
     __syncthreads();
   }
-  __threadfence();
+  if (tid == 0) bpre[nb] = carry;
   __syncthreads();
-  if (tid <= E) {
-    const int p = offsets[tid];
-    rep_offsets[tid] = (p < S) ? load_flag(&rep_index[p]) : carry;
+  const int p = blockIdx.x * 1024 + tid;
+  if (p < S) {
+    const int q = rep_of_pos[p];
+    const int row = bpre[q >> 10] + local[q];
+    rep_row[p] = row;
+    if (q == p) rep_token[row] = perm_token[p];
   }
-}
-
-__global__ __launch_bounds__(256) void rep_row_kernel(const int32_t* __restrict__ offsets, int E,
-                                                      const int32_t* __restrict__ rep_of_pos,
-                                                      const int32_t* __restrict__ rep_index,
-                                                      int32_t* __restrict__ rep_row) {
-  const int p = blockIdx.x * 256 + threadIdx.x;
-  if (p >= offsets[E]) return;
-  rep_row[p] = rep_index[rep_of_pos[p]];
+  if (blockIdx.x == 0 && tid <= E) {
+    const int o = offsets[tid];
+    rep_offsets[tid] = o < S ? bpre[o >> 10] + local[o] : bpre[nb];
+  }
+  (void)max_blocks;
 }
 
 __global__ __launch_bounds__(256) void gather_kernel(const uint8_t* __restrict__ x, size_t row_bytes,
@@ -529,9 +614,11 @@ struct CondenseWs {
   int32_t* tile_off;
   long long* bm_off;
   int* err;
+  int* undecided;
   int32_t* deg;
   int32_t* state;
-  int32_t* rep_index;
+  int32_t* local;
+  int32_t* bsum;
   uint64_t* bitmask;
   long long cap_words;
 };
@@ -543,24 +630,16 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket) {
   w.tile_off = c.take<int32_t>(E + 1);
   w.bm_off = c.take<long long>(E + 1);
   w.err = c.take<int>(1);
+  w.undecided = c.take<int>(kGreedyGridRounds + 1);
   w.deg = c.take<int32_t>(S);
   w.state = c.take<int32_t>(S);
-  w.rep_index = c.take<int32_t>(S);
+  w.local = c.take<int32_t>(S);
+  w.bsum = c.take<int32_t>((S + 1023) / 1024 + 1);
   w.cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
   w.bitmask = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
   return w;
 }
 
-int gram_grid() {
-  static int grid = 0;
-  if (!grid) {
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess)
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    grid = 2 * cus;
-  }
-  return grid;
-}
 
 }  // namespace
 }  // namespace luffy
@@ -592,8 +671,8 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   if (threshold != threshold) return fail(LUFFY_E_INVALID, "luffy_condense: threshold is NaN");
   if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: E=%d > %d", E, kMaxExperts);
   if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: d=%d not a multiple of 64", d);
-  if (static_cast<long long>(T) * k >= (1ll << 31))
-    return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: T*k too large");
+  if (static_cast<long long>(T) * k > (1ll << 24))
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: T*k > 2^24");
   const size_t need = luffy_condense_workspace_size(T, d, E, k, max_bucket);
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "luffy_condense: workspace needs %zu bytes, 256-aligned", need);
@@ -604,50 +683,53 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const int S = T * k;
   const bool bf16 = dtype == LUFFY_BF16;
 
+  const int norm_blocks = (T + 3) / 4;
   {
     ProfileScope prof_("norm", s);
-    if (bf16) norm_kernel<true><<<(T + 3) / 4, 256, 0, s>>>(x, T, d, ws.inv_norm);
-    else norm_kernel<false><<<(T + 3) / 4, 256, 0, s>>>(x, T, d, ws.inv_norm);
+    if (bf16) norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state);
+    else norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state);
   }
   {
     ProfileScope prof_("gram_prep", s);
-    gram_prep_kernel<<<1, 64, 0, s>>>(offsets, E, max_bucket, ws.cap_words, ws.tile_off, ws.bm_off, ws.err);
+    gram_prep_kernel<<<1, 64, 0, s>>>(offsets, E, max_bucket, bf16 ? kTile : kTileF32, ws.cap_words,
+                                      ws.tile_off, ws.bm_off, ws.err, ws.undecided);
   }
   {
     ProfileScope prof_("gram", s);
     if (bf16)
-      gram_kernel_bf16<<<gram_grid(), 256, 0, s>>>(static_cast<const uint16_t*>(x), d, perm_token, offsets, E,
-                                                 ws.inv_norm, threshold, ws.tile_off, ws.bm_off, ws.err,
-                                                 ws.bitmask);
+      gram_kernel_bf16<<<persistent_grid(), GemmBig::THREADS, 0, s>>>(
+          static_cast<const uint16_t*>(x), d, perm_token, offsets, E, ws.inv_norm, threshold, ws.tile_off,
+          ws.bm_off, ws.err, ws.bitmask, ws.deg);
     else
-      gram_kernel_f32<<<gram_grid(), 256, 0, s>>>(static_cast<const float*>(x), d, perm_token, offsets, E,
-                                                  ws.inv_norm, threshold, ws.tile_off, ws.bm_off, ws.err,
-                                                  ws.bitmask);
+      gram_kernel_f32<<<2 * persistent_grid(), 256, 0, s>>>(
+          static_cast<const float*>(x), d, perm_token, offsets, E, ws.inv_norm, threshold, ws.tile_off,
+          ws.bm_off, ws.err, ws.bitmask, ws.deg);
   }
   const int wave_blocks = (S + 3) / 4;
-  {
-    ProfileScope prof_("degree", s);
-    degree_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, degree);
-  }
   for (int r = 0; r < kGreedyGridRounds; ++r) {
     ProfileScope prof_("greedy_round", s);
-    greedy_round_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state);
+    greedy_round_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+                                                    ws.state, r, ws.undecided, degree);
   }
   {
     ProfileScope prof_("greedy_finish", s);
-    greedy_finish_kernel<<<E, 1024, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state);
+    greedy_finish_kernel<<<E, 1024, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
+                                            ws.undecided);
   }
   {
     ProfileScope prof_("assign", s);
-    assign_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, rep_of_pos);
+    assign_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
+                                              rep_of_pos);
+  }
+  const int pos_blocks = (S + 1023) / 1024;
+  {
+    ProfileScope prof_("rep_local", s);
+    rep_local_kernel<<<pos_blocks, 1024, 0, s>>>(offsets, E, rep_of_pos, ws.local, ws.bsum);
   }
   {
-    ProfileScope prof_("rep_scan", s);
-    rep_scan_kernel<<<1, 1024, 0, s>>>(offsets, E, rep_of_pos, perm_token, ws.rep_index, rep_token, rep_offsets);
-  }
-  {
-    ProfileScope prof_("rep_row", s);
-    rep_row_kernel<<<(S + 255) / 256, 256, 0, s>>>(offsets, E, rep_of_pos, ws.rep_index, rep_row);
+    ProfileScope prof_("rep_finalize", s);
+    rep_finalize_kernel<<<pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s>>>(
+        offsets, E, rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, pos_blocks);
   }
   if (x_rep) {
     ProfileScope prof_("gather", s);

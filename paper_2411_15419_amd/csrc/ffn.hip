@@ -2,12 +2,12 @@
 //   H = act(X_rep W1_e^T)   (rounded to the element type)
 //   Y = H W2_e^T
 // Row counts per expert live on the device.  The grid is sized from the
-// upper bound ceil(max_rows/128) + E row tiles; each block finds its expert
+// upper bound ceil(max_rows/BN) + E row tiles; each block finds its expert
 // and row range from rep_offsets and exits when it has none.
 //
-// bf16: 128 x 128 MFMA tiles.  The weight rows are the P operand and the
-// token rows the Q operand, so each lane ends with four consecutive output
-// columns of one row and stores them as one 8-byte word.
+// bf16: 256 x 256 MFMA tiles (GemmBig).  The weight rows are the P operand
+// and the token rows the Q operand, so each lane ends with groups of four
+// consecutive output columns of one row and stores each as one 8-byte word.
 // fp32: 64 x 64 tiles of plain FMA (4 x 4 per thread).
 #include "gemm_core.h"
 #include "luffy_common.h"
@@ -53,50 +53,83 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
   return true;
 }
 
-template <int ACT, bool FIRST>
-__global__ __launch_bounds__(256, 2) void ffn_kernel_bf16(
+// Persistent grouped GEMM.  Tiles are numbered expert by expert; inside an
+// expert, output-column tiles come in groups of 4 with the row tile major
+// inside a group, so the ~32 tiles one XCD runs together share few weight
+// and token rows in its L2.
+template <class G, int ACT, bool FIRST>
+__global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
     const uint16_t* __restrict__ W, uint16_t* __restrict__ out) {
-  __shared__ uint16_t lds[kTileLdsElems];
-  int e, row0, rows;
-  if (!locate_row_tile(rep_offsets, E, kTile, blockIdx.x, e, row0, rows)) return;
+  // P = weight rows (outputs n), Q = token rows (m)
+  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
-  const int n0 = blockIdx.y * kTile;
-  const uint16_t* We = W + static_cast<size_t>(e) * N * K;
-  const uint16_t* prow[4];
-  const uint16_t* qrow[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = (tid >> 3) + 32 * q;
-    const int n = min(n0 + r, N - 1);
-    prow[q] = We + static_cast<size_t>(n) * K;
-    const int m = row0 + min(r, rows - 1);
-    const int src = row_index ? row_index[m] : m;
-    qrow[q] = A + static_cast<size_t>(src) * K;
+  const int wm = w / G::WN, wn = w % G::WN;
+  const int NT = (N + G::BM - 1) / G::BM;
+  // lane e: row tiles of expert e and the inclusive prefix of tile counts
+  int elo = 0, ehi = 0, mt = 0;
+  if (lane < E) {
+    elo = rep_offsets[lane];
+    ehi = rep_offsets[lane + 1];
+    mt = (ehi - elo + G::BN - 1) / G::BN;
   }
-  f32x4 acc[4][4];
-  zero_acc(acc);
-  gemm_tile_bf16(prow, qrow, K, lds, acc);
+  int incl = mt * NT;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = n0 + 64 * wm + 16 * i + 4 * (lane >> 4);
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const int total = __shfl(incl, 63, 64);
+  for (int t = xcd_virtual_block(); t < total; t += gridDim.x) {
+    const int e = __popcll(__ballot(lane < E && incl <= t));
+    const int excl = __shfl(incl, e, 64) - __shfl(mt, e, 64) * NT;
+    const int me = __shfl(mt, e, 64);
+    // inside the expert: output-column tiles in groups of 4, row tile major
+    // inside a group, so 32 consecutive tiles span ~8 row x 4 column tiles
+    const int r = t - excl;
+    const int ng = (NT + 3) / 4;
+    const int g = min(r / (4 * me), ng - 1);
+    const int r2 = r - 4 * g * me;
+    const int wg = min(4, NT - 4 * g);
+    const int ms = r2 / wg, nt = 4 * g + r2 % wg;
+    const int row0 = __shfl(elo, e, 64) + ms * G::BN;
+    const int rows = min(G::BN, __shfl(ehi, e, 64) - row0);
+    const int n0 = nt * G::BM;
+    const uint16_t* We = W + static_cast<size_t>(e) * N * K;
+    uint32_t poff[G::LOADS / 2], qoff[G::LOADS / 2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int ml = 64 * wn + 16 * j + (lane & 15);
-      if (ml < rows && n < N) {
-        uint16_t v[4];
+    for (int j = 0; j < G::LOADS / 2; ++j) {
+      poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
+      const int m = row0 + min(G::load_row(j + G::LOADS / 2) - G::BM, rows - 1);
+      qoff[j] = static_cast<uint32_t>(row_index ? row_index[m] : m) * K;
+    }
+    typename G::Acc acc;
+    G::zero(acc);
+    G::run(We, poff, A, qoff, K, lds, acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float z = acc[i][j][r];
-          if constexpr (FIRST) z = act_fn<ACT>(z);
-          v[r] = f32_to_bf16(z);
+    for (int fm = 0; fm < G::FM; ++fm) {
+#pragma unroll
+      for (int fn = 0; fn < G::FN; ++fn) {
+        const int ml = wn * G::WTN + 32 * fn + (lane & 31);
+        if (ml >= rows) continue;
+        uint16_t* orow = out + static_cast<size_t>(row0 + ml) * N;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = n0 + wm * G::WTM + 32 * fm + 8 * g + 4 * (lane >> 5);
+          if (n >= N) continue;
+          uint16_t v[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float z = acc[fm][fn][4 * g + q];
+            if constexpr (FIRST) z = act_fn<ACT>(z);
+            v[q] = f32_to_bf16(z);
+          }
+          uint2 pk;
+          pk.x = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 16);
+          pk.y = static_cast<uint32_t>(v[2]) | (static_cast<uint32_t>(v[3]) << 16);
+          *reinterpret_cast<uint2*>(orow + n) = pk;
         }
-        uint2 pk;
-        pk.x = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 16);
-        pk.y = static_cast<uint32_t>(v[2]) | (static_cast<uint32_t>(v[3]) << 16);
-        *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n) = pk;
       }
     }
   }
@@ -157,22 +190,26 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   }
 }
 
+#ifndef LUFFY_FFN_GEMM
+#define LUFFY_FFN_GEMM GemmBig
+#endif
+using FfnGemm = LUFFY_FFN_GEMM;
+
 template <int ACT>
 void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d,
                 int d_ff, int dtype, const void* w1, const void* w2, int max_rows, void* y_rep,
                 void* hidden, hipStream_t s) {
   if (dtype == LUFFY_BF16) {
-    const int mt = (max_rows + kTile - 1) / kTile + E;
-    dim3 g1(mt, (d_ff + kTile - 1) / kTile), g2(mt, (d + kTile - 1) / kTile);
+    const int grid = persistent_grid();
     {
       ProfileScope prof_("ffn1", s);
-      ffn_kernel_bf16<ACT, true><<<g1, 256, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
+      ffn_kernel_bf16<FfnGemm, ACT, true><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
                                                     d_ff, static_cast<const uint16_t*>(w1),
                                                     static_cast<uint16_t*>(hidden));
     }
     {
       ProfileScope prof_("ffn2", s);
-      ffn_kernel_bf16<ACT, false><<<g2, 256, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
+      ffn_kernel_bf16<FfnGemm, ACT, false><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
                                                      E, d_ff, d, static_cast<const uint16_t*>(w2),
                                                      static_cast<uint16_t*>(y_rep));
     }

@@ -1,99 +1,273 @@
-// 128 x 128 output tile of C[i][j] = sum_k P[i][k] * Q[j][k] on bf16 MFMA.
+// Output tile of C[i][j] = sum_k P[i][k] * Q[j][k] on bf16 MFMA (gfx950).
 //
-// Both operands are row-major with the contraction index contiguous, so the
-// same core serves the similarity (Gram) tiles, where P and Q are gathered
-// token rows, and the FFN tiles, where P holds weight rows ([out, in]
-// layout) and Q gathered token rows.
+// Both operands are row-major with the contraction index contiguous, so one
+// core serves the similarity tiles (P and Q are gathered token rows of one
+// bucket) and the FFN tiles (P = weight rows in [out, in] layout, Q =
+// gathered token rows).
 //
-// 256 threads = 4 waves in a 2 x 2 grid, each wave owning a 64 x 64 sub-tile
-// made of 4 x 4 MFMA 16x16x32 blocks.  K advances 64 at a time through
-// double-buffered LDS (rows padded by 8 elements against bank conflicts);
-// the next K slice is fetched into registers while the current one is
-// multiplied.
+// Block tile 256 x 256; waves form a WM x WN grid, each owning a
+// (256/WM) x (256/WN) sub-tile of v_mfma_f32_32x32x16_bf16 blocks.
 //
-// Result layout: acc[i][j][r] holds
-//   P row  64*(wave/2) + 16*i + 4*(lane/16) + r
-//   Q row  64*(wave%2) + 16*j + lane%16
+// K advances 32 at a time through a ring of 4 LDS stages (32 KB each).
+// Operands go from global memory straight into LDS with
+// global_load_lds_dwordx4 (no staging registers): while stage kt is
+// multiplied from registers, stage kt+1 is read out of LDS and stages
+// kt+2..kt+4 are in flight.  LDS rows are 64 bytes with no padding; the four
+// 16-byte chunks of row r are stored XOR-permuted by (r>>2) & 3, so the 16
+// lanes the LDS serves together in a fragment read (16 consecutive rows, one
+// chunk) hit 16 distinct 16-byte bank groups, while each DMA instruction
+// still writes one contiguous 1 KB block.
+//
+// Operand rows are given as 32-bit element offsets from a base pointer
+// (every operand here has fewer than 2^31 elements).
+//
+// Result layout of acc[fm][fn][v] in lane l of wave w:
+//   P row  (w / WN) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
+//   Q row  (w % WN) * WTN + 32*fn + l%32
 #pragma once
 
 #include "luffy_common.h"
 
 namespace luffy {
 
-constexpr int kTile = 128;
-constexpr int kTileK = 64;
-constexpr int kLdsStride = kTileK + 8;                 // bf16 elements per LDS row
-constexpr int kTileLdsElems = 4 * kTile * kLdsStride;  // P and Q, double-buffered
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
-// Rows this thread loads: (tid / 8) + 32 * q, q = 0..3, columns (tid % 8) * 8.
-__device__ __forceinline__ void gemm_tile_bf16(const uint16_t* const prow[4],
-                                               const uint16_t* const qrow[4], int K,
-                                               uint16_t* __restrict__ lds,
-                                               f32x4 (&acc)[4][4]) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
-  const int col = (tid & 7) * 8;
-  const int lrow = tid >> 3;
-  // buffer b of P at lds + b*BUF, of Q at lds + (2+b)*BUF
-  constexpr int BUF = kTile * kLdsStride;
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
 
-  uint4 pr[4], qr[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    pr[q] = *reinterpret_cast<const uint4*>(prow[q] + col);
-    qr[q] = *reinterpret_cast<const uint4*>(qrow[q] + col);
+// Workgroup barrier without the memory fences of __syncthreads(): the fence
+// would make the compiler wait for every outstanding DMA load.  LDS
+// visibility is handled explicitly: each wave waits (vmcnt) for its own DMA
+// writes before the barrier, and LDS reads are issued after it.
+__device__ __forceinline__ void raw_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt with only the vector-memory counter constrained (<= N, N < 64;
+// the 6-bit count is split over bits 3:0 and 15:14).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
+template <int WM_, int WN_>
+struct Gemm256 {
+  static constexpr int BM = 256, BN = 256, WM = WM_, WN = WN_;
+  static constexpr int BK = 32;                      // K per stage
+  static constexpr int STAGES = 4;
+  static constexpr int THREADS = 64 * WM * WN;       // 512
+  static constexpr int WTM = BM / WM, WTN = BN / WN; // 128 x 64
+  static constexpr int FM = WTM / 32, FN = WTN / 32; // 4 x 2
+  static constexpr int ROW_BYTES = BK * 2;           // 64
+  static constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;   // 32 KB
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;      // 128 KB
+  // each wave instruction fills 16 rows (1 KB); 32 per stage
+  static constexpr int NWAVES = WM * WN;
+  static constexpr int LOADS = (BM + BN) / 16 / NWAVES;
+  static_assert(LOADS * NWAVES * 16 == BM + BN && LOADS % 2 == 0, "load plan");
+
+  using Acc = f32x16[FM][FN];
+
+  static __device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
+
+  // Stage row this lane fills in load j: P rows 0..255 then Q rows 256..511
+  // (loads 0 .. LOADS/2-1 fill P rows, the rest Q rows).
+  static __device__ __forceinline__ int load_row(int j) {
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    return (w + NWAVES * j) * 16 + (lane >> 2);
   }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    *reinterpret_cast<uint4*>(lds + (lrow + 32 * q) * kLdsStride + col) = pr[q];
-    *reinterpret_cast<uint4*>(lds + 2 * BUF + (lrow + 32 * q) * kLdsStride + col) = qr[q];
-  }
-  __syncthreads();
 
-  const int nk = K / kTileK;
-  const int arow = (lane & 15) * kLdsStride + 8 * (lane >> 4);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    // the last iteration re-reads its own slice, so no branch guards the
-    // register prefetch (keeps pr/qr in registers)
-    const int k0 = (kt + 1 < nk ? kt + 1 : kt) * kTileK + col;
+  static __device__ __forceinline__ void zero(Acc& acc) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      pr[q] = *reinterpret_cast<const uint4*>(prow[q] + k0);
-      qr[q] = *reinterpret_cast<const uint4*>(qrow[q] + k0);
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  }
+
+  // Issue the DMA of K slice [k0, k0+32) into stage buffer `st`.
+  // goff[j]: element offset of the row load_row(j) (rows 0..255 from pbase,
+  // 256..511 from qbase), already including this lane's XOR-permuted chunk.
+  using lds_ptr = __attribute__((address_space(3))) uint8_t*;
+
+  static __device__ __forceinline__ void issue(const uint16_t* __restrict__ pbase,
+                                               const uint16_t* __restrict__ qbase,
+                                               const uint32_t (&goff)[LOADS], int k0,
+                                               lds_ptr st) {
+    const int w = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      const uint16_t* src = (j < LOADS / 2 ? pbase : qbase) + goff[j] + k0;
+      lds_ptr dst = st + (w + NWAVES * j) * 16 * ROW_BYTES;
+      __builtin_amdgcn_global_load_lds(src, reinterpret_cast<__attribute__((address_space(3))) void*>(dst),
+                                       16, 0, 0);
     }
-    const uint16_t* P = lds + cur * BUF + (64 * wm) * kLdsStride + arow;
-    const uint16_t* Q = lds + (2 + cur) * BUF + (64 * wn) * kLdsStride + arow;
+  }
+
+  struct Frags {
+    bf16x8 a[2][FM], b[2][FN];
+  };
+
+  // LDS -> registers: both 16-wide substeps of one stage.
+  static __device__ __forceinline__ void read_frags(lds_ptr S, int prow0, int qrow0, int half, int sw,
+                                                    Frags& f) {
 #pragma unroll
-    for (int kk = 0; kk < kTileK; kk += 32) {
-      bf16x8 a[4], b[4];
+    for (int kk = 0; kk < 2; ++kk) {
+      const int pc = ((2 * kk + half) ^ sw) * 16;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(P + 16 * i * kLdsStride + kk);
+      for (int i = 0; i < FM; ++i)
+        f.a[kk][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
+            S + prow0 + 32 * i * ROW_BYTES + pc);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(Q + 16 * j * kLdsStride + kk);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a[i], b[j], acc[i][j]);
+      for (int j = 0; j < FN; ++j)
+        f.b[kk][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
+            S + qrow0 + 32 * j * ROW_BYTES + pc);
     }
+  }
+
+  static __device__ __forceinline__ void mma(const Frags& f, Acc& acc) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *reinterpret_cast<uint4*>(lds + (cur ^ 1) * BUF + (lrow + 32 * q) * kLdsStride + col) = pr[q];
-      *reinterpret_cast<uint4*>(lds + (3 - cur) * BUF + (lrow + 32 * q) * kLdsStride + col) = qr[q];
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(f.a[kk][i], f.b[kk][j], acc[i][j]);
+  }
+
+  // Wait until the DMA of a stage has landed in this wave while the loads of
+  // `later` (0..3) stages issued after it stay in flight.
+  static __device__ __forceinline__ void wait_stage(int later) {
+    if (later >= 3) wait_vmcnt<3 * LOADS>();
+    else if (later == 2) wait_vmcnt<2 * LOADS>();
+    else if (later == 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+  }
+
+  // poff[j] (j < LOADS/2): element offset of P row load_row(j);
+  // qoff[j] (j < LOADS/2): element offset of Q row load_row(j + LOADS/2) - 256.
+  // K must be a multiple of 32.  Ends with a barrier after which the LDS may
+  // be reused.
+  //
+  // Iteration kt: wait for stage kt+1 (DMA) and for this wave's reads of
+  // stage kt, barrier, issue the DMA of stage kt+4 into stage kt's buffer,
+  // request stage kt+1's fragments, then multiply stage kt from registers,
+  // so the LDS reads of one stage overlap the MFMAs of the previous one.
+  static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase,
+                                             const uint32_t (&poff)[LOADS / 2],
+                                             const uint16_t* __restrict__ qbase,
+                                             const uint32_t (&qoff)[LOADS / 2], int K,
+                                             uint8_t* lds_generic, Acc& acc) {
+    const lds_ptr lds = (lds_ptr)lds_generic;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int wm = w / WN, wn = w % WN;
+    // DMA: lane fills physical chunk lane%4 of its row with logical chunk
+    // (lane%4) ^ swz(row)
+    uint32_t goff[LOADS];
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      const int r = load_row(j);
+      const uint32_t lc = static_cast<uint32_t>((lane & 3) ^ swz(r));
+      goff[j] = (j < LOADS / 2 ? poff[j] : qoff[j - LOADS / 2]) + lc * 8;
+    }
+    const int nk = K / BK;
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st)
+      if (st < nk) issue(pbase, qbase, goff, st * BK, lds + st * STAGE_BYTES);
+
+    // fragment reads: lane reads row (l%32) of each 32-row block, logical
+    // chunk kk/8 + l/32
+    const int sw = swz(lane & 31);
+    const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
+    const int qrow0 = (BM + wn * WTN + (lane & 31)) * ROW_BYTES;
+    const int half = lane >> 5;
+
+    Frags f0, f1;
+    wait_stage(min(nk - 1, STAGES - 1));   // stages 1..3 may still be in flight
+    raw_barrier();
+    read_frags(lds, prow0, qrow0, half, sw, f0);
+    auto step = [&](int kt, Frags& cur, Frags& nxt) {
+      if (kt + 1 < nk) {
+        // issued so far: stages up to min(nk-1, kt+3); stage kt+4 comes below
+        wait_stage(min(nk - 1, kt + STAGES - 1) - (kt + 1));
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
+        raw_barrier();
+        if (kt + STAGES < nk)
+          issue(pbase, qbase, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES);
+        read_frags(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
+      }
+      mma(cur, acc);
+    };
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      step(kt, f0, f1);
+      step(kt + 1, f1, f0);
+    }
+    if (kt < nk) step(kt, f0, f1);
+    __syncthreads();
+  }
+
+  // Same contract as run() with one fragment set: each stage's fragments are
+  // read after its barrier and multiplied right away.  Fewer live registers,
+  // for kernels whose epilogue needs them (the similarity tiles).
+  static __device__ __forceinline__ void run_single(const uint16_t* __restrict__ pbase,
+                                                    const uint32_t (&poff)[LOADS / 2],
+                                                    const uint16_t* __restrict__ qbase,
+                                                    const uint32_t (&qoff)[LOADS / 2], int K,
+                                                    uint8_t* lds_generic, Acc& acc) {
+    const lds_ptr lds = (lds_ptr)lds_generic;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int wm = w / WN, wn = w % WN;
+    uint32_t goff[LOADS];
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      const int r = load_row(j);
+      const uint32_t lc = static_cast<uint32_t>((lane & 3) ^ swz(r));
+      goff[j] = (j < LOADS / 2 ? poff[j] : qoff[j - LOADS / 2]) + lc * 8;
+    }
+    const int nk = K / BK;
+#pragma unroll
+    for (int st = 0; st < STAGES - 1; ++st)
+      if (st < nk) issue(pbase, qbase, goff, st * BK, lds + st * STAGE_BYTES);
+    const int sw = swz(lane & 31);
+    const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
+    const int qrow0 = (BM + wn * WTN + (lane & 31)) * ROW_BYTES;
+    const int half = lane >> 5;
+    for (int kt = 0; kt < nk; ++kt) {
+      // issued: stages up to min(nk-1, kt+2)
+      wait_stage(min(nk - 1, kt + STAGES - 2) - kt);
+      raw_barrier();
+      if (kt + STAGES - 1 < nk)
+        issue(pbase, qbase, goff, (kt + STAGES - 1) * BK, lds + ((kt + STAGES - 1) % STAGES) * STAGE_BYTES);
+      Frags f;
+      read_frags(lds + (kt % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, f);
+      mma(f, acc);
     }
     __syncthreads();
   }
-}
+};
 
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[4][4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+// 512 threads, wave tile 128 x 64.
+using GemmBig = Gemm256<2, 4>;
+// 256 threads, wave tile 128 x 128 (accumulators fill the AGPRs).
+using GemmWide = Gemm256<2, 2>;
+
+// Persistent-kernel block order: consecutive virtual ids share an XCD
+// (workgroups are dealt to the 8 XCDs round-robin), so the tiles that run
+// together on one XCD are neighbours in tile order and share its L2.
+__device__ __forceinline__ int xcd_virtual_block() {
+  constexpr int kXcds = 8;
+  const int g = gridDim.x, b = blockIdx.x;
+  if (g % kXcds) return b;
+  return (b % kXcds) * (g / kXcds) + b / kXcds;
 }
 
 }  // namespace luffy

@@ -37,6 +37,18 @@ int check_launch(const char* what) {
   return LUFFY_OK;
 }
 
+int persistent_grid() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int cus = 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
+
 // ---------------------------------------------------------------- profiling
 namespace {
 std::atomic<bool> g_prof_on{false};

@@ -52,6 +52,9 @@ __device__ __forceinline__ void store_flag(int* p, int v) {
 void set_error(const char* fmt, ...);
 int fail(int status, const char* fmt, ...);
 int check_launch(const char* what);
+// Compute units of the current device (cached); grid of the persistent
+// kernels, which run one 512-thread block per CU.
+int persistent_grid();
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

@@ -3,14 +3,15 @@
 // Kernels (all on the caller's stream, no host synchronisation):
 //   gate_kernel      64 tokens per block.  bf16: the four waves split the
 //                    contraction over d and each accumulates a 64 x E logit
-//                    tile on MFMA (16x16x32); fp32: plain FMA.  Top-k, gates
-//                    and the float64 re-decision of close calls follow in
-//                    the epilogue.
-//   slot_hist_kernel 1024 slots per block in slot-id order: stable rank of
-//                    every slot among the block's slots of its expert
-//                    (wave ballots) and the per-block expert counts.
-//   slot_scan_kernel one block: exclusive scan of the block counts per
-//                    expert, capacity clamp, bucket offsets.
+//                    tile on MFMA (16x16x32); fp32: plain FMA.  The epilogue
+//                    takes top-k, gates and the float64 re-decision of close
+//                    calls, then ranks every slot among the block's slots of
+//                    the same expert (wave ballots) and writes the block's
+//                    per-expert counts.  A chunk is (choice j, block b), and
+//                    chunks in (j, b) order are slots in slot-id order.
+//   slot_scan_kernel one block per expert: exclusive scan of its chunk
+//                    counts; the last block to finish writes the
+//                    capacity-clamped bucket offsets.
 //   slot_scatter_kernel  bucket position of every slot, capacity drop,
 //                    perm_token.
 #include <cmath>
@@ -20,17 +21,7 @@
 namespace luffy {
 namespace {
 
-constexpr int kGateTok = 64;     // tokens per gate block
-constexpr int kSlotChunk = 1024; // slots per histogram block
-
-template <bool BF16>
-__device__ __forceinline__ double elem_f64(const void* base, size_t i) {
-  if constexpr (BF16) {
-    return static_cast<double>(bf16_to_f32(static_cast<const uint16_t*>(base)[i]));
-  } else {
-    return static_cast<double>(static_cast<const float*>(base)[i]);
-  }
-}
+constexpr int kGateTok = 64;     // tokens per gate block (= slots per chunk)
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
   // xor butterfly: every lane ends with the same, bit-identical sum
@@ -42,12 +33,17 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 template <bool BF16>
 __global__ __launch_bounds__(256) void gate_kernel(
     const void* __restrict__ xv, const void* __restrict__ wv,
-    const float* __restrict__ bias, int T, int d, int E, int k,
-    int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate) {
+    const float* __restrict__ bias_g, int T, int d, int E, int k,
+    int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate,
+    int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done) {
   __shared__ float part[4][kGateTok][kMaxExperts + 1];
+  __shared__ float bias[kMaxExperts];
+  __shared__ int cnt[kMaxExperts];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int t0 = blockIdx.x * kGateTok;
+  if (threadIdx.x < E) bias[threadIdx.x] = bias_g ? bias_g[threadIdx.x] : 0.f;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *scan_done = 0;   // armed for slot_scan_kernel
 
   if constexpr (BF16) {
     const uint16_t* X = static_cast<const uint16_t*>(xv);
@@ -131,8 +127,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
   float v0 = NEG, v1 = NEG, v2 = NEG;
   int i0 = 0, i1 = 0;
   for (int e = 0; e < E; ++e) {
-    float v = part[0][lane][e] + part[1][lane][e] + part[2][lane][e] + part[3][lane][e];
-    if (bias) v += bias[e];
+    const float v = part[0][lane][e] + part[1][lane][e] + part[2][lane][e] + part[3][lane][e] + bias[e];
     part[0][lane][e] = v;
     if (v > v0) { v2 = v1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
     else if (v > v1) { v2 = v1; v1 = v; i1 = e; }
@@ -160,108 +155,122 @@ __global__ __launch_bounds__(256) void gate_kernel(
     for (int e = 0; e < E; ++e) {
       if (!((cm >> e) & 1ull)) continue;
       double s = 0.0;
-      for (int i = lane; i < d; i += 64)
-        s += elem_f64<BF16>(xv, xt + i) * elem_f64<BF16>(wv, static_cast<size_t>(e) * d + i);
+      if constexpr (BF16) {
+        const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
+        const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
+        for (int c = lane * 8; c < d; c += 512) {
+          Pack16 xa, wa;
+          xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
+          wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
+        }
+      } else {
+        const float* xr = static_cast<const float*>(xv) + xt;
+        const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
+        for (int c = lane * 4; c < d; c += 256) {
+          const float4 xa = *reinterpret_cast<const float4*>(xr + c);
+          const float4 wa = *reinterpret_cast<const float4*>(wr + c);
+          s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
+               static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
+        }
+      }
       s = wave_sum_f64(s);
-      if (bias) s += static_cast<double>(bias[e]);
+      s += static_cast<double>(bias[e]);
       if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
       else if (s > b1) { b1 = s; j1 = e; }
     }
     if (lane == tl) { i0 = j0; i1 = j1; }
   }
-  if (!valid) return;
-  float den = 0.f;
-  for (int e = 0; e < E; ++e) den += expf(part[0][lane][e] - v0);
-  if (k == 1) {
-    topk_idx[t] = i0;
-    topk_gate[t] = expf(part[0][lane][i0] - v0) / den;
-  } else {
-    const float ga = expf(part[0][lane][i0] - v0);
-    const float gb = expf(part[0][lane][i1] - v0);
-    topk_idx[2 * t] = i0;
-    topk_idx[2 * t + 1] = i1;
-    topk_gate[2 * t] = ga / (ga + gb);
-    topk_gate[2 * t + 1] = gb / (ga + gb);
+  if (valid) {
+    float den = 0.f;
+    for (int e = 0; e < E; ++e) den += expf(part[0][lane][e] - v0);
+    if (k == 1) {
+      topk_idx[t] = i0;
+      topk_gate[t] = expf(part[0][lane][i0] - v0) / den;
+    } else {
+      const float ga = expf(part[0][lane][i0] - v0);
+      const float gb = expf(part[0][lane][i1] - v0);
+      topk_idx[2 * t] = i0;
+      topk_idx[2 * t + 1] = i1;
+      topk_gate[2 * t] = ga / (ga + gb);
+      topk_gate[2 * t + 1] = gb / (ga + gb);
+    }
   }
-}
-
-// Rank of every slot among the slots of the same expert in its 1024-slot
-// block (slot id order), and the block's per-expert counts.
-__global__ __launch_bounds__(1024) void slot_hist_kernel(
-    const int32_t* __restrict__ topk_idx, int T, int k, int E,
-    int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist) {
-  __shared__ int cnt[16][kMaxExperts];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  for (int i = tid; i < 16 * kMaxExperts; i += 1024) (&cnt[0][0])[i] = 0;
-  __syncthreads();
-  const long long s = static_cast<long long>(blockIdx.x) * kSlotChunk + tid;
-  const long long S = static_cast<long long>(T) * k;
-  int e = -1, t = 0, j = 0;
-  if (s < S) {
-    j = static_cast<int>(s / T);
-    t = static_cast<int>(s - static_cast<long long>(j) * T);
-    e = topk_idx[static_cast<size_t>(t) * k + j];
-  }
-  const int key = e < 0 ? 127 : e;
-  uint64_t same = ~0ull;
+  // stable rank of each slot among this chunk's slots of the same expert:
+  // lanes holding the same expert are found with 7 ballots on its bits
+  const int nblk = gridDim.x;
+  for (int j = 0; j < k; ++j) {
+    const int e = valid ? (j == 0 ? i0 : i1) : -1;
+    const int key = e < 0 ? 127 : e;
+    uint64_t same = ~0ull;
 #pragma unroll
-  for (int b = 0; b < 7; ++b) {
-    const bool bit = (key >> b) & 1;
-    const uint64_t bb = __ballot(bit);
-    same &= bit ? bb : ~bb;
-  }
-  const int rank = __popcll(same & lanemask_lt());
-  if (e >= 0 && rank == 0) cnt[wv][e] = __popcll(same);
-  __syncthreads();
-  if (tid < E) {
-    int run = 0;
-    for (int w2 = 0; w2 < 16; ++w2) {
-      const int c = cnt[w2][tid];
-      cnt[w2][tid] = run;
-      run += c;
+    for (int b = 0; b < 7; ++b) {
+      const bool bit = (key >> b) & 1;
+      const uint64_t bb = __ballot(bit);
+      same &= bit ? bb : ~bb;
     }
-    hist[static_cast<size_t>(blockIdx.x) * E + tid] = run;
+    const int rank = __popcll(same & lanemask_lt());
+    if (lane < E) cnt[lane] = 0;
+    __builtin_amdgcn_wave_barrier();
+    if (e >= 0 && rank == 0) cnt[e] = __popcll(same);
+    __builtin_amdgcn_wave_barrier();
+    if (lane < E) hist[(static_cast<size_t>(j) * nblk + blockIdx.x) * E + lane] = cnt[lane];
+    if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
+    __builtin_amdgcn_wave_barrier();
   }
-  __syncthreads();
-  if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = cnt[wv][e] + rank;
 }
 
-// One block: per-expert exclusive scan of the block counts (in place, they
-// become block bases), capacity clamp and bucket offsets.
+// One block per expert: exclusive scan of that expert's chunk counts (in
+// place, they become chunk bases) and its total.  The last block to finish
+// (a counter, no waiting) turns the totals into capacity-clamped bucket
+// offsets and re-arms the counter for the next call.
 __global__ __launch_bounds__(1024) void slot_scan_kernel(
-    int32_t* __restrict__ hist, int nch, int E, int C, int32_t* __restrict__ offsets) {
-  constexpr int kLds = 8192;
-  __shared__ int buf[kLds];
-  __shared__ int run[kMaxExperts];
-  const int tid = threadIdx.x;
-  if (tid < E) run[tid] = 0;
-  const int rows_per_piece = kLds / E;
-  for (int c0 = 0; c0 < nch; c0 += rows_per_piece) {
-    const int rows = min(rows_per_piece, nch - c0);
-    __syncthreads();
-    for (int i = tid; i < rows * E; i += 1024) buf[i] = hist[static_cast<size_t>(c0) * E + i];
-    __syncthreads();
-    if (tid < E) {
-      int r = run[tid];
-      for (int c = 0; c < rows; ++c) {
-        const int v = buf[c * E + tid];
-        buf[c * E + tid] = r;
-        r += v;
-      }
-      run[tid] = r;
+    int32_t* __restrict__ hist, int nch, int E, int C, int32_t* __restrict__ offsets,
+    int* __restrict__ totals, int* __restrict__ done) {
+  __shared__ int wsum[16];
+  __shared__ bool last;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int e = blockIdx.x;
+  int carry = 0;
+  for (int c0 = 0; c0 < nch; c0 += 1024) {
+    const int c = c0 + tid;
+    const size_t o = static_cast<size_t>(c) * E + e;
+    const int v = c < nch ? hist[o] : 0;
+    int incl = v;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) {
+      const int u = __shfl_up(incl, sh, 64);
+      if (lane >= sh) incl += u;
     }
+    if (lane == 63) wsum[wv] = incl;
     __syncthreads();
-    for (int i = tid; i < rows * E; i += 1024) hist[static_cast<size_t>(c0) * E + i] = buf[i];
+    int wb = 0, tot = 0;
+    for (int i = 0; i < 16; ++i) {
+      wb += i < wv ? wsum[i] : 0;
+      tot += wsum[i];
+    }
+    if (c < nch) hist[o] = carry + wb + incl - v;
+    carry += tot;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    store_flag(&totals[e], carry);
+    __threadfence();
+    last = atomicAdd(done, 1) == E - 1;
   }
   __syncthreads();
-  if (tid == 0) {
+  if (last && tid == 0) {
+    __threadfence();
     int o = 0;
-    for (int e = 0; e < E; ++e) {
-      offsets[e] = o;
-      const int n = run[e];
+    for (int ee = 0; ee < E; ++ee) {
+      const int n = load_flag(&totals[ee]);
+      offsets[ee] = o;
       o += (C > 0 && n > C) ? C : n;
     }
     offsets[E] = o;
+    store_flag(done, 0);
   }
 }
 
@@ -275,7 +284,8 @@ __global__ __launch_bounds__(256) void slot_scatter_kernel(
   const int t = static_cast<int>(s - static_cast<long long>(j) * T);
   const size_t o = static_cast<size_t>(t) * k + j;
   const int e = topk_idx[o];
-  const int pos = base[static_cast<size_t>(s / kSlotChunk) * E + e] + slot_pos[o];
+  const int nblk = (T + kGateTok - 1) / kGateTok;
+  const int pos = base[(static_cast<size_t>(j) * nblk + t / kGateTok) * E + e] + slot_pos[o];
   if (C > 0 && pos >= C) {
     slot_pos[o] = -1;
   } else {
@@ -287,13 +297,16 @@ __global__ __launch_bounds__(256) void slot_scatter_kernel(
 
 struct RouteWs {
   int32_t* hist;
+  int* totals;
+  int* done;
 };
 
 RouteWs carve_route(Carver& c, int T, int E, int k) {
   RouteWs w;
-  const long long S = static_cast<long long>(T) * k;
-  const long long nch = (S + kSlotChunk - 1) / kSlotChunk;
+  const long long nch = static_cast<long long>(k) * ((T + kGateTok - 1) / kGateTok);
   w.hist = c.take<int32_t>(static_cast<size_t>(nch) * E);
+  w.totals = c.take<int>(E);
+  w.done = c.take<int>(1);
   return w;
 }
 
@@ -345,23 +358,20 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
   RouteWs ws = carve_route(c, T, E, k);
   const int C = capacity_slots(T, k, E, capacity_factor);
   const long long S = static_cast<long long>(T) * k;
-  const int nch = static_cast<int>((S + kSlotChunk - 1) / kSlotChunk);
-
   const int gblocks = (T + kGateTok - 1) / kGateTok;
+  const int nch = k * gblocks;
   {
     ProfileScope prof_("gate", s);
     if (dtype == LUFFY_BF16)
-      gate_kernel<true><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate);
+      gate_kernel<true><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
+                                                slot_pos, ws.hist, ws.done);
     else
-      gate_kernel<false><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate);
-  }
-  {
-    ProfileScope prof_("slot_hist", s);
-    slot_hist_kernel<<<nch, 1024, 0, s>>>(topk_idx, T, k, E, slot_pos, ws.hist);
+      gate_kernel<false><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
+                                                 slot_pos, ws.hist, ws.done);
   }
   {
     ProfileScope prof_("slot_scan", s);
-    slot_scan_kernel<<<1, 1024, 0, s>>>(ws.hist, nch, E, C, offsets);
+    slot_scan_kernel<<<E, 1024, 0, s>>>(ws.hist, nch, E, C, offsets, ws.totals, ws.done);
   }
   {
     ProfileScope prof_("slot_scatter", s);
