@@ -185,8 +185,8 @@ int luffy_combine(const void* y_rep, const int32_t* rep_row,
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram_prep, gram,
- * greedy_round, greedy_finish, assign, rep_local, rep_finalize, gather,
- * ffn1, ffn2, combine.
+ * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
+ * ffn1, ffn2, ffn2_reduce, combine.
  * ---------------------------------------------------------------------- */
 int luffy_profile_kernel(const char* name);
 int luffy_profile_read(double* total_ms, int* launches);

@@ -179,8 +179,8 @@ def profile_read():
 
 
 KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram_prep", "gram", "greedy_round",
-           "greedy_finish", "assign", "rep_local", "rep_finalize", "gather", "ffn1", "ffn2",
-           "combine")
+           "greedy_finish", "claim", "rep_local", "rep_finalize", "gather", "ffn1", "ffn2",
+           "ffn2_reduce", "combine")
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:

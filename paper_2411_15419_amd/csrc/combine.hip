@@ -1,5 +1,6 @@
 // luffy_combine: y[t] = sum over kept slots j of gate[t,j] * y_rep[rep_row[slot_pos[t,j]]]
-// One wave per token; 16-byte vector loads and stores; float32 sums.
+// One wave per token; 16-byte vector loads and stores (four per lane in
+// flight per source row); float32 sums.
 #include "luffy_common.h"
 
 namespace luffy {
@@ -23,37 +24,66 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
       g[j] = gate[static_cast<size_t>(t) * k + j];
     }
   }
+  // four 16-byte chunks per lane per pass, all loads issued before use
   if constexpr (BF16) {
     const uint16_t* src = static_cast<const uint16_t*>(y_rep);
     uint16_t* dst = static_cast<uint16_t*>(y) + static_cast<size_t>(t) * d;
-    for (int c = lane * 8; c < d; c += 512) {
-      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < k; ++j) {
-        if (row[j] < 0) continue;
-        Pack16 v;
-        v.u4 = *reinterpret_cast<const uint4*>(src + static_cast<size_t>(row[j]) * d + c);
+    for (int c0 = lane * 8; c0 < d; c0 += 4 * 512) {
+      Pack16 v[2][4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] = fmaf(g[j], bf16_to_f32(v.h[i]), acc[i]);
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int c = c0 + u * 512;
+          if (j < k && row[j] >= 0 && c < d)
+            v[j][u].u4 = *reinterpret_cast<const uint4*>(src + static_cast<size_t>(row[j]) * d + c);
+          else
+            v[j][u].u4 = make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u * 512;
+        if (c >= d) break;
+        Pack16 o;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float a = 0.f;
+#pragma unroll
+          for (int j = 0; j < 2; ++j) a = fmaf(g[j], bf16_to_f32(v[j][u].h[i]), a);
+          o.h[i] = f32_to_bf16(a);
+        }
+        *reinterpret_cast<uint4*>(dst + c) = o.u4;
       }
-      Pack16 o;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o.h[i] = f32_to_bf16(acc[i]);
-      *reinterpret_cast<uint4*>(dst + c) = o.u4;
     }
   } else {
     const float* src = static_cast<const float*>(y_rep);
     float* dst = static_cast<float*>(y) + static_cast<size_t>(t) * d;
-    for (int c = lane * 4; c < d; c += 256) {
-      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int j = 0; j < k; ++j) {
-        if (row[j] < 0) continue;
-        const float4 v = *reinterpret_cast<const float4*>(src + static_cast<size_t>(row[j]) * d + c);
-        acc.x = fmaf(g[j], v.x, acc.x);
-        acc.y = fmaf(g[j], v.y, acc.y);
-        acc.z = fmaf(g[j], v.z, acc.z);
-        acc.w = fmaf(g[j], v.w, acc.w);
+    for (int c0 = lane * 4; c0 < d; c0 += 4 * 256) {
+      float4 v[2][4];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int c = c0 + u * 256;
+          if (j < k && row[j] >= 0 && c < d)
+            v[j][u] = *reinterpret_cast<const float4*>(src + static_cast<size_t>(row[j]) * d + c);
+          else
+            v[j][u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u * 256;
+        if (c >= d) break;
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          a.x = fmaf(g[j], v[j][u].x, a.x);
+          a.y = fmaf(g[j], v[j][u].y, a.y);
+          a.z = fmaf(g[j], v[j][u].z, a.z);
+          a.w = fmaf(g[j], v[j][u].w, a.w);
+        }
+        *reinterpret_cast<float4*>(dst + c) = a;
       }
-      *reinterpret_cast<float4*>(dst + c) = acc;
     }
   }
 }

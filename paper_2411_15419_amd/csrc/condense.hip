@@ -12,13 +12,15 @@
 //                        bitmask word is written exactly once) and adds each
 //                        row's edge count to its degree.
 //   greedy_round_kernel  one round of the parallel form of the greedy walk
-//                        (launched a fixed number of times; a round exits at
-//                        once when the previous one left nothing undecided).
+//                        (launched a fixed number of times; decided
+//                        positions return at once).
 //   greedy_finish_kernel one workgroup per bucket repeats rounds until the
-//                        bucket is fully decided (exits at once if nothing is
-//                        left).
-//   assign_kernel        every absorbed position picks its first-visited
-//                        adjacent representative.
+//                        bucket is fully decided (after a coalesced check
+//                        that anything is left).
+//   claim_kernel         every kept position offers itself to its
+//                        neighbours (64-bit atomic max of degree, ~position):
+//                        an absorbed position ends with its first-visited
+//                        kept neighbour.
 //   rep_local_kernel, rep_finalize_kernel  representative rows by a two-pass
 //                        scan: rep_row, rep_token, rep_offsets.
 //   gather_kernel        optional copy of the representative rows.
@@ -36,7 +38,7 @@
 namespace luffy {
 namespace {
 
-constexpr int kGreedyGridRounds = 4;
+constexpr int kGreedyGridRounds = 3;
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig)
 constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
@@ -66,11 +68,13 @@ __device__ __forceinline__ int bucket_of(const int32_t* __restrict__ offsets, in
 template <bool BF16>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, int T, int d,
                                                    float* __restrict__ inv_norm, int S,
-                                                   int32_t* __restrict__ deg, int32_t* __restrict__ state) {
-  // also clears the degree counters and walk states of all S positions
+                                                   int32_t* __restrict__ deg, int32_t* __restrict__ state,
+                                                   unsigned long long* __restrict__ claim) {
+  // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
     state[p] = 0;
+    claim[p] = 0ull;
   }
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -106,9 +110,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
 // workspace.
 __global__ void gram_prep_kernel(const int32_t* __restrict__ offsets, int E, int max_bucket,
                                  int tile, long long cap_words, int32_t* __restrict__ tile_off,
-                                 long long* __restrict__ bm_off, int* __restrict__ err,
-                                 int* __restrict__ undecided) {
-  if (threadIdx.x <= kGreedyGridRounds) undecided[threadIdx.x] = 0;
+                                 long long* __restrict__ bm_off, int* __restrict__ err) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   long long words = 0;
   int tiles = 0, bad = 0;
@@ -395,25 +397,51 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
 }
 
 // Decides position p if its neighbours allow it; returns true when p is
-// still undecided afterwards (wave-uniform).
+// still undecided afterwards (wave-uniform).  Each lane walks its words of
+// the adjacency row (four word loads in flight) and gathers the state and
+// degree of up to 8 neighbours at a time before testing them.  The grid
+// rounds use plain loads (FRESH = false): a state written by another XCD in
+// the same launch may be seen late, which only delays a decision (states
+// change once, from undecided to final).  The single-workgroup finishing
+// pass, which relies on seeing the previous iteration's decisions, reads
+// the states with coherent atomic loads (FRESH = true).
+template <bool FRESH>
 __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
                                              const uint64_t* __restrict__ row,
                                              const int32_t* __restrict__ deg, int32_t* state) {
   const int lane = threadIdx.x & 63;
   const int dp = deg[p];
   bool kept_nb = false, blocked = false;
-  for (int wd = lane; wd < W && !kept_nb; wd += 64) {
-    uint64_t bits = row[wd];
-    while (bits) {
-      const int b = __ffsll(static_cast<long long>(bits)) - 1;
-      bits &= bits - 1;
-      if (wd * 64 + b >= n) break;   // defensive: no bit lies past the bucket
-      const int q = lo + wd * 64 + b;
-      const int st = load_flag(&state[q]);
-      if (st == kStateKept) { kept_nb = true; break; }
-      if (st == kStateUndecided) {
-        const int dq = deg[q];
-        if (dq > dp || (dq == dp && q < p)) blocked = true;
+  for (int wd0 = lane; wd0 < W && !kept_nb; wd0 += 256) {
+    uint64_t wv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) wv[u] = wd0 + 64 * u < W ? row[wd0 + 64 * u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint64_t bits = wv[u];
+      const int cbase = (wd0 + 64 * u) * 64;
+      while (bits) {
+        int q[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          q[i] = -1;
+          if (bits) {
+            const int b = __ffsll(static_cast<long long>(bits)) - 1;
+            bits &= bits - 1;
+            if (cbase + b < n) q[i] = lo + cbase + b;   // no bit lies past the bucket
+          }
+        }
+        int st[8], dq[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          st[i] = q[i] >= 0 ? (FRESH ? load_flag(&state[q[i]]) : state[q[i]]) : kStateAbsorbed;
+          dq[i] = q[i] >= 0 ? deg[q[i]] : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (st[i] == kStateKept) kept_nb = true;
+          else if (st[i] == kStateUndecided && (dq[i] > dp || (dq[i] == dp && q[i] < p))) blocked = true;
+        }
       }
     }
   }
@@ -430,28 +458,21 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
   return true;
 }
 
-// One round over all positions (one wave each).  Round r exits at once when
-// round r-1 left nothing undecided; a position still undecided after its
-// visit sets undecided[r].  Round 0 also publishes the degrees.
+// One round over all positions (one wave each); decided positions return at
+// once.  Round 0 also publishes the degrees.
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int r, int* __restrict__ undecided,
-    int32_t* __restrict__ degree_out) {
+    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out) {
   if (*err) return;
-  if (r > 0 && load_flag(&undecided[r - 1]) == 0) return;
   const int lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (p >= offsets[E]) return;
   if (r == 0 && degree_out && lane == 0) degree_out[p] = deg[p];
-  if (load_flag(&state[p]) != kStateUndecided) return;
+  if (state[p] != kStateUndecided) return;
   const int e = bucket_of(offsets, E, p);
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
-  // flag (not count) positions left undecided: a read before the store keeps
-  // the number of writes to the shared word small
-  if (greedy_visit(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg, state) &&
-      lane == 0 && load_flag(&undecided[r]) == 0)
-    store_flag(&undecided[r], 1);
+  greedy_visit<false>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg, state);
 }
 
 // One workgroup per bucket: rounds until every position is decided.  Each
@@ -460,70 +481,71 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
 __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, const int* __restrict__ undecided) {
+    const int32_t* __restrict__ deg, int32_t* state) {
   if (*err) return;
-  if (load_flag(&undecided[kGreedyGridRounds - 1]) == 0) return;
   const int e = blockIdx.x;
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   if (n == 0) return;
+  // coalesced check first: most buckets are fully decided by the grid rounds
+  int any = 0;
+  for (int i = threadIdx.x; i < n; i += 1024) any |= state[lo + i] == kStateUndecided;
+  if (!__syncthreads_or(any)) return;
   const int wv = threadIdx.x >> 6;
   for (int it = 0; it <= n; ++it) {
     int undecided = 0;
     for (int pl = wv; pl < n; pl += 16) {
       const int p = lo + pl;
       if (load_flag(&state[p]) != kStateUndecided) continue;
-      if (greedy_visit(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(pl) * W, deg, state))
+      if (greedy_visit<true>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(pl) * W, deg, state))
         undecided = 1;
     }
     if (!__syncthreads_or(undecided)) break;
   }
 }
 
-__global__ __launch_bounds__(256) void assign_kernel(
+// Each kept position offers itself to every neighbour: claim[b] keeps the
+// largest key (degree << 32 | ~position), i.e. the neighbour's first kept
+// neighbour in walk order.  Only kept positions scan their rows.
+__global__ __launch_bounds__(256) void claim_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
     const int32_t* __restrict__ deg, const int32_t* __restrict__ state,
-    int32_t* __restrict__ rep_of_pos) {
+    unsigned long long* __restrict__ claim) {
+  if (*err) return;
   const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= offsets[E]) return;
-  // after a layout error nothing was decided: every position keeps itself
-  if (*err || state[p] != kStateAbsorbed) {
-    if (lane == 0) rep_of_pos[p] = p;
-    return;
-  }
-  const int e = bucket_of(offsets, E, p);
+  const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (q >= offsets[E] || state[q] != kStateKept) return;
+  const int e = bucket_of(offsets, E, q);
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
-  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
-  // priority key: higher degree first, then lower position
-  unsigned long long best = 0;
-  for (int wd = lane; wd < W; wd += 64) {
-    uint64_t bits = row[wd];
-    while (bits) {
-      const int b = __ffsll(static_cast<long long>(bits)) - 1;
-      bits &= bits - 1;
-      if (wd * 64 + b >= n) break;
-      const int q = lo + wd * 64 + b;
-      if (state[q] == kStateKept) {
-        const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
-                                       static_cast<unsigned int>(~static_cast<unsigned int>(q));
-        best = key > best ? key : best;
+  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
+  const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
+                                 static_cast<unsigned int>(~static_cast<unsigned int>(q));
+  for (int wd0 = lane; wd0 < W; wd0 += 256) {
+    uint64_t wv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) wv[u] = wd0 + 64 * u < W ? row[wd0 + 64 * u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint64_t bits = wv[u];
+      const int cbase = (wd0 + 64 * u) * 64;
+      while (bits) {
+        const int b = __ffsll(static_cast<long long>(bits)) - 1;
+        bits &= bits - 1;
+        if (cbase + b < n) atomicMax(&claim[lo + cbase + b], key);
       }
     }
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned long long other = __shfl_xor(best, o, 64);
-    best = other > best ? other : best;
-  }
-  if (lane == 0) rep_of_pos[p] = static_cast<int>(~static_cast<unsigned int>(best & 0xffffffffull));
 }
 
 // Representative rows, in two passes over 1024-position blocks.
-// rep_local_kernel: rank of each representative inside its block (wave
-// ballots + LDS prefix of the 16 wave counts) and the block's count.
+// rep_local_kernel: the duplicate->representative map, then the rank of each
+// representative inside its block (wave ballots + LDS prefix of the 16 wave
+// counts) and the block's count.
 __global__ __launch_bounds__(1024) void rep_local_kernel(const int32_t* __restrict__ offsets, int E,
-                                                        const int32_t* __restrict__ rep_of_pos,
+                                                        const int* __restrict__ err,
+                                                        const int32_t* __restrict__ state,
+                                                        const unsigned long long* __restrict__ claim,
+                                                        int32_t* __restrict__ rep_of_pos,
                                                         int32_t* __restrict__ local,
                                                         int32_t* __restrict__ bsum) {
   __shared__ int wcnt[16];
@@ -532,7 +554,14 @@ __global__ __launch_bounds__(1024) void rep_local_kernel(const int32_t* __restri
   const int base = blockIdx.x * 1024;
   if (base >= S) return;
   const int p = base + tid;
-  const bool f = p < S && rep_of_pos[p] == p;
+  // rep_of_pos: absorbed -> claimed representative; otherwise itself (also
+  // after a layout error, when nothing was decided)
+  bool f = false;
+  if (p < S) {
+    const bool absorbed = !*err && state[p] == kStateAbsorbed;
+    rep_of_pos[p] = absorbed ? static_cast<int>(~static_cast<unsigned int>(claim[p] & 0xffffffffull)) : p;
+    f = !absorbed;
+  }
   const uint64_t bal = __ballot(f);
   if (lane == 0) wcnt[wv] = __popcll(bal);
   __syncthreads();
@@ -614,9 +643,9 @@ struct CondenseWs {
   int32_t* tile_off;
   long long* bm_off;
   int* err;
-  int* undecided;
   int32_t* deg;
   int32_t* state;
+  unsigned long long* claim;
   int32_t* local;
   int32_t* bsum;
   uint64_t* bitmask;
@@ -630,9 +659,9 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket) {
   w.tile_off = c.take<int32_t>(E + 1);
   w.bm_off = c.take<long long>(E + 1);
   w.err = c.take<int>(1);
-  w.undecided = c.take<int>(kGreedyGridRounds + 1);
   w.deg = c.take<int32_t>(S);
   w.state = c.take<int32_t>(S);
+  w.claim = c.take<unsigned long long>(S);
   w.local = c.take<int32_t>(S);
   w.bsum = c.take<int32_t>((S + 1023) / 1024 + 1);
   w.cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
@@ -686,13 +715,13 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const int norm_blocks = (T + 3) / 4;
   {
     ProfileScope prof_("norm", s);
-    if (bf16) norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state);
-    else norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state);
+    if (bf16) norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim);
+    else norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim);
   }
   {
     ProfileScope prof_("gram_prep", s);
     gram_prep_kernel<<<1, 64, 0, s>>>(offsets, E, max_bucket, bf16 ? kTile : kTileF32, ws.cap_words,
-                                      ws.tile_off, ws.bm_off, ws.err, ws.undecided);
+                                      ws.tile_off, ws.bm_off, ws.err);
   }
   {
     ProfileScope prof_("gram", s);
@@ -709,22 +738,22 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   for (int r = 0; r < kGreedyGridRounds; ++r) {
     ProfileScope prof_("greedy_round", s);
     greedy_round_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-                                                    ws.state, r, ws.undecided, degree);
+                                                    ws.state, r, degree);
   }
   {
     ProfileScope prof_("greedy_finish", s);
-    greedy_finish_kernel<<<E, 1024, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
-                                            ws.undecided);
+    greedy_finish_kernel<<<E, 1024, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state);
   }
   {
-    ProfileScope prof_("assign", s);
-    assign_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
-                                              rep_of_pos);
+    ProfileScope prof_("claim", s);
+    claim_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
+                                             ws.claim);
   }
   const int pos_blocks = (S + 1023) / 1024;
   {
     ProfileScope prof_("rep_local", s);
-    rep_local_kernel<<<pos_blocks, 1024, 0, s>>>(offsets, E, rep_of_pos, ws.local, ws.bsum);
+    rep_local_kernel<<<pos_blocks, 1024, 0, s>>>(offsets, E, ws.err, ws.state, ws.claim, rep_of_pos, ws.local,
+                                                 ws.bsum);
   }
   {
     ProfileScope prof_("rep_finalize", s);

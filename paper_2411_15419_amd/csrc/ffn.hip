@@ -57,45 +57,71 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
 // expert, output-column tiles come in groups of 4 with the row tile major
 // inside a group, so the ~32 tiles one XCD runs together share few weight
 // and token rows in its L2.
-template <class G, int ACT, bool FIRST>
-__global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
-    const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
-    const int32_t* __restrict__ rep_offsets, int E, int K, int N,
-    const uint16_t* __restrict__ W, uint16_t* __restrict__ out) {
-  // P = weight rows (outputs n), Q = token rows (m)
-  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w / G::WN, wn = w % G::WN;
-  const int NT = (N + G::BM - 1) / G::BM;
-  // lane e: row tiles of expert e and the inclusive prefix of tile counts
-  int elo = 0, ehi = 0, mt = 0;
-  if (lane < E) {
-    elo = rep_offsets[lane];
-    ehi = rep_offsets[lane + 1];
-    mt = (ehi - elo + G::BN - 1) / G::BN;
-  }
-  int incl = mt * NT;
+// Tile map of the grouped GEMM: rep_offsets held one expert per lane.
+template <class G>
+struct FfnTiles {
+  int elo, ehi, mt, incl, NT, tiles;
+  __device__ __forceinline__ FfnTiles(const int32_t* __restrict__ rep_offsets, int E, int N) {
+    const int lane = threadIdx.x & 63;
+    NT = (N + G::BM - 1) / G::BM;
+    elo = ehi = mt = 0;
+    if (lane < E) {
+      elo = rep_offsets[lane];
+      ehi = rep_offsets[lane + 1];
+      mt = (ehi - elo + G::BN - 1) / G::BN;
+    }
+    incl = mt * NT;
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += v;
+    }
+    tiles = __shfl(incl, 63, 64);
   }
-  const int total = __shfl(incl, 63, 64);
-  for (int t = xcd_virtual_block(); t < total; t += gridDim.x) {
-    const int e = __popcll(__ballot(lane < E && incl <= t));
-    const int excl = __shfl(incl, e, 64) - __shfl(mt, e, 64) * NT;
+  // Tile t -> expert e, first token row row0, row count, first output n0.
+  // Inside an expert, output-column tiles come in groups of 4 with the row
+  // tile major inside a group, so ~32 consecutive tiles span ~8 row x 4
+  // column tiles.
+  __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0) const {
+    const int lane = threadIdx.x & 63;
+    e = __popcll(__ballot(lane < E && incl <= t));
     const int me = __shfl(mt, e, 64);
-    // inside the expert: output-column tiles in groups of 4, row tile major
-    // inside a group, so 32 consecutive tiles span ~8 row x 4 column tiles
+    const int excl = __shfl(incl, e, 64) - me * NT;
     const int r = t - excl;
     const int ng = (NT + 3) / 4;
     const int g = min(r / (4 * me), ng - 1);
     const int r2 = r - 4 * g * me;
     const int wg = min(4, NT - 4 * g);
     const int ms = r2 / wg, nt = 4 * g + r2 % wg;
-    const int row0 = __shfl(elo, e, 64) + ms * G::BN;
-    const int rows = min(G::BN, __shfl(ehi, e, 64) - row0);
-    const int n0 = nt * G::BM;
+    row0 = __shfl(elo, e, 64) + ms * G::BN;
+    rows = min(G::BN, __shfl(ehi, e, 64) - row0);
+    n0 = nt * G::BM;
+  }
+};
+
+// One product of the FFN for every tile of every expert (persistent).
+// The second product (FIRST = false) has few output columns (d); with few
+// representatives it can have fewer tiles than CUs, and it then splits K
+// (decided on the device from the actual tile count): parts store float32
+// partial tiles and ffn_split_reduce_kernel finishes them.
+template <class G, int ACT, bool FIRST>
+__global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
+    const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
+    const int32_t* __restrict__ rep_offsets, int E, int K, int N,
+    const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots) {
+  using SK = SplitK<G>;
+  // P = weight rows (outputs n), Q = token rows (m)
+  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w / G::WN, wn = w % G::WN;
+  const FfnTiles<G> map(rep_offsets, E, N);
+  const int nk = K / G::BK;
+  const int S = FIRST ? 1 : SK::parts(map.tiles, gridDim.x, nk);
+  const int total = map.tiles * S;
+  for (int tt = xcd_virtual_block(); tt < total; tt += gridDim.x) {
+    const int t = tt / S, part = tt - t * S;
+    int e, row0, rows, n0;
+    map.decode(t, E, e, row0, rows, n0);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
     uint32_t poff[G::LOADS / 2], qoff[G::LOADS / 2];
 #pragma unroll
@@ -104,9 +130,12 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
       const int m = row0 + min(G::load_row(j + G::LOADS / 2) - G::BM, rows - 1);
       qoff[j] = static_cast<uint32_t>(row_index ? row_index[m] : m) * K;
     }
+    // K range of this part, in whole 32-wide stages
+    const int k0 = (part * nk / S) * G::BK, k1 = ((part + 1) * nk / S) * G::BK;
     typename G::Acc acc;
     G::zero(acc);
-    G::run(We, poff, A, qoff, K, lds, acc);
+    G::run(We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
+    float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * SK::SLOT_FLOATS : nullptr;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
@@ -116,8 +145,15 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
         uint16_t* orow = out + static_cast<size_t>(row0 + ml) * N;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int n = n0 + wm * G::WTM + 32 * fm + 8 * g + 4 * (lane >> 5);
+          const int nl = wm * G::WTM + 32 * fm + 8 * g + 4 * (lane >> 5);
+          const int n = n0 + nl;
           if (n >= N) continue;
+          if (slot) {
+            *reinterpret_cast<float4*>(slot + ml * G::BM + nl) =
+                make_float4(acc[fm][fn][4 * g], acc[fm][fn][4 * g + 1], acc[fm][fn][4 * g + 2],
+                            acc[fm][fn][4 * g + 3]);
+            continue;
+          }
           uint16_t v[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -132,6 +168,42 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
         }
       }
     }
+  }
+}
+
+// Sums the split parts of every output tile in part order and stores bf16.
+// Recomputes the same tile map and split count, so it does nothing when the
+// product was not split.
+template <class G>
+__global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __restrict__ rep_offsets, int E,
+                                                               int K, int N, const float* __restrict__ split_slots,
+                                                               uint16_t* __restrict__ out, int grid_parts) {
+  using SK = SplitK<G>;
+  const FfnTiles<G> map(rep_offsets, E, N);
+  const int S = SK::parts(map.tiles, grid_parts, K / G::BK);
+  if (S == 1) return;
+  // work unit = (tile, 4 rows): 64 threads x 4 columns per row
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int units = map.tiles * (G::BN / 4);
+  for (int u = blockIdx.x; u < units; u += gridDim.x) {
+    const int t = u / (G::BN / 4), ml = (u - t * (G::BN / 4)) * 4 + q;
+    int e, row0, rows, n0;
+    map.decode(t, E, e, row0, rows, n0);
+    const int c4 = lane * 4;
+    if (ml >= rows || n0 + c4 >= N) continue;
+    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS + ml * G::BM + c4;
+    float4 v[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      if (p < S) v[p] = *reinterpret_cast<const float4*>(src + p * SK::SLOT_FLOATS);
+    float4 sum = v[0];
+#pragma unroll
+    for (int p = 1; p < 4; ++p)
+      if (p < S) { sum.x += v[p].x; sum.y += v[p].y; sum.z += v[p].z; sum.w += v[p].w; }
+    uint2 pk;
+    pk.x = static_cast<uint32_t>(f32_to_bf16(sum.x)) | (static_cast<uint32_t>(f32_to_bf16(sum.y)) << 16);
+    pk.y = static_cast<uint32_t>(f32_to_bf16(sum.z)) | (static_cast<uint32_t>(f32_to_bf16(sum.w)) << 16);
+    *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n0 + c4) = pk;
   }
 }
 
@@ -190,6 +262,22 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   }
 }
 
+struct FfnWs {
+  void* hidden;
+  float* split_slots;
+};
+
+FfnWs carve_ffn(Carver& c, int max_rows, int d_ff, int dtype) {
+  FfnWs w;
+  w.hidden = c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
+  w.split_slots = nullptr;
+  if (dtype == LUFFY_BF16) {
+    using SK = SplitK<GemmBig>;
+    w.split_slots = c.take<float>(SK::SLOT_FLOATS * SK::MAX_SLOTS);
+  }
+  return w;
+}
+
 #ifndef LUFFY_FFN_GEMM
 #define LUFFY_FFN_GEMM GemmBig
 #endif
@@ -198,20 +286,26 @@ using FfnGemm = LUFFY_FFN_GEMM;
 template <int ACT>
 void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d,
                 int d_ff, int dtype, const void* w1, const void* w2, int max_rows, void* y_rep,
-                void* hidden, hipStream_t s) {
+                const FfnWs& ws, hipStream_t s) {
+  void* hidden = ws.hidden;
   if (dtype == LUFFY_BF16) {
     const int grid = persistent_grid();
     {
       ProfileScope prof_("ffn1", s);
       ffn_kernel_bf16<FfnGemm, ACT, true><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
                                                     d_ff, static_cast<const uint16_t*>(w1),
-                                                    static_cast<uint16_t*>(hidden));
+                                                    static_cast<uint16_t*>(hidden), ws.split_slots);
     }
     {
       ProfileScope prof_("ffn2", s);
       ffn_kernel_bf16<FfnGemm, ACT, false><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
                                                      E, d_ff, d, static_cast<const uint16_t*>(w2),
-                                                     static_cast<uint16_t*>(y_rep));
+                                                     static_cast<uint16_t*>(y_rep), ws.split_slots);
+    }
+    {
+      ProfileScope prof_("ffn2_reduce", s);
+      ffn_split_reduce_kernel<FfnGemm><<<8 * grid, 256, 0, s>>>(rep_offsets, E, d_ff, d, ws.split_slots,
+                                                               static_cast<uint16_t*>(y_rep), grid);
     }
   } else {
     const int mt = (max_rows + kF32Tile - 1) / kF32Tile + E;
@@ -239,7 +333,7 @@ extern "C" size_t luffy_expert_ffn_workspace_size(int max_rows, int E, int d_ff,
   (void)E;
   if (max_rows <= 0 || d_ff <= 0) return 0;
   Carver c(nullptr);
-  c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
+  carve_ffn(c, max_rows, d_ff, dtype);
   return c.size();
 }
 
@@ -263,9 +357,11 @@ extern "C" int luffy_expert_ffn(const void* x, const int32_t* row_index,
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "luffy_expert_ffn: workspace needs %zu bytes, 256-aligned", need);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(workspace);
+  const FfnWs ws = carve_ffn(c, max_rows, d_ff, dtype);
   if (act == LUFFY_ACT_GELU)
-    launch_ffn<LUFFY_ACT_GELU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, workspace, s);
+    launch_ffn<LUFFY_ACT_GELU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, ws, s);
   else
-    launch_ffn<LUFFY_ACT_SILU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, workspace, s);
+    launch_ffn<LUFFY_ACT_SILU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, ws, s);
   return check_launch("luffy_expert_ffn");
 }

@@ -255,6 +255,23 @@ struct Gemm256 {
   }
 };
 
+// Split-K for persistent kernels with fewer output tiles than CUs: each
+// output tile's K range is cut into S parts that run as separate tiles and
+// store float32 partial tiles; a separate reduction kernel (the kernel
+// boundary makes the partials visible across XCDs) adds them in part order.
+template <class G>
+struct SplitK {
+  static constexpr int MAX_SLOTS = 512;                       // >= CUs
+  static constexpr size_t SLOT_FLOATS = static_cast<size_t>(G::BM) * G::BN;
+
+  // parts per output tile: fill the grid once, at most 4, >= 4 K-stages each
+  static __device__ __forceinline__ int parts(int tiles, int grid, int nk) {
+    const int cap = min(grid, MAX_SLOTS);
+    if (tiles <= 0 || tiles * 2 > cap) return 1;
+    return max(1, min(min(cap / tiles, 4), nk / 4));
+  }
+};
+
 // 512 threads, wave tile 128 x 64.
 using GemmBig = Gemm256<2, 4>;
 // 256 threads, wave tile 128 x 128 (accumulators fill the AGPRs).

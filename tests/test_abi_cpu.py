@@ -50,7 +50,7 @@ def test_workspace_sizes(lib):
     c3 = L.condense_workspace_size(32768, 2048, 32, 2, 32768)
     assert c3 >= 65536 * 512 * 8
     assert L.condense_workspace_size(65536, 1024, 64, 1, 1024) < c3
-    assert L.expert_ffn_workspace_size(65536, 32, 8192, L.LUFFY_BF16) == 65536 * 8192 * 2
+    assert L.expert_ffn_workspace_size(65536, 32, 8192, L.LUFFY_BF16) >= 65536 * 8192 * 2
     assert L.route_workspace_size(0, 16, 2) == 0
 
 
