@@ -74,7 +74,7 @@ def roofline(name, cfg, counts, sec_per_launch):
                 frac=ach / HBM_PEAK_GBS, traffic=None)
 
 
-def cpu_baseline(inp, h, budget_s=12.0):
+def cpu_baseline(inp, h, budget_s=15.0):
     """The oracle as it stands, on the host cores, on a bounded sample."""
     import numpy as np
     from oracle import luffy_oracle as O
@@ -93,7 +93,7 @@ def cpu_baseline(inp, h, budget_s=12.0):
                     capacity_factor=cfg.capacity_factor)
         runs += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or runs >= 5:
+        if el >= budget_s:
             break
     sample = (f"whole layer on the first {T_s} of {cfg.T} tokens" if T_s < cfg.T
               else f"whole layer on all {cfg.T} tokens") + f", {runs} run(s), {el:.1f} s"

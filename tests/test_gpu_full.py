@@ -1,0 +1,151 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+throughput benchmark times (one MoELayer call on inputs resident in HBM).
+
+Indices (routing, buckets, degrees, representatives, compaction) are compared
+bit-exactly with the oracle over the whole batch.  Layer outputs are compared
+on a seeded sample of tokens: the oracle evaluates the expert FFN in fp64 for
+just the representatives those tokens use (the index maps having been found
+identical first), then gate-weights them as its combine does."""
+import numpy as np
+import pytest
+
+import luffy_gen as G
+from oracle import luffy_oracle as O
+from tests.layer_runner import (TOL, assert_condense_equal, assert_route_equal, fetch,
+                                make_layer, upload)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+N_SAMPLE = 96
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2411_15419_amd as L
+    L.load_library()
+
+
+def print_case(name, **kw):
+    print(f"[case] {name} {kw}", flush=True)
+
+
+def run_layer(inp, dev, h):
+    layer = make_layer(inp, dev, h)
+    layer(dev["x"])
+    return fetch(layer)
+
+
+def sample_tokens(o, T, seed):
+    """Seeded token sample that always includes condensed (non-representative)
+    slots, multi-slot tokens and, where they exist, fully dropped tokens."""
+    rng = np.random.default_rng([seed, 17])
+    picks = set(rng.choice(T, size=min(N_SAMPLE // 2, T), replace=False).tolist())
+    kept = o.slot_pos >= 0
+    dup = np.zeros(T, bool)
+    for j in range(o.slot_pos.shape[1]):
+        pos = o.slot_pos[kept[:, j], j]
+        dup[np.flatnonzero(kept[:, j])] |= o.rep_of_pos[pos] != pos
+    for mask in (dup, ~kept.any(axis=1), kept.all(axis=1)):
+        cand = np.flatnonzero(mask)
+        if cand.size:
+            picks.update(rng.choice(cand, size=min(N_SAMPLE // 6, cand.size),
+                                    replace=False).tolist())
+    return np.array(sorted(picks))
+
+
+def sampled_expected(inp, o, tokens):
+    """fp64 y_t for the sampled tokens and Y_rep for the rows they read."""
+    rows = sorted({int(o.rep_row[p]) for t in tokens for p in o.slot_pos[t] if p >= 0})
+    rows = np.array(rows, np.int64)
+    expert = np.searchsorted(o.rep_offsets, rows, side="right") - 1
+    E = inp.cfg.E
+    sub_off = np.zeros(E + 1, np.int64)
+    np.add.at(sub_off, expert + 1, 1)
+    sub_off = np.cumsum(sub_off)
+    x_sub = inp.x[o.rep_token[rows]].astype(np.float64)   # rows ascend, so experts do too
+    y_sub = O.expert_ffn(x_sub, sub_off, inp.w1, inp.w2, inp.cfg.act)
+    where = {int(r): i for i, r in enumerate(rows)}
+    y = np.zeros((tokens.size, inp.cfg.d), np.float64)
+    for i, t in enumerate(tokens):
+        for j, p in enumerate(o.slot_pos[t]):
+            if p >= 0:
+                y[i] += float(o.topk_gate[t, j]) * y_sub[where[int(o.rep_row[p])]]
+    return rows, y_sub, y
+
+
+def assert_sampled_close(g, inp, tokens, rows, y_sub, y_ref):
+    tol = TOL[inp.cfg.dtype]
+    den = np.abs(y_sub).max(axis=1)
+    err_rep = np.abs(g["y_rep"][rows] - y_sub).max(axis=1) / den
+    assert err_rep.max() <= tol, f"Y_rep max row rel err {err_rep.max():.3g}"
+    gy = g["y"][tokens]
+    dropped = np.abs(y_ref).max(axis=1) == 0
+    assert np.all(gy[dropped] == 0), "fully dropped tokens must be zero"
+    err = np.abs(gy[~dropped] - y_ref[~dropped]).max(axis=1) / np.abs(y_ref[~dropped]).max(axis=1)
+    assert err.size == 0 or err.max() <= tol, f"y max row rel err {err.max():.3g}"
+    print(f"[sampled] {tokens.size} tokens, {rows.size} rows, y err {err.max():.3g}, "
+          f"Y_rep err {err_rep.max():.3g}", flush=True)
+
+
+def assert_clique_union(inp, o):
+    """On clustered inputs the threshold graph is a union of cliques, one per
+    centre and bucket, so the representative of a slot is the first position
+    of its bucket drawn from the same centre (independent of any similarity
+    code; the oracle's own cosines confirm the premise in the CPU tests)."""
+    cid = inp.centre_id[o.perm_token]
+    for e in range(len(o.offsets) - 1):
+        lo, hi = int(o.offsets[e]), int(o.offsets[e + 1])
+        _, first = np.unique(cid[lo:hi], return_index=True)
+        first_of = dict(zip(cid[lo:hi][first].tolist(), (first + lo).tolist()))
+        want = np.array([first_of[c] for c in cid[lo:hi].tolist()], np.int64)
+        assert np.array_equal(o.rep_of_pos[lo:hi], want), f"bucket {e} is not a clique union"
+
+
+# The fp64 oracle's Gram over the largest workload takes tens of seconds on
+# the host, so these tests get longer limits than the per-test default.
+@pytest.mark.parametrize("name", [
+    pytest.param("c2", marks=pytest.mark.timeout(300)),
+    pytest.param("c3", marks=pytest.mark.timeout(600)),
+    pytest.param("c5", marks=pytest.mark.timeout(300)),
+])
+def test_full_size_layer(name):
+    inp = G.make_inputs(name, seed=0)
+    cfg = inp.cfg
+    print_case(name, T=cfg.T, d=cfg.d, E=cfg.E, k=cfg.k, d_ff=cfg.d_ff, h=cfg.h)
+    dev = upload(inp)
+    g = run_layer(inp, dev, cfg.h)
+    o = run_oracle_indices(inp, cfg.h)
+    assert_route_equal(g, o)
+    assert_condense_equal(g, o)
+    assert_clique_union(inp, o)
+    tokens = sample_tokens(o, cfg.T, seed=0)
+    rows, y_sub, y_ref = sampled_expected(inp, o, tokens)
+    assert_sampled_close(g, inp, tokens, rows, y_sub, y_ref)
+
+
+def run_oracle_indices(inp, h):
+    cfg = inp.cfg
+    return O.moe_layer(inp.x, inp.w_g, inp.b_g, None, None, k=cfg.k, h=h, act=cfg.act,
+                       capacity_factor=cfg.capacity_factor, with_ffn=False)
+
+
+@pytest.mark.timeout(400)
+def test_full_size_c4_threshold_sweep():
+    inp = G.make_inputs("c4", seed=0)
+    cfg = inp.cfg
+    dev = upload(inp)
+    ref = None
+    for h in cfg.thresholds:
+        print_case("c4", T=cfg.T, d=cfg.d, E=cfg.E, d_ff=cfg.d_ff, h=h)
+        g = run_layer(inp, dev, h)
+        o = run_oracle_indices(inp, h)
+        assert_route_equal(g, o)
+        assert_condense_equal(g, o)
+        assert o.rep_offsets[-1] == o.offsets[-1], "i.i.d. tokens should not merge"
+        if ref is None:
+            tokens = sample_tokens(o, cfg.T, seed=0)
+            ref = (tokens,) + sampled_expected(inp, o, tokens)
+        assert_sampled_close(g, inp, *ref)
