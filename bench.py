@@ -6,12 +6,22 @@ line with tokens/s, the roofline of the dominant kernel (timed live with HIP
 events on the stream it runs on) and the CPU oracle timed on the host cores.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config c2]
+    python bench.py --copy-calibration      # plain 1 GiB device copies, for
+                                            # scaling the HBM byte counters
+
+The roofline's "traffic" field is the HBM bytes per launch of the dominant
+kernel read back from rocprofv3 FETCH_SIZE / WRITE_SIZE runs recorded under
+profiles/ (hbm_traffic_<config>.md), each counter scaled by what it reads for
+the plain copy; it is null when the kernel sources have changed since.
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -74,6 +84,44 @@ def roofline(name, cfg, counts, sec_per_launch):
                 frac=ach / HBM_PEAK_GBS, traffic=None)
 
 
+def source_digest():
+    """sha256 over the HIP sources of the library (file names and contents)."""
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(ROOT, "paper_2411_15419_amd", "csrc", "*"))):
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(config, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary of
+    this workload, or None if there is none or the sources have changed."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{config}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != source_digest() or kernel not in rec.get("kernels", {}):
+        return None
+    k = rec["kernels"][kernel]
+    return (k["fetch_kib"] * 1024 * rec["fetch_scale"] + k["write_kib"] * 1024 * rec["write_scale"])
+
+
+def copy_calibration(n_bytes=1 << 30, reps=5):
+    """Plain device-to-device copies of a known size; rocprofv3 counter runs
+    over this give the FETCH_SIZE / WRITE_SIZE scale factors."""
+    import torch
+    src = torch.ones(n_bytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n_bytes, "copy_bytes_written": n_bytes, "reps": reps}))
+
+
 def cpu_baseline(inp, h, budget_s=15.0):
     """The oracle as it stands, on the host cores, on a bounded sample."""
     import numpy as np
@@ -110,6 +158,7 @@ def main():
     ap.add_argument("--threshold", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -124,6 +173,9 @@ def main():
     import paper_2411_15419_amd as L
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        copy_calibration()
+        return
     L.load_library()
     torch.cuda.set_device(0)
     cfg = G.config(args.config)
@@ -186,6 +238,10 @@ def main():
     dropped = cfg.T * cfg.k - counts["S"]
 
     rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
+    traffic = recorded_traffic(args.config, dominant)
+    rl["traffic"] = traffic
+    rl["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)"
+    rl["algorithmic_bytes"] = kernel_work(dominant, cfg, counts)["bytes"]
     rl["kernel"] = dominant
     rl["us_per_launch"] = dom_ms / dom_n * 1e3
     kernels = {}
