@@ -220,7 +220,8 @@ __global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
   using G = GemmBig;
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
-  __shared__ float inv_a[kTile], inv_b[kTile];
+  __shared__ __attribute__((aligned(16))) float inv_a[kTile];
+  __shared__ float inv_b[kTile];
   // after the K loop the operand buffers hold the tile's adjacency pieces:
   // dbits[row][32-column group], tbits[column][32-row group]
   uint32_t (*dbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds);
@@ -242,27 +243,46 @@ __global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
     else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
     G::Acc acc;
     G::zero(acc);
-    G::run_single(X, poff, X, qoff, d, lds, acc);  // ends with a barrier
+    G::run(X, poff, X, qoff, d, lds, acc);  // ends with a barrier
 
     // Each (fm, fn) block is 32 x 32: ballot v covers rows
     // abase + 8(v/4) + (v%4) (bits 0..31) and that row + 4 (bits 32..63),
     // bit position within a half = column.  Lanes 0..31 store one 32-bit
     // row piece and one 32-bit column piece each, so every piece of the tile
-    // is written exactly once.
-    const int vsel = (lane & 31) >> 1, half = lane & 1, l31 = lane & 31;
+    // is written exactly once.  Edge test: dot * (1/|a|) * (1/|b|) >= h,
+    // for rows and columns inside the bucket, never a token with itself.
+    const int vsel = (lane & 31) >> 1, half = lane & 1, l31 = lane & 31, hi = lane >> 5;
+    const bool same_tile = c.ti == c.tj;
+    const int nrow_a = c.n - c.ti * kTile, nrow_b = c.n - c.tj * kTile;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
+      const int abase = wm * G::WTM + 32 * fm;
+      // this lane's 16 rows: abase + 8q + 4hi + r, as 4 runs of 4.  Rows
+      // (and columns) outside the bucket get a NaN scale, which fails every
+      // comparison.
+      const float nan = __builtin_nanf("");
+      float ia[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int al0 = abase + 8 * q + 4 * hi;
+        const float4 f = *reinterpret_cast<const float4*>(&inv_a[al0]);
+        const float fv[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ia[4 * q + r] = al0 + r < nrow_a ? fv[r] : nan;
+      }
 #pragma unroll
       for (int fn = 0; fn < G::FN; ++fn) {
-        const int bl = wn * G::WTN + 32 * fn + l31;
-        const int b = c.tj * kTile + bl;
-        const float ib = inv_b[bl];
-        const int abase = wm * G::WTM + 32 * fm;
+        const int bbase = wn * G::WTN + 32 * fn;
+        const int bl = bbase + l31;
+        const float ib = bl < nrow_b ? inv_b[bl] : nan;
+        const bool diag = same_tile && abase == bbase;   // wave-uniform
         auto edge = [&](int v) {
-          const int al = abase + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          const int a = c.ti * kTile + al;
-          return a < c.n && b < c.n && a != b && acc[fm][fn][v] * inv_a[al] * ib >= h;
+          const bool e = acc[fm][fn][v] * ia[v] * ib >= h;
+          if (!diag) return e;
+          const int al = 8 * (v >> 2) + 4 * hi + (v & 3);   // row within the block
+          return e && al != l31;
         };
+        // first pass: any edge in the block (most blocks have none)
         uint64_t any = 0;
 #pragma unroll
         for (int v = 0; v < 16; ++v) any |= __ballot(edge(v));
@@ -278,7 +298,7 @@ __global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
           }
         }
         if (lane < 32) {
-          dbits[abase + 8 * (vsel >> 2) + 4 * half + (vsel & 3)][(wn * G::WTN + 32 * fn) >> 5] = piece;
+          dbits[abase + 8 * (vsel >> 2) + 4 * half + (vsel & 3)][bbase >> 5] = piece;
           tbits[bl][abase >> 5] = tv;
         }
       }

@@ -9,10 +9,13 @@
 // (256/WM) x (256/WN) sub-tile of v_mfma_f32_32x32x16_bf16 blocks.
 //
 // K advances 32 at a time through a ring of 4 LDS stages (32 KB each).
-// Operands go from global memory straight into LDS with
-// global_load_lds_dwordx4 (no staging registers): while stage kt is
-// multiplied from registers, stage kt+1 is read out of LDS and stages
-// kt+2..kt+4 are in flight.  LDS rows are 64 bytes with no padding; the four
+// Operands go from global memory straight into LDS with buffer loads
+// (buffer_load_dwordx4 ... lds, no staging registers; 32-bit byte offsets
+// from a buffer resource, so each operand must span less than 4 GiB):
+// while stage kt is multiplied from registers, stage kt+1 is read out of
+// LDS and stages kt+2..kt+4 are in flight.  In the steady state the
+// multiplies of a stage are interleaved one-to-one with the buffer loads
+// and LDS reads of later stages.  LDS rows are 64 bytes with no padding; the four
 // 16-byte chunks of row r are stored XOR-permuted by (r>>2) & 3, so the 16
 // lanes the LDS serves together in a fragment read (16 consecutive rows, one
 // chunk) hit 16 distinct 16-byte bank groups, while each DMA instruction
@@ -76,8 +79,10 @@ struct Gemm256 {
 
   // Stage row this lane fills in load j: P rows 0..255 then Q rows 256..511
   // (loads 0 .. LOADS/2-1 fill P rows, the rest Q rows).
+  static __device__ __forceinline__ int wave() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
   static __device__ __forceinline__ int load_row(int j) {
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int w = wave(), lane = threadIdx.x & 63;
     return (w + NWAVES * j) * 16 + (lane >> 2);
   }
 
@@ -91,21 +96,26 @@ struct Gemm256 {
   }
 
   // Issue the DMA of K slice [k0, k0+32) into stage buffer `st`.
-  // goff[j]: element offset of the row load_row(j) (rows 0..255 from pbase,
-  // 256..511 from qbase), already including this lane's XOR-permuted chunk.
+  // goff[j]: byte offset of the row load_row(j) (rows 0..255 from the P
+  // resource, 256..511 from the Q resource), already including this lane's
+  // XOR-permuted chunk.  w: wave index (wave-uniform).
   using lds_ptr = __attribute__((address_space(3))) uint8_t*;
 
-  static __device__ __forceinline__ void issue(const uint16_t* __restrict__ pbase,
-                                               const uint16_t* __restrict__ qbase,
-                                               const uint32_t (&goff)[LOADS], int k0,
-                                               lds_ptr st) {
-    const int w = threadIdx.x >> 6;
+  static __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
+    // raw buffer (no stride), full 32-bit range; 0x00020000: gfx9 word 3
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                             static_cast<int>(0xFFFFFFFFu), 0x00020000);
+  }
+
+  static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t prs, __amdgpu_buffer_rsrc_t qrs,
+                                               const uint32_t (&goff)[LOADS], int k0, lds_ptr st,
+                                               int w) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      const uint16_t* src = (j < LOADS / 2 ? pbase : qbase) + goff[j] + k0;
       lds_ptr dst = st + (w + NWAVES * j) * 16 * ROW_BYTES;
-      __builtin_amdgcn_global_load_lds(src, reinterpret_cast<__attribute__((address_space(3))) void*>(dst),
-                                       16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(j < LOADS / 2 ? prs : qrs,
+                                               reinterpret_cast<__attribute__((address_space(3))) void*>(dst),
+                                               16, goff[j], k0 * 2, 0, 0);
     }
   }
 
@@ -139,6 +149,38 @@ struct Gemm256 {
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(f.a[kk][i], f.b[kk][j], acc[i][j]);
   }
 
+  // DMA: lane fills physical chunk lane%4 of its row with logical chunk
+  // (lane%4) ^ swz(row); byte offsets.
+  static __device__ __forceinline__ void dma_offsets(const uint32_t (&poff)[LOADS / 2],
+                                                     const uint32_t (&qoff)[LOADS / 2],
+                                                     uint32_t (&goff)[LOADS]) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      const int r = load_row(j);
+      const uint32_t lc = static_cast<uint32_t>((lane & 3) ^ swz(r));
+      goff[j] = ((j < LOADS / 2 ? poff[j] : qoff[j - LOADS / 2]) + lc * 8) * 2u;
+    }
+  }
+
+  // Scheduling of one steady-state stage: each MFMA is followed by one of
+  // the stage's buffer loads, then by one LDS read, until they run out.
+  static __device__ __forceinline__ void interleave() {
+    constexpr int NMF = FM * FN * 2, NDS = (FM + FN) * 2, NVM = LOADS;
+    static_assert(NMF >= NVM + NDS, "interleave plan");
+#pragma unroll
+    for (int i = 0; i < NVM; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+    }
+#pragma unroll
+    for (int i = 0; i < NDS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+    }
+    if constexpr (NMF > NVM + NDS) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NVM - NDS, 0);
+  }
+
   // Wait until the DMA of a stage has landed in this wave while the loads of
   // `later` (0..3) stages issued after it stay in flight.
   static __device__ __forceinline__ void wait_stage(int later) {
@@ -165,21 +207,15 @@ struct Gemm256 {
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = wave();
     const int wm = w / WN, wn = w % WN;
-    // DMA: lane fills physical chunk lane%4 of its row with logical chunk
-    // (lane%4) ^ swz(row)
+    const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
     uint32_t goff[LOADS];
-#pragma unroll
-    for (int j = 0; j < LOADS; ++j) {
-      const int r = load_row(j);
-      const uint32_t lc = static_cast<uint32_t>((lane & 3) ^ swz(r));
-      goff[j] = (j < LOADS / 2 ? poff[j] : qoff[j - LOADS / 2]) + lc * 8;
-    }
+    dma_offsets(poff, qoff, goff);
     const int nk = K / BK;
 #pragma unroll
     for (int st = 0; st < STAGES; ++st)
-      if (st < nk) issue(pbase, qbase, goff, st * BK, lds + st * STAGE_BYTES);
+      if (st < nk) issue(prs, qrs, goff, st * BK, lds + st * STAGE_BYTES, w);
 
     // fragment reads: lane reads row (l%32) of each 32-row block, logical
     // chunk kk/8 + l/32
@@ -192,19 +228,39 @@ struct Gemm256 {
     wait_stage(min(nk - 1, STAGES - 1));   // stages 1..3 may still be in flight
     raw_barrier();
     read_frags(lds, prow0, qrow0, half, sw, f0);
+    // Steady state (stage kt+4 exists): straight-line code with constant
+    // waits, so the compiler's wait-count tracking sees that the fragments
+    // multiplied were already waited for at the barrier and does not make
+    // the multiplies wait for the reads of the next stage.
+    auto steady = [&](int kt, Frags& cur, Frags& nxt) {
+      wait_vmcnt<(STAGES - 2) * LOADS>();    // stage kt+1 landed, kt+2..kt+3 in flight
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
+      raw_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(prs, qrs, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES, w);
+      read_frags(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
+      mma(cur, acc);
+      interleave();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // Last stages: fewer loads in flight, no more issues.
     auto step = [&](int kt, Frags& cur, Frags& nxt) {
       if (kt + 1 < nk) {
         // issued so far: stages up to min(nk-1, kt+3); stage kt+4 comes below
         wait_stage(min(nk - 1, kt + STAGES - 1) - (kt + 1));
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
+        __builtin_amdgcn_s_waitcnt(0xC07F);
         raw_barrier();
         if (kt + STAGES < nk)
-          issue(pbase, qbase, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES);
+          issue(prs, qrs, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES, w);
         read_frags(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
       }
       mma(cur, acc);
     };
     int kt = 0;
+    for (; kt + 1 + STAGES < nk; kt += 2) {
+      steady(kt, f0, f1);
+      steady(kt + 1, f1, f0);
+    }
     for (; kt + 1 < nk; kt += 2) {
       step(kt, f0, f1);
       step(kt + 1, f1, f0);
@@ -224,19 +280,15 @@ struct Gemm256 {
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = wave();
     const int wm = w / WN, wn = w % WN;
+    const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
     uint32_t goff[LOADS];
-#pragma unroll
-    for (int j = 0; j < LOADS; ++j) {
-      const int r = load_row(j);
-      const uint32_t lc = static_cast<uint32_t>((lane & 3) ^ swz(r));
-      goff[j] = (j < LOADS / 2 ? poff[j] : qoff[j - LOADS / 2]) + lc * 8;
-    }
+    dma_offsets(poff, qoff, goff);
     const int nk = K / BK;
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st)
-      if (st < nk) issue(pbase, qbase, goff, st * BK, lds + st * STAGE_BYTES);
+      if (st < nk) issue(prs, qrs, goff, st * BK, lds + st * STAGE_BYTES, w);
     const int sw = swz(lane & 31);
     const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
     const int qrow0 = (BM + wn * WTN + (lane & 31)) * ROW_BYTES;
@@ -246,7 +298,7 @@ struct Gemm256 {
       wait_stage(min(nk - 1, kt + STAGES - 2) - kt);
       raw_barrier();
       if (kt + STAGES - 1 < nk)
-        issue(pbase, qbase, goff, (kt + STAGES - 1) * BK, lds + ((kt + STAGES - 1) % STAGES) * STAGE_BYTES);
+        issue(prs, qrs, goff, (kt + STAGES - 1) * BK, lds + ((kt + STAGES - 1) % STAGES) * STAGE_BYTES, w);
       Frags f;
       read_frags(lds + (kt % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, f);
       mma(f, acc);
