@@ -184,7 +184,7 @@ int luffy_combine(const void* y_rep, const int32_t* rep_row,
  * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
- * Kernel names: gate, slot_scan, slot_scatter, norm, gram_prep, gram,
+ * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
  * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
  * ffn1, ffn2, ffn2_reduce, combine.
  * ---------------------------------------------------------------------- */

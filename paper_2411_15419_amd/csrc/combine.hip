@@ -44,15 +44,15 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
       for (int u = 0; u < 4; ++u) {
         const int c = c0 + u * 512;
         if (c >= d) break;
-        Pack16 o;
+        float a[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          float a = 0.f;
+          a[i] = 0.f;
 #pragma unroll
-          for (int j = 0; j < 2; ++j) a = fmaf(g[j], bf16_to_f32(v[j][u].h[i]), a);
-          o.h[i] = f32_to_bf16(a);
+          for (int j = 0; j < 2; ++j) a[i] = fmaf(g[j], bf16_to_f32(v[j][u].h[i]), a[i]);
         }
-        *reinterpret_cast<uint4*>(dst + c) = o.u4;
+        *reinterpret_cast<uint4*>(dst + c) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
+                                                        pack_bf16x2(a[4], a[5]), pack_bf16x2(a[6], a[7]));
       }
     }
   } else {

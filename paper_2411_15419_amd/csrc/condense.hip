@@ -3,17 +3,18 @@
 //
 // Kernels, in launch order:
 //   norm_kernel          1/|x_t| per token (one wave per row); clears the
-//                        degree counters and walk states.
-//   gram_prep_kernel     per-bucket tile counts and bitmask offsets.
+//                        degree counters and walk states; its first wave
+//                        lays out every bucket's tiles and bitmask.
 //   gram_kernel_{bf16,f32}  persistent loop over the upper-triangle tiles
 //                        (256 rows bf16, 128 rows fp32) of every bucket's Gram
 //                        matrix.  The epilogue turns cos >= h into adjacency
 //                        bits, writes both the tile and its transpose (every
 //                        bitmask word is written exactly once) and adds each
 //                        row's edge count to its degree.
-//   greedy_round_kernel  one round of the parallel form of the greedy walk
-//                        (launched a fixed number of times; decided
-//                        positions return at once).
+//   greedy_round_kernel  one round of the parallel form of the greedy walk,
+//                        16 lanes per position (launched twice, which
+//                        decides every position of a union of cliques;
+//                        decided positions return at once).
 //   greedy_finish_kernel one workgroup per bucket repeats rounds until the
 //                        bucket is fully decided (after a coalesced check
 //                        that anything is left).
@@ -38,7 +39,7 @@
 namespace luffy {
 namespace {
 
-constexpr int kGreedyGridRounds = 3;
+constexpr int kGreedyGridRounds = 2;
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig)
 constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
@@ -65,11 +66,51 @@ __device__ __forceinline__ int bucket_of(const int32_t* __restrict__ offsets, in
   return lo;
 }
 
+// Tile and bitmask layout of every bucket, by one wave (lane e: expert e,
+// E <= 64).  Flags an error (and schedules no tile) when a bucket exceeds
+// max_bucket or the bitmask exceeds the workspace.
+__device__ __forceinline__ void gram_layout(const int32_t* __restrict__ offsets, int E, int max_bucket,
+                                            int tile, long long cap_words, int32_t* __restrict__ tile_off,
+                                            long long* __restrict__ bm_off, int* __restrict__ err) {
+  const int lane = threadIdx.x & 63;
+  const int n = lane < E ? offsets[lane + 1] - offsets[lane] : 0;
+  const int nt = (n + tile - 1) / tile;
+  const int tiles = nt * (nt + 1) / 2;
+  const long long words = static_cast<long long>(n) * ((n + 63) / 64);
+  int tincl = tiles;
+  long long wincl = words;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int tu = __shfl_up(tincl, o, 64);
+    const long long wu = __shfl_up(wincl, o, 64);
+    if (lane >= o) {
+      tincl += tu;
+      wincl += wu;
+    }
+  }
+  const long long wtotal = __shfl(wincl, 63, 64);
+  const bool bad = __ballot(lane < E && (n < 0 || n > max_bucket)) != 0 || wtotal > cap_words;
+  if (lane < E) {
+    tile_off[lane] = bad ? 0 : tincl - tiles;
+    bm_off[lane] = wincl - words;
+  }
+  if (lane == 63) {
+    tile_off[E] = bad ? 0 : tincl;
+    bm_off[E] = wincl;
+    *err = bad ? 1 : 0;
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, int T, int d,
                                                    float* __restrict__ inv_norm, int S,
                                                    int32_t* __restrict__ deg, int32_t* __restrict__ state,
-                                                   unsigned long long* __restrict__ claim) {
+                                                   unsigned long long* __restrict__ claim,
+                                                   const int32_t* __restrict__ offsets, int E, int max_bucket,
+                                                   int tile, long long cap_words, int32_t* __restrict__ tile_off,
+                                                   long long* __restrict__ bm_off, int* __restrict__ err) {
+  if (blockIdx.x == 0 && threadIdx.x < 64)
+    gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
   // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
@@ -103,32 +144,6 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
   }
   s = wave_sum_f32(s);
   if (lane == 0) inv_norm[t] = s > 0.f ? 1.0f / sqrtf(s) : 0.f;
-}
-
-// Tile and bitmask layout of every bucket.  Flags an error (and schedules no
-// tile) when a bucket exceeds max_bucket or the bitmask exceeds the
-// workspace.
-__global__ void gram_prep_kernel(const int32_t* __restrict__ offsets, int E, int max_bucket,
-                                 int tile, long long cap_words, int32_t* __restrict__ tile_off,
-                                 long long* __restrict__ bm_off, int* __restrict__ err) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  long long words = 0;
-  int tiles = 0, bad = 0;
-  for (int e = 0; e < E; ++e) {
-    const int n = offsets[e + 1] - offsets[e];
-    if (n < 0 || n > max_bucket) bad = 1;
-    const int nt = (n + tile - 1) / tile;
-    tile_off[e] = tiles;
-    bm_off[e] = words;
-    tiles += nt * (nt + 1) / 2;
-    words += static_cast<long long>(n) * ((n + 63) / 64);
-  }
-  tile_off[E] = tiles;
-  bm_off[E] = words;
-  if (words > cap_words) bad = 1;
-  if (bad)
-    for (int e = 0; e <= E; ++e) tile_off[e] = 0;
-  *err = bad;
 }
 
 struct TileCoord {
@@ -417,29 +432,33 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
 }
 
 // Decides position p if its neighbours allow it; returns true when p is
-// still undecided afterwards (wave-uniform).  Each lane walks its words of
-// the adjacency row (four word loads in flight) and gathers the state and
+// still undecided afterwards (uniform over the GW-lane group that visits p,
+// GW = 16 or 64, aligned inside the wave).  Each lane walks its words of the
+// adjacency row (four word loads in flight) and gathers the state and
 // degree of up to 8 neighbours at a time before testing them.  The grid
 // rounds use plain loads (FRESH = false): a state written by another XCD in
 // the same launch may be seen late, which only delays a decision (states
 // change once, from undecided to final).  The single-workgroup finishing
 // pass, which relies on seeing the previous iteration's decisions, reads
 // the states with coherent atomic loads (FRESH = true).
-template <bool FRESH>
+template <bool FRESH, int GW>
 __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
                                              const uint64_t* __restrict__ row,
                                              const int32_t* __restrict__ deg, int32_t* state) {
   const int lane = threadIdx.x & 63;
+  const int gl = lane & (GW - 1);
+  const int gshift = lane & ~(GW - 1);
+  const uint64_t gmask = GW == 64 ? ~0ull : ((1ull << (GW & 63)) - 1);
   const int dp = deg[p];
   bool kept_nb = false, blocked = false;
-  for (int wd0 = lane; wd0 < W && !kept_nb; wd0 += 256) {
+  for (int wd0 = gl; wd0 < W && !kept_nb; wd0 += 4 * GW) {
     uint64_t wv[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = wd0 + 64 * u < W ? row[wd0 + 64 * u] : 0ull;
+    for (int u = 0; u < 4; ++u) wv[u] = wd0 + GW * u < W ? row[wd0 + GW * u] : 0ull;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       uint64_t bits = wv[u];
-      const int cbase = (wd0 + 64 * u) * 64;
+      const int cbase = (wd0 + GW * u) * 64;
       while (bits) {
         int q[8];
 #pragma unroll
@@ -465,34 +484,46 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
       }
     }
   }
-  const bool any_kept = __ballot(kept_nb) != 0;
-  const bool any_blocked = __ballot(blocked) != 0;
+  const bool any_kept = ((__ballot(kept_nb) >> gshift) & gmask) != 0;
+  const bool any_blocked = ((__ballot(blocked) >> gshift) & gmask) != 0;
   if (any_kept) {
-    if (lane == 0) store_flag(&state[p], kStateAbsorbed);
+    if (gl == 0) store_flag(&state[p], kStateAbsorbed);
     return false;
   }
   if (!any_blocked) {
-    if (lane == 0) store_flag(&state[p], kStateKept);
+    if (gl == 0) store_flag(&state[p], kStateKept);
     return false;
   }
   return true;
 }
 
-// One round over all positions (one wave each); decided positions return at
-// once.  Round 0 also publishes the degrees.
+constexpr int kVisitLanes = 16;                       // lanes per position in the grid passes
+constexpr int kVisitPerBlock = 256 / kVisitLanes;     // positions per 256-thread block
+
+// Bucket offsets of the current call in LDS (E <= 64).
+__device__ __forceinline__ void load_offsets(const int32_t* __restrict__ offsets, int E, int* soff) {
+  if (threadIdx.x <= static_cast<unsigned>(E)) soff[threadIdx.x] = offsets[threadIdx.x];
+  __syncthreads();
+}
+
+// One round over all positions (16 lanes each); decided positions return
+// at once.  Round 0 also publishes the degrees.
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
     const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out) {
+  __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
-  const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= offsets[E]) return;
-  if (r == 0 && degree_out && lane == 0) degree_out[p] = deg[p];
+  load_offsets(offsets, E, soff);
+  const int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
+  const int gl = threadIdx.x & (kVisitLanes - 1);
+  if (p >= soff[E]) return;
+  if (r == 0 && degree_out && gl == 0) degree_out[p] = deg[p];
   if (state[p] != kStateUndecided) return;
-  const int e = bucket_of(offsets, E, p);
-  const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
-  greedy_visit<false>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg, state);
+  const int e = bucket_of(soff, E, p);
+  const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
+  greedy_visit<false, kVisitLanes>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg,
+                                   state);
 }
 
 // One workgroup per bucket: rounds until every position is decided.  Each
@@ -516,7 +547,7 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     for (int pl = wv; pl < n; pl += 16) {
       const int p = lo + pl;
       if (load_flag(&state[p]) != kStateUndecided) continue;
-      if (greedy_visit<true>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(pl) * W, deg, state))
+      if (greedy_visit<true, 64>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(pl) * W, deg, state))
         undecided = 1;
     }
     if (!__syncthreads_or(undecided)) break;
@@ -525,29 +556,32 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
 
 // Each kept position offers itself to every neighbour: claim[b] keeps the
 // largest key (degree << 32 | ~position), i.e. the neighbour's first kept
-// neighbour in walk order.  Only kept positions scan their rows.
+// neighbour in walk order.  Only kept positions scan their rows (16 lanes
+// each).
 __global__ __launch_bounds__(256) void claim_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
     const int32_t* __restrict__ deg, const int32_t* __restrict__ state,
     unsigned long long* __restrict__ claim) {
+  __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
-  const int lane = threadIdx.x & 63;
-  const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (q >= offsets[E] || state[q] != kStateKept) return;
-  const int e = bucket_of(offsets, E, q);
-  const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
+  load_offsets(offsets, E, soff);
+  const int q = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
+  const int gl = threadIdx.x & (kVisitLanes - 1);
+  if (q >= soff[E] || state[q] != kStateKept) return;
+  const int e = bucket_of(soff, E, q);
+  const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
   const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
   const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
                                  static_cast<unsigned int>(~static_cast<unsigned int>(q));
-  for (int wd0 = lane; wd0 < W; wd0 += 256) {
+  for (int wd0 = gl; wd0 < W; wd0 += 4 * kVisitLanes) {
     uint64_t wv[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = wd0 + 64 * u < W ? row[wd0 + 64 * u] : 0ull;
+    for (int u = 0; u < 4; ++u) wv[u] = wd0 + kVisitLanes * u < W ? row[wd0 + kVisitLanes * u] : 0ull;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       uint64_t bits = wv[u];
-      const int cbase = (wd0 + 64 * u) * 64;
+      const int cbase = (wd0 + kVisitLanes * u) * 64;
       while (bits) {
         const int b = __ffsll(static_cast<long long>(bits)) - 1;
         bits &= bits - 1;
@@ -735,13 +769,15 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const int norm_blocks = (T + 3) / 4;
   {
     ProfileScope prof_("norm", s);
-    if (bf16) norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim);
-    else norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim);
-  }
-  {
-    ProfileScope prof_("gram_prep", s);
-    gram_prep_kernel<<<1, 64, 0, s>>>(offsets, E, max_bucket, bf16 ? kTile : kTileF32, ws.cap_words,
-                                      ws.tile_off, ws.bm_off, ws.err);
+    const int tile = bf16 ? kTile : kTileF32;
+    if (bf16)
+      norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets,
+                                                    E, max_bucket, tile, ws.cap_words, ws.tile_off, ws.bm_off,
+                                                    ws.err);
+    else
+      norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets,
+                                                     E, max_bucket, tile, ws.cap_words, ws.tile_off, ws.bm_off,
+                                                     ws.err);
   }
   {
     ProfileScope prof_("gram", s);
@@ -755,9 +791,10 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
           ws.bm_off, ws.err, ws.bitmask, ws.deg);
   }
   const int wave_blocks = (S + 3) / 4;
+  const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
   for (int r = 0; r < kGreedyGridRounds; ++r) {
     ProfileScope prof_("greedy_round", s);
-    greedy_round_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+    greedy_round_kernel<<<visit_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
                                                     ws.state, r, degree);
   }
   {
@@ -766,7 +803,7 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   }
   {
     ProfileScope prof_("claim", s);
-    claim_kernel<<<wave_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
+    claim_kernel<<<visit_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
                                              ws.claim);
   }
   const int pos_blocks = (S + 1023) / 1024;

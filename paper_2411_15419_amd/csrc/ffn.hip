@@ -5,9 +5,11 @@
 // upper bound ceil(max_rows/BN) + E row tiles; each block finds its expert
 // and row range from rep_offsets and exits when it has none.
 //
-// bf16: 256 x 256 MFMA tiles (GemmBig).  The weight rows are the P operand
-// and the token rows the Q operand, so each lane ends with groups of four
-// consecutive output columns of one row and stores each as one 8-byte word.
+// bf16: 256 x 256 MFMA tiles (GemmRagged).  The weight rows are the P
+// operand and the token rows the Q operand, so each lane ends with groups of
+// four consecutive output columns of one row and stores each as one 8-byte
+// word.  The last row tile of an expert usually holds fewer than 256 rows;
+// its waves skip the MFMAs of the missing rows.
 // fp32: 64 x 64 tiles of plain FMA (4 x 4 per thread).
 #include "gemm_core.h"
 #include "luffy_common.h"
@@ -15,12 +17,43 @@
 namespace luffy {
 namespace {
 
+// Activations of the float32 path: exact erf-GELU and SiLU from the device
+// math library.
 template <int ACT>
 __device__ __forceinline__ float act_fn(float z) {
   if constexpr (ACT == LUFFY_ACT_GELU) {
     return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
   } else {
     return z / (1.0f + expf(-z));
+  }
+}
+
+// Activations of the bf16 path, whose results are rounded to bf16 (relative
+// step 2^-8): a dozen VALU operations instead of the library erf, which
+// dominated the epilogue of the first product.
+//   GELU: erf from Abramowitz & Stegun 7.1.26 (Hastings' rational
+//   approximation), erf(u) = 1 - q(u), q(u) = t (a1 + t (a2 + ... + t a5))
+//   e^{-u^2}, t = 1 / (1 + p u), u >= 0, |error| <= 1.5e-7.  With
+//   u = |z| / sqrt(2): GELU(z) = z (1 - q/2) for z >= 0 and z q/2 for z < 0.
+//   SiLU: z / (1 + 2^{-z log2 e}).
+// The hardware exp2 and reciprocal are accurate to about 1 ulp.
+template <int ACT>
+__device__ __forceinline__ float act_fast(float z) {
+  if constexpr (ACT == LUFFY_ACT_GELU) {
+    constexpr float kP = 0.3275911f;
+    constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
+    constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
+    constexpr float kInvSqrt2 = 0.70710678118654752f;
+    constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
+    const float u = fabsf(z) * kInvSqrt2;
+    const float t = __builtin_amdgcn_rcpf(fmaf(kP, u, 1.0f));
+    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, kA5, kA4), kA3), kA2), kA1);
+    const float e = __builtin_amdgcn_exp2f(z * z * kHalfLog2e);   // e^{-u^2}
+    const float hq = 0.5f * poly * e;
+    return z * (z >= 0.f ? 1.0f - hq : hq);
+  } else {
+    constexpr float kNegLog2e = -1.44269504088896341f;
+    return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * kNegLog2e));
   }
 }
 
@@ -53,51 +86,109 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
   return true;
 }
 
-// Persistent grouped GEMM.  Tiles are numbered expert by expert; inside an
-// expert, output-column tiles come in groups of 4 with the row tile major
-// inside a group, so the ~32 tiles one XCD runs together share few weight
-// and token rows in its L2.
-// Tile map of the grouped GEMM: rep_offsets held one expert per lane.
+// Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
+// expert per lane, E <= 64).  An output tile is 256 output columns (weight
+// rows, the P operand) by up to 256 token rows (the Q operand).  Every expert
+// has floor(R_e/256) full row tiles and, when 256 does not divide R_e, one
+// partial row tile with R_e mod 256 rows.  Full tiles come first, expert by
+// expert; inside an expert the output-column tiles come in groups of 4 with
+// the row tile major inside a group, so ~32 consecutive tiles span ~8 row x
+// 4 column tiles.  Partial tiles follow, experts by descending partial size
+// (ties: lower expert first), so that the persistent blocks, which take
+// tiles round-robin, get the long tiles first.
 template <class G>
 struct FfnTiles {
-  int elo, ehi, mt, incl, NT, tiles;
+  int elo, nfull, tail, incl, rank, NT, full_tiles, tiles;
   __device__ __forceinline__ FfnTiles(const int32_t* __restrict__ rep_offsets, int E, int N) {
     const int lane = threadIdx.x & 63;
     NT = (N + G::BM - 1) / G::BM;
-    elo = ehi = mt = 0;
+    elo = nfull = tail = 0;
     if (lane < E) {
       elo = rep_offsets[lane];
-      ehi = rep_offsets[lane + 1];
-      mt = (ehi - elo + G::BN - 1) / G::BN;
+      const int r = rep_offsets[lane + 1] - elo;
+      nfull = r / G::BN;
+      tail = r - nfull * G::BN;
     }
-    incl = mt * NT;
+    incl = nfull * NT;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const int v = __shfl_up(incl, o, 64);
       if (lane >= o) incl += v;
     }
-    tiles = __shfl(incl, 63, 64);
+    full_tiles = __shfl(incl, 63, 64);
+    rank = 0;
+    for (int o = 0; o < E; ++o) {
+      const int to = __shfl(tail, o, 64);
+      rank += (to > tail || (to == tail && o < lane)) ? 1 : 0;
+    }
+    const int ntail = __popcll(__ballot(lane < E && tail > 0));
+    tiles = full_tiles + ntail * NT;
   }
   // Tile t -> expert e, first token row row0, row count, first output n0.
-  // Inside an expert, output-column tiles come in groups of 4 with the row
-  // tile major inside a group, so ~32 consecutive tiles span ~8 row x 4
-  // column tiles.
   __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0) const {
     const int lane = threadIdx.x & 63;
-    e = __popcll(__ballot(lane < E && incl <= t));
-    const int me = __shfl(mt, e, 64);
-    const int excl = __shfl(incl, e, 64) - me * NT;
-    const int r = t - excl;
-    const int ng = (NT + 3) / 4;
-    const int g = min(r / (4 * me), ng - 1);
-    const int r2 = r - 4 * g * me;
-    const int wg = min(4, NT - 4 * g);
-    const int ms = r2 / wg, nt = 4 * g + r2 % wg;
-    row0 = __shfl(elo, e, 64) + ms * G::BN;
-    rows = min(G::BN, __shfl(ehi, e, 64) - row0);
-    n0 = nt * G::BM;
+    if (t < full_tiles) {
+      e = __popcll(__ballot(lane < E && incl <= t));
+      const int me = __shfl(nfull, e, 64);
+      const int excl = __shfl(incl, e, 64) - me * NT;
+      const int r = t - excl;
+      const int ng = (NT + 3) / 4;
+      const int g = min(r / (4 * me), ng - 1);
+      const int r2 = r - 4 * g * me;
+      const int wg = min(4, NT - 4 * g);
+      const int ms = r2 / wg, nt = 4 * g + r2 % wg;
+      row0 = __shfl(elo, e, 64) + ms * G::BN;
+      rows = G::BN;
+      n0 = nt * G::BM;
+    } else {
+      const int q = t - full_tiles;
+      const int i = q / NT;
+      e = __ffsll(static_cast<long long>(__ballot(lane < E && tail > 0 && rank == i))) - 1;
+      row0 = __shfl(elo, e, 64) + __shfl(nfull, e, 64) * G::BN;
+      rows = __shfl(tail, e, 64);
+      n0 = (q - i * NT) * G::BM;
+    }
+  }
+  // Split-K parts per tile (second product only): the largest split of at
+  // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
+  // the partial-tile slots and, counting a partial tile as a quarter, still
+  // leaves about one work item per block.
+  __device__ __forceinline__ int parts(int grid, int nk) const {
+    using SK = SplitK<G>;
+    if (tiles <= 0) return 1;
+    const int work = full_tiles + (tiles - full_tiles + 3) / 4;
+    int s = 1;
+    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= SK::MAX_SLOTS && work * s < grid) s *= 2;
+    return s;
   }
 };
+
+// Multiplies with only the first nq of the wave's Q blocks (wave-uniform
+// nq in 0..FN), so the MFMAs of token rows past a partial tile are skipped.
+// With eight Q blocks per wave, nq is taken in steps of two.
+template <class G>
+__device__ __forceinline__ void run_ragged(int nq, const uint16_t* pbase, const uint32_t (&poff)[G::LOADS / 2],
+                                           const uint16_t* qbase, const uint32_t (&qoff)[G::LOADS / 2], int K,
+                                           uint8_t* lds, typename G::Acc& acc) {
+  if constexpr (G::FN == 4) {
+    switch (nq) {
+      case 4: G::template run<4>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 3: G::template run<3>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 2: G::template run<2>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 1: G::template run<1>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      default: G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc); break;
+    }
+  } else {
+    static_assert(G::FN == 8, "ragged dispatch for four or eight Q blocks per wave");
+    switch ((nq + 1) >> 1) {
+      case 4: G::template run<8>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 3: G::template run<6>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 2: G::template run<4>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      case 1: G::template run<2>(pbase, poff, qbase, qoff, K, lds, acc); break;
+      default: G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc); break;
+    }
+  }
+}
 
 // One product of the FFN for every tile of every expert (persistent).
 // The second product (FIRST = false) has few output columns (d); with few
@@ -113,10 +204,10 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
   // P = weight rows (outputs n), Q = token rows (m)
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w / G::WN, wn = w % G::WN;
+  const int wm = G::wave_m(w), wn = G::wave_n(w);
   const FfnTiles<G> map(rep_offsets, E, N);
   const int nk = K / G::BK;
-  const int S = FIRST ? 1 : SK::parts(map.tiles, gridDim.x, nk);
+  const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
   const int total = map.tiles * S;
   for (int tt = xcd_virtual_block(); tt < total; tt += gridDim.x) {
     const int t = tt / S, part = tt - t * S;
@@ -132,9 +223,10 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
     }
     // K range of this part, in whole 32-wide stages
     const int k0 = (part * nk / S) * G::BK, k1 = ((part + 1) * nk / S) * G::BK;
+    const int nq = min(max((rows - wn * G::WTN + 31) / 32, 0), G::FN);
     typename G::Acc acc;
     G::zero(acc);
-    G::run(We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
+    run_ragged<G>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * SK::SLOT_FLOATS : nullptr;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
@@ -149,22 +241,21 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
           const int n = n0 + nl;
           if (n >= N) continue;
           if (slot) {
-            *reinterpret_cast<float4*>(slot + ml * G::BM + nl) =
+            // partial tiles keep the accumulator layout: 1 KB per store
+            // instruction; the reduction maps it back to rows and columns
+            const int u = ((w * G::FM + fm) * G::FN + fn) * 4 + g;
+            *reinterpret_cast<float4*>(slot + u * 256 + lane * 4) =
                 make_float4(acc[fm][fn][4 * g], acc[fm][fn][4 * g + 1], acc[fm][fn][4 * g + 2],
                             acc[fm][fn][4 * g + 3]);
             continue;
           }
-          uint16_t v[4];
+          float z[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            float z = acc[fm][fn][4 * g + q];
-            if constexpr (FIRST) z = act_fn<ACT>(z);
-            v[q] = f32_to_bf16(z);
+            z[q] = acc[fm][fn][4 * g + q];
+            if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
           }
-          uint2 pk;
-          pk.x = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 16);
-          pk.y = static_cast<uint32_t>(v[2]) | (static_cast<uint32_t>(v[3]) << 16);
-          *reinterpret_cast<uint2*>(orow + n) = pk;
+          *reinterpret_cast<uint2*>(orow + n) = make_uint2(pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3]));
         }
       }
     }
@@ -173,25 +264,32 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
 
 // Sums the split parts of every output tile in part order and stores bf16.
 // Recomputes the same tile map and split count, so it does nothing when the
-// product was not split.
+// product was not split.  Partial tiles are in the accumulator layout of the
+// product kernel: float4 unit u = ((w*FM + fm)*FN + fn)*4 + g of lane l holds
+// acc[fm][fn][4g..4g+3] of wave w, i.e. four consecutive output columns of
+// one token row.
 template <class G>
 __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __restrict__ rep_offsets, int E,
                                                                int K, int N, const float* __restrict__ split_slots,
                                                                uint16_t* __restrict__ out, int grid_parts) {
   using SK = SplitK<G>;
+  constexpr int UNITS = G::NWAVES * G::FM * G::FN * 4 * 64;   // float4 per tile
   const FfnTiles<G> map(rep_offsets, E, N);
-  const int S = SK::parts(map.tiles, grid_parts, K / G::BK);
+  const int S = map.parts(grid_parts, K / G::BK);
   if (S == 1) return;
-  // work unit = (tile, 4 rows): 64 threads x 4 columns per row
-  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int units = map.tiles * (G::BN / 4);
-  for (int u = blockIdx.x; u < units; u += gridDim.x) {
-    const int t = u / (G::BN / 4), ml = (u - t * (G::BN / 4)) * 4 + q;
+  const long long total = static_cast<long long>(map.tiles) * UNITS;
+  for (long long i = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x; i < total;
+       i += static_cast<long long>(gridDim.x) * 256) {
+    const int t = static_cast<int>(i / UNITS);          // wave-uniform: UNITS is a multiple of 64
+    const int u = static_cast<int>(i - static_cast<long long>(t) * UNITS);
     int e, row0, rows, n0;
     map.decode(t, E, e, row0, rows, n0);
-    const int c4 = lane * 4;
-    if (ml >= rows || n0 + c4 >= N) continue;
-    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS + ml * G::BM + c4;
+    const int l = u & 63, g = (u >> 6) & 3, q = u >> 8;
+    const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
+    const int ml = G::wave_n(w) * G::WTN + 32 * fn + (l & 31);
+    const int nl = G::wave_m(w) * G::WTM + 32 * fm + 8 * g + 4 * (l >> 5);
+    if (ml >= rows || n0 + nl >= N) continue;
+    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS + static_cast<size_t>(u) * 4;
     float4 v[4];
 #pragma unroll
     for (int p = 0; p < 4; ++p)
@@ -200,10 +298,8 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
 #pragma unroll
     for (int p = 1; p < 4; ++p)
       if (p < S) { sum.x += v[p].x; sum.y += v[p].y; sum.z += v[p].z; sum.w += v[p].w; }
-    uint2 pk;
-    pk.x = static_cast<uint32_t>(f32_to_bf16(sum.x)) | (static_cast<uint32_t>(f32_to_bf16(sum.y)) << 16);
-    pk.y = static_cast<uint32_t>(f32_to_bf16(sum.z)) | (static_cast<uint32_t>(f32_to_bf16(sum.w)) << 16);
-    *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n0 + c4) = pk;
+    *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n0 + nl) =
+        make_uint2(pack_bf16x2(sum.x, sum.y), pack_bf16x2(sum.z, sum.w));
   }
 }
 
@@ -262,6 +358,8 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   }
 }
 
+using FfnGemm = GemmRagged;
+
 struct FfnWs {
   void* hidden;
   float* split_slots;
@@ -272,16 +370,12 @@ FfnWs carve_ffn(Carver& c, int max_rows, int d_ff, int dtype) {
   w.hidden = c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
   w.split_slots = nullptr;
   if (dtype == LUFFY_BF16) {
-    using SK = SplitK<GemmBig>;
+    using SK = SplitK<FfnGemm>;
     w.split_slots = c.take<float>(SK::SLOT_FLOATS * SK::MAX_SLOTS);
   }
   return w;
 }
 
-#ifndef LUFFY_FFN_GEMM
-#define LUFFY_FFN_GEMM GemmBig
-#endif
-using FfnGemm = LUFFY_FFN_GEMM;
 
 template <int ACT>
 void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d,

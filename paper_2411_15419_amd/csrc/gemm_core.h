@@ -6,7 +6,12 @@
 // gathered token rows).
 //
 // Block tile 256 x 256; waves form a WM x WN grid, each owning a
-// (256/WM) x (256/WN) sub-tile of v_mfma_f32_32x32x16_bf16 blocks.
+// (256/WM) x (256/WN) sub-tile of v_mfma_f32_32x32x16_bf16 blocks.  Waves
+// are dealt to the four SIMDs of a CU round-robin (wave w on SIMD w % 4).
+// With MFAST the wave's P-block index varies fastest (wm = w % WM), so with
+// WM = 4 every SIMD holds one P quarter and every Q part: a tile whose Q
+// rows are only partly valid can skip the MFMAs of its invalid 32-row Q
+// blocks (run<NQ>) and still keep the four SIMDs equally loaded.
 //
 // K advances 32 at a time through a ring of 4 LDS stages (32 KB each).
 // Operands go from global memory straight into LDS with buffer loads
@@ -25,8 +30,8 @@
 // (every operand here has fewer than 2^31 elements).
 //
 // Result layout of acc[fm][fn][v] in lane l of wave w:
-//   P row  (w / WN) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
-//   Q row  (w % WN) * WTN + 32*fn + l%32
+//   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
+//   Q row  wave_n(w) * WTN + 32*fn + l%32
 #pragma once
 
 #include "luffy_common.h"
@@ -57,7 +62,7 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
-template <int WM_, int WN_>
+template <int WM_, int WN_, bool MFAST_ = false>
 struct Gemm256 {
   static constexpr int BM = 256, BN = 256, WM = WM_, WN = WN_;
   static constexpr int BK = 32;                      // K per stage
@@ -76,6 +81,10 @@ struct Gemm256 {
   using Acc = f32x16[FM][FN];
 
   static __device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
+
+  // wave -> (P block, Q block) of the wave grid
+  static __device__ __forceinline__ int wave_m(int w) { return MFAST_ ? w % WM : w / WN; }
+  static __device__ __forceinline__ int wave_n(int w) { return MFAST_ ? w / WM : w % WN; }
 
   // Stage row this lane fills in load j: P rows 0..255 then Q rows 256..511
   // (loads 0 .. LOADS/2-1 fill P rows, the rest Q rows).
@@ -123,30 +132,35 @@ struct Gemm256 {
     bf16x8 a[2][FM], b[2][FN];
   };
 
-  // LDS -> registers: both 16-wide substeps of one stage.
+  // LDS -> registers: both 16-wide substeps of one stage, for the first NQ
+  // of the wave's FN Q blocks (none at all when NQ = 0).
+  template <int NQ = FN>
   static __device__ __forceinline__ void read_frags(lds_ptr S, int prow0, int qrow0, int half, int sw,
                                                     Frags& f) {
+    if constexpr (NQ > 0) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int pc = ((2 * kk + half) ^ sw) * 16;
+      for (int kk = 0; kk < 2; ++kk) {
+        const int pc = ((2 * kk + half) ^ sw) * 16;
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        f.a[kk][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
-            S + prow0 + 32 * i * ROW_BYTES + pc);
+        for (int i = 0; i < FM; ++i)
+          f.a[kk][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
+              S + prow0 + 32 * i * ROW_BYTES + pc);
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        f.b[kk][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
-            S + qrow0 + 32 * j * ROW_BYTES + pc);
+        for (int j = 0; j < NQ; ++j)
+          f.b[kk][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
+              S + qrow0 + 32 * j * ROW_BYTES + pc);
+      }
     }
   }
 
+  template <int NQ = FN>
   static __device__ __forceinline__ void mma(const Frags& f, Acc& acc) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(f.a[kk][i], f.b[kk][j], acc[i][j]);
+        for (int j = 0; j < NQ; ++j) acc[i][j] = mfma32x32x16(f.a[kk][i], f.b[kk][j], acc[i][j]);
   }
 
   // DMA: lane fills physical chunk lane%4 of its row with logical chunk
@@ -164,21 +178,26 @@ struct Gemm256 {
   }
 
   // Scheduling of one steady-state stage: each MFMA is followed by one of
-  // the stage's buffer loads, then by one LDS read, until they run out.
+  // the stage's buffer loads, then by one LDS read, until they run out;
+  // loads and reads left over (few Q blocks) follow the last MFMA.
+  template <int NQ = FN>
   static __device__ __forceinline__ void interleave() {
-    constexpr int NMF = FM * FN * 2, NDS = (FM + FN) * 2, NVM = LOADS;
-    static_assert(NMF >= NVM + NDS, "interleave plan");
+    constexpr int NMF = FM * NQ * 2, NDS = NQ > 0 ? (FM + NQ) * 2 : 0, NVM = LOADS;
+    constexpr int PV = NMF < NVM ? NMF : NVM;
+    constexpr int PD = (NMF - PV) < NDS ? (NMF - PV) : NDS;
 #pragma unroll
-    for (int i = 0; i < NVM; ++i) {
+    for (int i = 0; i < PV; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
     }
 #pragma unroll
-    for (int i = 0; i < NDS; ++i) {
+    for (int i = 0; i < PD; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
     }
-    if constexpr (NMF > NVM + NDS) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NVM - NDS, 0);
+    if constexpr (NMF > PV + PD) __builtin_amdgcn_sched_group_barrier(0x008, NMF - PV - PD, 0);
+    if constexpr (NVM > PV) __builtin_amdgcn_sched_group_barrier(0x020, NVM - PV, 0);
+    if constexpr (NDS > PD) __builtin_amdgcn_sched_group_barrier(0x100, NDS - PD, 0);
   }
 
   // Wait until the DMA of a stage has landed in this wave while the loads of
@@ -193,12 +212,15 @@ struct Gemm256 {
   // poff[j] (j < LOADS/2): element offset of P row load_row(j);
   // qoff[j] (j < LOADS/2): element offset of Q row load_row(j + LOADS/2) - 256.
   // K must be a multiple of 32.  Ends with a barrier after which the LDS may
-  // be reused.
+  // be reused.  NQ: the wave multiplies only its first NQ Q blocks (the
+  // accumulators of the others stay as they are); every wave still loads
+  // its share of the operands and takes every barrier, whatever its NQ.
   //
   // Iteration kt: wait for stage kt+1 (DMA) and for this wave's reads of
   // stage kt, barrier, issue the DMA of stage kt+4 into stage kt's buffer,
   // request stage kt+1's fragments, then multiply stage kt from registers,
   // so the LDS reads of one stage overlap the MFMAs of the previous one.
+  template <int NQ = FN>
   static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase,
                                              const uint32_t (&poff)[LOADS / 2],
                                              const uint16_t* __restrict__ qbase,
@@ -208,7 +230,7 @@ struct Gemm256 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = wave();
-    const int wm = w / WN, wn = w % WN;
+    const int wm = wave_m(w), wn = wave_n(w);
     const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
     uint32_t goff[LOADS];
     dma_offsets(poff, qoff, goff);
@@ -227,7 +249,7 @@ struct Gemm256 {
     Frags f0, f1;
     wait_stage(min(nk - 1, STAGES - 1));   // stages 1..3 may still be in flight
     raw_barrier();
-    read_frags(lds, prow0, qrow0, half, sw, f0);
+    read_frags<NQ>(lds, prow0, qrow0, half, sw, f0);
     // Steady state (stage kt+4 exists): straight-line code with constant
     // waits, so the compiler's wait-count tracking sees that the fragments
     // multiplied were already waited for at the barrier and does not make
@@ -238,9 +260,9 @@ struct Gemm256 {
       raw_barrier();
       __builtin_amdgcn_sched_barrier(0);
       issue(prs, qrs, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES, w);
-      read_frags(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
-      mma(cur, acc);
-      interleave();
+      read_frags<NQ>(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
+      mma<NQ>(cur, acc);
+      interleave<NQ>();
       __builtin_amdgcn_sched_barrier(0);
     };
     // Last stages: fewer loads in flight, no more issues.
@@ -252,9 +274,9 @@ struct Gemm256 {
         raw_barrier();
         if (kt + STAGES < nk)
           issue(prs, qrs, goff, (kt + STAGES) * BK, lds + (kt % STAGES) * STAGE_BYTES, w);
-        read_frags(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
+        read_frags<NQ>(lds + ((kt + 1) % STAGES) * STAGE_BYTES, prow0, qrow0, half, sw, nxt);
       }
-      mma(cur, acc);
+      mma<NQ>(cur, acc);
     };
     int kt = 0;
     for (; kt + 1 + STAGES < nk; kt += 2) {
@@ -281,7 +303,7 @@ struct Gemm256 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = wave();
-    const int wm = w / WN, wn = w % WN;
+    const int wm = wave_m(w), wn = wave_n(w);
     const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
     uint32_t goff[LOADS];
     dma_offsets(poff, qoff, goff);
@@ -326,6 +348,9 @@ struct SplitK {
 
 // 512 threads, wave tile 128 x 64.
 using GemmBig = Gemm256<2, 4>;
+// 512 threads, wave tile 64 x 128; SIMD s holds P rows 64s..64s+63 of both
+// Q halves (for Q tiles with a ragged number of valid rows).
+using GemmRagged = Gemm256<4, 2, true>;
 // 256 threads, wave tile 128 x 128 (accumulators fill the AGPRs).
 using GemmWide = Gemm256<2, 2>;
 

@@ -1,9 +1,9 @@
 // luffy_route: gate logits, top-k, gates and the stable dispatch order.
 //
 // Kernels (all on the caller's stream, no host synchronisation):
-//   gate_kernel      64 tokens per block.  bf16: the four waves split the
-//                    contraction over d and each accumulates a 64 x E logit
-//                    tile on MFMA (16x16x32); fp32: plain FMA.  The epilogue
+//   gate_kernel      32 tokens per block; the four waves split the
+//                    contraction over d and accumulate 32 x E logit tiles
+//                    on MFMA (16x16x32); fp32: plain FMA.  The epilogue
 //                    takes top-k, gates and the float64 re-decision of close
 //                    calls, then ranks every slot among the block's slots of
 //                    the same expert (wave ballots) and writes the block's
@@ -21,7 +21,7 @@
 namespace luffy {
 namespace {
 
-constexpr int kGateTok = 64;     // tokens per gate block (= slots per chunk)
+constexpr int kGateTok = 32;     // tokens per gate block (= slots per chunk)
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
   // xor butterfly: every lane ends with the same, bit-identical sum
@@ -30,6 +30,16 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
+// One block of four waves per chunk of 32 tokens.  bf16: wave w takes the
+// w-th quarter of the contraction over d and accumulates the 32 x E logits
+// of the chunk on MFMA (16x16x32: two 16-token blocks per 16-expert block),
+// four K steps' token and weight loads in flight at a time; the four partial
+// tiles are added in LDS in a fixed order.  fp32: plain FMA.  Wave 0 then
+// runs the epilogue for the chunk (lane = token): top-k, gates, the float64
+// re-decision of close calls, and the rank of every slot among the chunk's
+// slots of the same expert (wave ballots) with the chunk's per-expert
+// counts.  A chunk is (choice j, chunk c), and chunks in (j, c) order are
+// slots in slot-id order.
 template <bool BF16>
 __global__ __launch_bounds__(256) void gate_kernel(
     const void* __restrict__ xv, const void* __restrict__ wv,
@@ -41,7 +51,9 @@ __global__ __launch_bounds__(256) void gate_kernel(
   __shared__ int cnt[kMaxExperts];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int t0 = blockIdx.x * kGateTok;
+  const int nchunks = gridDim.x;
+  const int ch = blockIdx.x;
+  const int t0 = ch * kGateTok;
   if (threadIdx.x < E) bias[threadIdx.x] = bias_g ? bias_g[threadIdx.x] : 0.f;
   if (blockIdx.x == 0 && threadIdx.x == 0) *scan_done = 0;   // armed for slot_scan_kernel
 
@@ -49,66 +61,61 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const uint16_t* X = static_cast<const uint16_t*>(xv);
     const uint16_t* W = static_cast<const uint16_t*>(wv);
     const int nE16 = (E + 15) >> 4;
-    f32x4 acc[4][4];
+    f32x4 acc[2][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* arow[4];
+    const uint16_t* arow[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int t = t0 + 16 * i + (lane & 15);
-      t = t < T ? t : T - 1;
-      arow[i] = X + static_cast<size_t>(t) * d + 8 * (lane >> 4);
-    }
+    for (int i = 0; i < 2; ++i)
+      arow[i] = X + static_cast<size_t>(min(t0 + 16 * i + (lane & 15), T - 1)) * d + 8 * (lane >> 4);
     const uint16_t* brow[4];
-    bool bval[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = 16 * j + (lane & 15);
-      bval[j] = e < E;
-      brow[j] = W + static_cast<size_t>(bval[j] ? e : 0) * d + 8 * (lane >> 4);
-    }
-    for (int k0 = w * 64; k0 < d; k0 += 256) {
-      Pack16 a[4][2], b[4][2];
+    for (int j = 0; j < 4; ++j)
+      brow[j] = W + static_cast<size_t>(min(16 * j + (lane & 15), E - 1)) * d + 8 * (lane >> 4);
+    const int nsteps = d / 32;
+    const int q = (nsteps + 3) / 4;
+    const int s_lo = w * q, s_hi = min(nsteps, s_lo + q);
+    constexpr int B = 4;   // K steps per batch
+    for (int s0 = s_lo; s0 < s_hi; s0 += B) {
+      Pack16 a[B][2], b[B][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int u = 0; u < B; ++u) {
+        const int st = s0 + u;
+        const bool in = st < s_hi;
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
-          a[i][h].u4 = *reinterpret_cast<const uint4*>(arow[i] + k0 + 32 * h);
+        for (int i = 0; i < 2; ++i)
+          a[u][i].u4 = in ? *reinterpret_cast<const uint4*>(arow[i] + 32 * st) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
+          b[u][j].u4 = (in && j < nE16) ? *reinterpret_cast<const uint4*>(brow[j] + 32 * st)
+                                        : make_uint4(0, 0, 0, 0);
+      }
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          if (j < nE16 && bval[j])
-            b[j][h].u4 = *reinterpret_cast<const uint4*>(brow[j] + k0 + 32 * h);
-          else
-            b[j][h].u4 = make_uint4(0, 0, 0, 0);
-        }
+      for (int u = 0; u < B; ++u)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+        for (int j = 0; j < 4; ++j)
+          if (j < nE16)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (j < nE16) acc[i][j] = mfma16x16x32(a[i][h].v, b[j][h].v, acc[i][j]);
+            for (int i = 0; i < 2; ++i) acc[i][j] = mfma16x16x32(a[u][i].v, b[u][j].v, acc[i][j]);
     }
     // lane holds logits of tokens 16i + 4(lane/16) + r, expert 16j + lane%16
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (j < nE16)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            part[w][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
+          for (int r = 0; r < 4; ++r) part[w][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
   } else {
-    // float32 inputs: one token per lane, experts strided over the waves
+    // float32 inputs: lane = token (lane % 32), experts strided over the
+    // two lane halves and the four waves
     const float* X = static_cast<const float*>(xv);
     const float* W = static_cast<const float*>(wv);
-    int t = t0 + lane;
-    t = t < T ? t : T - 1;
+    const int t = min(t0 + (lane & 31), T - 1);
     for (int e = w; e < E; e += 4) {
+      if ((lane >> 5) != 0) continue;
       float s = 0.f;
       for (int i = 0; i < d; ++i) s = fmaf(X[static_cast<size_t>(t) * d + i], W[static_cast<size_t>(e) * d + i], s);
       part[0][lane][e] = s;
@@ -119,106 +126,122 @@ __global__ __launch_bounds__(256) void gate_kernel(
   }
   __syncthreads();
   if (w != 0) return;
-
-  // ---- epilogue: lane = token
-  const int t = t0 + lane;
-  const bool valid = t < T;
-  const float NEG = -INFINITY;
-  float v0 = NEG, v1 = NEG, v2 = NEG;
-  int i0 = 0, i1 = 0;
-  for (int e = 0; e < E; ++e) {
-    const float v = part[0][lane][e] + part[1][lane][e] + part[2][lane][e] + part[3][lane][e] + bias[e];
-    part[0][lane][e] = v;
-    if (v > v0) { v2 = v1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
-    else if (v > v1) { v2 = v1; v1 = v; i1 = e; }
-    else if (v > v2) { v2 = v; }
-  }
-  // A choice is re-decided in float64 when a deciding gap is within the
-  // float32 error budget (about 1e-4 relative; the float32 sums here are
-  // accurate to ~1e-6).
-  const float delta = ldexpf(1.0f + fabsf(v0), -12);
-  const float vk1 = (k == 1) ? v0 : v1;     // k-th largest
-  const float vk = (k == 1) ? v1 : v2;      // (k+1)-th largest, -inf if none
-  const bool amb = valid && ((k == 2 && v0 - v1 <= delta) || (vk1 - vk <= delta));
-  uint64_t cand = 0;
-  if (amb)
-    for (int e = 0; e < E; ++e)
-      if (part[0][lane][e] >= vk1 - delta) cand |= 1ull << e;
-  uint64_t ambmask = __ballot(amb);
-  while (ambmask) {
-    const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;
-    ambmask &= ambmask - 1;
-    const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
-    const size_t xt = static_cast<size_t>(t0 + tl) * d;
-    double b0 = -INFINITY, b1 = -INFINITY;
-    int j0 = 0, j1 = 0;
-    for (int e = 0; e < E; ++e) {
-      if (!((cm >> e) & 1ull)) continue;
-      double s = 0.0;
-      if constexpr (BF16) {
-        const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
-        const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
-        for (int c = lane * 8; c < d; c += 512) {
-          Pack16 xa, wa;
-          xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
-          wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
+  float (*pw)[kMaxExperts + 1] = part[0];
+  // partial tiles summed in wave order (lane = token)
+  if (lane < kGateTok)
+    for (int e = 0; e < E; ++e) pw[lane][e] = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
+                                              part[3][lane][e] + bias[e];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  {
+    // ---- epilogue: lane = token (lanes 0..31)
+    const int t = t0 + lane;
+    const bool valid = lane < kGateTok && t < T;
+    const int tl_ = lane < kGateTok ? lane : 0;
+    const float NEG = -INFINITY;
+    float v0 = NEG, v1 = NEG, v2 = NEG;
+    int i0 = 0, i1 = 0;
+    for (int e0 = 0; e0 < E && valid; e0 += 8) {
+      float v8[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i)
-            s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
-        }
-      } else {
-        const float* xr = static_cast<const float*>(xv) + xt;
-        const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
-        for (int c = lane * 4; c < d; c += 256) {
-          const float4 xa = *reinterpret_cast<const float4*>(xr + c);
-          const float4 wa = *reinterpret_cast<const float4*>(wr + c);
-          s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
-               static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
-        }
+      for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? pw[tl_][e0 + u] : NEG;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float v = v8[u];
+        const int e = e0 + u;
+        if (v > v0) { v2 = v1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
+        else if (v > v1) { v2 = v1; v1 = v; i1 = e; }
+        else if (v > v2) { v2 = v; }
       }
-      s = wave_sum_f64(s);
-      s += static_cast<double>(bias[e]);
-      if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
-      else if (s > b1) { b1 = s; j1 = e; }
     }
-    if (lane == tl) { i0 = j0; i1 = j1; }
-  }
-  if (valid) {
-    float den = 0.f;
-    for (int e = 0; e < E; ++e) den += expf(part[0][lane][e] - v0);
-    if (k == 1) {
-      topk_idx[t] = i0;
-      topk_gate[t] = expf(part[0][lane][i0] - v0) / den;
-    } else {
-      const float ga = expf(part[0][lane][i0] - v0);
-      const float gb = expf(part[0][lane][i1] - v0);
-      topk_idx[2 * t] = i0;
-      topk_idx[2 * t + 1] = i1;
-      topk_gate[2 * t] = ga / (ga + gb);
-      topk_gate[2 * t + 1] = gb / (ga + gb);
-    }
-  }
-  // stable rank of each slot among this chunk's slots of the same expert:
-  // lanes holding the same expert are found with 7 ballots on its bits
-  const int nblk = gridDim.x;
-  for (int j = 0; j < k; ++j) {
-    const int e = valid ? (j == 0 ? i0 : i1) : -1;
-    const int key = e < 0 ? 127 : e;
-    uint64_t same = ~0ull;
+    // A choice is re-decided in float64 when a deciding gap is within the
+    // float32 error budget (about 1e-4 relative; the float32 sums here are
+    // accurate to ~1e-6).
+    const float delta = ldexpf(1.0f + fabsf(v0), -12);
+    const float vk1 = (k == 1) ? v0 : v1;     // k-th largest
+    const float vk = (k == 1) ? v1 : v2;      // (k+1)-th largest, -inf if none
+    const bool amb = valid && ((k == 2 && v0 - v1 <= delta) || (vk1 - vk <= delta));
+    uint64_t cand = 0;
+    if (amb)
+      for (int e = 0; e < E; ++e)
+        if (pw[tl_][e] >= vk1 - delta) cand |= 1ull << e;
+    uint64_t ambmask = __ballot(amb);
+    while (ambmask) {
+      const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;
+      ambmask &= ambmask - 1;
+      const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
+      const size_t xt = static_cast<size_t>(t0 + tl) * d;
+      double b0 = -INFINITY, b1 = -INFINITY;
+      int j0 = 0, j1 = 0;
+      for (int e = 0; e < E; ++e) {
+        if (!((cm >> e) & 1ull)) continue;
+        double s = 0.0;
+        if constexpr (BF16) {
+          const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
+          const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
+          for (int c = lane * 8; c < d; c += 512) {
+            Pack16 xa, wa;
+            xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
+            wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
 #pragma unroll
-    for (int b = 0; b < 7; ++b) {
-      const bool bit = (key >> b) & 1;
-      const uint64_t bb = __ballot(bit);
-      same &= bit ? bb : ~bb;
+            for (int i = 0; i < 8; ++i)
+              s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
+          }
+        } else {
+          const float* xr = static_cast<const float*>(xv) + xt;
+          const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
+          for (int c = lane * 4; c < d; c += 256) {
+            const float4 xa = *reinterpret_cast<const float4*>(xr + c);
+            const float4 wa = *reinterpret_cast<const float4*>(wr + c);
+            s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
+                 static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
+          }
+        }
+        s = wave_sum_f64(s);
+        s += static_cast<double>(bias[e]);
+        if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
+        else if (s > b1) { b1 = s; j1 = e; }
+      }
+      if (lane == tl) { i0 = j0; i1 = j1; }
     }
-    const int rank = __popcll(same & lanemask_lt());
-    if (lane < E) cnt[lane] = 0;
-    __builtin_amdgcn_wave_barrier();
-    if (e >= 0 && rank == 0) cnt[e] = __popcll(same);
-    __builtin_amdgcn_wave_barrier();
-    if (lane < E) hist[(static_cast<size_t>(j) * nblk + blockIdx.x) * E + lane] = cnt[lane];
-    if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
-    __builtin_amdgcn_wave_barrier();
+    if (valid) {
+      float den = 0.f;
+      for (int e = 0; e < E; ++e) den += expf(pw[lane][e] - v0);
+      if (k == 1) {
+        topk_idx[t] = i0;
+        topk_gate[t] = expf(pw[lane][i0] - v0) / den;
+      } else {
+        const float ga = expf(pw[lane][i0] - v0);
+        const float gb = expf(pw[lane][i1] - v0);
+        topk_idx[2 * t] = i0;
+        topk_idx[2 * t + 1] = i1;
+        topk_gate[2 * t] = ga / (ga + gb);
+        topk_gate[2 * t + 1] = gb / (ga + gb);
+      }
+    }
+    // stable rank of each slot among this chunk's slots of the same expert:
+    // lanes holding the same expert are found with 7 ballots on its bits
+    int* cw = cnt;
+    for (int j = 0; j < k; ++j) {
+      const int e = valid ? (j == 0 ? i0 : i1) : -1;
+      const int key = e < 0 ? 127 : e;
+      uint64_t same = ~0ull;
+#pragma unroll
+      for (int b = 0; b < 7; ++b) {
+        const bool bit = (key >> b) & 1;
+        const uint64_t bb = __ballot(bit);
+        same &= bit ? bb : ~bb;
+      }
+      const int rank = __popcll(same & lanemask_lt());
+      if (lane < E) cw[lane] = 0;
+      __builtin_amdgcn_wave_barrier();
+      if (e >= 0 && rank == 0) cw[e] = __popcll(same);
+      __builtin_amdgcn_wave_barrier();
+      if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
+      if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
+      __builtin_amdgcn_wave_barrier();
+    }
   }
 }
 
@@ -261,16 +284,20 @@ __global__ __launch_bounds__(1024) void slot_scan_kernel(
     last = atomicAdd(done, 1) == E - 1;
   }
   __syncthreads();
-  if (last && tid == 0) {
+  if (last && wv == 0) {
+    // capacity-clamped totals, one expert per lane (E <= 64), prefixed
     __threadfence();
-    int o = 0;
-    for (int ee = 0; ee < E; ++ee) {
-      const int n = load_flag(&totals[ee]);
-      offsets[ee] = o;
-      o += (C > 0 && n > C) ? C : n;
+    int n = lane < E ? load_flag(&totals[lane]) : 0;
+    if (C > 0 && n > C) n = C;
+    int incl = n;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) {
+      const int u = __shfl_up(incl, sh, 64);
+      if (lane >= sh) incl += u;
     }
-    offsets[E] = o;
-    store_flag(done, 0);
+    if (lane < E) offsets[lane] = incl - n;
+    if (lane == E - 1) offsets[E] = incl;
+    if (lane == 0) store_flag(done, 0);
   }
 }
 
@@ -362,12 +389,13 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
   const int nch = k * gblocks;
   {
     ProfileScope prof_("gate", s);
+    const int chunks = (T + kGateTok - 1) / kGateTok;
     if (dtype == LUFFY_BF16)
-      gate_kernel<true><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
-                                                slot_pos, ws.hist, ws.done);
+      gate_kernel<true><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
+                                               ws.hist, ws.done);
     else
-      gate_kernel<false><<<gblocks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
-                                                 slot_pos, ws.hist, ws.done);
+      gate_kernel<false><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
+                                                ws.hist, ws.done);
   }
   {
     ProfileScope prof_("slot_scan", s);

@@ -167,3 +167,43 @@ def test_gathered_rows_path_matches():
     assert_condense_equal(g, o)
     assert np.array_equal(g["x_rep"], inp.x[o.rep_token])
     assert_output_close(g, o, "bf16")
+
+
+def _bf16(a):
+    """Round float64 values to bfloat16 (nearest even) and back, in numpy."""
+    import torch
+    return torch.from_numpy(np.asarray(a, np.float64)).to(torch.bfloat16).double().numpy()
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_activation_values_bf16(act):
+    """Identity weights make the expert FFN return bf16(act(x)) for every
+    input element, so the device activation is compared value by value with
+    the oracle's exact one: equal, or one bf16 step apart where the exact
+    value lies next to a rounding boundary."""
+    import torch
+    import paper_2411_15419_amd as L
+    d = 64
+    z = _bf16(np.linspace(-9.0, 9.0, 512 * d)).reshape(512, d)
+    x = torch.from_numpy(z).to(torch.bfloat16).cuda()
+    eye = torch.eye(d, dtype=torch.bfloat16, device="cuda")[None]
+    off = torch.tensor([0, 512], dtype=torch.int32, device="cuda")
+    y = torch.empty(512, d, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(L.expert_ffn_workspace_size(512, 1, d, L.LUFFY_BF16), dtype=torch.uint8,
+                     device="cuda")
+    L.luffy_expert_ffn(x, None, off, eye, eye.clone(), act, 512, y, ws)
+    got = y.double().cpu().numpy()
+    exact = O.activation(z, act)
+    ref = _bf16(exact)
+    step = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7   # one bf16 ulp (upper bound)
+    # GELU's erf is within 1.5e-7 absolute (Abramowitz & Stegun 7.1.26), so
+    # GELU is within 0.5 |z| 1.5e-7 absolute; taken as 0.5 |z| 2e-7 to cover
+    # the ulps of the hardware exp2 and reciprocal.  That is below one bf16
+    # step except where GELU(z) is tiny (z < -4).
+    slack = 0.5 * np.abs(z) * 2e-7 if act == "gelu" else 0.0
+    bad = np.abs(got - ref) > step + slack
+    assert not bad.any(), (f"{bad.sum()} values off by more than one bf16 step, e.g. "
+                           f"x={z[bad][:4]} got={got[bad][:4]} want={ref[bad][:4]}")
+    # away from rounding boundaries the device value rounds to the same bf16
+    core = z >= -4.0
+    assert np.mean(got[core] == ref[core]) > 0.99
