@@ -40,7 +40,7 @@ namespace luffy {
 namespace {
 
 constexpr int kGreedyGridRounds = 2;
-constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig)
+constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig64)
 constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
 
@@ -228,12 +228,12 @@ __device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t
   return c;
 }
 
-__global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
+__global__ __launch_bounds__(GemmBig64::THREADS) void gram_kernel_bf16(
     const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
-  using G = GemmBig;
+  using G = GemmBig64;
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   __shared__ __attribute__((aligned(16))) float inv_a[kTile];
   __shared__ float inv_b[kTile];
@@ -243,17 +243,18 @@ __global__ __launch_bounds__(GemmBig::THREADS) void gram_kernel_bf16(
   uint32_t (*tbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kTile * kTile / 8);
   if (*err) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w / G::WN, wn = w % G::WN;
+  const int wm = G::wave_m(w), wn = G::wave_n(w);
   const int total = tile_off[E];
   for (int tile = xcd_virtual_block(); tile < total; tile += gridDim.x) {
     const TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
     const int32_t* pt = perm_token + c.lo;
-    uint32_t poff[G::LOADS / 2], qoff[G::LOADS / 2];
+    uint32_t poff[G::LP], qoff[G::LQ];
 #pragma unroll
-    for (int j = 0; j < G::LOADS / 2; ++j) {
+    for (int j = 0; j < G::LP; ++j)
       poff[j] = static_cast<uint32_t>(pt[min(c.ti * kTile + G::load_row(j), c.n - 1)]) * d;
-      qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(j + G::LOADS / 2) - G::BM, c.n - 1)]) * d;
-    }
+#pragma unroll
+    for (int j = 0; j < G::LQ; ++j)
+      qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)]) * d;
     if (tid < kTile) inv_a[tid] = inv_norm[pt[min(c.ti * kTile + tid, c.n - 1)]];
     else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
     G::Acc acc;
@@ -782,7 +783,7 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   {
     ProfileScope prof_("gram", s);
     if (bf16)
-      gram_kernel_bf16<<<persistent_grid(), GemmBig::THREADS, 0, s>>>(
+      gram_kernel_bf16<<<persistent_grid(), GemmBig64::THREADS, 0, s>>>(
           static_cast<const uint16_t*>(x), d, perm_token, offsets, E, ws.inv_norm, threshold, ws.tile_off,
           ws.bm_off, ws.err, ws.bitmask, ws.deg);
     else

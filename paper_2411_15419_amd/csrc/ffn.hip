@@ -5,7 +5,7 @@
 // upper bound ceil(max_rows/BN) + E row tiles; each block finds its expert
 // and row range from rep_offsets and exits when it has none.
 //
-// bf16: 256 x 256 MFMA tiles (GemmRagged).  The weight rows are the P
+// bf16: 256 x 256 MFMA tiles (GemmRagged64).  The weight rows are the P
 // operand and the token rows the Q operand, so each lane ends with groups of
 // four consecutive output columns of one row and stores each as one 8-byte
 // word.  The last row tile of an expert usually holds fewer than 256 rows;
@@ -165,28 +165,15 @@ struct FfnTiles {
 
 // Multiplies with only the first nq of the wave's Q blocks (wave-uniform
 // nq in 0..FN), so the MFMAs of token rows past a partial tile are skipped.
-// With eight Q blocks per wave, nq is taken in steps of two.
-template <class G>
-__device__ __forceinline__ void run_ragged(int nq, const uint16_t* pbase, const uint32_t (&poff)[G::LOADS / 2],
-                                           const uint16_t* qbase, const uint32_t (&qoff)[G::LOADS / 2], int K,
-                                           uint8_t* lds, typename G::Acc& acc) {
-  if constexpr (G::FN == 4) {
-    switch (nq) {
-      case 4: G::template run<4>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 3: G::template run<3>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 2: G::template run<2>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 1: G::template run<1>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      default: G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc); break;
-    }
+template <class G, int N>
+__device__ __forceinline__ void run_nq(int nq, const uint16_t* pbase, const uint32_t (&poff)[G::LP],
+                                       const uint16_t* qbase, const uint32_t (&qoff)[G::LQ], int K, uint8_t* lds,
+                                       typename G::Acc& acc) {
+  if constexpr (N == 0) {
+    G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc);
   } else {
-    static_assert(G::FN == 8, "ragged dispatch for four or eight Q blocks per wave");
-    switch ((nq + 1) >> 1) {
-      case 4: G::template run<8>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 3: G::template run<6>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 2: G::template run<4>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      case 1: G::template run<2>(pbase, poff, qbase, qoff, K, lds, acc); break;
-      default: G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc); break;
-    }
+    if (nq >= N) G::template run<N>(pbase, poff, qbase, qoff, K, lds, acc);
+    else run_nq<G, N - 1>(nq, pbase, poff, qbase, qoff, K, lds, acc);
   }
 }
 
@@ -205,6 +192,7 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = G::wave_m(w), wn = G::wave_n(w);
+  static_assert(G::FN <= 4, "ragged dispatch instantiates FN + 1 main loops");
   const FfnTiles<G> map(rep_offsets, E, N);
   const int nk = K / G::BK;
   const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
@@ -214,25 +202,26 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
     int e, row0, rows, n0;
     map.decode(t, E, e, row0, rows, n0);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
-    uint32_t poff[G::LOADS / 2], qoff[G::LOADS / 2];
+    uint32_t poff[G::LP], qoff[G::LQ];
 #pragma unroll
-    for (int j = 0; j < G::LOADS / 2; ++j) {
-      poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
-      const int m = row0 + min(G::load_row(j + G::LOADS / 2) - G::BM, rows - 1);
+    for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
+#pragma unroll
+    for (int j = 0; j < G::LQ; ++j) {
+      const int m = row0 + min(G::load_row(G::LP + j) - G::BM, rows - 1);
       qoff[j] = static_cast<uint32_t>(row_index ? row_index[m] : m) * K;
     }
     // K range of this part, in whole 32-wide stages
     const int k0 = (part * nk / S) * G::BK, k1 = ((part + 1) * nk / S) * G::BK;
-    const int nq = min(max((rows - wn * G::WTN + 31) / 32, 0), G::FN);
+    const int nq = G::active_q(wn, rows);
     typename G::Acc acc;
     G::zero(acc);
-    run_ragged<G>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
+    run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * SK::SLOT_FLOATS : nullptr;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
       for (int fn = 0; fn < G::FN; ++fn) {
-        const int ml = wn * G::WTN + 32 * fn + (lane & 31);
+        const int ml = G::q_row(wn, fn) + (lane & 31);
         if (ml >= rows) continue;
         uint16_t* orow = out + static_cast<size_t>(row0 + ml) * N;
 #pragma unroll
@@ -286,7 +275,7 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
     map.decode(t, E, e, row0, rows, n0);
     const int l = u & 63, g = (u >> 6) & 3, q = u >> 8;
     const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
-    const int ml = G::wave_n(w) * G::WTN + 32 * fn + (l & 31);
+    const int ml = G::q_row(G::wave_n(w), fn) + (l & 31);
     const int nl = G::wave_m(w) * G::WTM + 32 * fm + 8 * g + 4 * (l >> 5);
     if (ml >= rows || n0 + nl >= N) continue;
     const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS + static_cast<size_t>(u) * 4;
@@ -358,7 +347,7 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   }
 }
 
-using FfnGemm = GemmRagged;
+using FfnGemm = GemmRagged64;
 
 struct FfnWs {
   void* hidden;

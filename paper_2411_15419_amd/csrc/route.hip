@@ -1,8 +1,8 @@
 // luffy_route: gate logits, top-k, gates and the stable dispatch order.
 //
 // Kernels (all on the caller's stream, no host synchronisation):
-//   gate_kernel      32 tokens per block; the four waves split the
-//                    contraction over d and accumulate 32 x E logit tiles
+//   gate_kernel      64 tokens per block; the four waves split the
+//                    contraction over d and accumulate 64 x E logit tiles
 //                    on MFMA (16x16x32); fp32: plain FMA.  The epilogue
 //                    takes top-k, gates and the float64 re-decision of close
 //                    calls, then ranks every slot among the block's slots of
@@ -21,7 +21,8 @@
 namespace luffy {
 namespace {
 
-constexpr int kGateTok = 32;     // tokens per gate block (= slots per chunk)
+constexpr int kGateTok = 64;     // tokens per gate block (= slots per chunk)
+constexpr int kGateA = kGateTok / 16;   // 16-token MFMA row blocks per gate block
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
   // xor butterfly: every lane ends with the same, bit-identical sum
@@ -30,11 +31,11 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// One block of four waves per chunk of 32 tokens.  bf16: wave w takes the
-// w-th quarter of the contraction over d and accumulates the 32 x E logits
-// of the chunk on MFMA (16x16x32: two 16-token blocks per 16-expert block),
-// four K steps' token and weight loads in flight at a time; the four partial
-// tiles are added in LDS in a fixed order.  fp32: plain FMA.  Wave 0 then
+// One block of four waves per chunk of 64 tokens.  bf16: wave w takes the
+// w-th quarter of the contraction over d and accumulates the 64 x E logits
+// of the chunk on MFMA (16x16x32: four 16-token blocks per 16-expert
+// block), two K steps' token and weight loads in flight at a time; the four
+// partial tiles are added in LDS in a fixed order.  fp32: plain FMA.  Wave 0 then
 // runs the epilogue for the chunk (lane = token): top-k, gates, the float64
 // re-decision of close calls, and the rank of every slot among the chunk's
 // slots of the same expert (wave ballots) with the chunk's per-expert
@@ -49,6 +50,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
   __shared__ float part[4][kGateTok][kMaxExperts + 1];
   __shared__ float bias[kMaxExperts];
   __shared__ int cnt[kMaxExperts];
+  __shared__ int choice[kGateTok][2];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int nchunks = gridDim.x;
@@ -61,14 +63,14 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const uint16_t* X = static_cast<const uint16_t*>(xv);
     const uint16_t* W = static_cast<const uint16_t*>(wv);
     const int nE16 = (E + 15) >> 4;
-    f32x4 acc[2][4];
+    f32x4 acc[kGateA][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kGateA; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* arow[2];
+    const uint16_t* arow[kGateA];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kGateA; ++i)
       arow[i] = X + static_cast<size_t>(min(t0 + 16 * i + (lane & 15), T - 1)) * d + 8 * (lane >> 4);
     const uint16_t* brow[4];
 #pragma unroll
@@ -77,15 +79,15 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const int nsteps = d / 32;
     const int q = (nsteps + 3) / 4;
     const int s_lo = w * q, s_hi = min(nsteps, s_lo + q);
-    constexpr int B = 4;   // K steps per batch
+    constexpr int B = 2;   // K steps per batch
     for (int s0 = s_lo; s0 < s_hi; s0 += B) {
-      Pack16 a[B][2], b[B][4];
+      Pack16 a[B][kGateA], b[B][4];
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         const int st = s0 + u;
         const bool in = st < s_hi;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < kGateA; ++i)
           a[u][i].u4 = in ? *reinterpret_cast<const uint4*>(arow[i] + 32 * st) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
@@ -98,24 +100,22 @@ __global__ __launch_bounds__(256) void gate_kernel(
         for (int j = 0; j < 4; ++j)
           if (j < nE16)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) acc[i][j] = mfma16x16x32(a[u][i].v, b[u][j].v, acc[i][j]);
+            for (int i = 0; i < kGateA; ++i) acc[i][j] = mfma16x16x32(a[u][i].v, b[u][j].v, acc[i][j]);
     }
     // lane holds logits of tokens 16i + 4(lane/16) + r, expert 16j + lane%16
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kGateA; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (j < nE16)
 #pragma unroll
           for (int r = 0; r < 4; ++r) part[w][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
   } else {
-    // float32 inputs: lane = token (lane % 32), experts strided over the
-    // two lane halves and the four waves
+    // float32 inputs: lane = token, experts strided over the four waves
     const float* X = static_cast<const float*>(xv);
     const float* W = static_cast<const float*>(wv);
-    const int t = min(t0 + (lane & 31), T - 1);
+    const int t = min(t0 + lane, T - 1);
     for (int e = w; e < E; e += 4) {
-      if ((lane >> 5) != 0) continue;
       float s = 0.f;
       for (int i = 0; i < d; ++i) s = fmaf(X[static_cast<size_t>(t) * d + i], W[static_cast<size_t>(e) * d + i], s);
       part[0][lane][e] = s;
@@ -125,27 +125,26 @@ __global__ __launch_bounds__(256) void gate_kernel(
     }
   }
   __syncthreads();
-  if (w != 0) return;
-  float (*pw)[kMaxExperts + 1] = part[0];
-  // partial tiles summed in wave order (lane = token)
-  if (lane < kGateTok)
-    for (int e = 0; e < E; ++e) pw[lane][e] = ((part[0][lane][e] + part[1][lane][e]) + part[2][lane][e]) +
-                                              part[3][lane][e] + bias[e];
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // partial tiles summed in wave order into part[0], one (token, expert)
+  // pair per thread at a time
+  float (*logit)[kMaxExperts + 1] = part[0];
+  for (int i = threadIdx.x; i < kGateTok * E; i += 256) {
+    const int tl = i / E, e = i - tl * E;
+    logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
+  }
+  __syncthreads();
   {
-    // ---- epilogue: lane = token (lanes 0..31)
-    const int t = t0 + lane;
-    const bool valid = lane < kGateTok && t < T;
-    const int tl_ = lane < kGateTok ? lane : 0;
+    // ---- top-k: wave w takes tokens 16w .. 16w+15 (lane = token)
+    const int tl_ = 16 * w + (lane & 15);
+    const int t = t0 + tl_;
+    const bool valid = lane < 16 && t < T;
     const float NEG = -INFINITY;
     float v0 = NEG, v1 = NEG, v2 = NEG;
     int i0 = 0, i1 = 0;
     for (int e0 = 0; e0 < E && valid; e0 += 8) {
       float v8[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? pw[tl_][e0 + u] : NEG;
+      for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? logit[tl_][e0 + u] : NEG;
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const float v = v8[u];
@@ -165,13 +164,13 @@ __global__ __launch_bounds__(256) void gate_kernel(
     uint64_t cand = 0;
     if (amb)
       for (int e = 0; e < E; ++e)
-        if (pw[tl_][e] >= vk1 - delta) cand |= 1ull << e;
+        if (logit[tl_][e] >= vk1 - delta) cand |= 1ull << e;
     uint64_t ambmask = __ballot(amb);
     while (ambmask) {
       const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;
       ambmask &= ambmask - 1;
       const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
-      const size_t xt = static_cast<size_t>(t0 + tl) * d;
+      const size_t xt = static_cast<size_t>(t0 + 16 * w + tl) * d;
       double b0 = -INFINITY, b1 = -INFINITY;
       int j0 = 0, j1 = 0;
       for (int e = 0; e < E; ++e) {
@@ -207,41 +206,54 @@ __global__ __launch_bounds__(256) void gate_kernel(
     }
     if (valid) {
       float den = 0.f;
-      for (int e = 0; e < E; ++e) den += expf(pw[lane][e] - v0);
+      for (int e0 = 0; e0 < E; e0 += 8) {
+        float v8[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? logit[tl_][e0 + u] : NEG;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) den += expf(v8[u] - v0);
+      }
       if (k == 1) {
         topk_idx[t] = i0;
-        topk_gate[t] = expf(pw[lane][i0] - v0) / den;
+        topk_gate[t] = expf(logit[tl_][i0] - v0) / den;
       } else {
-        const float ga = expf(pw[lane][i0] - v0);
-        const float gb = expf(pw[lane][i1] - v0);
+        const float ga = expf(logit[tl_][i0] - v0);
+        const float gb = expf(logit[tl_][i1] - v0);
         topk_idx[2 * t] = i0;
         topk_idx[2 * t + 1] = i1;
         topk_gate[2 * t] = ga / (ga + gb);
         topk_gate[2 * t + 1] = gb / (ga + gb);
       }
+      choice[tl_][0] = i0;
+      choice[tl_][1] = i1;
     }
-    // stable rank of each slot among this chunk's slots of the same expert:
-    // lanes holding the same expert are found with 7 ballots on its bits
-    int* cw = cnt;
-    for (int j = 0; j < k; ++j) {
-      const int e = valid ? (j == 0 ? i0 : i1) : -1;
-      const int key = e < 0 ? 127 : e;
-      uint64_t same = ~0ull;
+  }
+  __syncthreads();
+  if (w != 0) return;
+  const int t = t0 + lane;
+  const bool valid = lane < kGateTok && t < T;
+  const int i0 = valid ? choice[lane][0] : 0, i1 = valid ? choice[lane][1] : 0;
+  // stable rank of each slot among this chunk's slots of the same expert:
+  // lanes holding the same expert are found with 7 ballots on its bits
+  int* cw = cnt;
+  for (int j = 0; j < k; ++j) {
+    const int e = valid ? (j == 0 ? i0 : i1) : -1;
+    const int key = e < 0 ? 127 : e;
+    uint64_t same = ~0ull;
 #pragma unroll
-      for (int b = 0; b < 7; ++b) {
-        const bool bit = (key >> b) & 1;
-        const uint64_t bb = __ballot(bit);
-        same &= bit ? bb : ~bb;
-      }
-      const int rank = __popcll(same & lanemask_lt());
-      if (lane < E) cw[lane] = 0;
-      __builtin_amdgcn_wave_barrier();
-      if (e >= 0 && rank == 0) cw[e] = __popcll(same);
-      __builtin_amdgcn_wave_barrier();
-      if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
-      if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
-      __builtin_amdgcn_wave_barrier();
+    for (int b = 0; b < 7; ++b) {
+      const bool bit = (key >> b) & 1;
+      const uint64_t bb = __ballot(bit);
+      same &= bit ? bb : ~bb;
     }
+    const int rank = __popcll(same & lanemask_lt());
+    if (lane < E) cw[lane] = 0;
+    __builtin_amdgcn_wave_barrier();
+    if (e >= 0 && rank == 0) cw[e] = __popcll(same);
+    __builtin_amdgcn_wave_barrier();
+    if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
+    if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
