@@ -30,9 +30,12 @@
  *    ABI.
  *  - Outputs must not alias inputs.  Integer outputs are deterministic: the
  *    same inputs give bit-identical indices on every run.
- *  - Supported sizes: d and d_ff multiples of 64, 1 <= E <= 64,
- *    k in {1, 2}, T*k < 2^31 (luffy_condense: T*k <= 2^24).  Other sizes
- *    return LUFFY_E_UNSUPPORTED.
+ *  - Supported sizes: d and d_ff multiples of 64 and at most 32768,
+ *    1 <= E <= 64, k in {1, 2}, T*k < 2^31 (luffy_condense: T*k <= 2^24),
+ *    every activation matrix and every expert's weight matrix smaller than
+ *    4 GiB - 64 KiB.  Other sizes return LUFFY_E_UNSUPPORTED where the call
+ *    can see them (x of luffy_expert_ffn, read through row_index, is the
+ *    caller's to keep within the limit).
  */
 #ifndef LUFFY_H
 #define LUFFY_H

@@ -259,7 +259,7 @@ __global__ __launch_bounds__(GemmBig64::THREADS) void gram_kernel_bf16(
     else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
     G::Acc acc;
     G::zero(acc);
-    G::run(X, poff, X, qoff, d, lds, acc);  // ends with a barrier
+    G::run(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, acc);  // ends with a barrier
 
     // Each (fm, fn) block is 32 x 32: ballot v covers rows
     // abase + 8(v/4) + (v%4) (bits 0..31) and that row + 4 (bits 32..63),
@@ -755,6 +755,9 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   if (threshold != threshold) return fail(LUFFY_E_INVALID, "luffy_condense: threshold is NaN");
   if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: E=%d > %d", E, kMaxExperts);
   if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: d=%d not a multiple of 64", d);
+  if (d > 32768) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: d=%d > 32768", d);
+  if (static_cast<long long>(T) * d * elem_bytes(dtype) > 0xFFFF0000ll)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: x exceeds 4 GiB - 64 KiB");
   if (static_cast<long long>(T) * k > (1ll << 24))
     return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: T*k > 2^24");
   const size_t need = luffy_condense_workspace_size(T, d, E, k, max_bucket);

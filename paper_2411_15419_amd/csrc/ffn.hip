@@ -167,13 +167,13 @@ struct FfnTiles {
 // nq in 0..FN), so the MFMAs of token rows past a partial tile are skipped.
 template <class G, int N>
 __device__ __forceinline__ void run_nq(int nq, const uint16_t* pbase, const uint32_t (&poff)[G::LP],
-                                       const uint16_t* qbase, const uint32_t (&qoff)[G::LQ], int K, uint8_t* lds,
-                                       typename G::Acc& acc) {
+                                       const uint16_t* qbase, const uint32_t (&qoff)[G::LQ], int K, int pvalid,
+                                       int qvalid, uint8_t* lds, typename G::Acc& acc) {
   if constexpr (N == 0) {
-    G::template run<0>(pbase, poff, qbase, qoff, K, lds, acc);
+    G::template run<0>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
   } else {
-    if (nq >= N) G::template run<N>(pbase, poff, qbase, qoff, K, lds, acc);
-    else run_nq<G, N - 1>(nq, pbase, poff, qbase, qoff, K, lds, acc);
+    if (nq >= N) G::template run<N>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
+    else run_nq<G, N - 1>(nq, pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
   }
 }
 
@@ -215,7 +215,8 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
     const int nq = G::active_q(wn, rows);
     typename G::Acc acc;
     G::zero(acc);
-    run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, lds, acc);
+    run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, N - n0, rows, lds,
+                     acc);
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * SK::SLOT_FLOATS : nullptr;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
@@ -436,6 +437,11 @@ extern "C" int luffy_expert_ffn(const void* x, const int32_t* row_index,
   if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: E=%d > %d", E, kMaxExperts);
   if (d % 64 != 0 || d_ff % 64 != 0)
     return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: d=%d d_ff=%d must be multiples of 64", d, d_ff);
+  if (d > 32768 || d_ff > 32768)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: d=%d d_ff=%d must be at most 32768", d, d_ff);
+  if (static_cast<long long>(max_rows) * d_ff * elem_bytes(dtype) > 0xFFFF0000ll ||
+      static_cast<long long>(d) * d_ff * elem_bytes(dtype) > 0xFFFF0000ll)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn: hidden activations or one expert's weights exceed 4 GiB - 64 KiB");
   const size_t need = luffy_expert_ffn_workspace_size(max_rows, E, d_ff, dtype);
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "luffy_expert_ffn: workspace needs %zu bytes, 256-aligned", need);

@@ -111,9 +111,15 @@ struct GemmK64 {
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   }
 
+  // Raw buffer resource over [base, base + kRange).  A row whose offset is
+  // set to kRange is out of range: its buffer loads fetch nothing from
+  // memory (robust buffer access), which is how rows past the valid ones
+  // of a partial tile are skipped.  Valid rows need offset + K*2 <= kRange
+  // (operands below 4 GiB - 64 KiB, K <= 32768).
+  static constexpr uint32_t kRange = 0xFFFF0000u;
   static __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                             static_cast<int>(0xFFFFFFFFu), 0x00020000);
+                                             static_cast<int>(kRange), 0x00020000);
   }
 
   static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t prs, __amdgpu_buffer_rsrc_t qrs,
@@ -128,15 +134,17 @@ struct GemmK64 {
   }
 
   // lane fills physical chunk lane%8 of its row with logical chunk
-  // (lane%8) ^ swz(row); byte offsets
+  // (lane%8) ^ swz(row); byte offsets.  P rows from pvalid on and Q rows
+  // from qvalid on are marked out of range (not fetched).
   static __device__ __forceinline__ void dma_offsets(const uint32_t (&poff)[LP], const uint32_t (&qoff)[LQ],
-                                                     uint32_t (&goff)[LOADS]) {
+                                                     int pvalid, int qvalid, uint32_t (&goff)[LOADS]) {
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int r = load_row(j);
       const uint32_t lc = static_cast<uint32_t>((lane & 7) ^ swz(r));
-      goff[j] = ((j < LP ? poff[j] : qoff[j - LP]) + lc * 8) * 2u;
+      const bool valid = j < LP ? r < pvalid : r - BM < qvalid;
+      goff[j] = valid ? ((j < LP ? poff[j] : qoff[j - LP]) + lc * 8) * 2u : kRange;
     }
   }
 
@@ -198,9 +206,11 @@ struct GemmK64 {
 
   // poff[j] (j < LP): element offset of P row load_row(j);
   // qoff[j] (j < LQ): element offset of Q row load_row(LP + j) - BM.
-  // Ends with a barrier after which the LDS may be reused.  NQ: the wave
-  // multiplies only its first NQ Q blocks; every wave still loads its share
-  // of the operands and takes every barrier.
+  // Only the first pvalid P rows and qvalid Q rows are fetched; the LDS
+  // rows of the others hold stale values, which only reach accumulator rows
+  // and columns of invalid rows.  Ends with a barrier after which the LDS
+  // may be reused.  NQ: the wave multiplies only its first NQ Q blocks;
+  // every wave still issues its share of the loads and takes every barrier.
   //
   // Stage kt (buffer kt % 2): [A] read half 1 of stage kt while multiplying
   // half 0; [B] wait for stage kt+1 and for this wave's reads, barrier (all
@@ -209,14 +219,14 @@ struct GemmK64 {
   template <int NQ = FN>
   static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase, const uint32_t (&poff)[LP],
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
-                                             int K, uint8_t* lds_generic, Acc& acc) {
+                                             int K, int pvalid, int qvalid, uint8_t* lds_generic, Acc& acc) {
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int lane = threadIdx.x & 63;
     const int w = wave();
     const int wm = wave_m(w), wn = wave_n(w);
     const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
     uint32_t goff[LOADS];
-    dma_offsets(poff, qoff, goff);
+    dma_offsets(poff, qoff, pvalid, qvalid, goff);
     const int nk = __builtin_amdgcn_readfirstlane(K / BK);
     issue(prs, qrs, goff, 0, lds, w);
     if (nk > 1) {
