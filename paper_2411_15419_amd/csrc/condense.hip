@@ -44,12 +44,6 @@ constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig64)
 constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
 
-__device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 __device__ __forceinline__ float wave_sum_f32(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -434,9 +428,12 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
 
 // Decides position p if its neighbours allow it; returns true when p is
 // still undecided afterwards (uniform over the GW-lane group that visits p,
-// GW = 16 or 64, aligned inside the wave).  Each lane walks its words of the
-// adjacency row (four word loads in flight) and gathers the state and
-// degree of up to 8 neighbours at a time before testing them.  The grid
+// GW = 16 or 64, aligned inside the wave).  The group walks the adjacency
+// row 4*GW words at a time (four word loads in flight per lane), gathers the
+// state and degree of up to 8 neighbours at a time before testing them, and
+// stops after the first batch of words that shows a kept neighbour (p is
+// absorbed) or an undecided neighbour of higher priority (p stays
+// undecided for a later round).  The grid
 // rounds use plain loads (FRESH = false): a state written by another XCD in
 // the same launch may be seen late, which only delays a decision (states
 // change once, from undecided to final).  The single-workgroup finishing
@@ -452,7 +449,8 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
   const uint64_t gmask = GW == 64 ? ~0ull : ((1ull << (GW & 63)) - 1);
   const int dp = deg[p];
   bool kept_nb = false, blocked = false;
-  for (int wd0 = gl; wd0 < W && !kept_nb; wd0 += 4 * GW) {
+  for (int b0 = 0; b0 < W; b0 += 4 * GW) {
+    const int wd0 = b0 + gl;
     uint64_t wv[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) wv[u] = wd0 + GW * u < W ? row[wd0 + GW * u] : 0ull;
@@ -484,6 +482,9 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
         }
       }
     }
+    // the group stops at its first kept or blocking neighbour: either way p
+    // cannot be kept now, and a position left undecided is decided later
+    if ((__ballot(kept_nb || blocked) >> gshift) & gmask) break;
   }
   const bool any_kept = ((__ballot(kept_nb) >> gshift) & gmask) != 0;
   const bool any_blocked = ((__ballot(blocked) >> gshift) & gmask) != 0;
