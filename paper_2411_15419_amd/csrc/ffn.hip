@@ -88,77 +88,55 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
 
 // Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
 // expert per lane, E <= 64).  An output tile is 256 output columns (weight
-// rows, the P operand) by up to 256 token rows (the Q operand).  Every expert
-// has floor(R_e/256) full row tiles and, when 256 does not divide R_e, one
-// partial row tile with R_e mod 256 rows.  Full tiles come first, expert by
-// expert; inside an expert the output-column tiles come in groups of 4 with
-// the row tile major inside a group, so ~32 consecutive tiles span ~8 row x
-// 4 column tiles.  Partial tiles follow, experts by descending partial size
-// (ties: lower expert first), so that the persistent blocks, which take
-// tiles round-robin, get the long tiles first.
+// rows, the P operand) by up to 256 token rows (the Q operand); the last row
+// tile of an expert is usually partial.  Tiles are numbered expert by
+// expert; inside an expert, output-column tiles come in groups of 4 with the
+// row tiles major inside a group, so the tiles that share a weight tile run
+// side by side and ~32 consecutive tiles (one XCD's share of a round, with
+// the XCD-aware block numbering) span few weight and token rows.
 template <class G>
 struct FfnTiles {
-  int elo, nfull, tail, incl, rank, NT, full_tiles, tiles;
+  int elo, ehi, mt, incl, NT, tiles;
   __device__ __forceinline__ FfnTiles(const int32_t* __restrict__ rep_offsets, int E, int N) {
     const int lane = threadIdx.x & 63;
     NT = (N + G::BM - 1) / G::BM;
-    elo = nfull = tail = 0;
+    elo = ehi = mt = 0;
     if (lane < E) {
       elo = rep_offsets[lane];
-      const int r = rep_offsets[lane + 1] - elo;
-      nfull = r / G::BN;
-      tail = r - nfull * G::BN;
+      ehi = rep_offsets[lane + 1];
+      mt = (ehi - elo + G::BN - 1) / G::BN;
     }
-    incl = nfull * NT;
+    incl = mt * NT;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const int v = __shfl_up(incl, o, 64);
       if (lane >= o) incl += v;
     }
-    full_tiles = __shfl(incl, 63, 64);
-    rank = 0;
-    for (int o = 0; o < E; ++o) {
-      const int to = __shfl(tail, o, 64);
-      rank += (to > tail || (to == tail && o < lane)) ? 1 : 0;
-    }
-    const int ntail = __popcll(__ballot(lane < E && tail > 0));
-    tiles = full_tiles + ntail * NT;
+    tiles = __shfl(incl, 63, 64);
   }
   // Tile t -> expert e, first token row row0, row count, first output n0.
   __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0) const {
     const int lane = threadIdx.x & 63;
-    if (t < full_tiles) {
-      e = __popcll(__ballot(lane < E && incl <= t));
-      const int me = __shfl(nfull, e, 64);
-      const int excl = __shfl(incl, e, 64) - me * NT;
-      const int r = t - excl;
-      const int ng = (NT + 3) / 4;
-      const int g = min(r / (4 * me), ng - 1);
-      const int r2 = r - 4 * g * me;
-      const int wg = min(4, NT - 4 * g);
-      const int ms = r2 / wg, nt = 4 * g + r2 % wg;
-      row0 = __shfl(elo, e, 64) + ms * G::BN;
-      rows = G::BN;
-      n0 = nt * G::BM;
-    } else {
-      const int q = t - full_tiles;
-      const int i = q / NT;
-      e = __ffsll(static_cast<long long>(__ballot(lane < E && tail > 0 && rank == i))) - 1;
-      row0 = __shfl(elo, e, 64) + __shfl(nfull, e, 64) * G::BN;
-      rows = __shfl(tail, e, 64);
-      n0 = (q - i * NT) * G::BM;
-    }
+    e = __popcll(__ballot(lane < E && incl <= t));
+    const int me = __shfl(mt, e, 64);
+    const int excl = __shfl(incl, e, 64) - me * NT;
+    const int r = t - excl;
+    const int ng = (NT + 3) / 4;
+    const int g = min(r / (4 * me), ng - 1);
+    const int r2 = r - 4 * g * me;
+    const int ms = r2 % me, nt = 4 * g + r2 / me;
+    row0 = __shfl(elo, e, 64) + ms * G::BN;
+    rows = min(G::BN, __shfl(ehi, e, 64) - row0);
+    n0 = nt * G::BM;
   }
   // Split-K parts per tile (second product only): the largest split of at
   // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
-  // the partial-tile slots and, counting a partial tile as a quarter, still
-  // leaves about one work item per block.
+  // the partial-tile slots and fewer work items than blocks.
   __device__ __forceinline__ int parts(int grid, int nk) const {
     using SK = SplitK<G>;
     if (tiles <= 0) return 1;
-    const int work = full_tiles + (tiles - full_tiles + 3) / 4;
     int s = 1;
-    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= SK::MAX_SLOTS && work * s < grid) s *= 2;
+    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= SK::MAX_SLOTS && tiles * s < grid) s *= 2;
     return s;
   }
 };
