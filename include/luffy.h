@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUFFY_ABI_VERSION 1
+#define LUFFY_ABI_VERSION 2
 
 typedef enum {
   LUFFY_OK = 0,
@@ -89,6 +89,9 @@ const char* luffy_last_error(void);
  *                             offsets[E] entries are written
  *   offsets    [E+1]  int32   bucket e holds positions offsets[e] ..
  *                             offsets[e+1]-1
+ *   inv_norm   [T] float or NULL   1/|x_t| (0 for a zero row), for
+ *                             luffy_condense: the gate pass reads every
+ *                             row anyway, so the similarity pass need not
  * A slot is (token t, choice j) with id s = j*T + t.  Buckets are stable in
  * s (all first choices in token order, then all second choices); with a
  * capacity the first C slots of a bucket stay and later ones are dropped.
@@ -98,7 +101,7 @@ int luffy_route(const void* x, int T, int d, int dtype,
                 const void* w_gate, const float* b_gate, int E, int k,
                 float capacity_factor,
                 int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
-                int32_t* perm_token, int32_t* offsets,
+                int32_t* perm_token, int32_t* offsets, float* inv_norm,
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
@@ -121,6 +124,8 @@ int luffy_route(const void* x, int T, int d, int dtype,
  *                make the call write nothing past the workspace and leave the
  *                outputs undefined.
  *   threshold    cosine threshold h (a value > 1 disables condensation)
+ *   inv_norm     [T] float, device, or NULL: 1/|x_t| as written by
+ *                luffy_route for the same x; NULL computes the norms here
  * Outputs (device):
  *   rep_of_pos   [T*k] int32  position of the representative of every
  *                             position (representatives map to themselves)
@@ -140,7 +145,7 @@ int luffy_condense(const void* x, int T, int d, int dtype,
                    int E, int k, int max_bucket, float threshold,
                    int32_t* rep_of_pos, int32_t* rep_row,
                    int32_t* rep_offsets, int32_t* rep_token,
-                   void* x_rep, int32_t* degree,
+                   void* x_rep, int32_t* degree, const float* inv_norm,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------

@@ -38,10 +38,10 @@ _SIGS = {
     "luffy_last_error": (ctypes.c_char_p, []),
     "luffy_route_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
     "luffy_route": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_float,
-                             _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+                             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
-                                _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+                                _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_expert_ffn_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                                   _c_int, _c_int, _vp, _vp, _c_size, _vp]),
@@ -124,25 +124,26 @@ def expert_ffn_workspace_size(max_rows: int, E: int, d_ff: int, dtype: int) -> i
 
 
 def luffy_route(x, w_gate, b_gate, k, capacity_factor, topk_idx, topk_gate, slot_pos,
-                perm_token, offsets, workspace, stream=None):
+                perm_token, offsets, workspace, stream=None, inv_norm=None):
     T, d = x.shape
     E = w_gate.shape[0]
     lib = load_library()
     _check(lib.luffy_route(_p(x), T, d, _dtype_code(x), _p(w_gate), _p(b_gate), E, k,
                            float(capacity_factor), _p(topk_idx), _p(topk_gate), _p(slot_pos),
-                           _p(perm_token), _p(offsets), _p(workspace), workspace.numel(),
-                           _stream(stream)), "luffy_route")
+                           _p(perm_token), _p(offsets), _p(inv_norm), _p(workspace),
+                           workspace.numel(), _stream(stream)), "luffy_route")
 
 
 def luffy_condense(x, perm_token, offsets, k, max_bucket, threshold, rep_of_pos, rep_row,
-                   rep_offsets, rep_token, x_rep, degree, workspace, stream=None):
+                   rep_offsets, rep_token, x_rep, degree, workspace, stream=None, inv_norm=None):
     T, d = x.shape
     E = offsets.numel() - 1
     lib = load_library()
     _check(lib.luffy_condense(_p(x), T, d, _dtype_code(x), _p(perm_token), _p(offsets), E, k,
                               max_bucket, float(threshold), _p(rep_of_pos), _p(rep_row),
                               _p(rep_offsets), _p(rep_token), _p(x_rep), _p(degree),
-                              _p(workspace), workspace.numel(), _stream(stream)), "luffy_condense")
+                              _p(inv_norm), _p(workspace), workspace.numel(), _stream(stream)),
+           "luffy_condense")
 
 
 def luffy_expert_ffn(x, row_index, rep_offsets, w1, w2, act, max_rows, y_rep, workspace,
@@ -203,6 +204,7 @@ class LayerBuffers:
     x_rep: Optional[torch.Tensor]
     y_rep: torch.Tensor
     y: torch.Tensor
+    inv_norm: torch.Tensor
     ws_route: torch.Tensor
     ws_condense: torch.Tensor
     ws_ffn: torch.Tensor
@@ -218,11 +220,12 @@ class MoELayer:
 
     def __init__(self, w_gate, b_gate, w1, w2, *, k: int, act: str, threshold: float,
                  capacity_factor: float = 0.0, T: int, keep_degree: bool = True,
-                 gather_x_rep: bool = False):
+                 gather_x_rep: bool = False, norms_from_route: bool = True):
         self.w_gate, self.b_gate, self.w1, self.w2 = w_gate, b_gate, w1, w2
         self.k, self.act, self.h, self.cf = k, act, threshold, capacity_factor
         self.E, self.d_ff, self.d = w1.shape
         self.T = T
+        self.norms_from_route = norms_from_route
         self.dtype = w1.dtype
         dev = w1.device
         S = T * k
@@ -243,6 +246,7 @@ class MoELayer:
             x_rep=torch.empty(S, self.d, dtype=self.dtype, device=dev) if gather_x_rep else None,
             y_rep=torch.empty(S, self.d, dtype=self.dtype, device=dev),
             y=torch.empty(T, self.d, dtype=self.dtype, device=dev),
+            inv_norm=torch.empty(T, dtype=torch.float32, device=dev),
             ws_route=_workspace(route_workspace_size(T, self.E, k), dev),
             ws_condense=_workspace(condense_workspace_size(T, self.d, self.E, k,
                                                            self.max_bucket), dev),
@@ -254,14 +258,14 @@ class MoELayer:
     def route(self, x, stream=None):
         b = self.buf
         luffy_route(x, self.w_gate, self.b_gate, self.k, self.cf, b.topk_idx, b.topk_gate,
-                    b.slot_pos, b.perm_token, b.offsets, b.ws_route, stream)
+                    b.slot_pos, b.perm_token, b.offsets, b.ws_route, stream, inv_norm=b.inv_norm)
 
     def condense(self, x, stream=None, threshold=None):
         b = self.buf
         h = self.h if threshold is None else threshold
         luffy_condense(x, b.perm_token, b.offsets, self.k, self.max_bucket, h, b.rep_of_pos,
                        b.rep_row, b.rep_offsets, b.rep_token, b.x_rep, b.degree, b.ws_condense,
-                       stream)
+                       stream, inv_norm=b.inv_norm if self.norms_from_route else None)
 
     def expert_ffn(self, x, stream=None):
         b = self.buf

@@ -33,6 +33,8 @@
 // absorbed is kept.  Both rules only read final decisions, so rounds may see
 // each other's updates early without changing the result, and every round
 // decides at least the highest-priority undecided position.
+#include <algorithm>
+
 #include "gemm_core.h"
 #include "luffy_common.h"
 
@@ -95,7 +97,9 @@ __device__ __forceinline__ void gram_layout(const int32_t* __restrict__ offsets,
   }
 }
 
-template <bool BF16>
+// NORMS = false: the norms were computed by the caller (luffy_route); only
+// the clearing and the layout run.
+template <bool BF16, bool NORMS>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, int T, int d,
                                                    float* __restrict__ inv_norm, int S,
                                                    int32_t* __restrict__ deg, int32_t* __restrict__ state,
@@ -111,6 +115,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
     state[p] = 0;
     claim[p] = 0ull;
   }
+  if constexpr (!NORMS) return;
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -744,7 +749,7 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
                               int E, int k, int max_bucket, float threshold,
                               int32_t* rep_of_pos, int32_t* rep_row,
                               int32_t* rep_offsets, int32_t* rep_token,
-                              void* x_rep, int32_t* degree,
+                              void* x_rep, int32_t* degree, const float* inv_norm,
                               void* workspace, size_t workspace_bytes, void* stream) {
   if (!x || !perm_token || !offsets || !rep_of_pos || !rep_row || !rep_offsets || !rep_token)
     return fail(LUFFY_E_INVALID, "luffy_condense: null pointer argument");
@@ -771,28 +776,32 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const int S = T * k;
   const bool bf16 = dtype == LUFFY_BF16;
 
-  const int norm_blocks = (T + 3) / 4;
+  // norms from the caller when given (the gate pass already read x)
+  const float* inv_norm_use = inv_norm ? inv_norm : ws.inv_norm;
+  const int norm_blocks = inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
   {
     ProfileScope prof_("norm", s);
     const int tile = bf16 ? kTile : kTileF32;
-    if (bf16)
-      norm_kernel<true><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets,
-                                                    E, max_bucket, tile, ws.cap_words, ws.tile_off, ws.bm_off,
-                                                    ws.err);
-    else
-      norm_kernel<false><<<norm_blocks, 256, 0, s>>>(x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets,
-                                                     E, max_bucket, tile, ws.cap_words, ws.tile_off, ws.bm_off,
-                                                     ws.err);
+#define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
+                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err
+    if (bf16) {
+      if (inv_norm) norm_kernel<true, false><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+      else norm_kernel<true, true><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+    } else {
+      if (inv_norm) norm_kernel<false, false><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+      else norm_kernel<false, true><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+    }
+#undef LUFFY_NORM_ARGS
   }
   {
     ProfileScope prof_("gram", s);
     if (bf16)
       gram_kernel_bf16<<<persistent_grid(), GemmBig64::THREADS, 0, s>>>(
-          static_cast<const uint16_t*>(x), d, perm_token, offsets, E, ws.inv_norm, threshold, ws.tile_off,
+          static_cast<const uint16_t*>(x), d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off,
           ws.bm_off, ws.err, ws.bitmask, ws.deg);
     else
       gram_kernel_f32<<<2 * persistent_grid(), 256, 0, s>>>(
-          static_cast<const float*>(x), d, perm_token, offsets, E, ws.inv_norm, threshold, ws.tile_off,
+          static_cast<const float*>(x), d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off,
           ws.bm_off, ws.err, ws.bitmask, ws.deg);
   }
   const int wave_blocks = (S + 3) / 4;

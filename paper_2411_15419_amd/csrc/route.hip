@@ -40,14 +40,18 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // re-decision of close calls, and the rank of every slot among the chunk's
 // slots of the same expert (wave ballots) with the chunk's per-expert
 // counts.  A chunk is (choice j, chunk c), and chunks in (j, c) order are
-// slots in slot-id order.
+// slots in slot-id order.  With inv_norm set, the sums of squares of the
+// token columns each lane loads are reduced the same way and 1/|x_t| is
+// stored for the similarity pass (0 for a zero row).
 template <bool BF16>
 __global__ __launch_bounds__(256) void gate_kernel(
     const void* __restrict__ xv, const void* __restrict__ wv,
     const float* __restrict__ bias_g, int T, int d, int E, int k,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate,
-    int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done) {
+    int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done,
+    float* __restrict__ inv_norm) {
   __shared__ float part[4][kGateTok][kMaxExperts + 1];
+  __shared__ float sumsq[4][kGateTok];
   __shared__ float bias[kMaxExperts];
   __shared__ int cnt[kMaxExperts];
   __shared__ int choice[kGateTok][2];
@@ -80,6 +84,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const int q = (nsteps + 3) / 4;
     const int s_lo = w * q, s_hi = min(nsteps, s_lo + q);
     constexpr int B = 2;   // K steps per batch
+    float sq[kGateA] = {};   // sum of squares of this lane's token columns
     for (int s0 = s_lo; s0 < s_hi; s0 += B) {
       Pack16 a[B][kGateA], b[B][4];
 #pragma unroll
@@ -101,6 +106,26 @@ __global__ __launch_bounds__(256) void gate_kernel(
           if (j < nE16)
 #pragma unroll
             for (int i = 0; i < kGateA; ++i) acc[i][j] = mfma16x16x32(a[u][i].v, b[u][j].v, acc[i][j]);
+      if (inv_norm) {
+#pragma unroll
+        for (int u = 0; u < B; ++u)
+#pragma unroll
+          for (int i = 0; i < kGateA; ++i)
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+              const float f = bf16_to_f32(a[u][i].h[c]);
+              sq[i] = fmaf(f, f, sq[i]);
+            }
+      }
+    }
+    if (inv_norm) {
+      // the four 8-column pieces of a token row sit in lanes l, l+16, l+32, l+48
+#pragma unroll
+      for (int i = 0; i < kGateA; ++i) {
+        sq[i] += __shfl_xor(sq[i], 16, 64);
+        sq[i] += __shfl_xor(sq[i], 32, 64);
+        if (lane < 16) sumsq[w][16 * i + lane] = sq[i];
+      }
     }
     // lane holds logits of tokens 16i + 4(lane/16) + r, expert 16j + lane%16
 #pragma unroll
@@ -123,8 +148,17 @@ __global__ __launch_bounds__(256) void gate_kernel(
       part[2][lane][e] = 0.f;
       part[3][lane][e] = 0.f;
     }
+    if (inv_norm) {
+      float s = 0.f;
+      for (int i = w; i < d; i += 4) s = fmaf(X[static_cast<size_t>(t) * d + i], X[static_cast<size_t>(t) * d + i], s);
+      sumsq[w][lane] = s;
+    }
   }
   __syncthreads();
+  if (inv_norm && threadIdx.x < kGateTok && t0 + static_cast<int>(threadIdx.x) < T) {
+    const float ss = ((sumsq[0][threadIdx.x] + sumsq[1][threadIdx.x]) + sumsq[2][threadIdx.x]) + sumsq[3][threadIdx.x];
+    inv_norm[t0 + threadIdx.x] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
+  }
   // partial tiles summed in wave order into part[0], one (token, expert)
   // pair per thread at a time
   float (*logit)[kMaxExperts + 1] = part[0];
@@ -371,7 +405,7 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
                            const void* w_gate, const float* b_gate, int E, int k,
                            float capacity_factor,
                            int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
-                           int32_t* perm_token, int32_t* offsets,
+                           int32_t* perm_token, int32_t* offsets, float* inv_norm,
                            void* workspace, size_t workspace_bytes, void* stream) {
   if (!x || !w_gate || !topk_idx || !topk_gate || !slot_pos || !perm_token || !offsets)
     return fail(LUFFY_E_INVALID, "luffy_route: null pointer argument");
@@ -404,10 +438,10 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
     const int chunks = (T + kGateTok - 1) / kGateTok;
     if (dtype == LUFFY_BF16)
       gate_kernel<true><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
-                                               ws.hist, ws.done);
+                                               ws.hist, ws.done, inv_norm);
     else
       gate_kernel<false><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
-                                                ws.hist, ws.done);
+                                                ws.hist, ws.done, inv_norm);
   }
   {
     ProfileScope prof_("slot_scan", s);

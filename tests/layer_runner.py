@@ -36,7 +36,7 @@ def upload(inp):
     return dev
 
 
-def make_layer(inp, dev, h=None, gather_x_rep=False):
+def make_layer(inp, dev, h=None, gather_x_rep=False, norms_from_route=True):
     import paper_2411_15419_amd as L
     cfg = inp.cfg
     w1, w2 = dev["w1"], dev["w2"]
@@ -47,7 +47,7 @@ def make_layer(inp, dev, h=None, gather_x_rep=False):
     return L.MoELayer(dev["w_g"], dev["b_g"], w1, w2, k=cfg.k, act=cfg.act,
                       threshold=cfg.h if h is None else h,
                       capacity_factor=cfg.capacity_factor, T=cfg.T,
-                      gather_x_rep=gather_x_rep)
+                      gather_x_rep=gather_x_rep, norms_from_route=norms_from_route)
 
 
 def fetch(layer, with_ffn=True):
@@ -75,9 +75,9 @@ def fetch(layer, with_ffn=True):
     return out
 
 
-def run_gpu(inp, h=None, with_ffn=True, gather_x_rep=False, dev=None):
+def run_gpu(inp, h=None, with_ffn=True, gather_x_rep=False, dev=None, norms_from_route=True):
     dev = dev or upload(inp)
-    layer = make_layer(inp, dev, h, gather_x_rep)
+    layer = make_layer(inp, dev, h, gather_x_rep, norms_from_route)
     x = dev["x"]
     layer.route(x)
     layer.condense(x, threshold=h)

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.luffy_abi_version() == 1
+    assert lib.luffy_abi_version() == 2
     assert lib.luffy_status_string(0) == b"ok"
     assert lib.luffy_status_string(-3).startswith(b"workspace")
 
@@ -58,28 +58,28 @@ def test_invalid_arguments_rejected_on_host(lib):
     fake = ctypes.c_void_p(256)     # never dereferenced: validation fails first
     # null pointers
     assert lib.luffy_route(None, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
-                           fake, fake, 1 << 20, None) == -1
+                           fake, None, fake, 1 << 20, None) == -1
     # k out of range, k > E
     assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 3, 0.0, fake, fake, fake, fake,
-                           fake, fake, 1 << 20, None) == -1
+                           fake, None, fake, 1 << 20, None) == -1
     assert lib.luffy_route(fake, 8, 64, 1, fake, None, 1, 2, 0.0, fake, fake, fake, fake,
-                           fake, fake, 1 << 20, None) == -1
+                           fake, None, fake, 1 << 20, None) == -1
     # unsupported sizes
     assert lib.luffy_route(fake, 8, 65, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
-                           fake, fake, 1 << 20, None) == -2
+                           fake, None, fake, 1 << 20, None) == -2
     assert lib.luffy_route(fake, 8, 64, 1, fake, None, 65, 1, 0.0, fake, fake, fake, fake,
-                           fake, fake, 1 << 20, None) == -2
+                           fake, None, fake, 1 << 20, None) == -2
     # workspace too small / misaligned
     assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
-                           fake, fake, 0, None) == -3
+                           fake, None, fake, 0, None) == -3
     assert lib.luffy_route(fake, 8, 64, 1, fake, None, 4, 1, 0.0, fake, fake, fake, fake,
-                           fake, ctypes.c_void_p(260), 1 << 20, None) == -3
+                           fake, None, ctypes.c_void_p(260), 1 << 20, None) == -3
     assert b"workspace" in lib.luffy_last_error()
     # condense: NaN threshold, bad dtype
     assert lib.luffy_condense(fake, 8, 64, 1, fake, fake, 4, 1, 8, float("nan"), fake, fake,
-                              fake, fake, None, None, fake, 1 << 30, None) == -1
+                              fake, fake, None, None, None, fake, 1 << 30, None) == -1
     assert lib.luffy_condense(fake, 8, 64, 7, fake, fake, 4, 1, 8, 0.9, fake, fake,
-                              fake, fake, None, None, fake, 1 << 30, None) == -1
+                              fake, fake, None, None, None, fake, 1 << 30, None) == -1
     # ffn: unknown activation, d_ff not a multiple of 64
     assert lib.luffy_expert_ffn(fake, None, fake, 4, 64, 128, 1, fake, fake, 9, 8, fake,
                                 fake, 1 << 30, None) == -1

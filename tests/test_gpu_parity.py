@@ -160,6 +160,17 @@ def test_deterministic_indices():
     assert np.array_equal(a["y"], b["y"])
 
 
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_norms_computed_by_condense(name):
+    # luffy_condense computing the norms itself (no inv_norm from luffy_route)
+    inp = G.make_inputs(name, seed=0, **REDUCED[name])
+    g = run_gpu(inp, norms_from_route=False)
+    o = run_oracle(inp)
+    assert_route_equal(g, o)
+    assert_condense_equal(g, o)
+    assert_output_close(g, o, inp.cfg.dtype)
+
+
 def test_gathered_rows_path_matches():
     inp = G.make_inputs("c2", seed=0, **REDUCED["c2"])
     g = run_gpu(inp, gather_x_rep=True)
