@@ -233,41 +233,62 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
 // Sums the split parts of every output tile in part order and stores bf16.
 // Recomputes the same tile map and split count, so it does nothing when the
 // product was not split.  Partial tiles are in the accumulator layout of the
-// product kernel: float4 unit u = ((w*FM + fm)*FN + fn)*4 + g of lane l holds
+// product kernel: float4 unit ((w*FM + fm)*FN + fn)*4 + g of lane l holds
 // acc[fm][fn][4g..4g+3] of wave w, i.e. four consecutive output columns of
-// one token row.
+// one token row.  Each thread takes one (w, fm, fn, l): 16 columns of a
+// 32-column block of one row, lanes l and l+32 sharing the row; they swap
+// halves so that each stores 16 consecutive bf16 (two 16-byte stores).
 template <class G>
 __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __restrict__ rep_offsets, int E,
                                                                int K, int N, const float* __restrict__ split_slots,
                                                                uint16_t* __restrict__ out, int grid_parts) {
   using SK = SplitK<G>;
-  constexpr int UNITS = G::NWAVES * G::FM * G::FN * 4 * 64;   // float4 per tile
+  constexpr int LANES = G::NWAVES * G::FM * G::FN * 64;   // (w, fm, fn, lane) per tile
+  constexpr int PER_TILE = LANES / 256;                    // blocks per tile
+  static_assert(LANES % 256 == 0, "reduction blocks");
   const FfnTiles<G> map(rep_offsets, E, N);
   const int S = map.parts(grid_parts, K / G::BK);
   if (S == 1) return;
-  const long long total = static_cast<long long>(map.tiles) * UNITS;
-  for (long long i = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x; i < total;
-       i += static_cast<long long>(gridDim.x) * 256) {
-    const int t = static_cast<int>(i / UNITS);          // wave-uniform: UNITS is a multiple of 64
-    const int u = static_cast<int>(i - static_cast<long long>(t) * UNITS);
+  const int l = threadIdx.x & 63, hi = l >> 5;
+  for (int b = blockIdx.x; b < map.tiles * PER_TILE; b += gridDim.x) {
+    const int t = b / PER_TILE;
+    const int q = ((b - t * PER_TILE) * 256 + threadIdx.x) >> 6;   // (w*FM + fm)*FN + fn
     int e, row0, rows, n0;
     map.decode(t, E, e, row0, rows, n0);
-    const int l = u & 63, g = (u >> 6) & 3, q = u >> 8;
     const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
     const int ml = G::q_row(G::wave_n(w), fn) + (l & 31);
-    const int nl = G::wave_m(w) * G::WTM + 32 * fm + 8 * g + 4 * (l >> 5);
-    if (ml >= rows || n0 + nl >= N) continue;
-    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS + static_cast<size_t>(u) * 4;
+    const int nb = G::wave_m(w) * G::WTM + 32 * fm;   // first column of the 32-column block
+    if (ml >= rows || n0 + nb >= N) continue;          // same for lanes l and l+32
+    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS +
+                       static_cast<size_t>(q) * 4 * 256 + l * 4;
     float4 v[4];
 #pragma unroll
-    for (int p = 0; p < 4; ++p)
-      if (p < S) v[p] = *reinterpret_cast<const float4*>(src + p * SK::SLOT_FLOATS);
-    float4 sum = v[0];
+    for (int g = 0; g < 4; ++g) {
+      v[g] = *reinterpret_cast<const float4*>(src + g * 256);
 #pragma unroll
-    for (int p = 1; p < 4; ++p)
-      if (p < S) { sum.x += v[p].x; sum.y += v[p].y; sum.z += v[p].z; sum.w += v[p].w; }
-    *reinterpret_cast<uint2*>(out + static_cast<size_t>(row0 + ml) * N + n0 + nl) =
-        make_uint2(pack_bf16x2(sum.x, sum.y), pack_bf16x2(sum.z, sum.w));
+      for (int p = 1; p < 4; ++p)
+        if (p < S) {
+          const float4 u = *reinterpret_cast<const float4*>(src + p * SK::SLOT_FLOATS + g * 256);
+          v[g].x += u.x; v[g].y += u.y; v[g].z += u.z; v[g].w += u.w;
+        }
+    }
+    // lane l (< 32) holds columns 8g..8g+3, lane l+32 columns 8g+4..8g+7:
+    // the low lane keeps columns 0..15, the high lane 16..31
+    float4 send[2] = {hi ? v[0] : v[2], hi ? v[1] : v[3]};
+    float4 recv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      recv[i].x = __shfl_xor(send[i].x, 32, 64);
+      recv[i].y = __shfl_xor(send[i].y, 32, 64);
+      recv[i].z = __shfl_xor(send[i].z, 32, 64);
+      recv[i].w = __shfl_xor(send[i].w, 32, 64);
+    }
+    const float4 c[4] = {hi ? recv[0] : v[0], hi ? v[2] : recv[0], hi ? recv[1] : v[1], hi ? v[3] : recv[1]};
+    uint4* dst = reinterpret_cast<uint4*>(out + static_cast<size_t>(row0 + ml) * N + n0 + nb + 16 * hi);
+    dst[0] = make_uint4(pack_bf16x2(c[0].x, c[0].y), pack_bf16x2(c[0].z, c[0].w), pack_bf16x2(c[1].x, c[1].y),
+                        pack_bf16x2(c[1].z, c[1].w));
+    dst[1] = make_uint4(pack_bf16x2(c[2].x, c[2].y), pack_bf16x2(c[2].z, c[2].w), pack_bf16x2(c[3].x, c[3].y),
+                        pack_bf16x2(c[3].z, c[3].w));
   }
 }
 
