@@ -83,29 +83,31 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const int nsteps = d / 32;
     const int q = (nsteps + 3) / 4;
     const int s_lo = w * q, s_hi = min(nsteps, s_lo + q);
-    constexpr int B = 2;   // K steps per batch
+    constexpr int B = 2;   // K steps per batch; the next batch is loaded while one is multiplied
     float sq[kGateA] = {};   // sum of squares of this lane's token columns
-    for (int s0 = s_lo; s0 < s_hi; s0 += B) {
-      Pack16 a[B][kGateA], b[B][4];
+    Pack16 a[2][B][kGateA], b[2][B][4];
+    auto load = [&](int s0, Pack16 (&aa)[B][kGateA], Pack16 (&bb)[B][4]) {
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         const int st = s0 + u;
         const bool in = st < s_hi;
 #pragma unroll
         for (int i = 0; i < kGateA; ++i)
-          a[u][i].u4 = in ? *reinterpret_cast<const uint4*>(arow[i] + 32 * st) : make_uint4(0, 0, 0, 0);
+          aa[u][i].u4 = in ? *reinterpret_cast<const uint4*>(arow[i] + 32 * st) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          b[u][j].u4 = (in && j < nE16) ? *reinterpret_cast<const uint4*>(brow[j] + 32 * st)
-                                        : make_uint4(0, 0, 0, 0);
+          bb[u][j].u4 = (in && j < nE16) ? *reinterpret_cast<const uint4*>(brow[j] + 32 * st)
+                                         : make_uint4(0, 0, 0, 0);
       }
+    };
+    auto compute = [&](const Pack16 (&aa)[B][kGateA], const Pack16 (&bb)[B][4]) {
 #pragma unroll
       for (int u = 0; u < B; ++u)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           if (j < nE16)
 #pragma unroll
-            for (int i = 0; i < kGateA; ++i) acc[i][j] = mfma16x16x32(a[u][i].v, b[u][j].v, acc[i][j]);
+            for (int i = 0; i < kGateA; ++i) acc[i][j] = mfma16x16x32(aa[u][i].v, bb[u][j].v, acc[i][j]);
       if (inv_norm) {
 #pragma unroll
         for (int u = 0; u < B; ++u)
@@ -113,10 +115,19 @@ __global__ __launch_bounds__(256) void gate_kernel(
           for (int i = 0; i < kGateA; ++i)
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
-              const float f = bf16_to_f32(a[u][i].h[c]);
+              const float f = bf16_to_f32(aa[u][i].h[c]);
               sq[i] = fmaf(f, f, sq[i]);
             }
       }
+    };
+    if (s_lo < s_hi) load(s_lo, a[0], b[0]);
+    // unrolled by two so that both register sets are indexed statically
+    for (int s0 = s_lo; s0 < s_hi; s0 += 2 * B) {
+      if (s0 + B < s_hi) load(s0 + B, a[1], b[1]);
+      compute(a[0], b[0]);
+      if (s0 + B >= s_hi) break;
+      if (s0 + 2 * B < s_hi) load(s0 + 2 * B, a[0], b[0]);
+      compute(a[1], b[1]);
     }
     if (inv_norm) {
       // the four 8-column pieces of a token row sit in lanes l, l+16, l+32, l+48
