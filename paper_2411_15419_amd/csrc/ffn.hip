@@ -112,7 +112,7 @@ struct FfnTiles {
       const int v = __shfl_up(incl, o, 64);
       if (lane >= o) incl += v;
     }
-    tiles = __shfl(incl, 63, 64);
+    tiles = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
   }
   // Tile t -> expert e, first token row row0, row count, first output n0.
   __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0) const {
@@ -125,9 +125,11 @@ struct FfnTiles {
     const int g = min(r / (4 * me), ng - 1);
     const int r2 = r - 4 * g * me;
     const int ms = r2 % me, nt = 4 * g + r2 / me;
-    row0 = __shfl(elo, e, 64) + ms * G::BN;
-    rows = min(G::BN, __shfl(ehi, e, 64) - row0);
-    n0 = nt * G::BM;
+    // shuffles return vector registers: made scalar again so that the
+    // buffer resources built from them stay in scalar registers
+    row0 = __builtin_amdgcn_readfirstlane(__shfl(elo, e, 64) + ms * G::BN);
+    rows = __builtin_amdgcn_readfirstlane(min(G::BN, __shfl(ehi, e, 64) - row0));
+    n0 = __builtin_amdgcn_readfirstlane(nt * G::BM);
   }
   // Split-K parts per tile (second product only): the largest split of at
   // most 4 (each part >= 4 K-stages) that keeps every tile's parts within

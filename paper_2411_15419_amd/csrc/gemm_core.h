@@ -116,9 +116,16 @@ struct GemmK64 {
   // memory (robust buffer access), which is how rows past the valid ones
   // of a partial tile are skipped.  Valid rows need offset + K*2 <= kRange
   // (operands below 4 GiB - 64 KiB, K <= 32768).
+  // The base is read from the first lane (it is wave-uniform by contract),
+  // so the resource lives in scalar registers even when the compiler cannot
+  // prove uniformity; a resource in vector registers would wrap every DMA
+  // instruction in a readfirstlane loop.
   static constexpr uint32_t kRange = 0xFFFF0000u;
   static __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+    const uint64_t v = reinterpret_cast<uint64_t>(base);
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v)));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32)));
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>((hi << 32) | lo), static_cast<short>(0),
                                              static_cast<int>(kRange), 0x00020000);
   }
 
