@@ -177,7 +177,10 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
   const int nk = K / G::BK;
   const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
   const int total = map.tiles * S;
-  for (int tt = xcd_virtual_block(); tt < total; tt += gridDim.x) {
+  const int vb = xcd_virtual_block();
+  for (int round = 0; round * static_cast<int>(gridDim.x) < total; ++round) {
+    const int tt = serpentine_item(round, vb);
+    if (tt >= total) continue;
     const int t = tt / S, part = tt - t * S;
     int e, row0, rows, n0;
     map.decode(t, E, e, row0, rows, n0);

@@ -47,10 +47,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 // which lets L2-resident operands stream into LDS at roughly twice the rate.
 // The eight 16-byte chunks of row r are stored XOR-permuted by (r >> 1) & 7,
 // so the 16 lanes of a fragment read (16 consecutive rows, one chunk) hit 16
-// distinct bank groups.  Fragments are double-buffered per half stage (two
-// 16-wide K steps): while one half is multiplied the other is read from LDS,
-// and the DMA of stage kt+2 is issued in the middle of stage kt, once every
-// wave has read stage kt's second half.  K must be a multiple of 64.
+// distinct bank groups.  Fragments are double-buffered per 16-wide K step
+// (see run) and the DMA of stage kt+2 is issued once every wave has read
+// stage kt.  K must be a multiple of 64.
 //
 // Wave placement: MFAST puts the P-block index fastest (wm = w % WM), so
 // with WM = 4 each SIMD holds one P quarter of every Q part; QIL
@@ -155,45 +154,58 @@ struct GemmK64 {
     }
   }
 
+  // Fragments of one 16-wide K step (chunks 2*step and 2*step+1 of every
+  // row: lanes 0-31 take the low chunk, lanes 32-63 the high one).
   struct Frags {
-    bf16x8 a[2][FM], b[2][FN];
+    bf16x8 a[FM], b[FN];
   };
 
-  // Half stage h (K steps 2h, 2h+1 of 16) of the first NQ Q blocks.
-  template <int NQ = FN>
-  static __device__ __forceinline__ void read_frags(lds_ptr S, int prow0, int qrow0, int half, int sw, int h,
-                                                    Frags& f) {
+  // K step `step` (0..3) of the stage at S, first NQ Q blocks.
+  template <int NQ>
+  static __device__ __forceinline__ void read_step(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
+                                                   Frags& f) {
     if constexpr (NQ > 0) {
+      const int pc = ((2 * step + half) ^ sw) * 16;
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int pc = ((2 * (2 * h + kk) + half) ^ sw) * 16;
+      for (int i = 0; i < FM; ++i)
+        f.a[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + prow0 + 32 * i * ROW_BYTES +
+                                                                                      pc);
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
-          f.a[kk][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
-              S + prow0 + 32 * i * ROW_BYTES + pc);
-#pragma unroll
-        for (int j = 0; j < NQ; ++j)
-          f.b[kk][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(
-              S + qrow0 + QSTEP * j * ROW_BYTES + pc);
-      }
+      for (int j = 0; j < NQ; ++j)
+        f.b[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + qrow0 +
+                                                                                      QSTEP * j * ROW_BYTES + pc);
     }
   }
 
-  template <int NQ = FN>
-  static __device__ __forceinline__ void mma(const Frags& f, Acc& acc) {
+  template <int NQ>
+  static __device__ __forceinline__ void mma_step(const Frags& f, Acc& acc) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < NQ; ++j) acc[i][j] = mfma32x32x16(f.a[kk][i], f.b[kk][j], acc[i][j]);
+      for (int j = 0; j < NQ; ++j) acc[i][j] = mfma32x32x16(f.a[i], f.b[j], acc[i][j]);
   }
 
-  // Interleave of one half stage: MFMAs paired first with the NVM buffer
-  // loads, then with the LDS reads; leftovers after the last MFMA.
-  template <int NQ, int NVM>
-  static __device__ __forceinline__ void interleave() {
-    constexpr int NMF = FM * NQ * 2, NDS = NQ > 0 ? (FM + NQ) * 2 : 0;
+  // Schedule of a step without buffer loads: the LDS reads of the next step
+  // go out two per MFMA from the first MFMA on, so they have landed when the
+  // next step starts.
+  template <int NQ>
+  static __device__ __forceinline__ void interleave_reads() {
+    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? FM + NQ : 0;
+#pragma unroll
+    for (int i = 0; i < NMF; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      if (2 * i + 1 < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+      else if (2 * i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (NDS > 2 * NMF) __builtin_amdgcn_sched_group_barrier(0x100, NDS - 2 * NMF, 0);
+  }
+
+  // Schedule of the step after the barrier: the buffer loads of stage kt+2
+  // go out first (one per MFMA), then the LDS reads; their latency is the
+  // longer one.
+  template <int NQ>
+  static __device__ __forceinline__ void interleave_loads() {
+    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? FM + NQ : 0, NVM = LOADS;
     constexpr int PV = NMF < NVM ? NMF : NVM;
     constexpr int PD = (NMF - PV) < NDS ? (NMF - PV) : NDS;
 #pragma unroll
@@ -203,8 +215,8 @@ struct GemmK64 {
     }
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     if constexpr (NMF > PV + PD) __builtin_amdgcn_sched_group_barrier(0x008, NMF - PV - PD, 0);
     if constexpr (NVM > PV) __builtin_amdgcn_sched_group_barrier(0x020, NVM - PV, 0);
@@ -219,10 +231,13 @@ struct GemmK64 {
   // may be reused.  NQ: the wave multiplies only its first NQ Q blocks;
   // every wave still issues its share of the loads and takes every barrier.
   //
-  // Stage kt (buffer kt % 2): [A] read half 1 of stage kt while multiplying
-  // half 0; [B] wait for stage kt+1 and for this wave's reads, barrier (all
-  // waves are done with buffer kt % 2), issue the DMA of stage kt+2 into it,
-  // read half 0 of stage kt+1 while multiplying half 1 of stage kt.
+  // Fragments are double-buffered per 16-wide K step (fa, fb): while the
+  // MFMAs of step s run, the fragments of step s+1 are read.  Stage kt
+  // (buffer kt % 2): steps 0-2 read steps 1-3; then wait for stage kt+1 and
+  // for this wave's reads, barrier (every wave is done with buffer kt % 2),
+  // issue the DMA of stage kt+2 into it and read step 0 of stage kt+1 while
+  // step 3 is multiplied.  Holding one step per buffer (not two) keeps the
+  // FFN tile within 256 registers per lane without register reuse stalls.
   template <int NQ = FN>
   static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase, const uint32_t (&poff)[LP],
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
@@ -247,40 +262,52 @@ struct GemmK64 {
     const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
     const int qrow0 = (BM + q_row(wn, 0) + (lane & 31)) * ROW_BYTES;
     const int half = lane >> 5;
-    Frags f0, f1;
-    read_frags<NQ>(lds, prow0, qrow0, half, sw, 0, f0);
+    Frags fa, fb;
+    read_step<NQ>(lds, prow0, qrow0, half, sw, 0, fa);
     int kt = 0;
     // steady state: stage kt+2 exists
     for (; kt + 2 < nk; ++kt) {
       const lds_ptr cur = lds + (kt & 1) * STAGE_BYTES;
       const lds_ptr nxt = lds + ((kt + 1) & 1) * STAGE_BYTES;
       __builtin_amdgcn_sched_barrier(0);
-      read_frags<NQ>(cur, prow0, qrow0, half, sw, 1, f1);
-      mma<NQ>(f0, acc);
-      interleave<NQ, 0>();
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 1, fb);
+      mma_step<NQ>(fa, acc);
+      interleave_reads<NQ>();
+      __builtin_amdgcn_sched_barrier(0);
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 2, fa);
+      mma_step<NQ>(fb, acc);
+      interleave_reads<NQ>();
+      __builtin_amdgcn_sched_barrier(0);
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 3, fb);
+      mma_step<NQ>(fa, acc);
+      interleave_reads<NQ>();
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<0>();                      // stage kt+1 landed (this wave's part)
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
       raw_barrier();
       __builtin_amdgcn_sched_barrier(0);
       issue(prs, qrs, goff, (kt + 2) * BK, cur, w);
-      read_frags<NQ>(nxt, prow0, qrow0, half, sw, 0, f0);
-      mma<NQ>(f1, acc);
-      interleave<NQ, LOADS>();
+      read_step<NQ>(nxt, prow0, qrow0, half, sw, 0, fa);
+      mma_step<NQ>(fb, acc);
+      interleave_loads<NQ>();
       __builtin_amdgcn_sched_barrier(0);
     }
     // last one or two stages: nothing more to issue
     for (; kt < nk; ++kt) {
       const lds_ptr cur = lds + (kt & 1) * STAGE_BYTES;
-      read_frags<NQ>(cur, prow0, qrow0, half, sw, 1, f1);
-      mma<NQ>(f0, acc);
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 1, fb);
+      mma_step<NQ>(fa, acc);
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 2, fa);
+      mma_step<NQ>(fb, acc);
+      read_step<NQ>(cur, prow0, qrow0, half, sw, 3, fb);
+      mma_step<NQ>(fa, acc);
       if (kt + 1 < nk) {
         wait_vmcnt<0>();
         __builtin_amdgcn_s_waitcnt(0xC07F);
         raw_barrier();
-        read_frags<NQ>(lds + ((kt + 1) & 1) * STAGE_BYTES, prow0, qrow0, half, sw, 0, f0);
+        read_step<NQ>(lds + ((kt + 1) & 1) * STAGE_BYTES, prow0, qrow0, half, sw, 0, fa);
       }
-      mma<NQ>(f1, acc);
+      mma_step<NQ>(fb, acc);
     }
     __syncthreads();
   }
@@ -318,6 +345,17 @@ __device__ __forceinline__ int xcd_virtual_block() {
   const int g = gridDim.x, b = blockIdx.x;
   if (g % kXcds) return b;
   return (b % kXcds) * (g / kXcds) + b / kXcds;
+}
+
+// Work item of round r of a persistent block with virtual id vb: rounds
+// alternate direction, so a block that drew one of the first items of a
+// round draws one of the last of the next.  With tiles of two alternating
+// kinds (a full and a partial token tile per weight tile) every block then
+// gets one of each instead of two of the same.  Every item below total is
+// visited exactly once.
+__device__ __forceinline__ int serpentine_item(int round, int vb) {
+  const int g = gridDim.x;
+  return round * g + ((round & 1) ? g - 1 - vb : vb);
 }
 
 }  // namespace luffy
