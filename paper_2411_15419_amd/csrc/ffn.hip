@@ -1,15 +1,16 @@
 // luffy_expert_ffn: grouped FFN over the representatives of every expert,
 //   H = act(X_rep W1_e^T)   (rounded to the element type)
 //   Y = H W2_e^T
-// Row counts per expert live on the device.  The grid is sized from the
-// upper bound ceil(max_rows/BN) + E row tiles; each block finds its expert
-// and row range from rep_offsets and exits when it has none.
+// Row counts per expert live on the device: the bf16 kernels are persistent
+// (one block per CU) and find their tiles from rep_offsets; the fp32 grid
+// is sized from the upper bound ceil(max_rows/64) + E row tiles and blocks
+// without a tile exit.
 //
-// bf16: 256 x 256 MFMA tiles (GemmRagged64).  The weight rows are the P
-// operand and the token rows the Q operand, so each lane ends with groups of
-// four consecutive output columns of one row and stores each as one 8-byte
-// word.  The last row tile of an expert usually holds fewer than 256 rows;
-// its waves skip the MFMAs of the missing rows.
+// bf16: MFMA tiles of 256 weight rows by 256 or 320 token rows.  The weight
+// rows are the P operand and the token rows the Q operand, so each lane
+// ends with groups of four consecutive output columns of one row and stores
+// each as one 8-byte word.  The last row tile of an expert usually holds
+// fewer rows; its waves skip the MFMAs of the missing rows.
 // fp32: 64 x 64 tiles of plain FMA (4 x 4 per thread).
 #include "gemm_core.h"
 #include "luffy_common.h"
@@ -86,25 +87,45 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
   return true;
 }
 
+// Tile shapes of the bf16 products: 256 output columns (weight rows, the P
+// operand) by up to 256 token rows (FfnGemm), or by up to 320 token rows
+// (FfnGemmWide).  A tile streams its 256 weight rows once per token tile, so
+// an expert whose row count lies in (256, 320] (or (512, 640], ...) needs one
+// weight pass fewer with the wide shape; every other expert keeps the
+// narrow shape, whose main loop runs a few percent faster (fewer registers,
+// smaller stages).  Both shapes share the block size, the LDS buffer and the
+// split-K slots.
+using FfnGemm = GemmRagged64;
+using FfnGemmWide = GemmK64<256, 320, 4, 2, true, false>;
+static_assert(FfnGemm::BM == FfnGemmWide::BM && FfnGemm::THREADS == FfnGemmWide::THREADS, "shared tile map");
+constexpr int kFfnLds = FfnGemmWide::LDS_BYTES > FfnGemm::LDS_BYTES ? FfnGemmWide::LDS_BYTES : FfnGemm::LDS_BYTES;
+// split-K partial tiles: one slot (the accumulators of a tile in register
+// layout) per work item, at most kFfnMaxSlots (>= CUs) work items
+constexpr int kFfnMaxSlots = 512;
+constexpr size_t kFfnSlotFloats = static_cast<size_t>(FfnGemm::BM) * FfnGemmWide::BN;
+
 // Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
-// expert per lane, E <= 64).  An output tile is 256 output columns (weight
-// rows, the P operand) by up to 256 token rows (the Q operand); the last row
-// tile of an expert is usually partial.  Tiles are numbered expert by
-// expert; inside an expert, output-column tiles come in groups of 4 with the
-// row tiles major inside a group, so the tiles that share a weight tile run
-// side by side and ~32 consecutive tiles (one XCD's share of a round, with
-// the XCD-aware block numbering) span few weight and token rows.
-template <class G>
+// expert per lane, E <= 64).  Expert e's rows are cut into tiles of rt_e
+// rows (256, or 320 where that takes fewer tiles); the last one is usually
+// partial.  Tiles are numbered expert by expert; inside an expert,
+// output-column tiles come in groups of 4 with the row tiles fastest inside
+// a group, so the tiles that share a weight tile run side by side and ~32
+// consecutive tiles (one XCD's share of a round, with the XCD-aware block
+// numbering) span few weight and token rows.
 struct FfnTiles {
-  int elo, ehi, mt, incl, NT, tiles;
+  int elo, ehi, rt, mt, incl, NT, tiles;
   __device__ __forceinline__ FfnTiles(const int32_t* __restrict__ rep_offsets, int E, int N) {
     const int lane = threadIdx.x & 63;
-    NT = (N + G::BM - 1) / G::BM;
+    NT = (N + FfnGemm::BM - 1) / FfnGemm::BM;
     elo = ehi = mt = 0;
+    rt = FfnGemm::BN;
     if (lane < E) {
       elo = rep_offsets[lane];
       ehi = rep_offsets[lane + 1];
-      mt = (ehi - elo + G::BN - 1) / G::BN;
+      const int n = ehi - elo;
+      constexpr int NB = FfnGemm::BN, WB = FfnGemmWide::BN;
+      rt = (n + WB - 1) / WB < (n + NB - 1) / NB ? WB : NB;
+      mt = (n + rt - 1) / rt;
     }
     incl = mt * NT;
 #pragma unroll
@@ -114,8 +135,9 @@ struct FfnTiles {
     }
     tiles = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
   }
-  // Tile t -> expert e, first token row row0, row count, first output n0.
-  __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0) const {
+  // Tile t -> expert e, first token row row0, row count, first output n0,
+  // and whether it is a wide tile.
+  __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0, bool& wide) const {
     const int lane = threadIdx.x & 63;
     e = __popcll(__ballot(lane < E && incl <= t));
     const int me = __shfl(mt, e, 64);
@@ -127,18 +149,19 @@ struct FfnTiles {
     const int ms = r2 % me, nt = 4 * g + r2 / me;
     // shuffles return vector registers: made scalar again so that the
     // buffer resources built from them stay in scalar registers
-    row0 = __builtin_amdgcn_readfirstlane(__shfl(elo, e, 64) + ms * G::BN);
-    rows = __builtin_amdgcn_readfirstlane(min(G::BN, __shfl(ehi, e, 64) - row0));
-    n0 = __builtin_amdgcn_readfirstlane(nt * G::BM);
+    const int rte = __builtin_amdgcn_readfirstlane(__shfl(rt, e, 64));
+    row0 = __builtin_amdgcn_readfirstlane(__shfl(elo, e, 64) + ms * rte);
+    rows = __builtin_amdgcn_readfirstlane(min(rte, __shfl(ehi, e, 64) - row0));
+    n0 = __builtin_amdgcn_readfirstlane(nt * FfnGemm::BM);
+    wide = rte == FfnGemmWide::BN;
   }
   // Split-K parts per tile (second product only): the largest split of at
   // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
   // the partial-tile slots and fewer work items than blocks.
   __device__ __forceinline__ int parts(int grid, int nk) const {
-    using SK = SplitK<G>;
     if (tiles <= 0) return 1;
     int s = 1;
-    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= SK::MAX_SLOTS && tiles * s < grid) s *= 2;
+    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= kFfnMaxSlots && tiles * s < grid) s *= 2;
     return s;
   }
 };
@@ -157,24 +180,78 @@ __device__ __forceinline__ void run_nq(int nq, const uint16_t* pbase, const uint
   }
 }
 
+// One output tile (or one K part of it) of shape G: rows row0.. of A
+// (through row_index when given) times the weight rows n0.. of We over K
+// range [k0, k1).  Stores bf16 (activation applied when FIRST), or, when
+// slot is given, the float32 accumulators in register layout: float4 unit
+// ((w*FM + fm)*FN + fn)*4 + g of lane l holds acc[fm][fn][4g..4g+3].
+template <class G, int ACT, bool FIRST>
+__device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
+                                         const uint16_t* __restrict__ We, int K, int N, int k0, int k1, int row0,
+                                         int rows, int n0, uint16_t* __restrict__ out, float* __restrict__ slot,
+                                         uint8_t* lds) {
+  static_assert(G::FN <= 5, "ragged dispatch instantiates FN + 1 main loops");
+  const int tid = opaque_tid(), lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = G::wave_m(w), wn = G::wave_n(w);
+  uint32_t poff[G::LP], qoff[G::LQ];
+#pragma unroll
+  for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
+#pragma unroll
+  for (int j = 0; j < G::LQ; ++j) {
+    const int m = row0 + min(G::load_row(G::LP + j) - G::BM, rows - 1);
+    qoff[j] = static_cast<uint32_t>(row_index ? row_index[m] : m) * K;
+  }
+  const int nq = G::active_q(wn, rows);
+  typename G::Acc acc;
+  G::zero(acc);
+  run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, N - n0, rows, lds,
+                   acc);
+#pragma unroll
+  for (int fm = 0; fm < G::FM; ++fm) {
+#pragma unroll
+    for (int fn = 0; fn < G::FN; ++fn) {
+      const int ml = G::q_row(wn, fn) + (lane & 31);
+      if (ml >= rows) continue;
+      uint16_t* orow = out + static_cast<size_t>(row0 + ml) * N;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int nl = wm * G::WTM + 32 * fm + 8 * g + 4 * (lane >> 5);
+        const int n = n0 + nl;
+        if (n >= N) continue;
+        if (slot) {
+          // partial tiles keep the accumulator layout: 1 KB per store
+          // instruction; the reduction maps it back to rows and columns
+          const int u = ((w * G::FM + fm) * G::FN + fn) * 4 + g;
+          *reinterpret_cast<float4*>(slot + u * 256 + lane * 4) =
+              make_float4(acc[fm][fn][4 * g], acc[fm][fn][4 * g + 1], acc[fm][fn][4 * g + 2],
+                          acc[fm][fn][4 * g + 3]);
+          continue;
+        }
+        float z[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          z[q] = acc[fm][fn][4 * g + q];
+          if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
+        }
+        *reinterpret_cast<uint2*>(orow + n) = make_uint2(pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3]));
+      }
+    }
+  }
+}
+
 // One product of the FFN for every tile of every expert (persistent).
 // The second product (FIRST = false) has few output columns (d); with few
 // representatives it can have fewer tiles than CUs, and it then splits K
 // (decided on the device from the actual tile count): parts store float32
 // partial tiles and ffn_split_reduce_kernel finishes them.
-template <class G, int ACT, bool FIRST>
-__global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
+template <int ACT, bool FIRST>
+__global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
     const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots) {
-  using SK = SplitK<G>;
-  // P = weight rows (outputs n), Q = token rows (m)
-  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = G::wave_m(w), wn = G::wave_n(w);
-  static_assert(G::FN <= 4, "ragged dispatch instantiates FN + 1 main loops");
-  const FfnTiles<G> map(rep_offsets, E, N);
-  const int nk = K / G::BK;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kFfnLds];
+  const FfnTiles map(rep_offsets, E, N);
+  const int nk = K / FfnGemm::BK;
   const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
   const int total = map.tiles * S;
   const int vb = xcd_virtual_block();
@@ -183,117 +260,90 @@ __global__ __launch_bounds__(G::THREADS) void ffn_kernel_bf16(
     if (tt >= total) continue;
     const int t = tt / S, part = tt - t * S;
     int e, row0, rows, n0;
-    map.decode(t, E, e, row0, rows, n0);
+    bool wide;
+    map.decode(t, E, e, row0, rows, n0, wide);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
-    uint32_t poff[G::LP], qoff[G::LQ];
-#pragma unroll
-    for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
-#pragma unroll
-    for (int j = 0; j < G::LQ; ++j) {
-      const int m = row0 + min(G::load_row(G::LP + j) - G::BM, rows - 1);
-      qoff[j] = static_cast<uint32_t>(row_index ? row_index[m] : m) * K;
-    }
-    // K range of this part, in whole 32-wide stages
-    const int k0 = (part * nk / S) * G::BK, k1 = ((part + 1) * nk / S) * G::BK;
-    const int nq = G::active_q(wn, rows);
-    typename G::Acc acc;
-    G::zero(acc);
-    run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, N - n0, rows, lds,
-                     acc);
-    float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * SK::SLOT_FLOATS : nullptr;
-#pragma unroll
-    for (int fm = 0; fm < G::FM; ++fm) {
-#pragma unroll
-      for (int fn = 0; fn < G::FN; ++fn) {
-        const int ml = G::q_row(wn, fn) + (lane & 31);
-        if (ml >= rows) continue;
-        uint16_t* orow = out + static_cast<size_t>(row0 + ml) * N;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int nl = wm * G::WTM + 32 * fm + 8 * g + 4 * (lane >> 5);
-          const int n = n0 + nl;
-          if (n >= N) continue;
-          if (slot) {
-            // partial tiles keep the accumulator layout: 1 KB per store
-            // instruction; the reduction maps it back to rows and columns
-            const int u = ((w * G::FM + fm) * G::FN + fn) * 4 + g;
-            *reinterpret_cast<float4*>(slot + u * 256 + lane * 4) =
-                make_float4(acc[fm][fn][4 * g], acc[fm][fn][4 * g + 1], acc[fm][fn][4 * g + 2],
-                            acc[fm][fn][4 * g + 3]);
-            continue;
-          }
-          float z[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            z[q] = acc[fm][fn][4 * g + q];
-            if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
-          }
-          *reinterpret_cast<uint2*>(orow + n) = make_uint2(pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3]));
-        }
-      }
-    }
+    // K range of this part, in whole 64-wide stages
+    const int k0 = (part * nk / S) * FfnGemm::BK, k1 = ((part + 1) * nk / S) * FfnGemm::BK;
+    float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
+    if (wide)
+      ffn_tile<FfnGemmWide, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, lds);
+    else
+      ffn_tile<FfnGemm, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, lds);
   }
+}
+
+// Sums the S split parts of unit q (= (w*FM + fm)*FN + fn) of one output
+// tile of shape G, lane l, and stores bf16.  The float4 units g = 0..3 of
+// lane l hold columns 8g..8g+3 (l < 32) or 8g+4..8g+7 (l >= 32) of a
+// 32-column block of one token row; lanes l and l+32 share the row and swap
+// halves so that each stores 16 consecutive bf16 (two 16-byte stores).
+template <class G>
+__device__ __forceinline__ void reduce_unit(const float* __restrict__ slots, int S, int q, int row0, int rows,
+                                            int n0, int N, uint16_t* __restrict__ out) {
+  const int l = threadIdx.x & 63, hi = l >> 5;
+  const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
+  const int ml = G::q_row(G::wave_n(w), fn) + (l & 31);
+  const int nb = G::wave_m(w) * G::WTM + 32 * fm;   // first column of the 32-column block
+  if (ml >= rows || n0 + nb >= N) return;            // same for lanes l and l+32
+  const float* src = slots + static_cast<size_t>(q) * 4 * 256 + l * 4;
+  float4 v[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    v[g] = *reinterpret_cast<const float4*>(src + g * 256);
+#pragma unroll
+    for (int p = 1; p < 4; ++p)
+      if (p < S) {
+        const float4 u = *reinterpret_cast<const float4*>(src + p * kFfnSlotFloats + g * 256);
+        v[g].x += u.x; v[g].y += u.y; v[g].z += u.z; v[g].w += u.w;
+      }
+  }
+  // lane l (< 32) holds columns 8g..8g+3, lane l+32 columns 8g+4..8g+7:
+  // the low lane keeps columns 0..15, the high lane 16..31
+  float4 send[2] = {hi ? v[0] : v[2], hi ? v[1] : v[3]};
+  float4 recv[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    recv[i].x = __shfl_xor(send[i].x, 32, 64);
+    recv[i].y = __shfl_xor(send[i].y, 32, 64);
+    recv[i].z = __shfl_xor(send[i].z, 32, 64);
+    recv[i].w = __shfl_xor(send[i].w, 32, 64);
+  }
+  const float4 c[4] = {hi ? recv[0] : v[0], hi ? v[2] : recv[0], hi ? recv[1] : v[1], hi ? v[3] : recv[1]};
+  uint4* dst = reinterpret_cast<uint4*>(out + static_cast<size_t>(row0 + ml) * N + n0 + nb + 16 * hi);
+  dst[0] = make_uint4(pack_bf16x2(c[0].x, c[0].y), pack_bf16x2(c[0].z, c[0].w), pack_bf16x2(c[1].x, c[1].y),
+                      pack_bf16x2(c[1].z, c[1].w));
+  dst[1] = make_uint4(pack_bf16x2(c[2].x, c[2].y), pack_bf16x2(c[2].z, c[2].w), pack_bf16x2(c[3].x, c[3].y),
+                      pack_bf16x2(c[3].z, c[3].w));
 }
 
 // Sums the split parts of every output tile in part order and stores bf16.
 // Recomputes the same tile map and split count, so it does nothing when the
-// product was not split.  Partial tiles are in the accumulator layout of the
-// product kernel: float4 unit ((w*FM + fm)*FN + fn)*4 + g of lane l holds
-// acc[fm][fn][4g..4g+3] of wave w, i.e. four consecutive output columns of
-// one token row.  Each thread takes one (w, fm, fn, l): 16 columns of a
-// 32-column block of one row, lanes l and l+32 sharing the row; they swap
-// halves so that each stores 16 consecutive bf16 (two 16-byte stores).
-template <class G>
+// product was not split.  One thread per (w, fm, fn, lane) unit of a tile;
+// a tile gets the block count of the wide shape (the narrow shape leaves
+// its last blocks idle).
+constexpr int kReduceUnits = FfnGemmWide::NWAVES * FfnGemmWide::FM * FfnGemmWide::FN * 64;
+static_assert(kReduceUnits % 256 == 0 &&
+                  FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN * 64 <= kReduceUnits, "reduction blocks");
+
 __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __restrict__ rep_offsets, int E,
                                                                int K, int N, const float* __restrict__ split_slots,
                                                                uint16_t* __restrict__ out, int grid_parts) {
-  using SK = SplitK<G>;
-  constexpr int LANES = G::NWAVES * G::FM * G::FN * 64;   // (w, fm, fn, lane) per tile
-  constexpr int PER_TILE = LANES / 256;                    // blocks per tile
-  static_assert(LANES % 256 == 0, "reduction blocks");
-  const FfnTiles<G> map(rep_offsets, E, N);
-  const int S = map.parts(grid_parts, K / G::BK);
+  constexpr int PER_TILE = kReduceUnits / 256;   // blocks per tile
+  const FfnTiles map(rep_offsets, E, N);
+  const int S = map.parts(grid_parts, K / FfnGemm::BK);
   if (S == 1) return;
-  const int l = threadIdx.x & 63, hi = l >> 5;
   for (int b = blockIdx.x; b < map.tiles * PER_TILE; b += gridDim.x) {
     const int t = b / PER_TILE;
     const int q = ((b - t * PER_TILE) * 256 + threadIdx.x) >> 6;   // (w*FM + fm)*FN + fn
     int e, row0, rows, n0;
-    map.decode(t, E, e, row0, rows, n0);
-    const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
-    const int ml = G::q_row(G::wave_n(w), fn) + (l & 31);
-    const int nb = G::wave_m(w) * G::WTM + 32 * fm;   // first column of the 32-column block
-    if (ml >= rows || n0 + nb >= N) continue;          // same for lanes l and l+32
-    const float* src = split_slots + static_cast<size_t>(t) * S * SK::SLOT_FLOATS +
-                       static_cast<size_t>(q) * 4 * 256 + l * 4;
-    float4 v[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      v[g] = *reinterpret_cast<const float4*>(src + g * 256);
-#pragma unroll
-      for (int p = 1; p < 4; ++p)
-        if (p < S) {
-          const float4 u = *reinterpret_cast<const float4*>(src + p * SK::SLOT_FLOATS + g * 256);
-          v[g].x += u.x; v[g].y += u.y; v[g].z += u.z; v[g].w += u.w;
-        }
-    }
-    // lane l (< 32) holds columns 8g..8g+3, lane l+32 columns 8g+4..8g+7:
-    // the low lane keeps columns 0..15, the high lane 16..31
-    float4 send[2] = {hi ? v[0] : v[2], hi ? v[1] : v[3]};
-    float4 recv[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      recv[i].x = __shfl_xor(send[i].x, 32, 64);
-      recv[i].y = __shfl_xor(send[i].y, 32, 64);
-      recv[i].z = __shfl_xor(send[i].z, 32, 64);
-      recv[i].w = __shfl_xor(send[i].w, 32, 64);
-    }
-    const float4 c[4] = {hi ? recv[0] : v[0], hi ? v[2] : recv[0], hi ? recv[1] : v[1], hi ? v[3] : recv[1]};
-    uint4* dst = reinterpret_cast<uint4*>(out + static_cast<size_t>(row0 + ml) * N + n0 + nb + 16 * hi);
-    dst[0] = make_uint4(pack_bf16x2(c[0].x, c[0].y), pack_bf16x2(c[0].z, c[0].w), pack_bf16x2(c[1].x, c[1].y),
-                        pack_bf16x2(c[1].z, c[1].w));
-    dst[1] = make_uint4(pack_bf16x2(c[2].x, c[2].y), pack_bf16x2(c[2].z, c[2].w), pack_bf16x2(c[3].x, c[3].y),
-                        pack_bf16x2(c[3].z, c[3].w));
+    bool wide;
+    map.decode(t, E, e, row0, rows, n0, wide);
+    const float* slots = split_slots + static_cast<size_t>(t) * S * kFfnSlotFloats;
+    if (wide)
+      reduce_unit<FfnGemmWide>(slots, S, q, row0, rows, n0, N, out);
+    else if (q < FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN)
+      reduce_unit<FfnGemm>(slots, S, q, row0, rows, n0, N, out);
   }
 }
 
@@ -352,8 +402,6 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   }
 }
 
-using FfnGemm = GemmRagged64;
-
 struct FfnWs {
   void* hidden;
   float* split_slots;
@@ -364,8 +412,7 @@ FfnWs carve_ffn(Carver& c, int max_rows, int d_ff, int dtype) {
   w.hidden = c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
   w.split_slots = nullptr;
   if (dtype == LUFFY_BF16) {
-    using SK = SplitK<FfnGemm>;
-    w.split_slots = c.take<float>(SK::SLOT_FLOATS * SK::MAX_SLOTS);
+    w.split_slots = c.take<float>(kFfnSlotFloats * kFfnMaxSlots);
   }
   return w;
 }
@@ -380,19 +427,19 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
     const int grid = persistent_grid();
     {
       ProfileScope prof_("ffn1", s);
-      ffn_kernel_bf16<FfnGemm, ACT, true><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
+      ffn_kernel_bf16<ACT, true><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
                                                     d_ff, static_cast<const uint16_t*>(w1),
                                                     static_cast<uint16_t*>(hidden), ws.split_slots);
     }
     {
       ProfileScope prof_("ffn2", s);
-      ffn_kernel_bf16<FfnGemm, ACT, false><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
+      ffn_kernel_bf16<ACT, false><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
                                                      E, d_ff, d, static_cast<const uint16_t*>(w2),
                                                      static_cast<uint16_t*>(y_rep), ws.split_slots);
     }
     {
       ProfileScope prof_("ffn2_reduce", s);
-      ffn_split_reduce_kernel<FfnGemm><<<8 * grid, 256, 0, s>>>(rep_offsets, E, d_ff, d, ws.split_slots,
+      ffn_split_reduce_kernel<<<8 * grid, 256, 0, s>>>(rep_offsets, E, d_ff, d, ws.split_slots,
                                                                static_cast<uint16_t*>(y_rep), grid);
     }
   } else {

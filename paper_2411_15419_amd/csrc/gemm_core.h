@@ -61,6 +61,16 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Result layout of acc[fm][fn][v] in lane l of wave w:
 //   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
 //   Q row  q_row(wave_n(w), fn) + l%32
+// threadIdx.x behind an empty volatile asm: values derived from it are
+// recomputed where they are used instead of being hoisted out of a
+// persistent kernel's tile loop, where they would stay live (and spill)
+// across every tile shape the loop dispatches to.
+__device__ __forceinline__ int opaque_tid() {
+  int v = static_cast<int>(threadIdx.x);
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_>
 struct GemmK64 {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
@@ -85,7 +95,7 @@ struct GemmK64 {
   static __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
   static __device__ __forceinline__ int wave_m(int w) { return MFAST_ ? w % WM : w / WN; }
   static __device__ __forceinline__ int wave_n(int w) { return MFAST_ ? w / WM : w % WN; }
-  static __device__ __forceinline__ int wave() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+  static __device__ __forceinline__ int wave() { return __builtin_amdgcn_readfirstlane(opaque_tid() >> 6); }
   // first Q row of Q block fn of wave-column wn, and the row step between blocks
   static constexpr int QSTEP = QIL_ ? 32 * WN : 32;
   static __device__ __forceinline__ int q_row(int wn, int fn) { return (QIL_ ? 32 * wn : wn * WTN) + QSTEP * fn; }
@@ -97,7 +107,7 @@ struct GemmK64 {
 
   // Stage row this lane fills in load j: P rows 0..BM-1 (j < LP), then Q rows.
   static __device__ __forceinline__ int load_row(int j) {
-    const int w = wave(), lane = threadIdx.x & 63;
+    const int w = wave(), lane = opaque_tid() & 63;
     return (w + NWAVES * j) * 8 + (lane >> 3);
   }
 
@@ -144,7 +154,7 @@ struct GemmK64 {
   // from qvalid on are marked out of range (not fetched).
   static __device__ __forceinline__ void dma_offsets(const uint32_t (&poff)[LP], const uint32_t (&qoff)[LQ],
                                                      int pvalid, int qvalid, uint32_t (&goff)[LOADS]) {
-    const int lane = threadIdx.x & 63;
+    const int lane = opaque_tid() & 63;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int r = load_row(j);
@@ -243,7 +253,7 @@ struct GemmK64 {
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
                                              int K, int pvalid, int qvalid, uint8_t* lds_generic, Acc& acc) {
     const lds_ptr lds = (lds_ptr)lds_generic;
-    const int lane = threadIdx.x & 63;
+    const int lane = opaque_tid() & 63;
     const int w = wave();
     const int wm = wave_m(w), wn = wave_n(w);
     const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
@@ -318,24 +328,6 @@ using GemmBig64 = GemmK64<256, 256, 2, 4, false, false>;
 // 256 x 256, 512 threads, wave tile 64 x 128 (SIMD s holds P rows
 // 64s..64s+63 of both Q halves).
 using GemmRagged64 = GemmK64<256, 256, 4, 2, true, false>;
-
-// Split-K for persistent kernels with fewer output tiles than CUs: each
-// output tile's K range is cut into S parts that run as separate tiles and
-// store float32 partial tiles; a separate reduction kernel (the kernel
-// boundary makes the partials visible across XCDs) adds them in part order.
-template <class G>
-struct SplitK {
-  static constexpr int MAX_SLOTS = 512;                       // >= CUs
-  static constexpr size_t SLOT_FLOATS = static_cast<size_t>(G::BM) * G::BN;
-
-  // parts per output tile: fill the grid once, at most 4, >= 4 K-stages each
-  static __device__ __forceinline__ int parts(int tiles, int grid, int nk) {
-    const int cap = min(grid, MAX_SLOTS);
-    if (tiles <= 0 || tiles * 2 > cap) return 1;
-    return max(1, min(min(cap / tiles, 4), nk / 4));
-  }
-};
-
 
 // Persistent-kernel block order: consecutive virtual ids share an XCD
 // (workgroups are dealt to the 8 XCDs round-robin), so the tiles that run
