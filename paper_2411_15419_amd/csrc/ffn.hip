@@ -96,13 +96,16 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
 // smaller stages).  Both shapes share the block size, the LDS buffer and the
 // split-K slots.
 using FfnGemm = GemmRagged64;
-using FfnGemmWide = GemmK64<256, 320, 4, 2, true, false>;
+using FfnGemmWide = GemmCore<256, 320, 4, 2, true, false>;
 static_assert(FfnGemm::BM == FfnGemmWide::BM && FfnGemm::THREADS == FfnGemmWide::THREADS, "shared tile map");
 constexpr int kFfnLds = FfnGemmWide::LDS_BYTES > FfnGemm::LDS_BYTES ? FfnGemmWide::LDS_BYTES : FfnGemm::LDS_BYTES;
 // split-K partial tiles: one slot (the accumulators of a tile in register
 // layout) per work item, at most kFfnMaxSlots (>= CUs) work items
 constexpr int kFfnMaxSlots = 512;
 constexpr size_t kFfnSlotFloats = static_cast<size_t>(FfnGemm::BM) * FfnGemmWide::BN;
+// split-K parts cut K at multiples of this (a multiple of both stage widths)
+constexpr int kFfnKUnit = 64;
+static_assert(kFfnKUnit % FfnGemm::BK == 0 && kFfnKUnit % FfnGemmWide::BK == 0, "K unit");
 
 // Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
 // expert per lane, E <= 64).  Expert e's rows are cut into tiles of rt_e
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kFfnLds];
   const FfnTiles map(rep_offsets, E, N);
-  const int nk = K / FfnGemm::BK;
+  const int nk = K / kFfnKUnit;
   const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
   const int total = map.tiles * S;
   const int vb = xcd_virtual_block();
@@ -263,8 +266,8 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     bool wide;
     map.decode(t, E, e, row0, rows, n0, wide);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
-    // K range of this part, in whole 64-wide stages
-    const int k0 = (part * nk / S) * FfnGemm::BK, k1 = ((part + 1) * nk / S) * FfnGemm::BK;
+    // K range of this part, in whole 64-wide units
+    const int k0 = (part * nk / S) * kFfnKUnit, k1 = ((part + 1) * nk / S) * kFfnKUnit;
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
     if (wide)
       ffn_tile<FfnGemmWide, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, lds);
@@ -331,7 +334,7 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
                                                                uint16_t* __restrict__ out, int grid_parts) {
   constexpr int PER_TILE = kReduceUnits / 256;   // blocks per tile
   const FfnTiles map(rep_offsets, E, N);
-  const int S = map.parts(grid_parts, K / FfnGemm::BK);
+  const int S = map.parts(grid_parts, K / kFfnKUnit);
   if (S == 1) return;
   for (int b = blockIdx.x; b < map.tiles * PER_TILE; b += gridDim.x) {
     const int t = b / PER_TILE;

@@ -39,28 +39,6 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
-// Tile core with K advancing 64 at a time through two LDS stages (double
-// buffering): output tile BM (P rows) x BN (Q rows), waves in a WM x WN
-// grid, v_mfma_f32_32x32x16_bf16 blocks.  Each operand row contributes 128
-// contiguous bytes per stage, a whole cache line: a DMA instruction fills 8
-// rows x 128 B, half as many line requests per byte as 64-byte row pieces,
-// which lets L2-resident operands stream into LDS at roughly twice the rate.
-// The eight 16-byte chunks of row r are stored XOR-permuted by (r >> 1) & 7,
-// so the 16 lanes of a fragment read (16 consecutive rows, one chunk) hit 16
-// distinct bank groups.  Fragments are double-buffered per 16-wide K step
-// (see run) and the DMA of stage kt+2 is issued once every wave has read
-// stage kt.  K must be a multiple of 64.
-//
-// Wave placement: MFAST puts the P-block index fastest (wm = w % WM), so
-// with WM = 4 each SIMD holds one P quarter of every Q part; QIL
-// interleaves the Q blocks of the waves (wave wn owns 32-row Q blocks wn,
-// wn + WN, ...), so with WN = 8 a partly valid Q tile spreads its valid
-// blocks over all four SIMDs.  In both cases a tile whose Q rows are only
-// partly valid can skip the MFMAs of its invalid Q blocks (run<NQ>).
-//
-// Result layout of acc[fm][fn][v] in lane l of wave w:
-//   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
-//   Q row  q_row(wave_n(w), fn) + l%32
 // threadIdx.x behind an empty volatile asm: values derived from it are
 // recomputed where they are used instead of being hoisted out of a
 // persistent kernel's tile loop, where they would stay live (and spill)
@@ -71,28 +49,57 @@ __device__ __forceinline__ int opaque_tid() {
   return v;
 }
 
-template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_>
-struct GemmK64 {
+// Tile core: output tile BM (P rows) x BN (Q rows), waves in a WM x WN
+// grid, v_mfma_f32_32x32x16_bf16 blocks.  K advances BK (32 or 64) per
+// stage through a ring of STAGES LDS stages; while one stage is multiplied
+// the DMA of the next STAGES-1 is in flight.  Each operand row contributes
+// BK*2 contiguous bytes per stage (a whole 128-byte line at BK = 64, which
+// streams L2-resident operands at about twice the rate of 64-byte pieces;
+// BK = 32 halves the stage and so allows a deeper ring, for operands that
+// stream from HBM).  A DMA instruction fills 1 KB: 1024/(2*BK) rows.
+// The 16-byte chunks of row r are stored XOR-permuted (BK = 64: by
+// (r >> 1) & 7 over 8 chunks; BK = 32: by (r >> 2) & 3 over 4 chunks), so
+// the 16 lanes of a fragment read (16 consecutive rows, one chunk) hit 16
+// distinct bank groups.  K must be a multiple of BK.
+//
+// Wave placement: MFAST puts the P-block index fastest (wm = w % WM), so
+// with WM = 4 each SIMD holds one P quarter of every Q part; QIL
+// interleaves the Q blocks of the waves (wave wn owns 32-row Q blocks wn,
+// wn + WN, ...).  In both cases a tile whose Q rows are only partly valid
+// can skip the MFMAs of its invalid Q blocks (run<NQ>).
+//
+// Result layout of acc[fm][fn][v] in lane l of wave w:
+//   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
+//   Q row  q_row(wave_n(w), fn) + l%32
+template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_, int BK_ = 64, int STAGES_ = 2>
+struct GemmCore {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
-  static constexpr int BK = 64;                      // K per stage
-  static constexpr int STAGES = 2;
+  static constexpr bool QIL = QIL_;
+  static constexpr int BK = BK_;                     // K per stage
+  static constexpr int STAGES = STAGES_;
+  static_assert(BK == 32 || BK == 64, "stage width");
+  static_assert(STAGES >= 2 && STAGES <= 5, "ring depth");
   static constexpr int THREADS = 64 * WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int FM = WTM / 32, FN = WTN / 32;
-  static constexpr int ROW_BYTES = BK * 2;           // 128
+  static constexpr int ROW_BYTES = BK * 2;
+  static constexpr int CPR = ROW_BYTES / 16;         // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;               // rows per DMA instruction
+  static constexpr int STEPS = BK / 16;              // MFMA K steps per stage
   static constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
   static constexpr int NWAVES = WM * WN;
-  // each wave instruction fills 8 rows (1 KB): LP of them P rows, LQ Q rows
-  static constexpr int LP = BM / 8 / NWAVES, LQ = BN / 8 / NWAVES;
+  // DMA instructions per wave and stage: LP of them P rows, LQ Q rows
+  static constexpr int LP = BM / RPI / NWAVES, LQ = BN / RPI / NWAVES;
   static constexpr int LOADS = LP + LQ;
-  static_assert(LP * NWAVES * 8 == BM && LQ * NWAVES * 8 == BN, "load plan");
+  static_assert(LP * NWAVES * RPI == BM && LQ * NWAVES * RPI == BN, "load plan");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
 
   using Acc = f32x16[FM][FN];
   using lds_ptr = __attribute__((address_space(3))) uint8_t*;
 
-  static __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+  static __device__ __forceinline__ int swz(int r) { return BK == 64 ? (r >> 1) & 7 : (r >> 2) & 3; }
   static __device__ __forceinline__ int wave_m(int w) { return MFAST_ ? w % WM : w / WN; }
   static __device__ __forceinline__ int wave_n(int w) { return MFAST_ ? w / WM : w % WN; }
   static __device__ __forceinline__ int wave() { return __builtin_amdgcn_readfirstlane(opaque_tid() >> 6); }
@@ -108,7 +115,7 @@ struct GemmK64 {
   // Stage row this lane fills in load j: P rows 0..BM-1 (j < LP), then Q rows.
   static __device__ __forceinline__ int load_row(int j) {
     const int w = wave(), lane = opaque_tid() & 63;
-    return (w + NWAVES * j) * 8 + (lane >> 3);
+    return (w + NWAVES * j) * RPI + lane / CPR;
   }
 
   static __device__ __forceinline__ void zero(Acc& acc) {
@@ -142,15 +149,15 @@ struct GemmK64 {
                                                const uint32_t (&goff)[LOADS], int k0, lds_ptr st, int w) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      lds_ptr dst = st + (w + NWAVES * j) * 8 * ROW_BYTES;
+      lds_ptr dst = st + (w + NWAVES * j) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(j < LP ? prs : qrs,
                                                reinterpret_cast<__attribute__((address_space(3))) void*>(dst),
                                                16, goff[j], k0 * 2, 0, 0);
     }
   }
 
-  // lane fills physical chunk lane%8 of its row with logical chunk
-  // (lane%8) ^ swz(row); byte offsets.  P rows from pvalid on and Q rows
+  // lane fills physical chunk lane%CPR of its row with logical chunk
+  // (lane%CPR) ^ swz(row); byte offsets.  P rows from pvalid on and Q rows
   // from qvalid on are marked out of range (not fetched).
   static __device__ __forceinline__ void dma_offsets(const uint32_t (&poff)[LP], const uint32_t (&qoff)[LQ],
                                                      int pvalid, int qvalid, uint32_t (&goff)[LOADS]) {
@@ -158,7 +165,7 @@ struct GemmK64 {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int r = load_row(j);
-      const uint32_t lc = static_cast<uint32_t>((lane & 7) ^ swz(r));
+      const uint32_t lc = static_cast<uint32_t>((lane % CPR) ^ swz(r));
       const bool valid = j < LP ? r < pvalid : r - BM < qvalid;
       goff[j] = valid ? ((j < LP ? poff[j] : qoff[j - LP]) + lc * 8) * 2u : kRange;
     }
@@ -170,7 +177,7 @@ struct GemmK64 {
     bf16x8 a[FM], b[FN];
   };
 
-  // K step `step` (0..3) of the stage at S, first NQ Q blocks.
+  // K step `step` of the stage at S, first NQ Q blocks.
   template <int NQ>
   static __device__ __forceinline__ void read_step(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
                                                    Frags& f) {
@@ -210,9 +217,9 @@ struct GemmK64 {
     if constexpr (NDS > 2 * NMF) __builtin_amdgcn_sched_group_barrier(0x100, NDS - 2 * NMF, 0);
   }
 
-  // Schedule of the step after the barrier: the buffer loads of stage kt+2
-  // go out first (one per MFMA), then the LDS reads; their latency is the
-  // longer one.
+  // Schedule of the step after the barrier: the buffer loads of the next
+  // stage to fetch go out first (one per MFMA), then the LDS reads; their
+  // latency is the longer one.
   template <int NQ>
   static __device__ __forceinline__ void interleave_loads() {
     constexpr int NMF = FM * NQ, NDS = NQ > 0 ? FM + NQ : 0, NVM = LOADS;
@@ -233,6 +240,33 @@ struct GemmK64 {
     if constexpr (NDS > PD) __builtin_amdgcn_sched_group_barrier(0x100, NDS - PD, 0);
   }
 
+  // Wait until at most n stages of this wave's DMA are outstanding
+  // (0 <= n <= STAGES - 2, wave-uniform).
+  static __device__ __forceinline__ void wait_stages(int n) {
+    if constexpr (STAGES > 4) {
+      if (n >= 3) { wait_vmcnt<3 * LOADS>(); return; }
+    }
+    if constexpr (STAGES > 3) {
+      if (n >= 2) { wait_vmcnt<2 * LOADS>(); return; }
+    }
+    if (n >= 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+  }
+
+  // Steps ST..STEPS-1 of a stage (no buffer loads): step s reads step s of
+  // the stage at S into f[s & 1] while multiplying f[(s - 1) & 1].
+  template <int NQ, int ST>
+  static __device__ __forceinline__ void inner_steps(lds_ptr S, int prow0, int qrow0, int half, int sw,
+                                                     Frags (&f)[2], Acc& acc, bool sched) {
+    if constexpr (ST < STEPS) {
+      if (sched) __builtin_amdgcn_sched_barrier(0);
+      read_step<NQ>(S, prow0, qrow0, half, sw, ST, f[ST & 1]);
+      mma_step<NQ>(f[(ST - 1) & 1], acc);
+      if (sched) interleave_reads<NQ>();
+      inner_steps<NQ, ST + 1>(S, prow0, qrow0, half, sw, f, acc, sched);
+    }
+  }
+
   // poff[j] (j < LP): element offset of P row load_row(j);
   // qoff[j] (j < LQ): element offset of Q row load_row(LP + j) - BM.
   // Only the first pvalid P rows and qvalid Q rows are fetched; the LDS
@@ -241,13 +275,14 @@ struct GemmK64 {
   // may be reused.  NQ: the wave multiplies only its first NQ Q blocks;
   // every wave still issues its share of the loads and takes every barrier.
   //
-  // Fragments are double-buffered per 16-wide K step (fa, fb): while the
-  // MFMAs of step s run, the fragments of step s+1 are read.  Stage kt
-  // (buffer kt % 2): steps 0-2 read steps 1-3; then wait for stage kt+1 and
-  // for this wave's reads, barrier (every wave is done with buffer kt % 2),
-  // issue the DMA of stage kt+2 into it and read step 0 of stage kt+1 while
-  // step 3 is multiplied.  Holding one step per buffer (not two) keeps the
-  // FFN tile within 256 registers per lane without register reuse stalls.
+  // Fragments are double-buffered per 16-wide K step: while the MFMAs of
+  // step s run, the fragments of step s+1 are read.  Stage kt (buffer
+  // kt % STAGES): steps 1..STEPS-1 are read while steps 0..STEPS-2 are
+  // multiplied; then wait for stage kt+1 and for this wave's reads, barrier
+  // (every wave is done with buffer kt % STAGES), issue the DMA of stage
+  // kt+STAGES into it and read step 0 of stage kt+1 while the last step is
+  // multiplied.  Holding one step per buffer keeps the FFN tile within 256
+  // registers per lane without register reuse stalls.
   template <int NQ = FN>
   static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase, const uint32_t (&poff)[LP],
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
@@ -260,74 +295,58 @@ struct GemmK64 {
     uint32_t goff[LOADS];
     dma_offsets(poff, qoff, pvalid, qvalid, goff);
     const int nk = __builtin_amdgcn_readfirstlane(K / BK);
-    issue(prs, qrs, goff, 0, lds, w);
-    if (nk > 1) {
-      issue(prs, qrs, goff, BK, lds + STAGE_BYTES, w);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    const int pro = min(nk, STAGES);
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+      if (s < pro) issue(prs, qrs, goff, s * BK, lds + s * STAGE_BYTES, w);
+    wait_stages(pro - 1);
     raw_barrier();
     const int sw = swz(lane & 31);
     const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
     const int qrow0 = (BM + q_row(wn, 0) + (lane & 31)) * ROW_BYTES;
     const int half = lane >> 5;
-    Frags fa, fb;
-    read_step<NQ>(lds, prow0, qrow0, half, sw, 0, fa);
-    int kt = 0;
-    // steady state: stage kt+2 exists
-    for (; kt + 2 < nk; ++kt) {
-      const lds_ptr cur = lds + (kt & 1) * STAGE_BYTES;
-      const lds_ptr nxt = lds + ((kt + 1) & 1) * STAGE_BYTES;
+    Frags f[2];
+    read_step<NQ>(lds, prow0, qrow0, half, sw, 0, f[0]);
+    int kt = 0, cb = 0;   // stage and its buffer
+    // steady state: stage kt+STAGES exists
+    for (; kt + STAGES < nk; ++kt) {
+      const lds_ptr cur = lds + cb * STAGE_BYTES;
+      cb = cb + 1 == STAGES ? 0 : cb + 1;
+      const lds_ptr nxt = lds + cb * STAGE_BYTES;
+      inner_steps<NQ, 1>(cur, prow0, qrow0, half, sw, f, acc, true);
       __builtin_amdgcn_sched_barrier(0);
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 1, fb);
-      mma_step<NQ>(fa, acc);
-      interleave_reads<NQ>();
-      __builtin_amdgcn_sched_barrier(0);
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 2, fa);
-      mma_step<NQ>(fb, acc);
-      interleave_reads<NQ>();
-      __builtin_amdgcn_sched_barrier(0);
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 3, fb);
-      mma_step<NQ>(fa, acc);
-      interleave_reads<NQ>();
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vmcnt<0>();                      // stage kt+1 landed (this wave's part)
+      wait_vmcnt<(STAGES - 2) * LOADS>();   // stage kt+1 landed (this wave's part)
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
       raw_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      issue(prs, qrs, goff, (kt + 2) * BK, cur, w);
-      read_step<NQ>(nxt, prow0, qrow0, half, sw, 0, fa);
-      mma_step<NQ>(fb, acc);
+      issue(prs, qrs, goff, (kt + STAGES) * BK, cur, w);
+      read_step<NQ>(nxt, prow0, qrow0, half, sw, 0, f[0]);
+      mma_step<NQ>(f[1], acc);
       interleave_loads<NQ>();
       __builtin_amdgcn_sched_barrier(0);
     }
-    // last one or two stages: nothing more to issue
+    // last stages: nothing more to issue
     for (; kt < nk; ++kt) {
-      const lds_ptr cur = lds + (kt & 1) * STAGE_BYTES;
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 1, fb);
-      mma_step<NQ>(fa, acc);
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 2, fa);
-      mma_step<NQ>(fb, acc);
-      read_step<NQ>(cur, prow0, qrow0, half, sw, 3, fb);
-      mma_step<NQ>(fa, acc);
+      const lds_ptr cur = lds + cb * STAGE_BYTES;
+      cb = cb + 1 == STAGES ? 0 : cb + 1;
+      inner_steps<NQ, 1>(cur, prow0, qrow0, half, sw, f, acc, false);
       if (kt + 1 < nk) {
-        wait_vmcnt<0>();
+        wait_stages(nk - 2 - kt);
         __builtin_amdgcn_s_waitcnt(0xC07F);
         raw_barrier();
-        read_step<NQ>(lds + ((kt + 1) & 1) * STAGE_BYTES, prow0, qrow0, half, sw, 0, fa);
+        read_step<NQ>(lds + cb * STAGE_BYTES, prow0, qrow0, half, sw, 0, f[0]);
       }
-      mma_step<NQ>(fb, acc);
+      mma_step<NQ>(f[1], acc);
     }
     __syncthreads();
   }
 };
 
-// 256 x 256, 512 threads, wave tile 128 x 64.
-using GemmBig64 = GemmK64<256, 256, 2, 4, false, false>;
+// 256 x 256, 512 threads, wave tile 128 x 64, 64-wide stages.
+using GemmBig64 = GemmCore<256, 256, 2, 4, false, false>;
 // 256 x 256, 512 threads, wave tile 64 x 128 (SIMD s holds P rows
-// 64s..64s+63 of both Q halves).
-using GemmRagged64 = GemmK64<256, 256, 4, 2, true, false>;
+// 64s..64s+63 of both Q halves), 64-wide stages.
+using GemmRagged64 = GemmCore<256, 256, 4, 2, true, false>;
 
 // Persistent-kernel block order: consecutive virtual ids share an XCD
 // (workgroups are dealt to the 8 XCDs round-robin), so the tiles that run
