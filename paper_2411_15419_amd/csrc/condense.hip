@@ -42,7 +42,7 @@ namespace luffy {
 namespace {
 
 constexpr int kGreedyGridRounds = 2;
-constexpr int kTile = 256;      // similarity tile of the bf16 path (GemmBig64)
+constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
 constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
 
@@ -227,12 +227,15 @@ __device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t
   return c;
 }
 
-__global__ __launch_bounds__(GemmBig64::THREADS) void gram_kernel_bf16(
+using GramGemm = GemmBig64;
+static_assert(GramGemm::BM == kTile && GramGemm::BN == kTile, "similarity tile");
+
+__global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
-  using G = GemmBig64;
+  using G = GramGemm;
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   __shared__ __attribute__((aligned(16))) float inv_a[kTile];
   __shared__ float inv_b[kTile];
@@ -254,8 +257,10 @@ __global__ __launch_bounds__(GemmBig64::THREADS) void gram_kernel_bf16(
 #pragma unroll
     for (int j = 0; j < G::LQ; ++j)
       qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)]) * d;
-    if (tid < kTile) inv_a[tid] = inv_norm[pt[min(c.ti * kTile + tid, c.n - 1)]];
-    else inv_b[tid - kTile] = inv_norm[pt[min(c.tj * kTile + tid - kTile, c.n - 1)]];
+    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
+      if (i < kTile) inv_a[i] = inv_norm[pt[min(c.ti * kTile + i, c.n - 1)]];
+      else inv_b[i - kTile] = inv_norm[pt[min(c.tj * kTile + i - kTile, c.n - 1)]];
+    }
     G::Acc acc;
     G::zero(acc);
     G::run(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, acc);  // ends with a barrier
@@ -320,9 +325,9 @@ __global__ __launch_bounds__(GemmBig64::THREADS) void gram_kernel_bf16(
     }
     __syncthreads();
     // degree: edges of each tile row (and, off the diagonal, of each mirrored row)
-    {
-      const bool mirror = tid >= kTile;
-      const int rl = mirror ? tid - kTile : tid;
+    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
+      const bool mirror = i >= kTile;
+      const int rl = mirror ? i - kTile : i;
       const uint32_t* pcs = mirror ? tbits[rl] : dbits[rl];
       int cnt = 0;
 #pragma unroll
@@ -796,7 +801,7 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   {
     ProfileScope prof_("gram", s);
     if (bf16)
-      gram_kernel_bf16<<<persistent_grid(), GemmBig64::THREADS, 0, s>>>(
+      gram_kernel_bf16<<<persistent_grid(), GramGemm::THREADS, 0, s>>>(
           static_cast<const uint16_t*>(x), d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off,
           ws.bm_off, ws.err, ws.bitmask, ws.deg);
     else
