@@ -227,6 +227,10 @@ __device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t
   return c;
 }
 
+// v_writelane_b32: `old` with lane `lane` replaced by the wave-uniform
+// `value` (the LLVM intrinsic, which clang does not expose as a builtin).
+__device__ int amdgcn_writelane(int value, int lane, int old) __asm("llvm.amdgcn.writelane");
+
 using GramGemm = GemmBig64;
 static_assert(GramGemm::BM == kTile && GramGemm::BN == kTile, "similarity tile");
 
@@ -265,13 +269,18 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     G::zero(acc);
     G::run(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, acc);  // ends with a barrier
 
-    // Each (fm, fn) block is 32 x 32: ballot v covers rows
-    // abase + 8(v/4) + (v%4) (bits 0..31) and that row + 4 (bits 32..63),
-    // bit position within a half = column.  Lanes 0..31 store one 32-bit
-    // row piece and one 32-bit column piece each, so every piece of the tile
-    // is written exactly once.  Edge test: dot * (1/|a|) * (1/|b|) >= h,
-    // for rows and columns inside the bucket, never a token with itself.
-    const int vsel = (lane & 31) >> 1, half = lane & 1, l31 = lane & 31, hi = lane >> 5;
+    // Each (fm, fn) block is 32 x 32.  Lane l holds column bbase + l%32 and,
+    // in accumulator v, row abase + rv(v) + 4*(l/32), rv(v) = 8(v/4) + v%4.
+    // Ballot v is then two row pieces: bits 0..31 are the columns of row
+    // abase + rv(v), bits 32..63 those of row abase + rv(v) + 4; lane r < 32
+    // receives row r's piece by writelane.  The column piece of column
+    // bbase + c has bit rv(v) (+4 in the upper half-wave) from accumulator v:
+    // each lane assembles its 16 bits with selects on its own compares, and
+    // lanes c and c+32 merge theirs with one cross-half exchange.  Every piece
+    // of the tile is written exactly once.  Edge test:
+    // dot * (1/|a|) * (1/|b|) >= h, for rows and columns inside the bucket,
+    // never a token with itself.
+    const int l31 = lane & 31, hi = lane >> 5;
     const bool same_tile = c.ti == c.tj;
     const int nrow_a = c.n - c.ti * kTile, nrow_b = c.n - c.tj * kTile;
 #pragma unroll
@@ -296,29 +305,21 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
         const int bl = bbase + l31;
         const float ib = bl < nrow_b ? inv_b[bl] : nan;
         const bool diag = same_tile && abase == bbase;   // wave-uniform
-        auto edge = [&](int v) {
-          const bool e = acc[fm][fn][v] * ia[v] * ib >= h;
-          if (!diag) return e;
-          const int al = 8 * (v >> 2) + 4 * hi + (v & 3);   // row within the block
-          return e && al != l31;
-        };
-        // first pass: any edge in the block (most blocks have none)
-        uint64_t any = 0;
+        uint32_t colbits = 0, piece = 0;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) any |= __ballot(edge(v));
-        uint32_t piece = 0, tv = 0;
-        if (any) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const uint64_t mv = __ballot(edge(v));
-            if (v == vsel) piece = static_cast<uint32_t>(mv >> (32 * half));
-            const int base = 8 * (v >> 2) + (v & 3);
-            tv |= static_cast<uint32_t>((mv >> l31) & 1ull) << base;
-            tv |= static_cast<uint32_t>((mv >> (32 + l31)) & 1ull) << (base + 4);
-          }
+        for (int v = 0; v < 16; ++v) {
+          const int rv = 8 * (v >> 2) + (v & 3);
+          bool e = acc[fm][fn][v] * ia[v] * ib >= h;
+          if (diag) e = e && rv + 4 * hi != l31;
+          const uint64_t m = __ballot(e);
+          piece = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(m)), rv, piece);
+          piece = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(m >> 32)), rv + 4, piece);
+          colbits |= e ? 1u << rv : 0u;
         }
+        colbits <<= 4 * hi;
+        const uint32_t tv = colbits | static_cast<uint32_t>(__shfl_xor(static_cast<int>(colbits), 32, 64));
         if (lane < 32) {
-          dbits[abase + 8 * (vsel >> 2) + 4 * half + (vsel & 3)][bbase >> 5] = piece;
+          dbits[abase + l31][bbase >> 5] = piece;
           tbits[bl][abase >> 5] = tv;
         }
       }
