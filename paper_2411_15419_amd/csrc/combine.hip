@@ -105,10 +105,9 @@ extern "C" int luffy_combine(const void* y_rep, const int32_t* rep_row,
   if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_combine: d=%d not a multiple of 64", d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int blocks = (T + 3) / 4;
-  ProfileScope prof_("combine", s);
   if (dtype == LUFFY_BF16)
-    combine_kernel<true><<<blocks, 256, 0, s>>>(y_rep, rep_row, slot_pos, topk_gate, T, k, d, y);
+    launch("combine", combine_kernel<true>, blocks, 256, 0, s, y_rep, rep_row, slot_pos, topk_gate, T, k, d, y);
   else
-    combine_kernel<false><<<blocks, 256, 0, s>>>(y_rep, rep_row, slot_pos, topk_gate, T, k, d, y);
+    launch("combine", combine_kernel<false>, blocks, 256, 0, s, y_rep, rep_row, slot_pos, topk_gate, T, k, d, y);
   return check_launch("luffy_combine");
 }

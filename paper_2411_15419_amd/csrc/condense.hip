@@ -786,62 +786,53 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const float* inv_norm_use = inv_norm ? inv_norm : ws.inv_norm;
   const int norm_blocks = inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
   {
-    ProfileScope prof_("norm", s);
     const int tile = bf16 ? kTile : kTileF32;
 #define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
                         ws.cap_words, ws.tile_off, ws.bm_off, ws.err
     if (bf16) {
-      if (inv_norm) norm_kernel<true, false><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
-      else norm_kernel<true, true><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+      if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+      else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
     } else {
-      if (inv_norm) norm_kernel<false, false><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
-      else norm_kernel<false, true><<<norm_blocks, 256, 0, s>>>(LUFFY_NORM_ARGS);
+      if (inv_norm) launch("norm", norm_kernel<false, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+      else launch("norm", norm_kernel<false, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
     }
 #undef LUFFY_NORM_ARGS
   }
   {
-    ProfileScope prof_("gram", s);
     if (bf16)
-      gram_kernel_bf16<<<persistent_grid(), GramGemm::THREADS, 0, s>>>(
-          static_cast<const uint16_t*>(x), d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off,
-          ws.bm_off, ws.err, ws.bitmask, ws.deg);
+      launch("gram", gram_kernel_bf16, persistent_grid(), GramGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
+             d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask,
+             ws.deg);
     else
-      gram_kernel_f32<<<2 * persistent_grid(), 256, 0, s>>>(
-          static_cast<const float*>(x), d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off,
-          ws.bm_off, ws.err, ws.bitmask, ws.deg);
+      launch("gram", gram_kernel_f32, 2 * persistent_grid(), 256, 0, s, static_cast<const float*>(x), d, perm_token,
+             offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg);
   }
   const int wave_blocks = (S + 3) / 4;
   const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
   for (int r = 0; r < kGreedyGridRounds; ++r) {
-    ProfileScope prof_("greedy_round", s);
-    greedy_round_kernel<<<visit_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-                                                    ws.state, r, degree);
+    launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
+           ws.deg, ws.state, r, degree);
   }
   {
-    ProfileScope prof_("greedy_finish", s);
-    greedy_finish_kernel<<<E, 1024, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state);
+    launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+           ws.state);
   }
   {
-    ProfileScope prof_("claim", s);
-    claim_kernel<<<visit_blocks, 256, 0, s>>>(offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state,
-                                             ws.claim);
+    launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+           ws.state, ws.claim);
   }
   const int pos_blocks = (S + 1023) / 1024;
   {
-    ProfileScope prof_("rep_local", s);
-    rep_local_kernel<<<pos_blocks, 1024, 0, s>>>(offsets, E, ws.err, ws.state, ws.claim, rep_of_pos, ws.local,
-                                                 ws.bsum);
+    launch("rep_local", rep_local_kernel, pos_blocks, 1024, 0, s, offsets, E, ws.err, ws.state, ws.claim,
+           rep_of_pos, ws.local, ws.bsum);
   }
   {
-    ProfileScope prof_("rep_finalize", s);
-    rep_finalize_kernel<<<pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s>>>(
-        offsets, E, rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, pos_blocks);
+    launch("rep_finalize", rep_finalize_kernel, pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s, offsets, E,
+           rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, pos_blocks);
   }
   if (x_rep) {
-    ProfileScope prof_("gather", s);
-    gather_kernel<<<wave_blocks, 256, 0, s>>>(static_cast<const uint8_t*>(x),
-                                              static_cast<size_t>(d) * elem_bytes(dtype), rep_offsets, E,
-                                              rep_token, static_cast<uint8_t*>(x_rep));
+    launch("gather", gather_kernel, wave_blocks, 256, 0, s, static_cast<const uint8_t*>(x),
+           static_cast<size_t>(d) * elem_bytes(dtype), rep_offsets, E, rep_token, static_cast<uint8_t*>(x_rep));
   }
   return check_launch("luffy_condense");
 }

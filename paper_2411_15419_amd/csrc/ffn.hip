@@ -429,35 +429,29 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
   if (dtype == LUFFY_BF16) {
     const int grid = persistent_grid();
     {
-      ProfileScope prof_("ffn1", s);
-      ffn_kernel_bf16<ACT, true><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(x), row_index, rep_offsets, E, d,
-                                                    d_ff, static_cast<const uint16_t*>(w1),
-                                                    static_cast<uint16_t*>(hidden), ws.split_slots);
+      launch("ffn1", ffn_kernel_bf16<ACT, true>, grid, FfnGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
+             row_index, rep_offsets, E, d, d_ff, static_cast<const uint16_t*>(w1), static_cast<uint16_t*>(hidden),
+             ws.split_slots);
     }
     {
-      ProfileScope prof_("ffn2", s);
-      ffn_kernel_bf16<ACT, false><<<grid, FfnGemm::THREADS, 0, s>>>(static_cast<const uint16_t*>(hidden), nullptr, rep_offsets,
-                                                     E, d_ff, d, static_cast<const uint16_t*>(w2),
-                                                     static_cast<uint16_t*>(y_rep), ws.split_slots);
+      launch("ffn2", ffn_kernel_bf16<ACT, false>, grid, FfnGemm::THREADS, 0, s,
+             static_cast<const uint16_t*>(hidden), nullptr, rep_offsets, E, d_ff, d,
+             static_cast<const uint16_t*>(w2), static_cast<uint16_t*>(y_rep), ws.split_slots);
     }
     {
-      ProfileScope prof_("ffn2_reduce", s);
-      ffn_split_reduce_kernel<<<8 * grid, 256, 0, s>>>(rep_offsets, E, d_ff, d, ws.split_slots,
-                                                               static_cast<uint16_t*>(y_rep), grid);
+      launch("ffn2_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots,
+             static_cast<uint16_t*>(y_rep), grid);
     }
   } else {
     const int mt = (max_rows + kF32Tile - 1) / kF32Tile + E;
     dim3 g1(mt, (d_ff + kF32Tile - 1) / kF32Tile), g2(mt, (d + kF32Tile - 1) / kF32Tile);
     {
-      ProfileScope prof_("ffn1", s);
-      ffn_kernel_f32<ACT, true><<<g1, 256, 0, s>>>(static_cast<const float*>(x), row_index, rep_offsets, E, d, d_ff,
-                                                   static_cast<const float*>(w1), static_cast<float*>(hidden));
+      launch("ffn1", ffn_kernel_f32<ACT, true>, g1, 256, 0, s, static_cast<const float*>(x), row_index, rep_offsets,
+             E, d, d_ff, static_cast<const float*>(w1), static_cast<float*>(hidden));
     }
     {
-      ProfileScope prof_("ffn2", s);
-      ffn_kernel_f32<ACT, false><<<g2, 256, 0, s>>>(static_cast<const float*>(hidden), nullptr, rep_offsets, E,
-                                                    d_ff, d, static_cast<const float*>(w2),
-                                                    static_cast<float*>(y_rep));
+      launch("ffn2", ffn_kernel_f32<ACT, false>, g2, 256, 0, s, static_cast<const float*>(hidden), nullptr,
+             rep_offsets, E, d_ff, d, static_cast<const float*>(w2), static_cast<float*>(y_rep));
     }
   }
 }

@@ -69,20 +69,21 @@ hipEvent_t take_event() {
 }
 }  // namespace
 
-ProfileScope::ProfileScope(const char* name, hipStream_t s) : stream_(s) {
-  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+bool profile_begin(const char* name, hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_prof_on.load(std::memory_order_relaxed)) return false;
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  if (std::strcmp(name, g_prof_name) != 0) return;
-  start_ = take_event();
-  stop_ = take_event();
-  if (start_ && stop_) hipEventRecord(start_, stream_);
+  if (std::strcmp(name, g_prof_name) != 0) return false;
+  *start = take_event();
+  *stop = take_event();
+  if (*start && *stop) return true;
+  if (*start) g_prof_pool.push_back(*start);
+  if (*stop) g_prof_pool.push_back(*stop);
+  return false;
 }
 
-ProfileScope::~ProfileScope() {
-  if (!start_ || !stop_) return;
-  hipEventRecord(stop_, stream_);
+void profile_end(hipEvent_t start, hipEvent_t stop) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  g_prof_done.emplace_back(start_, stop_);
+  g_prof_done.emplace_back(start, stop);
 }
 
 }  // namespace luffy

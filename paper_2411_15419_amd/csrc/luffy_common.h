@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -78,19 +79,28 @@ struct Carver {
 
 inline int elem_bytes(int dtype) { return dtype == LUFFY_BF16 ? 2 : 4; }
 
-// Brackets one kernel launch with HIP events on its stream when that kernel
-// is the one selected by luffy_profile_kernel(); otherwise does nothing.
-class ProfileScope {
- public:
-  ProfileScope(const char* name, hipStream_t s);
-  ~ProfileScope();
-  ProfileScope(const ProfileScope&) = delete;
-  ProfileScope& operator=(const ProfileScope&) = delete;
+// Timing hook (luffy_profile_kernel): when `name` is the selected kernel,
+// profile_begin returns true with two events; launch() hands them to
+// hipExtLaunchKernel, which records them with the kernel's own dispatch (its
+// start and its end) rather than as separate stream commands, so the
+// measured interval is the kernel alone.  profile_end queues the pair for
+// luffy_profile_read.
+bool profile_begin(const char* name, hipEvent_t* start, hipEvent_t* stop);
+void profile_end(hipEvent_t start, hipEvent_t stop);
 
- private:
-  hipStream_t stream_;
-  hipEvent_t start_ = nullptr, stop_ = nullptr;
-};
+// kernel<<<grid, block, shmem, s>>>(args...), timed when selected.
+template <typename... KArgs, typename... Args>
+inline void launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem, hipStream_t s,
+                   Args... args) {
+  hipEvent_t start = nullptr, stop = nullptr;
+  if (profile_begin(name, &start, &stop)) {
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(shmem), s, start, stop, 0,
+                          static_cast<KArgs>(args)...);
+    profile_end(start, stop);
+  } else {
+    kernel<<<grid, block, shmem, s>>>(static_cast<KArgs>(args)...);
+  }
+}
 
 constexpr int kMaxExperts = 64;
 

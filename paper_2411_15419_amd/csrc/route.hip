@@ -445,23 +445,20 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
   const int gblocks = (T + kGateTok - 1) / kGateTok;
   const int nch = k * gblocks;
   {
-    ProfileScope prof_("gate", s);
     const int chunks = (T + kGateTok - 1) / kGateTok;
     if (dtype == LUFFY_BF16)
-      gate_kernel<true><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
-                                               ws.hist, ws.done, inv_norm);
+      launch("gate", gate_kernel<true>, chunks, 256, 0, s, x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
+             slot_pos, ws.hist, ws.done, inv_norm);
     else
-      gate_kernel<false><<<chunks, 256, 0, s>>>(x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos,
-                                                ws.hist, ws.done, inv_norm);
+      launch("gate", gate_kernel<false>, chunks, 256, 0, s, x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
+             slot_pos, ws.hist, ws.done, inv_norm);
   }
   {
-    ProfileScope prof_("slot_scan", s);
-    slot_scan_kernel<<<E, 1024, 0, s>>>(ws.hist, nch, E, C, offsets, ws.totals, ws.done);
+    launch("slot_scan", slot_scan_kernel, E, 1024, 0, s, ws.hist, nch, E, C, offsets, ws.totals, ws.done);
   }
   {
-    ProfileScope prof_("slot_scatter", s);
-    slot_scatter_kernel<<<static_cast<int>((S + 255) / 256), 256, 0, s>>>(
-        topk_idx, ws.hist, offsets, T, k, E, C, slot_pos, perm_token);
+    launch("slot_scatter", slot_scatter_kernel, static_cast<int>((S + 255) / 256), 256, 0, s, topk_idx, ws.hist,
+           offsets, T, k, E, C, slot_pos, perm_token);
   }
   return check_launch("luffy_route");
 }
