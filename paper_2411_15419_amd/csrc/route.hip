@@ -179,25 +179,50 @@ __global__ __launch_bounds__(256) void gate_kernel(
   }
   __syncthreads();
   {
-    // ---- top-k: wave w takes tokens 16w .. 16w+15 (lane = token)
-    const int tl_ = 16 * w + (lane & 15);
+    // ---- top-k: wave w takes tokens 16w .. 16w+15, four lanes per token
+    // (lane = 4*token + sub); lane sub scans experts sub, sub+4, ... and the
+    // four sorted top-3 lists are merged with two shuffle steps.  Order:
+    // larger logit first, lower expert index first among equal logits.
+    const int sub = lane & 3;
+    const int tl_ = 16 * w + (lane >> 2);
     const int t = t0 + tl_;
-    const bool valid = lane < 16 && t < T;
+    const bool valid = t < T;
     const float NEG = -INFINITY;
     float v0 = NEG, v1 = NEG, v2 = NEG;
-    int i0 = 0, i1 = 0;
-    for (int e0 = 0; e0 < E && valid; e0 += 8) {
-      float v8[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? logit[tl_][e0 + u] : NEG;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float v = v8[u];
-        const int e = e0 + u;
-        if (v > v0) { v2 = v1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
-        else if (v > v1) { v2 = v1; v1 = v; i1 = e; }
-        else if (v > v2) { v2 = v; }
+    int i0 = kMaxExperts, i1 = kMaxExperts, i2 = kMaxExperts;
+    if (valid) {
+      for (int e = sub; e < E; e += 4) {
+        const float v = logit[tl_][e];
+        if (v > v0) { v2 = v1; i2 = i1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
+        else if (v > v1) { v2 = v1; i2 = i1; v1 = v; i1 = e; }
+        else if (v > v2) { v2 = v; i2 = e; }
       }
+    }
+    auto before = [](float va, int ia, float vb, int ib) { return va > vb || (va == vb && ia < ib); };
+#pragma unroll
+    for (int o = 1; o <= 2; o <<= 1) {
+      const float u0 = __shfl_xor(v0, o, 64), u1 = __shfl_xor(v1, o, 64), u2 = __shfl_xor(v2, o, 64);
+      const int j0 = __shfl_xor(i0, o, 64), j1 = __shfl_xor(i1, o, 64), j2 = __shfl_xor(i2, o, 64);
+      // merge (v0,v1,v2) and (u0,u1,u2), both sorted, keeping the first three
+      float a[3] = {v0, v1, v2}, b[3] = {u0, u1, u2};
+      int ai[3] = {i0, i1, i2}, bi[3] = {j0, j1, j2};
+      float r[3];
+      int ri[3];
+      int pa = 0, pb = 0;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const float av = pa == 0 ? a[0] : (pa == 1 ? a[1] : a[2]);
+        const int aix = pa == 0 ? ai[0] : (pa == 1 ? ai[1] : ai[2]);
+        const float bv = pb == 0 ? b[0] : (pb == 1 ? b[1] : b[2]);
+        const int bix = pb == 0 ? bi[0] : (pb == 1 ? bi[1] : bi[2]);
+        const bool ta = before(av, aix, bv, bix);
+        r[q] = ta ? av : bv;
+        ri[q] = ta ? aix : bix;
+        pa += ta ? 1 : 0;
+        pb += ta ? 0 : 1;
+      }
+      v0 = r[0]; v1 = r[1]; v2 = r[2];
+      i0 = ri[0]; i1 = ri[1]; i2 = ri[2];
     }
     // A choice is re-decided in float64 when a deciding gap is within the
     // float32 error budget (about 1e-4 relative; the float32 sums here are
@@ -208,14 +233,16 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const bool amb = valid && ((k == 2 && v0 - v1 <= delta) || (vk1 - vk <= delta));
     uint64_t cand = 0;
     if (amb)
-      for (int e = 0; e < E; ++e)
+      for (int e = sub; e < E; e += 4)
         if (logit[tl_][e] >= vk1 - delta) cand |= 1ull << e;
-    uint64_t ambmask = __ballot(amb);
+    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 1, 64));
+    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 2, 64));
+    uint64_t ambmask = __ballot(amb && sub == 0);
     while (ambmask) {
-      const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;
+      const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;   // lane 4 * token
       ambmask &= ambmask - 1;
       const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
-      const size_t xt = static_cast<size_t>(t0 + 16 * w + tl) * d;
+      const size_t xt = static_cast<size_t>(t0 + 16 * w + (tl >> 2)) * d;
       double b0 = -INFINITY, b1 = -INFINITY;
       int j0 = 0, j1 = 0;
       for (int e = 0; e < E; ++e) {
@@ -247,30 +274,31 @@ __global__ __launch_bounds__(256) void gate_kernel(
         if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
         else if (s > b1) { b1 = s; j1 = e; }
       }
-      if (lane == tl) { i0 = j0; i1 = j1; }
+      if ((lane >> 2) == (tl >> 2)) { i0 = j0; i1 = j1; }
     }
     if (valid) {
+      // softmax denominator: e^(l - max) by the hardware exp2 (about 1 ulp),
+      // each lane over its quarter of the experts, then summed over the four
+      constexpr float kLog2e = 1.44269504088896341f;
       float den = 0.f;
-      for (int e0 = 0; e0 < E; e0 += 8) {
-        float v8[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v8[u] = e0 + u < E ? logit[tl_][e0 + u] : NEG;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) den += expf(v8[u] - v0);
+      for (int e = sub; e < E; e += 4) den += __builtin_amdgcn_exp2f((logit[tl_][e] - v0) * kLog2e);
+      den += __shfl_xor(den, 1, 64);
+      den += __shfl_xor(den, 2, 64);
+      if (sub == 0) {
+        if (k == 1) {
+          topk_idx[t] = i0;
+          topk_gate[t] = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e) / den;
+        } else {
+          const float ga = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e);
+          const float gb = __builtin_amdgcn_exp2f((logit[tl_][i1] - v0) * kLog2e);
+          topk_idx[2 * t] = i0;
+          topk_idx[2 * t + 1] = i1;
+          topk_gate[2 * t] = ga / (ga + gb);
+          topk_gate[2 * t + 1] = gb / (ga + gb);
+        }
+        choice[tl_][0] = i0;
+        choice[tl_][1] = i1;
       }
-      if (k == 1) {
-        topk_idx[t] = i0;
-        topk_gate[t] = expf(logit[tl_][i0] - v0) / den;
-      } else {
-        const float ga = expf(logit[tl_][i0] - v0);
-        const float gb = expf(logit[tl_][i1] - v0);
-        topk_idx[2 * t] = i0;
-        topk_idx[2 * t + 1] = i1;
-        topk_gate[2 * t] = ga / (ga + gb);
-        topk_gate[2 * t + 1] = gb / (ga + gb);
-      }
-      choice[tl_][0] = i0;
-      choice[tl_][1] = i1;
     }
   }
   __syncthreads();
