@@ -1,8 +1,8 @@
 // luffy_route: gate logits, top-k, gates and the stable dispatch order.
 //
 // Kernels (all on the caller's stream, no host synchronisation):
-//   gate_kernel      64 tokens per block; the four waves split the
-//                    contraction over d and accumulate 64 x E logit tiles
+//   gate_kernel      32 or 64 tokens per block; the four waves split the
+//                    contraction over d and accumulate tokens x E logit tiles
 //                    on MFMA (16x16x32); fp32: plain FMA.  The epilogue
 //                    takes top-k, gates and the float64 re-decision of close
 //                    calls, then ranks every slot among the block's slots of
@@ -21,8 +21,12 @@
 namespace luffy {
 namespace {
 
-constexpr int kGateTok = 64;     // tokens per gate block (= slots per chunk)
-constexpr int kGateA = kGateTok / 16;   // 16-token MFMA row blocks per gate block
+// Tokens per gate block (= slots per chunk of the histogram): 64, or 32
+// when 64 would leave most CUs without a block (T below 32768 makes fewer
+// than 512 blocks of 64).  Depends on T only, so workspace sizing and the
+// launches always agree.
+constexpr int kGateTokMax = 64;
+inline int gate_tokens(int T) { return T >= 32768 ? 64 : 32; }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
   // xor butterfly: every lane ends with the same, bit-identical sum
@@ -43,23 +47,24 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // slots in slot-id order.  With inv_norm set, the sums of squares of the
 // token columns each lane loads are reduced the same way and 1/|x_t| is
 // stored for the similarity pass (0 for a zero row).
-template <bool BF16>
+template <bool BF16, int TOK>
 __global__ __launch_bounds__(256) void gate_kernel(
     const void* __restrict__ xv, const void* __restrict__ wv,
     const float* __restrict__ bias_g, int T, int d, int E, int k,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate,
     int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done,
     float* __restrict__ inv_norm) {
-  __shared__ float part[4][kGateTok][kMaxExperts + 1];
-  __shared__ float sumsq[4][kGateTok];
+  constexpr int kGateA = TOK / 16;   // 16-token MFMA row blocks
+  __shared__ float part[4][TOK][kMaxExperts + 1];
+  __shared__ float sumsq[4][TOK];
   __shared__ float bias[kMaxExperts];
   __shared__ int cnt[kMaxExperts];
-  __shared__ int choice[kGateTok][2];
+  __shared__ int choice[TOK][2];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int nchunks = gridDim.x;
   const int ch = blockIdx.x;
-  const int t0 = ch * kGateTok;
+  const int t0 = ch * TOK;
   if (threadIdx.x < E) bias[threadIdx.x] = bias_g ? bias_g[threadIdx.x] : 0.f;
   if (blockIdx.x == 0 && threadIdx.x == 0) *scan_done = 0;   // armed for slot_scan_kernel
 
@@ -147,11 +152,12 @@ __global__ __launch_bounds__(256) void gate_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r) part[w][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
   } else {
-    // float32 inputs: lane = token, experts strided over the four waves
+    // float32 inputs: lane = token (lanes past TOK have none), experts
+    // strided over the four waves
     const float* X = static_cast<const float*>(xv);
     const float* W = static_cast<const float*>(wv);
     const int t = min(t0 + lane, T - 1);
-    for (int e = w; e < E; e += 4) {
+    for (int e = w; e < E && lane < TOK; e += 4) {
       float s = 0.f;
       for (int i = 0; i < d; ++i) s = fmaf(X[static_cast<size_t>(t) * d + i], W[static_cast<size_t>(e) * d + i], s);
       part[0][lane][e] = s;
@@ -159,21 +165,21 @@ __global__ __launch_bounds__(256) void gate_kernel(
       part[2][lane][e] = 0.f;
       part[3][lane][e] = 0.f;
     }
-    if (inv_norm) {
+    if (inv_norm && lane < TOK) {
       float s = 0.f;
       for (int i = w; i < d; i += 4) s = fmaf(X[static_cast<size_t>(t) * d + i], X[static_cast<size_t>(t) * d + i], s);
       sumsq[w][lane] = s;
     }
   }
   __syncthreads();
-  if (inv_norm && threadIdx.x < kGateTok && t0 + static_cast<int>(threadIdx.x) < T) {
+  if (inv_norm && threadIdx.x < TOK && t0 + static_cast<int>(threadIdx.x) < T) {
     const float ss = ((sumsq[0][threadIdx.x] + sumsq[1][threadIdx.x]) + sumsq[2][threadIdx.x]) + sumsq[3][threadIdx.x];
     inv_norm[t0 + threadIdx.x] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
   }
   // partial tiles summed in wave order into part[0], one (token, expert)
   // pair per thread at a time
   float (*logit)[kMaxExperts + 1] = part[0];
-  for (int i = threadIdx.x; i < kGateTok * E; i += 256) {
+  for (int i = threadIdx.x; i < TOK * E; i += 256) {
     const int tl = i / E, e = i - tl * E;
     logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
   }
@@ -184,9 +190,9 @@ __global__ __launch_bounds__(256) void gate_kernel(
     // four sorted top-3 lists are merged with two shuffle steps.  Order:
     // larger logit first, lower expert index first among equal logits.
     const int sub = lane & 3;
-    const int tl_ = 16 * w + (lane >> 2);
+    const int tl_ = min(16 * w + (lane >> 2), TOK - 1);
     const int t = t0 + tl_;
-    const bool valid = t < T;
+    const bool valid = 16 * w < TOK && t < T;
     const float NEG = -INFINITY;
     float v0 = NEG, v1 = NEG, v2 = NEG;
     int i0 = kMaxExperts, i1 = kMaxExperts, i2 = kMaxExperts;
@@ -242,7 +248,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
       const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;   // lane 4 * token
       ambmask &= ambmask - 1;
       const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
-      const size_t xt = static_cast<size_t>(t0 + 16 * w + (tl >> 2)) * d;
+      const size_t xt = static_cast<size_t>(t0 + min(16 * w + (tl >> 2), TOK - 1)) * d;
       double b0 = -INFINITY, b1 = -INFINITY;
       int j0 = 0, j1 = 0;
       for (int e = 0; e < E; ++e) {
@@ -304,7 +310,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
   __syncthreads();
   if (w != 0) return;
   const int t = t0 + lane;
-  const bool valid = lane < kGateTok && t < T;
+  const bool valid = lane < TOK && t < T;
   const int i0 = valid ? choice[lane][0] : 0, i1 = valid ? choice[lane][1] : 0;
   // stable rank of each slot among this chunk's slots of the same expert:
   // lanes holding the same expert are found with 7 ballots on its bits
@@ -388,7 +394,7 @@ __global__ __launch_bounds__(1024) void slot_scan_kernel(
 
 __global__ __launch_bounds__(256) void slot_scatter_kernel(
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ base,
-    const int32_t* __restrict__ offsets, int T, int k, int E, int C,
+    const int32_t* __restrict__ offsets, int T, int k, int E, int C, int tok,
     int32_t* __restrict__ slot_pos, int32_t* __restrict__ perm_token) {
   const long long s = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
   if (s >= static_cast<long long>(T) * k) return;
@@ -396,8 +402,8 @@ __global__ __launch_bounds__(256) void slot_scatter_kernel(
   const int t = static_cast<int>(s - static_cast<long long>(j) * T);
   const size_t o = static_cast<size_t>(t) * k + j;
   const int e = topk_idx[o];
-  const int nblk = (T + kGateTok - 1) / kGateTok;
-  const int pos = base[(static_cast<size_t>(j) * nblk + t / kGateTok) * E + e] + slot_pos[o];
+  const int nblk = (T + tok - 1) / tok;
+  const int pos = base[(static_cast<size_t>(j) * nblk + t / tok) * E + e] + slot_pos[o];
   if (C > 0 && pos >= C) {
     slot_pos[o] = -1;
   } else {
@@ -415,7 +421,7 @@ struct RouteWs {
 
 RouteWs carve_route(Carver& c, int T, int E, int k) {
   RouteWs w;
-  const long long nch = static_cast<long long>(k) * ((T + kGateTok - 1) / kGateTok);
+  const long long nch = static_cast<long long>(k) * ((T + gate_tokens(T) - 1) / gate_tokens(T));
   w.hist = c.take<int32_t>(static_cast<size_t>(nch) * E);
   w.totals = c.take<int>(E);
   w.done = c.take<int>(1);
@@ -470,23 +476,26 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
   RouteWs ws = carve_route(c, T, E, k);
   const int C = capacity_slots(T, k, E, capacity_factor);
   const long long S = static_cast<long long>(T) * k;
-  const int gblocks = (T + kGateTok - 1) / kGateTok;
+  const int tok = gate_tokens(T);
+  const int gblocks = (T + tok - 1) / tok;
   const int nch = k * gblocks;
   {
-    const int chunks = (T + kGateTok - 1) / kGateTok;
-    if (dtype == LUFFY_BF16)
-      launch("gate", gate_kernel<true>, chunks, 256, 0, s, x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
-             slot_pos, ws.hist, ws.done, inv_norm);
-    else
-      launch("gate", gate_kernel<false>, chunks, 256, 0, s, x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate,
-             slot_pos, ws.hist, ws.done, inv_norm);
+#define LUFFY_GATE_ARGS x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos, ws.hist, ws.done, inv_norm
+    if (dtype == LUFFY_BF16) {
+      if (tok == 32) launch("gate", gate_kernel<true, 32>, gblocks, 256, 0, s, LUFFY_GATE_ARGS);
+      else launch("gate", gate_kernel<true, kGateTokMax>, gblocks, 256, 0, s, LUFFY_GATE_ARGS);
+    } else {
+      if (tok == 32) launch("gate", gate_kernel<false, 32>, gblocks, 256, 0, s, LUFFY_GATE_ARGS);
+      else launch("gate", gate_kernel<false, kGateTokMax>, gblocks, 256, 0, s, LUFFY_GATE_ARGS);
+    }
+#undef LUFFY_GATE_ARGS
   }
   {
     launch("slot_scan", slot_scan_kernel, E, 1024, 0, s, ws.hist, nch, E, C, offsets, ws.totals, ws.done);
   }
   {
     launch("slot_scatter", slot_scatter_kernel, static_cast<int>((S + 255) / 256), 256, 0, s, topk_idx, ws.hist,
-           offsets, T, k, E, C, slot_pos, perm_token);
+           offsets, T, k, E, C, tok, slot_pos, perm_token);
   }
   return check_launch("luffy_route");
 }
