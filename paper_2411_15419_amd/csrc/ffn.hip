@@ -160,7 +160,8 @@ struct FfnTiles {
   }
   // Split-K parts per tile (second product only): the largest split of at
   // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
-  // the partial-tile slots and fewer work items than blocks.
+  // the partial-tile slots and fewer work items than blocks.  Always 1, 2
+  // or 4 (the reduction is instantiated for 2 and 4).
   __device__ __forceinline__ int parts(int grid, int nk) const {
     if (tiles <= 0) return 1;
     int s = 1;
@@ -281,25 +282,31 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
 // lane l hold columns 8g..8g+3 (l < 32) or 8g+4..8g+7 (l >= 32) of a
 // 32-column block of one token row; lanes l and l+32 share the row and swap
 // halves so that each stores 16 consecutive bf16 (two 16-byte stores).
-template <class G>
-__device__ __forceinline__ void reduce_unit(const float* __restrict__ slots, int S, int q, int row0, int rows,
-                                            int n0, int N, uint16_t* __restrict__ out) {
+template <class G, int S>
+__device__ __forceinline__ void reduce_unit(const float* __restrict__ slots, int q, int row0, int rows, int n0,
+                                            int N, uint16_t* __restrict__ out) {
   const int l = threadIdx.x & 63, hi = l >> 5;
   const int fn = q % G::FN, fm = (q / G::FN) % G::FM, w = q / (G::FN * G::FM);
   const int ml = G::q_row(G::wave_n(w), fn) + (l & 31);
   const int nb = G::wave_m(w) * G::WTM + 32 * fm;   // first column of the 32-column block
   if (ml >= rows || n0 + nb >= N) return;            // same for lanes l and l+32
   const float* src = slots + static_cast<size_t>(q) * 4 * 256 + l * 4;
+  // every part's four float4 units loaded before any is added (S is a
+  // template constant, so no load waits behind a branch), then summed in
+  // part order
+  float4 u[S][4];
+#pragma unroll
+  for (int p = 0; p < S; ++p)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) u[p][g] = *reinterpret_cast<const float4*>(src + p * kFfnSlotFloats + g * 256);
   float4 v[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    v[g] = *reinterpret_cast<const float4*>(src + g * 256);
+    v[g] = u[0][g];
 #pragma unroll
-    for (int p = 1; p < 4; ++p)
-      if (p < S) {
-        const float4 u = *reinterpret_cast<const float4*>(src + p * kFfnSlotFloats + g * 256);
-        v[g].x += u.x; v[g].y += u.y; v[g].z += u.z; v[g].w += u.w;
-      }
+    for (int p = 1; p < S; ++p) {
+      v[g].x += u[p][g].x; v[g].y += u[p][g].y; v[g].z += u[p][g].z; v[g].w += u[p][g].w;
+    }
   }
   // lane l (< 32) holds columns 8g..8g+3, lane l+32 columns 8g+4..8g+7:
   // the low lane keeps columns 0..15, the high lane 16..31
@@ -343,10 +350,14 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
     bool wide;
     map.decode(t, E, e, row0, rows, n0, wide);
     const float* slots = split_slots + static_cast<size_t>(t) * S * kFfnSlotFloats;
-    if (wide)
-      reduce_unit<FfnGemmWide>(slots, S, q, row0, rows, n0, N, out);
-    else if (q < FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN)
-      reduce_unit<FfnGemm>(slots, S, q, row0, rows, n0, N, out);
+    const bool narrow_unit = q < FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN;
+    if (S == 4) {
+      if (wide) reduce_unit<FfnGemmWide, 4>(slots, q, row0, rows, n0, N, out);
+      else if (narrow_unit) reduce_unit<FfnGemm, 4>(slots, q, row0, rows, n0, N, out);
+    } else {
+      if (wide) reduce_unit<FfnGemmWide, 2>(slots, q, row0, rows, n0, N, out);
+      else if (narrow_unit) reduce_unit<FfnGemm, 2>(slots, q, row0, rows, n0, N, out);
+    }
   }
 }
 
