@@ -149,20 +149,35 @@ struct TileCoord {
   int e, ti, tj, lo, n, W;
 };
 
+// Bucket of tile `tile` (the last e with tile_off[e] <= tile, skipping
+// empty buckets), its first tile, first slot and size.  One load per lane
+// (lane e holds bucket e, E <= 64) and a ballot: a single round trip instead
+// of a walk of dependent loads.  Called by whole waves.
+__device__ __forceinline__ void locate_bucket(int tile, const int32_t* __restrict__ tile_off,
+                                              const int32_t* __restrict__ offsets, int E, int& e, int& tbase,
+                                              int& lo, int& n) {
+  const int lane = threadIdx.x & 63;
+  const bool in = lane < E;
+  const int to = in ? tile_off[lane] : 0;
+  const int o0 = in ? offsets[lane] : 0;
+  const int o1 = in ? offsets[lane + 1] : 0;
+  e = __popcll(__ballot(in && lane >= 1 && to <= tile));
+  tbase = __builtin_amdgcn_readfirstlane(__shfl(to, e, 64));
+  lo = __builtin_amdgcn_readfirstlane(__shfl(o0, e, 64));
+  n = __builtin_amdgcn_readfirstlane(__shfl(o1, e, 64)) - lo;
+}
+
 __device__ __forceinline__ TileCoord decode_tile(int tile, const int32_t* __restrict__ tile_off,
                                                  const int32_t* __restrict__ offsets, int E) {
   TileCoord c;
-  int e = 0;
-  while (e + 1 < E && tile_off[e + 1] <= tile) ++e;
-  const int q = tile - tile_off[e];
+  int tbase;
+  locate_bucket(tile, tile_off, offsets, E, c.e, tbase, c.lo, c.n);
+  const int q = tile - tbase;
   int tj = static_cast<int>((sqrtf(8.0f * q + 1.0f) - 1.0f) * 0.5f);
   while (tj * (tj + 1) / 2 > q) --tj;
   while ((tj + 1) * (tj + 2) / 2 <= q) ++tj;
-  c.e = e;
   c.tj = tj;
   c.ti = q - tj * (tj + 1) / 2;
-  c.lo = offsets[e];
-  c.n = offsets[e + 1] - c.lo;
   c.W = (c.n + 63) / 64;
   return c;
 }
@@ -201,14 +216,11 @@ __device__ __forceinline__ void write_tile_words(const TileCoord& c, const uint1
 __device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t* __restrict__ tile_off,
                                                          const int32_t* __restrict__ offsets, int E) {
   TileCoord c;
-  int e = 0;
-  while (e + 1 < E && tile_off[e + 1] <= tile) ++e;
-  c.e = e;
-  c.lo = offsets[e];
-  c.n = offsets[e + 1] - c.lo;
+  int tbase;
+  locate_bucket(tile, tile_off, offsets, E, c.e, tbase, c.lo, c.n);
   c.W = (c.n + 63) / 64;
   const int nt = (c.n + kTile - 1) / kTile;
-  const int q = tile - tile_off[e];
+  const int q = tile - tbase;
   // tiles before column group g: 8g^2 + 2g
   int g = static_cast<int>((sqrtf(4.0f + 32.0f * q) - 2.0f) / 16.0f);
   while (g > 0 && 8 * g * g + 2 * g > q) --g;
