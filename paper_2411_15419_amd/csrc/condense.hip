@@ -626,19 +626,25 @@ __global__ __launch_bounds__(1024) void rep_local_kernel(const int32_t* __restri
                                                         const unsigned long long* __restrict__ claim,
                                                         int32_t* __restrict__ rep_of_pos,
                                                         int32_t* __restrict__ local,
-                                                        int32_t* __restrict__ bsum) {
+                                                        int32_t* __restrict__ bsum, int slot_cap) {
   __shared__ int wcnt[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int p = blockIdx.x * 1024 + tid;
+  // state and claim of this position are read together with the slot count
+  // (positions past the arrays' T*k entries read nothing)
+  const bool mine = p < slot_cap;
+  const int st = mine ? state[p] : 0;
+  const unsigned long long cl = mine ? claim[p] : 0ull;
+  const int failed = *err;
   const int S = offsets[E];
   const int base = blockIdx.x * 1024;
   if (base >= S) return;
-  const int p = base + tid;
   // rep_of_pos: absorbed -> claimed representative; otherwise itself (also
   // after a layout error, when nothing was decided)
   bool f = false;
   if (p < S) {
-    const bool absorbed = !*err && state[p] == kStateAbsorbed;
-    rep_of_pos[p] = absorbed ? static_cast<int>(~static_cast<unsigned int>(claim[p] & 0xffffffffull)) : p;
+    const bool absorbed = !failed && st == kStateAbsorbed;
+    rep_of_pos[p] = absorbed ? static_cast<int>(~static_cast<unsigned int>(cl & 0xffffffffull)) : p;
     f = !absorbed;
   }
   const uint64_t bal = __ballot(f);
@@ -661,10 +667,17 @@ __global__ __launch_bounds__(1024) void rep_finalize_kernel(
     const int32_t* __restrict__ offsets, int E, const int32_t* __restrict__ rep_of_pos,
     const int32_t* __restrict__ perm_token, const int32_t* __restrict__ local,
     const int32_t* __restrict__ bsum, int32_t* __restrict__ rep_row, int32_t* __restrict__ rep_token,
-    int32_t* __restrict__ rep_offsets, int max_blocks) {
-  extern __shared__ int bpre[];   // max_blocks + 1 entries
+    int32_t* __restrict__ rep_offsets, int slot_cap) {
+  extern __shared__ int bpre[];   // one entry per block of the grid, plus one
   __shared__ int wsum[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  // this thread's position: its representative and token are read before
+  // the block-count scan (positions past the arrays' T*k entries read
+  // nothing; those past the kept slot count are read and not used)
+  const int p = blockIdx.x * 1024 + tid;
+  const bool mine = p < slot_cap;
+  const int q_pre = mine ? rep_of_pos[p] : 0;
+  const int tok_pre = mine ? perm_token[p] : 0;
   const int S = offsets[E];
   const int nb = (S + 1023) / 1024;
   // exclusive prefix of bsum[0..nb) into bpre, 1024 at a time
@@ -691,18 +704,16 @@ __global__ __launch_bounds__(1024) void rep_finalize_kernel(
   }
   if (tid == 0) bpre[nb] = carry;
   __syncthreads();
-  const int p = blockIdx.x * 1024 + tid;
   if (p < S) {
-    const int q = rep_of_pos[p];
+    const int q = q_pre;
     const int row = bpre[q >> 10] + local[q];
     rep_row[p] = row;
-    if (q == p) rep_token[row] = perm_token[p];
+    if (q == p) rep_token[row] = tok_pre;
   }
   if (blockIdx.x == 0 && tid <= E) {
     const int o = offsets[tid];
     rep_offsets[tid] = o < S ? bpre[o >> 10] + local[o] : bpre[nb];
   }
-  (void)max_blocks;
 }
 
 __global__ __launch_bounds__(256) void gather_kernel(const uint8_t* __restrict__ x, size_t row_bytes,
@@ -836,11 +847,11 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   const int pos_blocks = (S + 1023) / 1024;
   {
     launch("rep_local", rep_local_kernel, pos_blocks, 1024, 0, s, offsets, E, ws.err, ws.state, ws.claim,
-           rep_of_pos, ws.local, ws.bsum);
+           rep_of_pos, ws.local, ws.bsum, S);
   }
   {
     launch("rep_finalize", rep_finalize_kernel, pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s, offsets, E,
-           rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, pos_blocks);
+           rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, S);
   }
   if (x_rep) {
     launch("gather", gather_kernel, wave_blocks, 256, 0, s, static_cast<const uint8_t*>(x),

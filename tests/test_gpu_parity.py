@@ -218,3 +218,36 @@ def test_activation_values_bf16(act):
     # away from rounding boundaries the device value rounds to the same bf16
     core = z >= -4.0
     assert np.mean(got[core] == ref[core]) > 0.99
+
+
+@pytest.mark.parametrize("d_ff", [512, 1024])
+def test_expert_ffn_tile_shapes(d_ff):
+    """The bf16 expert FFN on expert sizes that pick every tile shape: empty,
+    1 row, 255-257 rows (narrow tiles, one of them partial), 300 and 320
+    (one 320-row tile instead of 256 + rest), 321 (narrow again), 600 (two
+    320-row tiles instead of three) and 700 (narrow); representative rows
+    gathered through a permuted row index.  d_ff = 512 splits the second
+    product in 2, 1024 in 4.  Each output row within the bf16 tolerance of
+    the oracle's fp64 product on the same bf16 inputs."""
+    import torch
+    import paper_2411_15419_amd as L
+    from tests.layer_runner import TOL, rel_err_rows
+    sizes = [0, 1, 255, 256, 257, 300, 320, 321, 600, 700]
+    print_case("expert_ffn", d_ff=d_ff, sizes=sizes)
+    E, d = len(sizes), 256
+    R = sum(sizes)
+    rng = np.random.default_rng(11)
+    x_all = _bf16(rng.standard_normal((R + 100, d)))
+    row_index = rng.permutation(R + 100)[:R].astype(np.int32)
+    w1 = _bf16(0.05 * rng.standard_normal((E, d_ff, d)))
+    w2 = _bf16(0.05 * rng.standard_normal((E, d, d_ff)))
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    dev = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    y = torch.empty(R, d, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(L.expert_ffn_workspace_size(R, E, d_ff, L.LUFFY_BF16), dtype=torch.uint8, device="cuda")
+    L.luffy_expert_ffn(dev(x_all), dev(row_index, torch.int32), dev(offsets, torch.int32), dev(w1), dev(w2),
+                       "gelu", R, y, ws)
+    got = y.double().cpu().numpy()
+    ref = O.expert_ffn(x_all[row_index], offsets, w1, w2, "gelu")
+    err, _ = rel_err_rows(got, ref)
+    assert err.max() <= TOL["bf16"], f"max row rel err {err.max():.3g}"
