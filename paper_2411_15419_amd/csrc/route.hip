@@ -35,6 +35,173 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
+// Epilogue of a gate chunk of TOK tokens starting at t0, once logit[tl][e]
+// (bias included) is in LDS for every token: top-k, gates, the float64
+// re-decision of close calls; then wave 0 ranks every slot among the chunk's
+// slots of the same expert and writes the chunk's per-expert counts.  Called
+// by all four waves of the block; ends with the ranking done (no barrier).
+template <bool BF16, int TOK>
+__device__ __forceinline__ void gate_select(float (*logit)[kMaxExperts + 1], const float* bias, int* cnt,
+                                            int (*choice)[2], const void* __restrict__ xv,
+                                            const void* __restrict__ wv, int T, int d, int E, int k, int t0,
+                                            int ch, int nchunks, int32_t* __restrict__ topk_idx,
+                                            float* __restrict__ topk_gate, int32_t* __restrict__ slot_rank,
+                                            int32_t* __restrict__ hist) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  {
+    // ---- top-k: wave w takes tokens 16w .. 16w+15, four lanes per token
+    // (lane = 4*token + sub); lane sub scans experts sub, sub+4, ... and the
+    // four sorted top-3 lists are merged with two shuffle steps.  Order:
+    // larger logit first, lower expert index first among equal logits.
+    const int sub = lane & 3;
+    const int tl_ = min(16 * w + (lane >> 2), TOK - 1);
+    const int t = t0 + tl_;
+    const bool valid = 16 * w < TOK && t < T;
+    const float NEG = -INFINITY;
+    float v0 = NEG, v1 = NEG, v2 = NEG;
+    int i0 = kMaxExperts, i1 = kMaxExperts, i2 = kMaxExperts;
+    if (valid) {
+      for (int e = sub; e < E; e += 4) {
+        const float v = logit[tl_][e];
+        if (v > v0) { v2 = v1; i2 = i1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
+        else if (v > v1) { v2 = v1; i2 = i1; v1 = v; i1 = e; }
+        else if (v > v2) { v2 = v; i2 = e; }
+      }
+    }
+    auto before = [](float va, int ia, float vb, int ib) { return va > vb || (va == vb && ia < ib); };
+#pragma unroll
+    for (int o = 1; o <= 2; o <<= 1) {
+      const float u0 = __shfl_xor(v0, o, 64), u1 = __shfl_xor(v1, o, 64), u2 = __shfl_xor(v2, o, 64);
+      const int j0 = __shfl_xor(i0, o, 64), j1 = __shfl_xor(i1, o, 64), j2 = __shfl_xor(i2, o, 64);
+      // merge (v0,v1,v2) and (u0,u1,u2), both sorted, keeping the first three
+      float a[3] = {v0, v1, v2}, b[3] = {u0, u1, u2};
+      int ai[3] = {i0, i1, i2}, bi[3] = {j0, j1, j2};
+      float r[3];
+      int ri[3];
+      int pa = 0, pb = 0;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const float av = pa == 0 ? a[0] : (pa == 1 ? a[1] : a[2]);
+        const int aix = pa == 0 ? ai[0] : (pa == 1 ? ai[1] : ai[2]);
+        const float bv = pb == 0 ? b[0] : (pb == 1 ? b[1] : b[2]);
+        const int bix = pb == 0 ? bi[0] : (pb == 1 ? bi[1] : bi[2]);
+        const bool ta = before(av, aix, bv, bix);
+        r[q] = ta ? av : bv;
+        ri[q] = ta ? aix : bix;
+        pa += ta ? 1 : 0;
+        pb += ta ? 0 : 1;
+      }
+      v0 = r[0]; v1 = r[1]; v2 = r[2];
+      i0 = ri[0]; i1 = ri[1]; i2 = ri[2];
+    }
+    // A choice is re-decided in float64 when a deciding gap is within the
+    // float32 error budget (about 1e-4 relative; the float32 sums here are
+    // accurate to ~1e-6).
+    const float delta = ldexpf(1.0f + fabsf(v0), -12);
+    const float vk1 = (k == 1) ? v0 : v1;     // k-th largest
+    const float vk = (k == 1) ? v1 : v2;      // (k+1)-th largest, -inf if none
+    const bool amb = valid && ((k == 2 && v0 - v1 <= delta) || (vk1 - vk <= delta));
+    uint64_t cand = 0;
+    if (amb)
+      for (int e = sub; e < E; e += 4)
+        if (logit[tl_][e] >= vk1 - delta) cand |= 1ull << e;
+    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 1, 64));
+    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 2, 64));
+    uint64_t ambmask = __ballot(amb && sub == 0);
+    while (ambmask) {
+      const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;   // lane 4 * token
+      ambmask &= ambmask - 1;
+      const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
+      const size_t xt = static_cast<size_t>(t0 + min(16 * w + (tl >> 2), TOK - 1)) * d;
+      double b0 = -INFINITY, b1 = -INFINITY;
+      int j0 = 0, j1 = 0;
+      for (int e = 0; e < E; ++e) {
+        if (!((cm >> e) & 1ull)) continue;
+        double s = 0.0;
+        if constexpr (BF16) {
+          const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
+          const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
+          for (int c = lane * 8; c < d; c += 512) {
+            Pack16 xa, wa;
+            xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
+            wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
+          }
+        } else {
+          const float* xr = static_cast<const float*>(xv) + xt;
+          const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
+          for (int c = lane * 4; c < d; c += 256) {
+            const float4 xa = *reinterpret_cast<const float4*>(xr + c);
+            const float4 wa = *reinterpret_cast<const float4*>(wr + c);
+            s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
+                 static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
+          }
+        }
+        s = wave_sum_f64(s);
+        s += static_cast<double>(bias[e]);
+        if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
+        else if (s > b1) { b1 = s; j1 = e; }
+      }
+      if ((lane >> 2) == (tl >> 2)) { i0 = j0; i1 = j1; }
+    }
+    if (valid) {
+      // softmax denominator: e^(l - max) by the hardware exp2 (about 1 ulp),
+      // each lane over its quarter of the experts, then summed over the four
+      constexpr float kLog2e = 1.44269504088896341f;
+      float den = 0.f;
+      for (int e = sub; e < E; e += 4) den += __builtin_amdgcn_exp2f((logit[tl_][e] - v0) * kLog2e);
+      den += __shfl_xor(den, 1, 64);
+      den += __shfl_xor(den, 2, 64);
+      if (sub == 0) {
+        if (k == 1) {
+          topk_idx[t] = i0;
+          topk_gate[t] = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e) / den;
+        } else {
+          const float ga = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e);
+          const float gb = __builtin_amdgcn_exp2f((logit[tl_][i1] - v0) * kLog2e);
+          topk_idx[2 * t] = i0;
+          topk_idx[2 * t + 1] = i1;
+          topk_gate[2 * t] = ga / (ga + gb);
+          topk_gate[2 * t + 1] = gb / (ga + gb);
+        }
+        choice[tl_][0] = i0;
+        choice[tl_][1] = i1;
+      }
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    const int t = t0 + lane;
+    const bool valid = lane < TOK && t < T;
+    const int i0 = valid ? choice[lane][0] : 0, i1 = valid ? choice[lane][1] : 0;
+    // stable rank of each slot among this chunk's slots of the same expert:
+    // lanes holding the same expert are found with 7 ballots on its bits
+    int* cw = cnt;
+    for (int j = 0; j < k; ++j) {
+      const int e = valid ? (j == 0 ? i0 : i1) : -1;
+      const int key = e < 0 ? 127 : e;
+      uint64_t same = ~0ull;
+#pragma unroll
+      for (int b = 0; b < 7; ++b) {
+        const bool bit = (key >> b) & 1;
+        const uint64_t bb = __ballot(bit);
+        same &= bit ? bb : ~bb;
+      }
+      const int rank = __popcll(same & lanemask_lt());
+      if (lane < E) cw[lane] = 0;
+      __builtin_amdgcn_wave_barrier();
+      if (e >= 0 && rank == 0) cw[e] = __popcll(same);
+      __builtin_amdgcn_wave_barrier();
+      if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
+      if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
 // One block of four waves per chunk of 64 tokens.  bf16: wave w takes the
 // w-th quarter of the contraction over d and accumulates the 64 x E logits
 // of the chunk on MFMA (16x16x32: four 16-token blocks per 16-expert
@@ -184,156 +351,8 @@ __global__ __launch_bounds__(256) void gate_kernel(
     logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
   }
   __syncthreads();
-  {
-    // ---- top-k: wave w takes tokens 16w .. 16w+15, four lanes per token
-    // (lane = 4*token + sub); lane sub scans experts sub, sub+4, ... and the
-    // four sorted top-3 lists are merged with two shuffle steps.  Order:
-    // larger logit first, lower expert index first among equal logits.
-    const int sub = lane & 3;
-    const int tl_ = min(16 * w + (lane >> 2), TOK - 1);
-    const int t = t0 + tl_;
-    const bool valid = 16 * w < TOK && t < T;
-    const float NEG = -INFINITY;
-    float v0 = NEG, v1 = NEG, v2 = NEG;
-    int i0 = kMaxExperts, i1 = kMaxExperts, i2 = kMaxExperts;
-    if (valid) {
-      for (int e = sub; e < E; e += 4) {
-        const float v = logit[tl_][e];
-        if (v > v0) { v2 = v1; i2 = i1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
-        else if (v > v1) { v2 = v1; i2 = i1; v1 = v; i1 = e; }
-        else if (v > v2) { v2 = v; i2 = e; }
-      }
-    }
-    auto before = [](float va, int ia, float vb, int ib) { return va > vb || (va == vb && ia < ib); };
-#pragma unroll
-    for (int o = 1; o <= 2; o <<= 1) {
-      const float u0 = __shfl_xor(v0, o, 64), u1 = __shfl_xor(v1, o, 64), u2 = __shfl_xor(v2, o, 64);
-      const int j0 = __shfl_xor(i0, o, 64), j1 = __shfl_xor(i1, o, 64), j2 = __shfl_xor(i2, o, 64);
-      // merge (v0,v1,v2) and (u0,u1,u2), both sorted, keeping the first three
-      float a[3] = {v0, v1, v2}, b[3] = {u0, u1, u2};
-      int ai[3] = {i0, i1, i2}, bi[3] = {j0, j1, j2};
-      float r[3];
-      int ri[3];
-      int pa = 0, pb = 0;
-#pragma unroll
-      for (int q = 0; q < 3; ++q) {
-        const float av = pa == 0 ? a[0] : (pa == 1 ? a[1] : a[2]);
-        const int aix = pa == 0 ? ai[0] : (pa == 1 ? ai[1] : ai[2]);
-        const float bv = pb == 0 ? b[0] : (pb == 1 ? b[1] : b[2]);
-        const int bix = pb == 0 ? bi[0] : (pb == 1 ? bi[1] : bi[2]);
-        const bool ta = before(av, aix, bv, bix);
-        r[q] = ta ? av : bv;
-        ri[q] = ta ? aix : bix;
-        pa += ta ? 1 : 0;
-        pb += ta ? 0 : 1;
-      }
-      v0 = r[0]; v1 = r[1]; v2 = r[2];
-      i0 = ri[0]; i1 = ri[1]; i2 = ri[2];
-    }
-    // A choice is re-decided in float64 when a deciding gap is within the
-    // float32 error budget (about 1e-4 relative; the float32 sums here are
-    // accurate to ~1e-6).
-    const float delta = ldexpf(1.0f + fabsf(v0), -12);
-    const float vk1 = (k == 1) ? v0 : v1;     // k-th largest
-    const float vk = (k == 1) ? v1 : v2;      // (k+1)-th largest, -inf if none
-    const bool amb = valid && ((k == 2 && v0 - v1 <= delta) || (vk1 - vk <= delta));
-    uint64_t cand = 0;
-    if (amb)
-      for (int e = sub; e < E; e += 4)
-        if (logit[tl_][e] >= vk1 - delta) cand |= 1ull << e;
-    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 1, 64));
-    cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 2, 64));
-    uint64_t ambmask = __ballot(amb && sub == 0);
-    while (ambmask) {
-      const int tl = __ffsll(static_cast<long long>(ambmask)) - 1;   // lane 4 * token
-      ambmask &= ambmask - 1;
-      const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
-      const size_t xt = static_cast<size_t>(t0 + min(16 * w + (tl >> 2), TOK - 1)) * d;
-      double b0 = -INFINITY, b1 = -INFINITY;
-      int j0 = 0, j1 = 0;
-      for (int e = 0; e < E; ++e) {
-        if (!((cm >> e) & 1ull)) continue;
-        double s = 0.0;
-        if constexpr (BF16) {
-          const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
-          const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
-          for (int c = lane * 8; c < d; c += 512) {
-            Pack16 xa, wa;
-            xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
-            wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-              s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
-          }
-        } else {
-          const float* xr = static_cast<const float*>(xv) + xt;
-          const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
-          for (int c = lane * 4; c < d; c += 256) {
-            const float4 xa = *reinterpret_cast<const float4*>(xr + c);
-            const float4 wa = *reinterpret_cast<const float4*>(wr + c);
-            s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
-                 static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
-          }
-        }
-        s = wave_sum_f64(s);
-        s += static_cast<double>(bias[e]);
-        if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
-        else if (s > b1) { b1 = s; j1 = e; }
-      }
-      if ((lane >> 2) == (tl >> 2)) { i0 = j0; i1 = j1; }
-    }
-    if (valid) {
-      // softmax denominator: e^(l - max) by the hardware exp2 (about 1 ulp),
-      // each lane over its quarter of the experts, then summed over the four
-      constexpr float kLog2e = 1.44269504088896341f;
-      float den = 0.f;
-      for (int e = sub; e < E; e += 4) den += __builtin_amdgcn_exp2f((logit[tl_][e] - v0) * kLog2e);
-      den += __shfl_xor(den, 1, 64);
-      den += __shfl_xor(den, 2, 64);
-      if (sub == 0) {
-        if (k == 1) {
-          topk_idx[t] = i0;
-          topk_gate[t] = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e) / den;
-        } else {
-          const float ga = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e);
-          const float gb = __builtin_amdgcn_exp2f((logit[tl_][i1] - v0) * kLog2e);
-          topk_idx[2 * t] = i0;
-          topk_idx[2 * t + 1] = i1;
-          topk_gate[2 * t] = ga / (ga + gb);
-          topk_gate[2 * t + 1] = gb / (ga + gb);
-        }
-        choice[tl_][0] = i0;
-        choice[tl_][1] = i1;
-      }
-    }
-  }
-  __syncthreads();
-  if (w != 0) return;
-  const int t = t0 + lane;
-  const bool valid = lane < TOK && t < T;
-  const int i0 = valid ? choice[lane][0] : 0, i1 = valid ? choice[lane][1] : 0;
-  // stable rank of each slot among this chunk's slots of the same expert:
-  // lanes holding the same expert are found with 7 ballots on its bits
-  int* cw = cnt;
-  for (int j = 0; j < k; ++j) {
-    const int e = valid ? (j == 0 ? i0 : i1) : -1;
-    const int key = e < 0 ? 127 : e;
-    uint64_t same = ~0ull;
-#pragma unroll
-    for (int b = 0; b < 7; ++b) {
-      const bool bit = (key >> b) & 1;
-      const uint64_t bb = __ballot(bit);
-      same &= bit ? bb : ~bb;
-    }
-    const int rank = __popcll(same & lanemask_lt());
-    if (lane < E) cw[lane] = 0;
-    __builtin_amdgcn_wave_barrier();
-    if (e >= 0 && rank == 0) cw[e] = __popcll(same);
-    __builtin_amdgcn_wave_barrier();
-    if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
-    if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
-    __builtin_amdgcn_wave_barrier();
-  }
+  gate_select<BF16, TOK>(logit, bias, cnt, choice, xv, wv, T, d, E, k, t0, ch, nchunks, topk_idx, topk_gate,
+                         slot_rank, hist);
 }
 
 // One block per expert: exclusive scan of that expert's chunk counts (in

@@ -251,3 +251,37 @@ def test_expert_ffn_tile_shapes(d_ff):
     ref = O.expert_ffn(x_all[row_index], offsets, w1, w2, "gelu")
     err, _ = rel_err_rows(got, ref)
     assert err.max() <= TOL["bf16"], f"max row rel err {err.max():.3g}"
+
+
+@pytest.mark.parametrize("d", [256, 2560])
+def test_route_large_batch(d):
+    """luffy_route at T = 32768, where the gate takes 64-token chunks (the
+    reduced layer tests use 32): top-k, gates, dispatch with capacity, and
+    1/|x_t| against the oracle.  E = 24 leaves half of the second 16-expert
+    MFMA block unused; d = 2560 is not a power of two."""
+    import torch
+    import paper_2411_15419_amd as L
+    T, E, k, cf = 32768, 24, 2, 1.25
+    print_case("route", T=T, d=d, E=E)
+    rng = np.random.default_rng(13)
+    x = _bf16(rng.standard_normal((T, d)))
+    wg = _bf16(rng.standard_normal((E, d)) / np.sqrt(d))
+    bg = (0.1 * rng.standard_normal(E)).astype(np.float32)
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    i32 = dict(dtype=torch.int32, device="cuda")
+    ti, sp = torch.empty(T, k, **i32), torch.empty(T, k, **i32)
+    tg = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    pt, off = torch.empty(T * k, **i32), torch.empty(E + 1, **i32)
+    nrm = torch.empty(T, dtype=torch.float32, device="cuda")
+    ws = torch.empty(L.route_workspace_size(T, E, k), dtype=torch.uint8, device="cuda")
+    L.luffy_route(dev(x, torch.bfloat16), dev(wg, torch.bfloat16), dev(bg, torch.float32), k, cf, ti, tg, sp, pt,
+                  off, ws, inv_norm=nrm)
+    o_idx, o_gate, _ = O.gate(x, wg, bg, k)
+    o_off, o_perm, o_pos = O.dispatch(o_idx, E, O.capacity_of(T, k, E, cf))
+    assert np.array_equal(ti.cpu().numpy(), o_idx), "topk_idx differs"
+    assert np.allclose(tg.cpu().numpy(), o_gate, rtol=0, atol=2e-6)
+    assert np.array_equal(off.cpu().numpy(), o_off), "offsets differ"
+    assert np.array_equal(sp.cpu().numpy(), o_pos), "slot_pos differs"
+    assert np.array_equal(pt.cpu().numpy()[:o_off[-1]], o_perm), "perm_token differs"
+    ref = 1.0 / np.sqrt((x.astype(np.float64) ** 2).sum(axis=1))
+    assert np.allclose(nrm.cpu().numpy(), ref, rtol=2e-6, atol=0)
