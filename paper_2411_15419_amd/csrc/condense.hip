@@ -389,6 +389,25 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
     const int32_t* pt = perm_token + c.lo;
     if (tid < kTileF32) inv_a[tid] = inv_norm[pt[min(c.ti * kTileF32 + tid, c.n - 1)]];
     else inv_b[tid - kTileF32] = inv_norm[pt[min(c.tj * kTileF32 + tid - kTileF32, c.n - 1)]];
+    // staged element i of this thread: tile row r0 + 16i, column kk; the
+    // token rows are looked up once per tile and the next chunk is loaded
+    // into registers while the current one is multiplied
+    constexpr int PER = kTileF32 * KC / 256;
+    const int kk = tid % KC, r0 = tid / KC;
+    const float* pp[PER];
+    const float* qp[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int r = r0 + (256 / KC) * i;
+      pp[i] = X + static_cast<size_t>(pt[min(c.ti * kTileF32 + r, c.n - 1)]) * d + kk;
+      qp[i] = X + static_cast<size_t>(pt[min(c.tj * kTileF32 + r, c.n - 1)]) * d + kk;
+    }
+    float vp[PER], vq[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      vp[i] = pp[i][0];
+      vq[i] = qp[i][0];
+    }
     float acc[8][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -396,21 +415,26 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
     for (int k0 = 0; k0 < d; k0 += KC) {
       __syncthreads();
-      for (int idx = tid; idx < kTileF32 * KC; idx += 256) {
-        const int r = idx / KC, kk = idx % KC;
-        const int a = min(c.ti * kTileF32 + r, c.n - 1);
-        const int b = min(c.tj * kTileF32 + r, c.n - 1);
-        Ps[r][kk] = X[static_cast<size_t>(pt[a]) * d + k0 + kk];
-        Qs[r][kk] = X[static_cast<size_t>(pt[b]) * d + k0 + kk];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        Ps[r0 + (256 / KC) * i][kk] = vp[i];
+        Qs[r0 + (256 / KC) * i][kk] = vq[i];
       }
       __syncthreads();
+      if (k0 + KC < d) {
 #pragma unroll
-      for (int kk = 0; kk < KC; ++kk) {
+        for (int i = 0; i < PER; ++i) {
+          vp[i] = pp[i][k0 + KC];
+          vq[i] = qp[i][k0 + KC];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
         float pa[8], qb[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) pa[i] = Ps[rb + i][kk];
+        for (int i = 0; i < 8; ++i) pa[i] = Ps[rb + i][k];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) qb[j] = Qs[cb + j][kk];
+        for (int j = 0; j < 8; ++j) qb[j] = Qs[cb + j][k];
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll

@@ -363,12 +363,17 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
 
 constexpr int kF32Tile = 64;
 
+// float32 products: 64 x 64 tiles, 4 x 4 outputs per thread, K in chunks of
+// 32 through LDS.  Each thread stages 8 elements of each operand per chunk;
+// its rows are fixed for the tile (looked up once), and the next chunk's
+// elements are loaded into registers while the current one is multiplied.
 template <int ACT, bool FIRST>
 __global__ __launch_bounds__(256) void ffn_kernel_f32(
     const float* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
     const float* __restrict__ W, float* __restrict__ out) {
-  constexpr int KC = 16;
+  constexpr int KC = 32;
+  constexpr int PER = kF32Tile * KC / 256;   // staged elements per thread and operand
   __shared__ float As[kF32Tile][KC + 1];
   __shared__ float Bs[kF32Tile][KC + 1];
   int e, row0, rows;
@@ -377,25 +382,46 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
   const int n0 = blockIdx.y * kF32Tile;
   const float* We = W + static_cast<size_t>(e) * N * K;
   const int rb = (tid >> 4) * 4, cb = (tid & 15) * 4;
+  // staged element i of this thread: row r0 + 8i (r0 = tid / 32), column kk
+  const int kk = tid % KC, r0 = tid / KC;
+  const float* ap[PER];
+  const float* bp[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int r = r0 + 8 * i;
+    const int m = row0 + min(r, rows - 1);
+    ap[i] = A + static_cast<size_t>(row_index ? row_index[m] : m) * K + kk;
+    bp[i] = We + static_cast<size_t>(min(n0 + r, N - 1)) * K + kk;
+  }
+  float va[PER], vb[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    va[i] = ap[i][0];
+    vb[i] = bp[i][0];
+  }
   float acc[4][4] = {};
   for (int k0 = 0; k0 < K; k0 += KC) {
     __syncthreads();
-    for (int idx = tid; idx < kF32Tile * KC; idx += 256) {
-      const int r = idx / KC, kk = idx % KC;
-      const int m = row0 + min(r, rows - 1);
-      const int src = row_index ? row_index[m] : m;
-      As[r][kk] = A[static_cast<size_t>(src) * K + k0 + kk];
-      const int n = min(n0 + r, N - 1);
-      Bs[r][kk] = We[static_cast<size_t>(n) * K + k0 + kk];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      As[r0 + 8 * i][kk] = va[i];
+      Bs[r0 + 8 * i][kk] = vb[i];
     }
     __syncthreads();
+    if (k0 + KC < K) {
 #pragma unroll
-    for (int kk = 0; kk < KC; ++kk) {
+      for (int i = 0; i < PER; ++i) {
+        va[i] = ap[i][k0 + KC];
+        vb[i] = bp[i][k0 + KC];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
       float a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[rb + i][kk];
+      for (int i = 0; i < 4; ++i) a[i] = As[rb + i][c];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[cb + j][kk];
+      for (int j = 0; j < 4; ++j) b[j] = Bs[cb + j][c];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
