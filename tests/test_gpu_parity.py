@@ -220,21 +220,23 @@ def test_activation_values_bf16(act):
     assert np.mean(got[core] == ref[core]) > 0.99
 
 
-@pytest.mark.parametrize("d_ff", [512, 1024])
-def test_expert_ffn_tile_shapes(d_ff):
+@pytest.mark.parametrize("d,d_ff", [(256, 512), (256, 1024), (64, 64), (128, 192), (192, 576), (64, 2048)])
+def test_expert_ffn_tile_shapes(d, d_ff):
     """The bf16 expert FFN on expert sizes that pick every tile shape: empty,
     1 row, 255-257 rows (narrow tiles, one of them partial), 300 and 320
     (one 320-row tile instead of 256 + rest), 321 (narrow again), 600 (two
     320-row tiles instead of three) and 700 (narrow); representative rows
     gathered through a permuted row index.  d_ff = 512 splits the second
-    product in 2, 1024 in 4.  Each output row within the bf16 tolerance of
-    the oracle's fp64 product on the same bf16 inputs."""
+    product in 2, 1024 and 2048 in 4, 576 in 2 parts of 4 and 5 64-wide
+    K stages; d and d_ff of 64 to 192 give products of 1 to 3 stages (the
+    pipeline's prologue and tail only).  Each output row within the bf16
+    tolerance of the oracle's fp64 product on the same bf16 inputs."""
     import torch
     import paper_2411_15419_amd as L
     from tests.layer_runner import TOL, rel_err_rows
     sizes = [0, 1, 255, 256, 257, 300, 320, 321, 600, 700]
-    print_case("expert_ffn", d_ff=d_ff, sizes=sizes)
-    E, d = len(sizes), 256
+    print_case("expert_ffn", d=d, d_ff=d_ff, sizes=sizes)
+    E = len(sizes)
     R = sum(sizes)
     rng = np.random.default_rng(11)
     x_all = _bf16(rng.standard_normal((R + 100, d)))
