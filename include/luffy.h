@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUFFY_ABI_VERSION 2
+#define LUFFY_ABI_VERSION 3
 
 typedef enum {
   LUFFY_OK = 0,
@@ -185,6 +185,25 @@ int luffy_expert_ffn(const void* x, const int32_t* row_index,
 int luffy_combine(const void* y_rep, const int32_t* rep_row,
                   const int32_t* slot_pos, const float* topk_gate,
                   int T, int k, int d, int dtype, void* y, void* stream);
+
+/* ------------------------------------------------------------------------
+ * luffy_adaptive_threshold - the condensation threshold h_t of training
+ * iteration t from the losses of the first and of the previous iteration
+ * (Sec. 5.2, Eq. 2):
+ *   l_norm = (l_ini - l_prev) / l_ini,   h_t = 1 / (1 + exp(l_norm)).
+ * Taken as printed: h_t = 1/2 while the loss has not moved, and it falls
+ * toward 1/(1+e) (about 0.269) as the loss falls to 0; a loss above l_ini
+ * gives h_t above 1/2.  For the first iteration, which has no previous loss,
+ * pass l_prev = l_ini (h_1 = 1/2).  The result is what luffy_condense takes
+ * as `threshold` for that iteration.  Host arithmetic in double precision;
+ * no device work, no stream.
+ *   l_ini   loss of the first iteration: finite and non-zero;
+ *   l_prev  loss of the previous iteration: finite;
+ *   h_out   host pointer that receives h_t, in [0, 1].
+ * Returns LUFFY_E_INVALID, leaving *h_out unchanged, for a null h_out, a zero
+ * or non-finite l_ini or a non-finite l_prev.
+ * ---------------------------------------------------------------------- */
+int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
 
 /* ------------------------------------------------------------------------
  * Measurement hook (not part of the layer).  luffy_profile_kernel(name)

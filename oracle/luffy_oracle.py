@@ -56,6 +56,7 @@ from scipy.special import erf as _erf
 __all__ = [
     "gate", "dispatch", "cosine", "adjacency", "greedy", "condense",
     "activation", "expert_ffn", "combine", "moe_layer", "capacity_of",
+    "adaptive_threshold",
 ]
 
 
@@ -312,3 +313,22 @@ def moe_layer(x, w_g, b_g, w1, w2, *, k, h, act, capacity_factor=0.0,
         out.y_rep = expert_ffn(x_rep, cz.rep_offsets, w1, w2, act)
         out.y = combine(out.y_rep, cz.rep_row, slot_pos, topk_gate)
     return out
+
+
+# --------------------------------------------------------------------------
+# Adaptive threshold (Sec. 5.2, Eq. 2)
+# --------------------------------------------------------------------------
+def adaptive_threshold(l_ini, l_prev):
+    """Sec. 5.2 Eq. 2, as printed: the loss decrease since the first
+    iteration, normalised by the first loss, through 1/(1 + e^x).
+
+    l_norm = (l_ini - l_prev) / l_ini;  h_t = 1 / (1 + exp(l_norm)).
+    The first iteration has no previous loss and takes l_prev = l_ini
+    (h = 1/2)."""
+    l_ini = float(l_ini)
+    l_prev = float(l_prev)
+    if not math.isfinite(l_ini) or l_ini == 0.0 or not math.isfinite(l_prev):
+        raise ValueError("l_ini must be finite and non-zero, l_prev finite")
+    l_norm = (l_ini - l_prev) / l_ini
+    return 1.0 / (1.0 + math.exp(l_norm))
+

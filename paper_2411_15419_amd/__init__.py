@@ -21,7 +21,7 @@ __all__ = [
     "LUFFY_ACT_SILU", "luffy_route", "luffy_condense", "luffy_expert_ffn",
     "luffy_combine", "route_workspace_size", "condense_workspace_size",
     "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
-    "profile_read", "KERNELS",
+    "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
@@ -46,6 +46,7 @@ _SIGS = {
     "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                                   _c_int, _c_int, _vp, _vp, _c_size, _vp]),
     "luffy_combine": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
+    "luffy_adaptive_threshold": (_c_int, [ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_double)]),
     "luffy_profile_kernel": (_c_int, [ctypes.c_char_p]),
     "luffy_profile_read": (_c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_c_int)]),
 }
@@ -163,6 +164,36 @@ def luffy_combine(y_rep, rep_row, slot_pos, topk_gate, y, stream=None):
     lib = load_library()
     _check(lib.luffy_combine(_p(y_rep), _p(rep_row), _p(slot_pos), _p(topk_gate), T, k, d,
                              _dtype_code(y), _p(y), _stream(stream)), "luffy_combine")
+
+
+def adaptive_threshold(l_ini: float, l_prev: float) -> float:
+    """h_t of Sec. 5.2 Eq. 2 from the first and the previous loss
+    (luffy_adaptive_threshold)."""
+    h = ctypes.c_double()
+    _check(load_library().luffy_adaptive_threshold(float(l_ini), float(l_prev), ctypes.byref(h)),
+           "luffy_adaptive_threshold")
+    return h.value
+
+
+class AdaptiveThreshold:
+    """The threshold schedule of Sec. 5.2 over a training run: threshold()
+    gives h_t for the coming iteration, record(loss) takes that iteration's
+    loss.  The first recorded loss is l_ini; before any loss, and for the
+    iteration after the first, h_t = 1/2."""
+
+    def __init__(self):
+        self.l_ini: Optional[float] = None
+        self.l_prev: Optional[float] = None
+
+    def threshold(self) -> float:
+        if self.l_ini is None:
+            return 0.5
+        return adaptive_threshold(self.l_ini, self.l_prev)
+
+    def record(self, loss: float) -> None:
+        if self.l_ini is None:
+            self.l_ini = float(loss)
+        self.l_prev = float(loss)
 
 
 def profile_kernel(name: Optional[str]) -> None:

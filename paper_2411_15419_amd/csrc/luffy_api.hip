@@ -1,5 +1,6 @@
 // Status strings, error reporting and ABI version.
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -131,6 +132,18 @@ extern "C" int luffy_profile_read(double* total_ms, int* launches) {
   *total_ms = sum;
   *launches = n;
   return status;
+}
+
+// Eq. 2 of Sec. 5.2, in double precision on the host.
+extern "C" int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out) {
+  if (!h_out) return luffy::fail(LUFFY_E_INVALID, "luffy_adaptive_threshold: h_out is null");
+  if (!std::isfinite(l_ini) || l_ini == 0.0)
+    return luffy::fail(LUFFY_E_INVALID, "luffy_adaptive_threshold: l_ini=%g must be finite and non-zero", l_ini);
+  if (!std::isfinite(l_prev))
+    return luffy::fail(LUFFY_E_INVALID, "luffy_adaptive_threshold: l_prev=%g must be finite", l_prev);
+  const double l_norm = (l_ini - l_prev) / l_ini;
+  *h_out = 1.0 / (1.0 + std::exp(l_norm));
+  return LUFFY_OK;
 }
 
 extern "C" int luffy_abi_version(void) { return LUFFY_ABI_VERSION; }
