@@ -56,7 +56,7 @@ from scipy.special import erf as _erf
 __all__ = [
     "gate", "dispatch", "cosine", "adjacency", "greedy", "condense",
     "activation", "expert_ffn", "combine", "moe_layer", "capacity_of",
-    "adaptive_threshold",
+    "adaptive_threshold", "activation_grad", "combine_backward", "expert_ffn_backward",
 ]
 
 
@@ -331,4 +331,76 @@ def adaptive_threshold(l_ini, l_prev):
         raise ValueError("l_ini must be finite and non-zero, l_prev finite")
     l_norm = (l_ini - l_prev) / l_ini
     return 1.0 / (1.0 + math.exp(l_norm))
+
+
+# --------------------------------------------------------------------------
+# Backward of the condensed layer (training, Sec. 3 and Sec. 7: the layer is
+# trained).  The paper does not say how gradients pass a condensed token.
+# Reading: the gradient of the function the forward computes, with every
+# discrete decision (routing, capacity, graph, representatives) held fixed:
+# a condensed slot's output is its representative's expert output, so its
+# gradient flows into that representative's row, and its own embedding
+# receives none through the expert.
+# --------------------------------------------------------------------------
+def combine_backward(dy, y_rep, rep_row, slot_pos, topk_gate):
+    """Transpose of combine for a given dy = dL/dy [T, d]:
+
+    dgate[t, j]  = <dy[t], Y_rep[rep_row[slot_pos[t, j]]]>  (0 for a dropped slot)
+    dy_rep[r]    = sum over kept slots (t, j) with rep_row[slot_pos[t, j]] = r
+                   of gate[t, j] * dy[t]
+    (every slot of a condensed group adds its own gate-weighted gradient to
+    the group's representative row)."""
+    dy = np.asarray(dy, np.float64)
+    y_rep = np.asarray(y_rep, np.float64)
+    T, k = slot_pos.shape
+    dy_rep = np.zeros_like(y_rep)
+    dgate = np.zeros((T, k), np.float64)
+    for t in range(T):
+        for j in range(k):
+            p = int(slot_pos[t, j])
+            if p < 0:
+                continue
+            r = int(rep_row[p])
+            dgate[t, j] = float(dy[t] @ y_rep[r])
+            dy_rep[r] += float(topk_gate[t, j]) * dy[t]
+    return dy_rep, dgate
+
+
+def activation_grad(z, act):
+    """Derivative of the expert activation: GELU'(z) = Phi(z) + z phi(z)
+    (Phi, phi: the standard normal CDF and density), SiLU'(z) =
+    s(z) (1 + z (1 - s(z))) with s the logistic function."""
+    z = np.asarray(z, np.float64)
+    if act == "gelu":
+        return 0.5 * (1.0 + _erf(z / math.sqrt(2.0))) + z * np.exp(-0.5 * z * z) / math.sqrt(2.0 * math.pi)
+    if act == "silu":
+        sg = 1.0 / (1.0 + np.exp(-z))
+        return sg * (1.0 + z * (1.0 - sg))
+    raise ValueError(act)
+
+
+def expert_ffn_backward(x_rep, rep_offsets, w1, w2, act, dy_rep):
+    """Gradients of Y_rep[r] = W2_e act(W1_e x_r) for dy_rep = dL/dY_rep:
+    with Z = X_e W1_e^T, A = act(Z), dA = dY_e W2_e, dZ = dA * act'(Z):
+    dx_rep = dZ W1_e, dW1_e = dZ^T X_e, dW2_e = dY_e^T A (zero for an
+    expert without representatives)."""
+    x_rep = np.asarray(x_rep, np.float64)
+    dy_rep = np.asarray(dy_rep, np.float64)
+    E = len(rep_offsets) - 1
+    dx = np.zeros_like(x_rep)
+    dw1 = np.zeros(np.shape(w1), np.float64)
+    dw2 = np.zeros(np.shape(w2), np.float64)
+    for e in range(E):
+        lo, hi = int(rep_offsets[e]), int(rep_offsets[e + 1])
+        if hi == lo:
+            continue
+        W1 = np.asarray(w1[e], np.float64)
+        W2 = np.asarray(w2[e], np.float64)
+        z = x_rep[lo:hi] @ W1.T
+        a = activation(z, act)
+        dz = (dy_rep[lo:hi] @ W2) * activation_grad(z, act)
+        dx[lo:hi] = dz @ W1
+        dw1[e] = dz.T @ x_rep[lo:hi]
+        dw2[e] = dy_rep[lo:hi].T @ a
+    return dx, dw1, dw2
 

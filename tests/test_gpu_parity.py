@@ -287,3 +287,54 @@ def test_route_large_batch(d):
     assert np.array_equal(pt.cpu().numpy()[:o_off[-1]], o_perm), "perm_token differs"
     ref = 1.0 / np.sqrt((x.astype(np.float64) ** 2).sum(axis=1))
     assert np.allclose(nrm.cpu().numpy(), ref, rtol=2e-6, atol=0)
+
+
+def test_graph_replay_matches_eager():
+    """The whole layer captured once in a HIP graph (every call is
+    asynchronous, allocates nothing and clears its scratch with kernels, so
+    it captures) and replayed four times, with unrelated eager work and a
+    synchronisation between replays and the input changed in place before
+    two of them: every replay equals the eager run on the same input,
+    indices and outputs bit for bit."""
+    import torch
+    from tests.layer_runner import make_layer, upload
+    inp = G.make_inputs("c2", seed=3, **REDUCED["c2"])
+    print_case("graph_replay", **REDUCED["c2"])
+    dev = upload(inp)
+    x = dev["x"]
+    x_other = torch.flip(x, dims=[0]).contiguous()
+    x_orig = x.clone()
+    layer = make_layer(inp, dev)
+    names = ["topk_idx", "slot_pos", "perm_token", "offsets", "rep_of_pos", "rep_row",
+             "rep_offsets", "rep_token", "y"]
+
+    def snapshot():
+        torch.cuda.synchronize()
+        return {n: getattr(layer.buf, n).clone() for n in names}
+
+    def eager(src):
+        x.copy_(src)
+        layer(x)
+        return snapshot()
+
+    # warm up on a side stream, as capture requires
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        layer(x)
+    torch.cuda.current_stream().wait_stream(s)
+    ref = {"orig": eager(x_orig), "other": eager(x_other)}
+    x.copy_(x_orig)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layer(x)
+    junk = torch.zeros(1 << 20, device="cuda")
+    for i, which in enumerate(["orig", "orig", "other", "orig"]):
+        x.copy_(x_orig if which == "orig" else x_other)
+        junk.add_(1.0)                     # unrelated eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        got = snapshot()
+        for n in names:
+            assert torch.equal(got[n], ref[which][n]), f"replay {i} ({which}): {n} differs"
