@@ -187,6 +187,55 @@ int luffy_combine(const void* y_rep, const int32_t* rep_row,
                   int T, int k, int d, int dtype, void* y, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Backward of the condensed layer.  The paper trains the layer but does not
+ * say how a gradient passes a condensed token; these calls differentiate the
+ * function the forward computes with every discrete decision (routing,
+ * capacity, similarity graph, representatives) held fixed, so a condensed
+ * slot's gradient reaches its representative's row.
+ *
+ * luffy_combine_backward - transpose of luffy_combine (Sec. 2.1 combine,
+ * Sec. 6 token_to_token), for dy = dL/dy:
+ *   dgate[t,j] = <dy[t], y_rep[r]>,  r = rep_row[slot_pos[t,j]]  (0 if dropped)
+ *   dy_rep[r]  = sum over kept slots (t,j) of representative r of
+ *                topk_gate[t,j] * dy[t]
+ *   dy [T, d] dtype; y_rep [max_rows, d] dtype (the forward's output);
+ *   rep_row, perm_token [T*k], slot_pos, topk_gate [T, k], offsets,
+ *   rep_offsets [E+1], all as the forward left them (R = rep_offsets[E]
+ *   rows in use, R <= max_rows); dy_rep [max_rows, d] dtype: rows 0..R-1
+ *   written; dgate [T, k] float32.  E <= 64.
+ * Row sums are float32 in no fixed order (several slots of a group may add
+ * at once), so dy_rep may differ in the last bits between runs; dgate is a
+ * fixed-order sum.  No workspace.
+ * ---------------------------------------------------------------------- */
+int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep_row,
+                           const int32_t* perm_token, const int32_t* slot_pos,
+                           const float* topk_gate, const int32_t* offsets,
+                           const int32_t* rep_offsets, int E, int T, int k, int d, int dtype,
+                           int max_rows, void* dy_rep, float* dgate, void* stream);
+
+/* ------------------------------------------------------------------------
+ * luffy_expert_ffn_backward - gradients of luffy_expert_ffn (Sec. 2.1: an
+ * expert is an FFN; Sec. 3: it runs on the representatives only) for
+ * dy_rep = dL/dY_rep, with Z = X W1_e^T and A = act(Z) per expert e:
+ *   dx_rep = (dY W2_e * act'(Z)) W1_e,  dW1_e = (dY W2_e * act'(Z))^T X,
+ *   dW2_e = dY^T A  (zero for an expert without representatives).
+ *   x, row_index, rep_offsets, w1, w2, act, max_rows: as for
+ *   luffy_expert_ffn (Z is recomputed, nothing of the forward is kept);
+ *   dy_rep [max_rows, d] bf16 (rows 0..R-1 used); dx_rep [max_rows, d] bf16
+ *   (rows 0..R-1 written); dw1 [E, d_ff, d] and dw2 [E, d, d_ff] float32.
+ * bf16 only (LUFFY_E_UNSUPPORTED for float32).  Intermediates (Z, dY W2,
+ * dZ and the transposed operands of the weight gradients) are bf16 in the
+ * workspace: luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff,
+ * dtype) bytes, which includes transposed copies of both weight tensors.
+ * ---------------------------------------------------------------------- */
+size_t luffy_expert_ffn_backward_workspace_size(int max_rows, int E, int d, int d_ff, int dtype);
+int luffy_expert_ffn_backward(const void* x, const int32_t* row_index, const int32_t* rep_offsets,
+                              int E, int d, int d_ff, int dtype, const void* w1, const void* w2,
+                              int act, int max_rows, const void* dy_rep, void* dx_rep,
+                              float* dw1, float* dw2, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* ------------------------------------------------------------------------
  * luffy_adaptive_threshold - the condensation threshold h_t of training
  * iteration t from the losses of the first and of the previous iteration
  * (Sec. 5.2, Eq. 2):
@@ -213,7 +262,9 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * milliseconds and the number of launches since the previous read.
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
  * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
- * ffn1, ffn2, ffn2_reduce, combine.
+ * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_rows, cbwd_gate,
+ * bwd_wt, bwd_z, bwd_da, bwd_dz, bwd_dx, bwd_dx_reduce, bwd_tr, bwd_dw2,
+ * bwd_dw1.
  * ---------------------------------------------------------------------- */
 int luffy_profile_kernel(const char* name);
 int luffy_profile_read(double* total_ms, int* launches);

@@ -22,6 +22,7 @@ __all__ = [
     "luffy_combine", "route_workspace_size", "condense_workspace_size",
     "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
     "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
+    "luffy_combine_backward", "luffy_expert_ffn_backward", "expert_ffn_backward_workspace_size",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
@@ -46,6 +47,11 @@ _SIGS = {
     "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                                   _c_int, _c_int, _vp, _vp, _c_size, _vp]),
     "luffy_combine": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
+    "luffy_combine_backward": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                        _c_int, _c_int, _c_int, _vp, _vp, _vp]),
+    "luffy_expert_ffn_backward_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
+    "luffy_expert_ffn_backward": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int,
+                                           _c_int, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_adaptive_threshold": (_c_int, [ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_double)]),
     "luffy_profile_kernel": (_c_int, [ctypes.c_char_p]),
     "luffy_profile_read": (_c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_c_int)]),
@@ -164,6 +170,37 @@ def luffy_combine(y_rep, rep_row, slot_pos, topk_gate, y, stream=None):
     lib = load_library()
     _check(lib.luffy_combine(_p(y_rep), _p(rep_row), _p(slot_pos), _p(topk_gate), T, k, d,
                              _dtype_code(y), _p(y), _stream(stream)), "luffy_combine")
+
+
+def luffy_combine_backward(dy, y_rep, rep_row, perm_token, slot_pos, topk_gate, offsets, rep_offsets,
+                           dy_rep, dgate, stream=None):
+    """Transpose of luffy_combine: dy_rep (the representatives' rows) and
+    dgate [T, k] from dy [T, d]."""
+    T, d = dy.shape
+    k = slot_pos.shape[1]
+    max_rows = y_rep.shape[0]
+    if dy_rep.shape != y_rep.shape or dy_rep.dtype != y_rep.dtype or dy.dtype != y_rep.dtype:
+        raise LuffyError("dy, y_rep and dy_rep must share dtype; dy_rep must have y_rep's shape")
+    E = rep_offsets.numel() - 1
+    _check(load_library().luffy_combine_backward(
+        _p(dy), _p(y_rep), _p(rep_row), _p(perm_token), _p(slot_pos), _p(topk_gate), _p(offsets),
+        _p(rep_offsets), E, T, k, d, _dtype_code(dy), max_rows, _p(dy_rep), _p(dgate), _stream(stream)),
+        "luffy_combine_backward")
+
+
+def expert_ffn_backward_workspace_size(max_rows: int, E: int, d: int, d_ff: int, dtype: int) -> int:
+    return int(load_library().luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff, dtype))
+
+
+def luffy_expert_ffn_backward(x, row_index, rep_offsets, w1, w2, act, max_rows, dy_rep, dx_rep, dw1, dw2,
+                              workspace, stream=None):
+    """Gradients of luffy_expert_ffn: dx_rep [max_rows, d] (bf16), dw1
+    [E, d_ff, d] and dw2 [E, d, d_ff] (float32) from dy_rep."""
+    E, d_ff, d = w1.shape
+    _check(load_library().luffy_expert_ffn_backward(
+        _p(x), _p(row_index), _p(rep_offsets), E, d, d_ff, _dtype_code(x), _p(w1), _p(w2), _ACTS[act],
+        max_rows, _p(dy_rep), _p(dx_rep), _p(dw1), _p(dw2), _p(workspace), workspace.numel(), _stream(stream)),
+        "luffy_expert_ffn_backward")
 
 
 def adaptive_threshold(l_ini: float, l_prev: float) -> float:

@@ -1,6 +1,8 @@
 // luffy_combine: y[t] = sum over kept slots j of gate[t,j] * y_rep[rep_row[slot_pos[t,j]]]
 // One wave per token; 16-byte vector loads and stores (four per lane in
 // flight per source row, eight in all); float32 sums.
+#include <algorithm>
+
 #include "luffy_common.h"
 
 namespace luffy {
@@ -89,6 +91,171 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
   }
 }
 
+
+// ---------------------------------------------------------------- backward
+// Transpose of combine (the condensation held fixed): every kept slot adds
+// gate * dy[t] to its representative's row, and takes <dy[t], y_rep[r]> as
+// its gate gradient.
+//
+// Row sums, one work item per (bucket e, range of up to kGatherReps of its
+// representatives, 64-column chunk): the item walks the bucket's positions
+// 64 at a time (lane = position), and every lane whose position belongs to
+// a representative of the range loads its 64 columns of dy (eight 16-byte
+// loads, all in flight together) and adds gate * dy into that
+// representative's row of an LDS accumulator (LDS float atomics: several
+// positions of one group may add at once, so the order of the additions is
+// not fixed).  The rows are then rounded into dy_rep.  A bucket's
+// representatives are a contiguous range of compact rows
+// [rep_offsets[e], rep_offsets[e+1]) and each one's members lie in its own
+// bucket, so nothing crosses items and no global atomics are needed.
+constexpr int kGatherCols = 64;
+constexpr int kGatherReps = 224;   // rows of the LDS accumulator (57 KB with padding)
+constexpr int kGatherPitch = kGatherCols + 1;   // padded: lanes on different rows, same column, differ in bank
+
+template <bool BF16, int K>
+__global__ __launch_bounds__(256) void cbwd_rows_kernel(const void* __restrict__ dy,
+                                                        const int32_t* __restrict__ rep_row,
+                                                        const int32_t* __restrict__ perm_token,
+                                                        const int32_t* __restrict__ slot_pos,
+                                                        const float* __restrict__ gate,
+                                                        const int32_t* __restrict__ offsets,
+                                                        const int32_t* __restrict__ rep_offsets, int E, int d,
+                                                        int max_rows, void* __restrict__ dy_rep) {
+  __shared__ float acc[kGatherReps * kGatherPitch];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // work map: lane e < E holds expert e's representative range count
+  int m = 0, rlo = 0, rhi = 0, plo = 0, phi = 0;
+  if (lane < E) {
+    rlo = rep_offsets[lane];
+    rhi = rep_offsets[lane + 1];
+    plo = offsets[lane];
+    phi = offsets[lane + 1];
+    m = (rhi - rlo + kGatherReps - 1) / kGatherReps;
+  }
+  int incl = m;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const int units = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
+  const int nc = d / kGatherCols;
+  const int total = units * nc;
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const int u = item / nc, cc = item - u * nc;
+    const int e = __popcll(__ballot(lane < E && incl <= u));
+    const int excl = __shfl(incl - m, e, 64);
+    const int ra = __shfl(rlo, e, 64) + (u - excl) * kGatherReps;
+    const int rb = min(ra + kGatherReps, __shfl(rhi, e, 64));
+    const int p_lo = __shfl(plo, e, 64), p_hi = __shfl(phi, e, 64);
+    for (int i = tid; i < kGatherReps * kGatherPitch; i += 256) acc[i] = 0.f;
+    __syncthreads();
+    const int c0 = cc * kGatherCols;
+    for (int p0 = p_lo + 64 * w; p0 < p_hi; p0 += 256) {
+      const int p = p0 + lane;
+      const int r = p < p_hi ? rep_row[p] : -1;
+      if (r >= ra && r < rb) {
+        const int t = perm_token[p];
+        const int j = (K == 2 && slot_pos[static_cast<size_t>(t) * K] != p) ? 1 : 0;
+        const float g = gate[static_cast<size_t>(t) * K + j];
+        float v[kGatherCols];
+        if constexpr (BF16) {
+          const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(dy) +
+                                                            static_cast<size_t>(t) * d + c0);
+          uint4 q[kGatherCols / 8];
+#pragma unroll
+          for (int i = 0; i < kGatherCols / 8; ++i) q[i] = src[i];
+#pragma unroll
+          for (int i = 0; i < kGatherCols / 8; ++i) {
+            const uint32_t wv[4] = {q[i].x, q[i].y, q[i].z, q[i].w};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              v[8 * i + 2 * h] = __uint_as_float(wv[h] << 16);
+              v[8 * i + 2 * h + 1] = __uint_as_float(wv[h] & 0xFFFF0000u);
+            }
+          }
+        } else {
+          const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(dy) +
+                                                              static_cast<size_t>(t) * d + c0);
+          float4 q[kGatherCols / 4];
+#pragma unroll
+          for (int i = 0; i < kGatherCols / 4; ++i) q[i] = src[i];
+#pragma unroll
+          for (int i = 0; i < kGatherCols / 4; ++i) {
+            v[4 * i] = q[i].x;
+            v[4 * i + 1] = q[i].y;
+            v[4 * i + 2] = q[i].z;
+            v[4 * i + 3] = q[i].w;
+          }
+        }
+        float* row = acc + (r - ra) * kGatherPitch;
+#pragma unroll
+        for (int c = 0; c < kGatherCols; ++c) atomicAdd(row + c, g * v[c]);
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < (rb - ra) * kGatherCols; i += 256) {
+      const int rl = i / kGatherCols, c = i - rl * kGatherCols;
+      const int r = ra + rl;
+      if (r >= max_rows) continue;
+      const float a = acc[rl * kGatherPitch + c];
+      const size_t o = static_cast<size_t>(r) * d + c0 + c;
+      if constexpr (BF16) static_cast<uint16_t*>(dy_rep)[o] = static_cast<uint16_t>(pack_bf16x2(a, 0.f) & 0xFFFFu);
+      else static_cast<float*>(dy_rep)[o] = a;
+    }
+    __syncthreads();
+  }
+}
+
+// Gate gradients: one wave per token, a fixed-order float32 dot product per
+// kept slot (0 for a dropped one).
+template <bool BF16, int K>
+__global__ __launch_bounds__(256) void cbwd_gate_kernel(const void* __restrict__ dy,
+                                                        const void* __restrict__ y_rep,
+                                                        const int32_t* __restrict__ rep_row,
+                                                        const int32_t* __restrict__ slot_pos, int max_rows,
+                                                        int T, int d, float* __restrict__ dgate) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  constexpr int EPC = BF16 ? 8 : 4;   // elements per 16-byte chunk
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const int p = slot_pos[static_cast<size_t>(t) * K + j];
+    const int r = p >= 0 ? rep_row[p] : -1;
+    float dot = 0.f;
+    if (r >= 0 && r < max_rows) {
+      for (int c = lane * EPC; c < d; c += 64 * EPC) {
+        if constexpr (BF16) {
+          const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(dy) +
+                                                          static_cast<size_t>(t) * d + c);
+          const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(y_rep) +
+                                                          static_cast<size_t>(r) * d + c);
+          const uint32_t uw[4] = {u.x, u.y, u.z, u.w}, vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            dot = fmaf(__uint_as_float(uw[i] << 16), __uint_as_float(vw[i] << 16), dot);
+            dot = fmaf(__uint_as_float(uw[i] & 0xFFFF0000u), __uint_as_float(vw[i] & 0xFFFF0000u), dot);
+          }
+        } else {
+          const float4 u = *reinterpret_cast<const float4*>(static_cast<const float*>(dy) +
+                                                            static_cast<size_t>(t) * d + c);
+          const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(y_rep) +
+                                                            static_cast<size_t>(r) * d + c);
+          dot = fmaf(u.x, v.x, dot);
+          dot = fmaf(u.y, v.y, dot);
+          dot = fmaf(u.z, v.z, dot);
+          dot = fmaf(u.w, v.w, dot);
+        }
+      }
+    }
+    // fixed-order butterfly: every lane holds the same sum
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o, 64);
+    if (lane == 0) dgate[static_cast<size_t>(t) * K + j] = dot;
+  }
+}
+
 }  // namespace
 }  // namespace luffy
 
@@ -122,3 +289,37 @@ extern "C" int luffy_combine(const void* y_rep, const int32_t* rep_row,
 #undef LUFFY_COMBINE
   return check_launch("luffy_combine");
 }
+
+extern "C" int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep_row,
+                                      const int32_t* perm_token, const int32_t* slot_pos,
+                                      const float* topk_gate, const int32_t* offsets,
+                                      const int32_t* rep_offsets, int E, int T, int k, int d, int dtype,
+                                      int max_rows, void* dy_rep, float* dgate, void* stream) {
+  if (!dy || !y_rep || !rep_row || !perm_token || !slot_pos || !topk_gate || !offsets || !rep_offsets ||
+      !dy_rep || !dgate)
+    return fail(LUFFY_E_INVALID, "luffy_combine_backward: null pointer argument");
+  if (T <= 0 || d <= 0 || E <= 0 || max_rows <= 0)
+    return fail(LUFFY_E_INVALID, "luffy_combine_backward: T=%d d=%d E=%d max_rows=%d", T, d, E, max_rows);
+  if (k != 1 && k != 2) return fail(LUFFY_E_INVALID, "luffy_combine_backward: k=%d must be 1 or 2", k);
+  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
+    return fail(LUFFY_E_INVALID, "luffy_combine_backward: unknown dtype %d", dtype);
+  if (E > 64) return fail(LUFFY_E_UNSUPPORTED, "luffy_combine_backward: E=%d > 64", E);
+  if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_combine_backward: d=%d not a multiple of 64", d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // work items: (representative ranges) x (d / 64); bounded by (max_rows / R + E) x (d / 64)
+  const long long items = (static_cast<long long>(max_rows) / kGatherReps + E) * (d / kGatherCols);
+  const int rows_blocks = static_cast<int>(std::min<long long>(items, 2048));
+  const int blocks = (T + 3) / 4;
+#define LUFFY_CBWD(BF, K_)                                                                                   \
+  do {                                                                                                       \
+    launch("cbwd_rows", cbwd_rows_kernel<BF, K_>, rows_blocks, 256, 0, s, dy, rep_row, perm_token, slot_pos, \
+           topk_gate, offsets, rep_offsets, E, d, max_rows, dy_rep);                                         \
+    launch("cbwd_gate", cbwd_gate_kernel<BF, K_>, blocks, 256, 0, s, dy, y_rep, rep_row, slot_pos, max_rows, \
+           T, d, dgate);                                                                                     \
+  } while (0)
+  if (dtype == LUFFY_BF16) { if (k == 1) LUFFY_CBWD(true, 1); else LUFFY_CBWD(true, 2); }
+  else { if (k == 1) LUFFY_CBWD(false, 1); else LUFFY_CBWD(false, 2); }
+#undef LUFFY_CBWD
+  return check_launch("luffy_combine_backward");
+}
+

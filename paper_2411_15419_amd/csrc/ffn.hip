@@ -38,9 +38,14 @@ __device__ __forceinline__ float act_fn(float z) {
 //   u = |z| / sqrt(2): GELU(z) = z (1 - q/2) for z >= 0 and z q/2 for z < 0.
 //   SiLU: z / (1 + 2^{-z log2 e}).
 // The hardware exp2 and reciprocal are accurate to about 1 ulp.
+// Activation code of a plain product (no activation), used by the backward.
+constexpr int kActNone = 2;
+
 template <int ACT>
 __device__ __forceinline__ float act_fast(float z) {
-  if constexpr (ACT == LUFFY_ACT_GELU) {
+  if constexpr (ACT == kActNone) {
+    return z;
+  } else if constexpr (ACT == LUFFY_ACT_GELU) {
     constexpr float kP = 0.3275911f;
     constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
     constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
@@ -493,6 +498,238 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
   }
 }
 
+// ---------------------------------------------------------------- backward
+// Gradients of Y = W2 act(W1 x) on the representatives (bf16):
+//   Z = X W1^T (recomputed), dA = dY W2, dZ = dA * act'(Z),
+//   dX = dZ W1, dW2 = dY^T act(Z), dW1 = dZ^T X.
+// The row products dA and dX run on the forward's grouped kernel with
+// transposed weights; the weight gradients contract over an expert's rows,
+// so those operands are first transposed per expert into [columns, Kp_e]
+// blocks (Kp_e = R_e rounded up to 64, zero-padded) and multiplied by a
+// grouped 256 x 256 tile kernel with float32 output.
+
+// Exact derivative of the activation (device math library erf / exp).
+template <int ACT>
+__device__ __forceinline__ float act_grad(float z) {
+  if constexpr (ACT == LUFFY_ACT_GELU) {
+    constexpr float kInvSqrt2 = 0.70710678118654752f, kInvSqrt2Pi = 0.39894228040143268f;
+    return 0.5f * (1.0f + erff(z * kInvSqrt2)) + z * kInvSqrt2Pi * expf(-0.5f * z * z);
+  } else {
+    const float sg = 1.0f / (1.0f + expf(-z));
+    return sg * (1.0f + z * (1.0f - sg));
+  }
+}
+
+// Batched transpose of [batch][rows][cols] bf16 into [batch][cols][rows]
+// (rows, cols multiples of 64), 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void transpose2d_kernel(const uint16_t* __restrict__ src, int rows, int cols,
+                                                          int batch, uint16_t* __restrict__ dst) {
+  __shared__ uint16_t tile[64][66];
+  const int rt = rows / 64, ct = cols / 64;
+  const long long total = static_cast<long long>(batch) * rt * ct;
+  for (long long it = blockIdx.x; it < total; it += gridDim.x) {
+    const int b = static_cast<int>(it / (rt * ct));
+    const int rem = static_cast<int>(it - static_cast<long long>(b) * rt * ct);
+    const int r0 = (rem / ct) * 64, c0 = (rem % ct) * 64;
+    const uint16_t* sb = src + static_cast<size_t>(b) * rows * cols;
+    uint16_t* db = dst + static_cast<size_t>(b) * rows * cols;
+    for (int i = threadIdx.x; i < 4096; i += 256) {
+      const int r = i >> 6, c = i & 63;
+      tile[r][c] = sb[static_cast<size_t>(r0 + r) * cols + c0 + c];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < 4096; i += 256) {
+      const int c = i >> 6, r = i & 63;
+      db[static_cast<size_t>(c0 + c) * rows + r0 + r] = tile[r][c];
+    }
+    __syncthreads();
+  }
+}
+
+// Per-expert layout of the transposed activations: expert e's block starts
+// at column offset kbase_e = sum of Kp over the experts before it.
+__device__ __forceinline__ void expert_kblock(const int32_t* __restrict__ rep_offsets, int e, int& kbase, int& kp) {
+  kbase = 0;
+  for (int i = 0; i < e; ++i) kbase += (rep_offsets[i + 1] - rep_offsets[i] + 63) / 64 * 64;
+  kp = (rep_offsets[e + 1] - rep_offsets[e] + 63) / 64 * 64;
+}
+
+// Expert e's rows [lo_e, hi_e) of src [*, C] (read through row_index when
+// given) into dst[C * kbase_e + c * Kp_e + k] = src[lo_e + k][c] for k < R_e,
+// 0 for R_e <= k < Kp_e; MODE applies act to the values (A = act(Z)).
+template <int MODE>
+__global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t* __restrict__ src,
+                                                             const int32_t* __restrict__ row_index,
+                                                             const int32_t* __restrict__ rep_offsets, int E, int C,
+                                                             uint16_t* __restrict__ dst) {
+  __shared__ uint16_t tile[64][66];
+  const int lane = threadIdx.x & 63;
+  int kt = 0, lo = 0, hi = 0;
+  if (lane < E) {
+    lo = rep_offsets[lane];
+    hi = rep_offsets[lane + 1];
+    kt = (hi - lo + 63) / 64;
+  }
+  int incl = kt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const int units = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
+  const int ct = C / 64;
+  for (int it = blockIdx.x; it < units * ct; it += gridDim.x) {
+    const int u = it / ct, c0 = (it - u * ct) * 64;
+    const int e = __popcll(__ballot(lane < E && incl <= u));
+    const int excl = __shfl(incl - kt, e, 64);   // k-tiles of the experts before e
+    const int elo = __shfl(lo, e, 64), ehi = __shfl(hi, e, 64);
+    const int kp = (ehi - elo + 63) / 64 * 64;
+    const int k0 = (u - excl) * 64;
+    for (int i = threadIdx.x; i < 4096; i += 256) {
+      const int r = i >> 6, c = i & 63;
+      const int row = elo + k0 + r;
+      uint16_t v = 0;
+      if (row < ehi) {
+        const int srow = row_index ? row_index[row] : row;
+        v = src[static_cast<size_t>(srow) * C + c0 + c];
+        if constexpr (MODE != 0) {
+          const float a = act_fast<MODE == 1 ? LUFFY_ACT_GELU : LUFFY_ACT_SILU>(bf16_to_f32(v));
+          v = static_cast<uint16_t>(pack_bf16x2(a, 0.f) & 0xFFFFu);
+        }
+      }
+      tile[r][c] = v;
+    }
+    __syncthreads();
+    uint16_t* db = dst + static_cast<size_t>(C) * (excl * 64);
+    for (int i = threadIdx.x; i < 4096; i += 256) {
+      const int c = i >> 6, r = i & 63;
+      db[static_cast<size_t>(c0 + c) * kp + k0 + r] = tile[r][c];
+    }
+    __syncthreads();
+  }
+}
+
+// dZ = dA * act'(Z), in place over the R = rep_offsets[E] rows of [*, d_ff].
+template <int ACT>
+__global__ __launch_bounds__(256) void dz_kernel(const int32_t* __restrict__ rep_offsets, int E, int d_ff,
+                                                 const uint16_t* __restrict__ z, uint16_t* __restrict__ da) {
+  const long long n2 = static_cast<long long>(rep_offsets[E]) * d_ff / 2;
+  const uint32_t* zz = reinterpret_cast<const uint32_t*>(z);
+  uint32_t* aa = reinterpret_cast<uint32_t*>(da);
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n2; i += static_cast<long long>(gridDim.x) * 256) {
+    const uint32_t zw = zz[i], aw = aa[i];
+    const float z0 = __uint_as_float(zw << 16), z1 = __uint_as_float(zw & 0xFFFF0000u);
+    const float a0 = __uint_as_float(aw << 16), a1 = __uint_as_float(aw & 0xFFFF0000u);
+    aa[i] = pack_bf16x2(a0 * act_grad<ACT>(z0), a1 * act_grad<ACT>(z1));
+  }
+}
+
+// Weight gradients: out[e][i][j] = sum_k P_e[i][k] Q_e[j][k] over k < Kp_e,
+// P_e = P + M * kbase_e ([M, Kp_e]), Q_e = Q + N * kbase_e ([N, Kp_e]);
+// float32 output [E][M][N]; an expert without rows gets zeros.
+using WgradGemm = GemmBig64;
+
+__global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_t* __restrict__ P,
+                                                                   const uint16_t* __restrict__ Q,
+                                                                   const int32_t* __restrict__ rep_offsets, int E,
+                                                                   int M, int N, float* __restrict__ out) {
+  using G = WgradGemm;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
+  const int mt = (M + G::BM - 1) / G::BM, nt = (N + G::BN - 1) / G::BN;
+  const int tpe = mt * nt;
+  for (int t = blockIdx.x; t < E * tpe; t += gridDim.x) {
+    const int e = t / tpe, r = t - e * tpe;
+    const int m0 = (r / nt) * G::BM, n0 = (r % nt) * G::BN;
+    int kbase, kp;
+    expert_kblock(rep_offsets, e, kbase, kp);
+    kbase = __builtin_amdgcn_readfirstlane(kbase);
+    kp = __builtin_amdgcn_readfirstlane(kp);
+    typename G::Acc acc;
+    G::zero(acc);
+    if (kp > 0) {
+      uint32_t poff[G::LP], qoff[G::LQ];
+#pragma unroll
+      for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(m0 + G::load_row(j), M - 1)) * kp;
+#pragma unroll
+      for (int j = 0; j < G::LQ; ++j)
+        qoff[j] = static_cast<uint32_t>(min(n0 + G::load_row(G::LP + j) - G::BM, N - 1)) * kp;
+      G::template run<G::FN>(P + static_cast<size_t>(M) * kbase, poff, Q + static_cast<size_t>(N) * kbase, qoff, kp,
+                             M - m0, N - n0, lds, acc);
+    }
+    const int tid = opaque_tid(), lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = G::wave_m(w), wn = G::wave_n(w);
+    float* oe = out + static_cast<size_t>(e) * M * N;
+#pragma unroll
+    for (int fm = 0; fm < G::FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < G::FN; ++fn) {
+        const int j = n0 + G::q_row(wn, fn) + (lane & 31);
+        if (j >= N) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int i = m0 + wm * G::WTM + 32 * fm + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+          if (i < M) oe[static_cast<size_t>(i) * N + j] = acc[fm][fn][v];
+        }
+      }
+  }
+}
+
+struct FfnBwdWs {
+  uint16_t *w1t, *w2t, *z, *da, *tp, *tq;
+  float* split_slots;
+};
+
+// Transposed activation blocks hold at most max_rows + 64 E columns.
+FfnBwdWs carve_ffn_bwd(Carver& c, int max_rows, int E, int d, int d_ff) {
+  FfnBwdWs w;
+  const size_t wsz = static_cast<size_t>(E) * d * d_ff;
+  const size_t kcols = static_cast<size_t>(max_rows) + 64 * static_cast<size_t>(E);
+  const int wide = d > d_ff ? d : d_ff;
+  w.w1t = c.take<uint16_t>(wsz);
+  w.w2t = c.take<uint16_t>(wsz);
+  w.z = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
+  w.da = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
+  w.tp = c.take<uint16_t>(kcols * wide);
+  w.tq = c.take<uint16_t>(kcols * wide);
+  w.split_slots = c.take<float>(kFfnSlotFloats * kFfnMaxSlots);
+  return w;
+}
+
+template <int ACT>
+void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d, int d_ff,
+                    const uint16_t* w1, const uint16_t* w2, int max_rows, const uint16_t* dy, uint16_t* dx,
+                    float* dw1, float* dw2, const FfnBwdWs& ws, hipStream_t s) {
+  const int grid = persistent_grid();
+  const int tgrid = 4 * grid;
+  // transposed weights: W1T [E][d][d_ff], W2T [E][d_ff][d]
+  launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w1, d_ff, d, E, ws.w1t);
+  launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w2, d, d_ff, E, ws.w2t);
+  // Z = X W1^T; dA = dY W2 (weights W2T, K = d); dZ = dA act'(Z)
+  launch("bwd_z", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, x, row_index, rep_offsets, E, d,
+         d_ff, w1, ws.z, ws.split_slots);
+  launch("bwd_da", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d,
+         d_ff, static_cast<const uint16_t*>(ws.w2t), ws.da, ws.split_slots);
+  launch("bwd_dz", dz_kernel<ACT>, tgrid, 256, 0, s, rep_offsets, E, d_ff, static_cast<const uint16_t*>(ws.z), ws.da);
+  // dX = dZ W1 (weights W1T, K = d_ff), split over K as in the forward's second product
+  launch("bwd_dx", ffn_kernel_bf16<kActNone, false>, grid, FfnGemm::THREADS, 0, s,
+         static_cast<const uint16_t*>(ws.da), nullptr, rep_offsets, E, d_ff, d,
+         static_cast<const uint16_t*>(ws.w1t), dx, ws.split_slots);
+  launch("bwd_dx_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots, dx,
+         grid);
+  // dW2 = dY^T act(Z): P = dY^T [d, Kp], Q = act(Z)^T [d_ff, Kp]
+  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, dy, nullptr, rep_offsets, E, d, ws.tp);
+  launch("bwd_tr", transpose_rows_kernel<ACT == LUFFY_ACT_GELU ? 1 : 2>, tgrid, 256, 0, s,
+         static_cast<const uint16_t*>(ws.z), nullptr, rep_offsets, E, d_ff, ws.tq);
+  launch("bwd_dw2", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.tp),
+         static_cast<const uint16_t*>(ws.tq), rep_offsets, E, d, d_ff, dw2);
+  // dW1 = dZ^T X: P = dZ^T [d_ff, Kp], Q = X^T [d, Kp]
+  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, static_cast<const uint16_t*>(ws.da), nullptr,
+         rep_offsets, E, d_ff, ws.tp);
+  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, x, row_index, rep_offsets, E, d, ws.tq);
+  launch("bwd_dw1", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.tp),
+         static_cast<const uint16_t*>(ws.tq), rep_offsets, E, d_ff, d, dw1);
+}
+
 }  // namespace
 }  // namespace luffy
 
@@ -539,3 +776,52 @@ extern "C" int luffy_expert_ffn(const void* x, const int32_t* row_index,
     launch_ffn<LUFFY_ACT_SILU>(x, row_index, rep_offsets, E, d, d_ff, dtype, w1, w2, max_rows, y_rep, ws, s);
   return check_launch("luffy_expert_ffn");
 }
+
+extern "C" size_t luffy_expert_ffn_backward_workspace_size(int max_rows, int E, int d, int d_ff, int dtype) {
+  if (max_rows <= 0 || E <= 0 || d <= 0 || d_ff <= 0 || dtype != LUFFY_BF16) return 0;
+  Carver c(nullptr);
+  carve_ffn_bwd(c, max_rows, E, d, d_ff);
+  return c.size();
+}
+
+extern "C" int luffy_expert_ffn_backward(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E,
+                                         int d, int d_ff, int dtype, const void* w1, const void* w2, int act,
+                                         int max_rows, const void* dy_rep, void* dx_rep, float* dw1, float* dw2,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!x || !rep_offsets || !w1 || !w2 || !dy_rep || !dx_rep || !dw1 || !dw2)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: null pointer argument");
+  if (E <= 0 || d <= 0 || d_ff <= 0 || max_rows <= 0)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: E=%d d=%d d_ff=%d max_rows=%d", E, d, d_ff, max_rows);
+  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: unknown dtype %d", dtype);
+  if (act != LUFFY_ACT_GELU && act != LUFFY_ACT_SILU)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: unknown activation %d", act);
+  if (dtype != LUFFY_BF16) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: bf16 only");
+  if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: E=%d > %d", E, kMaxExperts);
+  if (d % 64 != 0 || d_ff % 64 != 0)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: d=%d d_ff=%d must be multiples of 64", d, d_ff);
+  if (d > 32768 || d_ff > 32768)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: d=%d d_ff=%d must be at most 32768", d, d_ff);
+  const long long kcols = static_cast<long long>(max_rows) + 64ll * E;
+  if (static_cast<long long>(max_rows) * d_ff * 2 > 0xFFFF0000ll ||
+      static_cast<long long>(d) * d_ff * 2 > 0xFFFF0000ll ||
+      kcols * (d > d_ff ? d : d_ff) * 2 > 0xFFFF0000ll)
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: an operand exceeds 4 GiB - 64 KiB");
+  const size_t need = luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff, dtype);
+  if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LUFFY_E_WORKSPACE, "luffy_expert_ffn_backward: workspace needs %zu bytes, 256-aligned", need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver c(workspace);
+  const FfnBwdWs ws = carve_ffn_bwd(c, max_rows, E, d, d_ff);
+  const auto* xb = static_cast<const uint16_t*>(x);
+  const auto* w1b = static_cast<const uint16_t*>(w1);
+  const auto* w2b = static_cast<const uint16_t*>(w2);
+  const auto* dyb = static_cast<const uint16_t*>(dy_rep);
+  auto* dxb = static_cast<uint16_t*>(dx_rep);
+  if (act == LUFFY_ACT_GELU)
+    launch_ffn_bwd<LUFFY_ACT_GELU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2, ws, s);
+  else
+    launch_ffn_bwd<LUFFY_ACT_SILU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2, ws, s);
+  return check_launch("luffy_expert_ffn_backward");
+}
+
