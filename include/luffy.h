@@ -203,15 +203,18 @@ int luffy_combine(const void* y_rep, const int32_t* rep_row,
  *   rep_offsets [E+1], all as the forward left them (R = rep_offsets[E]
  *   rows in use, R <= max_rows); dy_rep [max_rows, d] dtype: rows 0..R-1
  *   written; dgate [T, k] float32.  E <= 64.
- * Row sums are float32 in no fixed order (several slots of a group may add
- * at once), so dy_rep may differ in the last bits between runs; dgate is a
- * fixed-order sum.  No workspace.
+ * Row sums are float32; the members of a group are added in an order that
+ * is not fixed, so dy_rep may differ in the last bits between runs; dgate
+ * is a fixed-order sum.  Workspace (the member lists):
+ * luffy_combine_backward_workspace_size(T, k, max_rows) bytes.
  * ---------------------------------------------------------------------- */
+size_t luffy_combine_backward_workspace_size(int T, int k, int max_rows);
 int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep_row,
                            const int32_t* perm_token, const int32_t* slot_pos,
                            const float* topk_gate, const int32_t* offsets,
                            const int32_t* rep_offsets, int E, int T, int k, int d, int dtype,
-                           int max_rows, void* dy_rep, float* dgate, void* stream);
+                           int max_rows, void* dy_rep, float* dgate,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * luffy_expert_ffn_backward - gradients of luffy_expert_ffn (Sec. 2.1: an
@@ -262,7 +265,7 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * milliseconds and the number of launches since the previous read.
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
  * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
- * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_rows, cbwd_gate,
+ * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
  * bwd_wt, bwd_z, bwd_da, bwd_dz, bwd_dx, bwd_dx_reduce, bwd_tr, bwd_dw2,
  * bwd_dw1.
  * ---------------------------------------------------------------------- */

@@ -22,7 +22,8 @@ __all__ = [
     "luffy_combine", "route_workspace_size", "condense_workspace_size",
     "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
     "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
-    "luffy_combine_backward", "luffy_expert_ffn_backward", "expert_ffn_backward_workspace_size",
+    "luffy_combine_backward", "combine_backward_workspace_size", "luffy_expert_ffn_backward",
+    "expert_ffn_backward_workspace_size",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
@@ -47,8 +48,9 @@ _SIGS = {
     "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                                   _c_int, _c_int, _vp, _vp, _c_size, _vp]),
     "luffy_combine": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
+    "luffy_combine_backward_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
     "luffy_combine_backward": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
-                                        _c_int, _c_int, _c_int, _vp, _vp, _vp]),
+                                        _c_int, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_expert_ffn_backward_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_expert_ffn_backward": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int,
                                            _c_int, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
@@ -172,8 +174,12 @@ def luffy_combine(y_rep, rep_row, slot_pos, topk_gate, y, stream=None):
                              _dtype_code(y), _p(y), _stream(stream)), "luffy_combine")
 
 
+def combine_backward_workspace_size(T: int, k: int, max_rows: int) -> int:
+    return int(load_library().luffy_combine_backward_workspace_size(T, k, max_rows))
+
+
 def luffy_combine_backward(dy, y_rep, rep_row, perm_token, slot_pos, topk_gate, offsets, rep_offsets,
-                           dy_rep, dgate, stream=None):
+                           dy_rep, dgate, workspace, stream=None):
     """Transpose of luffy_combine: dy_rep (the representatives' rows) and
     dgate [T, k] from dy [T, d]."""
     T, d = dy.shape
@@ -184,7 +190,8 @@ def luffy_combine_backward(dy, y_rep, rep_row, perm_token, slot_pos, topk_gate, 
     E = rep_offsets.numel() - 1
     _check(load_library().luffy_combine_backward(
         _p(dy), _p(y_rep), _p(rep_row), _p(perm_token), _p(slot_pos), _p(topk_gate), _p(offsets),
-        _p(rep_offsets), E, T, k, d, _dtype_code(dy), max_rows, _p(dy_rep), _p(dgate), _stream(stream)),
+        _p(rep_offsets), E, T, k, d, _dtype_code(dy), max_rows, _p(dy_rep), _p(dgate), _p(workspace),
+        workspace.numel(), _stream(stream)),
         "luffy_combine_backward")
 
 

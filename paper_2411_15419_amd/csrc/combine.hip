@@ -97,113 +97,138 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
 // gate * dy[t] to its representative's row, and takes <dy[t], y_rep[r]> as
 // its gate gradient.
 //
-// Row sums, one work item per (bucket e, range of up to kGatherReps of its
-// representatives, 64-column chunk): the item walks the bucket's positions
-// 64 at a time (lane = position), and every lane whose position belongs to
-// a representative of the range loads its 64 columns of dy (eight 16-byte
-// loads, all in flight together) and adds gate * dy into that
-// representative's row of an LDS accumulator (LDS float atomics: several
-// positions of one group may add at once, so the order of the additions is
-// not fixed).  The rows are then rounded into dy_rep.  A bucket's
-// representatives are a contiguous range of compact rows
-// [rep_offsets[e], rep_offsets[e+1]) and each one's members lie in its own
-// bucket, so nothing crosses items and no global atomics are needed.
-constexpr int kGatherCols = 64;
-constexpr int kGatherReps = 224;   // rows of the LDS accumulator (57 KB with padding)
-constexpr int kGatherPitch = kGatherCols + 1;   // padded: lanes on different rows, same column, differ in bank
+// Row sums through a member list: the kept positions are grouped by
+// representative (counts, an exclusive scan, then a fill with one cursor
+// per representative; the order inside a group is not fixed), and one wave
+// per (representative, 512-column chunk) adds gate * dy[t] of its members
+// in registers, four members' rows in flight at a time, and stores the row.
 
+// counts[r] = cursor[r] = 0 for the R rows in use.
+__global__ __launch_bounds__(256) void cbwd_clear_kernel(const int32_t* __restrict__ rep_offsets, int E,
+                                                         int max_rows, int* __restrict__ cnt,
+                                                         int* __restrict__ cursor) {
+  const int R = min(rep_offsets[E], max_rows);
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < R; i += gridDim.x * 256) {
+    cnt[i] = 0;
+    cursor[i] = 0;
+  }
+}
+
+// FILL = false: count the kept positions of each representative;
+// FILL = true: place each position in its representative's group.
+template <bool FILL>
+__global__ __launch_bounds__(256) void cbwd_group_kernel(const int32_t* __restrict__ rep_row,
+                                                         const int32_t* __restrict__ offsets, int E, int max_rows,
+                                                         int* __restrict__ cnt, const int* __restrict__ start,
+                                                         int* __restrict__ cursor, int* __restrict__ list) {
+  const int S = offsets[E];
+  for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
+    const int r = rep_row[p];
+    if (r < 0 || r >= max_rows) continue;
+    if constexpr (FILL) list[start[r] + atomicAdd(cursor + r, 1)] = p;
+    else atomicAdd(cnt + r, 1);
+  }
+}
+
+// start[r] = sum of cnt[r'] for r' < r over the R rows in use; one block of
+// 1024 threads, each scanning a contiguous run of rows.
+__global__ __launch_bounds__(1024) void cbwd_scan_kernel(const int32_t* __restrict__ rep_offsets, int E,
+                                                         int max_rows, const int* __restrict__ cnt,
+                                                         int* __restrict__ start) {
+  __shared__ int part[1024];
+  const int R = min(rep_offsets[E], max_rows);
+  const int per = (R + 1023) / 1024;
+  const int b = threadIdx.x * per, e = min(b + per, R);
+  int sum = 0;
+  for (int i = b; i < e; ++i) sum += cnt[i];
+  part[threadIdx.x] = sum;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int v = threadIdx.x >= o ? part[threadIdx.x - o] : 0;
+    __syncthreads();
+    part[threadIdx.x] += v;
+    __syncthreads();
+  }
+  int run = part[threadIdx.x] - sum;   // exclusive prefix of this thread's run
+  for (int i = b; i < e; ++i) {
+    start[i] = run;
+    run += cnt[i];
+  }
+  if (threadIdx.x == 1023) start[R] = part[1023];
+}
+
+// One wave per (representative r, 512-column chunk): lane l holds columns
+// c0 + 8l .. c0 + 8l + 7 (bf16: one 16-byte load per member row; float32:
+// two).
 template <bool BF16, int K>
 __global__ __launch_bounds__(256) void cbwd_rows_kernel(const void* __restrict__ dy,
-                                                        const int32_t* __restrict__ rep_row,
                                                         const int32_t* __restrict__ perm_token,
                                                         const int32_t* __restrict__ slot_pos,
                                                         const float* __restrict__ gate,
-                                                        const int32_t* __restrict__ offsets,
                                                         const int32_t* __restrict__ rep_offsets, int E, int d,
-                                                        int max_rows, void* __restrict__ dy_rep) {
-  __shared__ float acc[kGatherReps * kGatherPitch];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  // work map: lane e < E holds expert e's representative range count
-  int m = 0, rlo = 0, rhi = 0, plo = 0, phi = 0;
-  if (lane < E) {
-    rlo = rep_offsets[lane];
-    rhi = rep_offsets[lane + 1];
-    plo = offsets[lane];
-    phi = offsets[lane + 1];
-    m = (rhi - rlo + kGatherReps - 1) / kGatherReps;
-  }
-  int incl = m;
+                                                        int max_rows, const int* __restrict__ start,
+                                                        const int* __restrict__ list, void* __restrict__ dy_rep) {
+  const int lane = threadIdx.x & 63;
+  const int R = min(rep_offsets[E], max_rows);
+  const int nc = (d + 511) / 512;
+  const long long items = static_cast<long long>(R) * nc;
+  for (long long it = (static_cast<long long>(blockIdx.x) * 256 + threadIdx.x) >> 6; it < items;
+       it += static_cast<long long>(gridDim.x) * 4) {
+    const int r = static_cast<int>(it / nc);
+    const int c = static_cast<int>(it - static_cast<long long>(r) * nc) * 512 + lane * 8;
+    const bool col = c < d;
+    const int m0 = start[r], m1 = start[r + 1];
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int m = m0; m < m1; m += 4) {
+      int t[4];
+      float g[4];
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
-  }
-  const int units = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
-  const int nc = d / kGatherCols;
-  const int total = units * nc;
-  for (int item = blockIdx.x; item < total; item += gridDim.x) {
-    const int u = item / nc, cc = item - u * nc;
-    const int e = __popcll(__ballot(lane < E && incl <= u));
-    const int excl = __shfl(incl - m, e, 64);
-    const int ra = __shfl(rlo, e, 64) + (u - excl) * kGatherReps;
-    const int rb = min(ra + kGatherReps, __shfl(rhi, e, 64));
-    const int p_lo = __shfl(plo, e, 64), p_hi = __shfl(phi, e, 64);
-    for (int i = tid; i < kGatherReps * kGatherPitch; i += 256) acc[i] = 0.f;
-    __syncthreads();
-    const int c0 = cc * kGatherCols;
-    for (int p0 = p_lo + 64 * w; p0 < p_hi; p0 += 256) {
-      const int p = p0 + lane;
-      const int r = p < p_hi ? rep_row[p] : -1;
-      if (r >= ra && r < rb) {
-        const int t = perm_token[p];
-        const int j = (K == 2 && slot_pos[static_cast<size_t>(t) * K] != p) ? 1 : 0;
-        const float g = gate[static_cast<size_t>(t) * K + j];
-        float v[kGatherCols];
-        if constexpr (BF16) {
-          const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(dy) +
-                                                            static_cast<size_t>(t) * d + c0);
-          uint4 q[kGatherCols / 8];
+      for (int u = 0; u < 4; ++u) {
+        const int mm = min(m + u, m1 - 1);
+        const int p = list[mm];
+        t[u] = perm_token[p];
+        const int j = (K == 2 && slot_pos[static_cast<size_t>(t[u]) * K] != p) ? 1 : 0;
+        g[u] = m + u < m1 ? gate[static_cast<size_t>(t[u]) * K + j] : 0.f;
+      }
+      if (col) {
 #pragma unroll
-          for (int i = 0; i < kGatherCols / 8; ++i) q[i] = src[i];
-#pragma unroll
-          for (int i = 0; i < kGatherCols / 8; ++i) {
-            const uint32_t wv[4] = {q[i].x, q[i].y, q[i].z, q[i].w};
+        for (int u = 0; u < 4; ++u) {
+          if constexpr (BF16) {
+            const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(dy) +
+                                                            static_cast<size_t>(t[u]) * d + c);
+            const uint32_t wv[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
-              v[8 * i + 2 * h] = __uint_as_float(wv[h] << 16);
-              v[8 * i + 2 * h + 1] = __uint_as_float(wv[h] & 0xFFFF0000u);
+              acc[2 * h] = fmaf(g[u], __uint_as_float(wv[h] << 16), acc[2 * h]);
+              acc[2 * h + 1] = fmaf(g[u], __uint_as_float(wv[h] & 0xFFFF0000u), acc[2 * h + 1]);
             }
-          }
-        } else {
-          const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(dy) +
-                                                              static_cast<size_t>(t) * d + c0);
-          float4 q[kGatherCols / 4];
-#pragma unroll
-          for (int i = 0; i < kGatherCols / 4; ++i) q[i] = src[i];
-#pragma unroll
-          for (int i = 0; i < kGatherCols / 4; ++i) {
-            v[4 * i] = q[i].x;
-            v[4 * i + 1] = q[i].y;
-            v[4 * i + 2] = q[i].z;
-            v[4 * i + 3] = q[i].w;
+          } else {
+            const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(dy) +
+                                                                static_cast<size_t>(t[u]) * d + c);
+            const float4 a = src[0], b = src[1];
+            acc[0] = fmaf(g[u], a.x, acc[0]);
+            acc[1] = fmaf(g[u], a.y, acc[1]);
+            acc[2] = fmaf(g[u], a.z, acc[2]);
+            acc[3] = fmaf(g[u], a.w, acc[3]);
+            acc[4] = fmaf(g[u], b.x, acc[4]);
+            acc[5] = fmaf(g[u], b.y, acc[5]);
+            acc[6] = fmaf(g[u], b.z, acc[6]);
+            acc[7] = fmaf(g[u], b.w, acc[7]);
           }
         }
-        float* row = acc + (r - ra) * kGatherPitch;
-#pragma unroll
-        for (int c = 0; c < kGatherCols; ++c) atomicAdd(row + c, g * v[c]);
       }
     }
-    __syncthreads();
-    for (int i = tid; i < (rb - ra) * kGatherCols; i += 256) {
-      const int rl = i / kGatherCols, c = i - rl * kGatherCols;
-      const int r = ra + rl;
-      if (r >= max_rows) continue;
-      const float a = acc[rl * kGatherPitch + c];
-      const size_t o = static_cast<size_t>(r) * d + c0 + c;
-      if constexpr (BF16) static_cast<uint16_t*>(dy_rep)[o] = static_cast<uint16_t>(pack_bf16x2(a, 0.f) & 0xFFFFu);
-      else static_cast<float*>(dy_rep)[o] = a;
+    if (col) {
+      if constexpr (BF16) {
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(dy_rep) + static_cast<size_t>(r) * d + c) =
+            make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                       pack_bf16x2(acc[6], acc[7]));
+      } else {
+        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(dy_rep) + static_cast<size_t>(r) * d + c);
+        dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      }
     }
-    __syncthreads();
   }
 }
 
@@ -290,11 +315,32 @@ extern "C" int luffy_combine(const void* y_rep, const int32_t* rep_row,
   return check_launch("luffy_combine");
 }
 
+struct CbwdWs {
+  int *cnt, *start, *cursor, *list;
+};
+
+CbwdWs carve_cbwd(Carver& c, int max_rows, long long slots) {
+  CbwdWs w;
+  w.cnt = c.take<int>(static_cast<size_t>(max_rows));
+  w.start = c.take<int>(static_cast<size_t>(max_rows) + 1);
+  w.cursor = c.take<int>(static_cast<size_t>(max_rows));
+  w.list = c.take<int>(static_cast<size_t>(slots));
+  return w;
+}
+
+extern "C" size_t luffy_combine_backward_workspace_size(int T, int k, int max_rows) {
+  if (T <= 0 || k <= 0 || max_rows <= 0) return 0;
+  Carver c(nullptr);
+  carve_cbwd(c, max_rows, static_cast<long long>(T) * k);
+  return c.size();
+}
+
 extern "C" int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep_row,
                                       const int32_t* perm_token, const int32_t* slot_pos,
                                       const float* topk_gate, const int32_t* offsets,
                                       const int32_t* rep_offsets, int E, int T, int k, int d, int dtype,
-                                      int max_rows, void* dy_rep, float* dgate, void* stream) {
+                                      int max_rows, void* dy_rep, float* dgate, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
   if (!dy || !y_rep || !rep_row || !perm_token || !slot_pos || !topk_gate || !offsets || !rep_offsets ||
       !dy_rep || !dgate)
     return fail(LUFFY_E_INVALID, "luffy_combine_backward: null pointer argument");
@@ -303,19 +349,35 @@ extern "C" int luffy_combine_backward(const void* dy, const void* y_rep, const i
   if (k != 1 && k != 2) return fail(LUFFY_E_INVALID, "luffy_combine_backward: k=%d must be 1 or 2", k);
   if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
     return fail(LUFFY_E_INVALID, "luffy_combine_backward: unknown dtype %d", dtype);
-  if (E > 64) return fail(LUFFY_E_UNSUPPORTED, "luffy_combine_backward: E=%d > 64", E);
   if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_combine_backward: d=%d not a multiple of 64", d);
+  if (static_cast<long long>(T) * k >= (1ll << 31))
+    return fail(LUFFY_E_UNSUPPORTED, "luffy_combine_backward: T*k >= 2^31");
+  const size_t need = luffy_combine_backward_workspace_size(T, k, max_rows);
+  if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LUFFY_E_WORKSPACE, "luffy_combine_backward: workspace needs %zu bytes, 256-aligned", need);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // work items: (representative ranges) x (d / 64); bounded by (max_rows / R + E) x (d / 64)
-  const long long items = (static_cast<long long>(max_rows) / kGatherReps + E) * (d / kGatherCols);
-  const int rows_blocks = static_cast<int>(std::min<long long>(items, 2048));
+  Carver c(workspace);
+  const CbwdWs ws = carve_cbwd(c, max_rows, static_cast<long long>(T) * k);
+  const int S = T * k;
+  const int rblocks = std::max(1, std::min((max_rows + 255) / 256, 1024));
+  const int sblocks = std::max(1, std::min((S + 255) / 256, 2048));
+  launch("cbwd_group", cbwd_clear_kernel, rblocks, 256, 0, s, rep_offsets, E, max_rows, ws.cnt, ws.cursor);
+  launch("cbwd_group", cbwd_group_kernel<false>, sblocks, 256, 0, s, rep_row, offsets, E, max_rows, ws.cnt,
+         static_cast<const int*>(ws.start), ws.cursor, ws.list);
+  launch("cbwd_group", cbwd_scan_kernel, 1, 1024, 0, s, rep_offsets, E, max_rows, static_cast<const int*>(ws.cnt),
+         ws.start);
+  launch("cbwd_group", cbwd_group_kernel<true>, sblocks, 256, 0, s, rep_row, offsets, E, max_rows, ws.cnt,
+         static_cast<const int*>(ws.start), ws.cursor, ws.list);
+  const long long row_waves = static_cast<long long>(max_rows) * ((d + 511) / 512);
+  const int row_blocks = static_cast<int>(std::max(1ll, std::min((row_waves + 3) / 4, 8192ll)));
   const int blocks = (T + 3) / 4;
-#define LUFFY_CBWD(BF, K_)                                                                                   \
-  do {                                                                                                       \
-    launch("cbwd_rows", cbwd_rows_kernel<BF, K_>, rows_blocks, 256, 0, s, dy, rep_row, perm_token, slot_pos, \
-           topk_gate, offsets, rep_offsets, E, d, max_rows, dy_rep);                                         \
-    launch("cbwd_gate", cbwd_gate_kernel<BF, K_>, blocks, 256, 0, s, dy, y_rep, rep_row, slot_pos, max_rows, \
-           T, d, dgate);                                                                                     \
+#define LUFFY_CBWD(BF, K_)                                                                                     \
+  do {                                                                                                         \
+    launch("cbwd_rows", cbwd_rows_kernel<BF, K_>, row_blocks, 256, 0, s, dy, perm_token, slot_pos, topk_gate,  \
+           rep_offsets, E, d, max_rows, static_cast<const int*>(ws.start), static_cast<const int*>(ws.list),   \
+           dy_rep);                                                                                            \
+    launch("cbwd_gate", cbwd_gate_kernel<BF, K_>, blocks, 256, 0, s, dy, y_rep, rep_row, slot_pos, max_rows,   \
+           T, d, dgate);                                                                                       \
   } while (0)
   if (dtype == LUFFY_BF16) { if (k == 1) LUFFY_CBWD(true, 1); else LUFFY_CBWD(true, 2); }
   else { if (k == 1) LUFFY_CBWD(false, 1); else LUFFY_CBWD(false, 2); }

@@ -62,9 +62,11 @@ def test_combine_backward(name):
     dy = torch.from_numpy(dy_np.astype(np.float32)).to(dt).cuda()
     dy_rep = torch.full_like(b.y_rep, float("nan"))
     dgate = torch.full((T, k), float("nan"), dtype=torch.float32, device="cuda")
-    for rep in range(2):                        # a second call on the written outputs
+    ws = torch.empty(L.combine_backward_workspace_size(T, k, b.y_rep.shape[0]), dtype=torch.uint8,
+                     device="cuda")
+    for rep in range(2):                        # a second call on the written outputs and workspace
         L.luffy_combine_backward(dy, b.y_rep, b.rep_row, b.perm_token, b.slot_pos, b.topk_gate, b.offsets,
-                                 b.rep_offsets, dy_rep, dgate)
+                                 b.rep_offsets, dy_rep, dgate, ws)
         torch.cuda.synchronize()
         R = int(g["rep_offsets"][-1])
         ref_rep, ref_gate = O.combine_backward(dy_np, g["y_rep"].astype(np.float64), g["rep_row"],
