@@ -67,6 +67,23 @@ def kernel_work(name, cfg, counts):
         return dict(flops=2.0 * S * d, bytes=float(R * d * b + 12 * T * k + T * d * b))
     if name == "gather":
         return dict(flops=0.0, bytes=float(2 * R * d * b + 8 * S))
+    # backward (per launch)
+    if name == "bwd_wt":       # one weight tensor read and written transposed
+        return dict(flops=0.0, bytes=float(2 * E * d * dff * b))
+    if name in ("bwd_z", "bwd_da"):
+        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * d * b + R * dff * b))
+    if name == "bwd_dx":
+        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * dff * b + R * d * b))
+    if name in ("bwd_dw1", "bwd_dw2"):
+        return dict(flops=2.0 * R * d * dff, bytes=float(E * d * dff * 4 + R * (d + dff) * b))
+    if name == "bwd_dz":
+        return dict(flops=0.0, bytes=float(3 * R * dff * b))
+    if name == "bwd_tr":       # four launches (R x d, R x d_ff, R x d_ff, R x d): their mean
+        return dict(flops=0.0, bytes=float(R * (d + dff) * b))
+    if name == "cbwd_rows":
+        return dict(flops=2.0 * S * d, bytes=float(S * d * b + R * d * b + 12 * S))
+    if name == "cbwd_gate":
+        return dict(flops=2.0 * S * d, bytes=float(T * d * b + S * d * b + 12 * T * k))
     return dict(flops=0.0, bytes=0.0)
 
 
@@ -74,7 +91,7 @@ def roofline(name, cfg, counts, sec_per_launch):
     w = kernel_work(name, cfg, counts)
     mfma_peak = MFMA_PEAK_TFLOPS[cfg.dtype]
     ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-    mfma_kernel = name in ("gram", "ffn1", "ffn2")
+    mfma_kernel = name in ("gram", "ffn1", "ffn2", "bwd_z", "bwd_da", "bwd_dx", "bwd_dw1", "bwd_dw2")
     if mfma_kernel and (w["bytes"] == 0 or w["flops"] / w["bytes"] >= ridge):
         ach = w["flops"] / sec_per_launch / 1e12
         return dict(bound="mfma", achieved=ach, peak=mfma_peak, unit="TFLOP/s",
@@ -149,6 +166,104 @@ def cpu_baseline(inp, h, budget_s=15.0):
                 sample=sample)
 
 
+BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_wt", "bwd_z", "bwd_da", "bwd_dz", "bwd_dx",
+                    "bwd_dx_reduce", "bwd_tr", "bwd_dw2", "bwd_dw1")
+
+
+def bench_backward(args, cfg, layer, x, L, torch, np):
+    """One step = luffy_combine_backward + luffy_expert_ffn_backward for a
+    synthetic dL/dy after one forward (the condensation of that forward is
+    held fixed); prints one JSON line like the forward's."""
+    if cfg.dtype != "bf16":
+        print("bench.py --backward: the expert FFN backward is bf16 only", file=sys.stderr)
+        sys.exit(2)
+    b = layer.buf
+    T, d = b.y.shape
+    k = cfg.k
+    E, dff, _ = layer.w1.shape
+    S = T * k
+    g = torch.Generator(device="cuda").manual_seed(args.seed)
+    dy = torch.randn(T, d, device="cuda", generator=g).to(b.y.dtype)
+    dy_rep = torch.empty_like(b.y_rep)
+    dgate = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    dx_rep = torch.empty(S, d, dtype=b.y.dtype, device="cuda")
+    dw1 = torch.empty(E, dff, d, dtype=torch.float32, device="cuda")
+    dw2 = torch.empty(E, d, dff, dtype=torch.float32, device="cuda")
+    ws_c = torch.empty(L.combine_backward_workspace_size(T, k, S), dtype=torch.uint8, device="cuda")
+    ws_f = torch.empty(L.expert_ffn_backward_workspace_size(S, E, d, dff, L.LUFFY_BF16), dtype=torch.uint8,
+                       device="cuda")
+
+    def step():
+        L.luffy_combine_backward(dy, b.y_rep, b.rep_row, b.perm_token, b.slot_pos, b.topk_gate, b.offsets,
+                                 b.rep_offsets, dy_rep, dgate, ws_c)
+        L.luffy_expert_ffn_backward(x, b.rep_token, b.rep_offsets, layer.w1, layer.w2, cfg.act, S, dy_rep,
+                                    dx_rep, dw1, dw2, ws_f)
+
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    per_kernel = {}
+    for name in BACKWARD_KERNELS:
+        L.profile_kernel(name)
+        for _ in range(3):
+            step()
+        ms, n = L.profile_read()
+        if n:
+            per_kernel[name] = dict(ms_per_step=ms / 3, launches_per_step=n / 3, ms_per_launch=ms / n)
+    L.profile_kernel(None)
+    dominant = max(per_kernel, key=lambda kname: per_kernel[kname]["ms_per_step"])
+    L.profile_kernel(dominant)
+    L.profile_read()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    dom_ms, dom_n = L.profile_read()
+    L.profile_kernel(None)
+    off = b.offsets.cpu().numpy()
+    ro = b.rep_offsets.cpu().numpy()
+    counts = dict(S=int(off[-1]), R=int(ro[-1]), bucket_sizes=np.diff(off).tolist(),
+                  used_experts=int((np.diff(ro) > 0).sum()))
+    rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
+    rl.update(traffic=None, algorithmic_bytes=kernel_work(dominant, cfg, counts)["bytes"], kernel=dominant,
+              us_per_launch=dom_ms / dom_n * 1e3)
+    kernels = {}
+    for name, v in per_kernel.items():
+        r = roofline(name, cfg, counts, v["ms_per_launch"] / 1e3)
+        kernels[name] = dict(us_per_launch=round(v["ms_per_launch"] * 1e3, 2),
+                             launches_per_step=v["launches_per_step"], bound=r["bound"],
+                             achieved=round(r["achieved"], 1), unit=r["unit"], frac=round(r["frac"], 4))
+    out = {
+        "metric": "condensed MoE-layer backward tokens/s on 1 MI355X",
+        "value": cfg.T / (ms_per_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "wall_s": wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded clustered tokens, random-init weights, normal dL/dy)",
+        "config": {"workload": WORKLOAD_NAMES[args.config] + ", backward (combine + expert FFN)",
+                   "name": args.config, "T": cfg.T, "d_model": cfg.d, "E": cfg.E, "top_k": cfg.k,
+                   "d_ff": cfg.d_ff, "act": cfg.act},
+        "condensation": {"slots_kept": counts["S"], "representatives": counts["R"]},
+        "roofline": rl,
+        "kernels": kernels,
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -159,6 +274,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward of the layer (combine and expert FFN) instead of the forward")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -197,6 +314,10 @@ def main():
     for _ in range(max(args.warmup, 1)):
         layer(x)
     torch.cuda.synchronize()
+
+    if args.backward:
+        bench_backward(args, cfg, layer, x, L, torch, np)
+        return
 
     # per-kernel breakdown (untimed pass) to find the dominant kernel
     per_kernel = {}

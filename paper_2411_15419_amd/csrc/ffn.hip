@@ -508,40 +508,76 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
 // blocks (Kp_e = R_e rounded up to 64, zero-padded) and multiplied by a
 // grouped 256 x 256 tile kernel with float32 output.
 
-// Exact derivative of the activation (device math library erf / exp).
+// Derivative of the activation, with the approximations of act_fast (the
+// result is rounded to bf16): GELU'(z) = Phi(z) + z phi(z), Phi from the
+// same Hastings erf (Phi(z) = 1 - q/2 for z >= 0, q/2 below), phi(z) =
+// e^{-z^2/2} / sqrt(2 pi) from the same exp2; SiLU'(z) = s (1 + z (1 - s)).
 template <int ACT>
 __device__ __forceinline__ float act_grad(float z) {
   if constexpr (ACT == LUFFY_ACT_GELU) {
+    constexpr float kP = 0.3275911f;
+    constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
+    constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
     constexpr float kInvSqrt2 = 0.70710678118654752f, kInvSqrt2Pi = 0.39894228040143268f;
-    return 0.5f * (1.0f + erff(z * kInvSqrt2)) + z * kInvSqrt2Pi * expf(-0.5f * z * z);
+    constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
+    const float u = fabsf(z) * kInvSqrt2;
+    const float t = __builtin_amdgcn_rcpf(fmaf(kP, u, 1.0f));
+    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, kA5, kA4), kA3), kA2), kA1);
+    const float e = __builtin_amdgcn_exp2f(z * z * kHalfLog2e);   // e^{-z^2/2}
+    const float hq = 0.5f * poly * e;
+    return (z >= 0.f ? 1.0f - hq : hq) + z * kInvSqrt2Pi * e;
   } else {
-    const float sg = 1.0f / (1.0f + expf(-z));
+    constexpr float kNegLog2e = -1.44269504088896341f;
+    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * kNegLog2e));
     return sg * (1.0f + z * (1.0f - sg));
   }
 }
 
+// 64 x 64 bf16 tile transposes through LDS with 16-byte global accesses:
+// thread i loads 8 consecutive elements of source rows i/8 and i/8 + 32
+// (uint4), and stores 8 consecutive elements of destination rows i/8 and
+// i/8 + 32, gathered from an LDS column.  The LDS row pitch of 66 elements
+// (33 words) spreads a column over the banks.
+constexpr int kTrPitch = 66;
+
+__device__ __forceinline__ void tile_put8(uint16_t (*tile)[kTrPitch], int r, int c, uint4 v) {
+  uint32_t* row = reinterpret_cast<uint32_t*>(&tile[r][c]);
+  row[0] = v.x;
+  row[1] = v.y;
+  row[2] = v.z;
+  row[3] = v.w;
+}
+
+__device__ __forceinline__ uint4 tile_col8(const uint16_t (*tile)[kTrPitch], int r, int c) {
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    w[q] = static_cast<uint32_t>(tile[r + 2 * q][c]) | (static_cast<uint32_t>(tile[r + 2 * q + 1][c]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // Batched transpose of [batch][rows][cols] bf16 into [batch][cols][rows]
-// (rows, cols multiples of 64), 64 x 64 tiles through LDS.
+// (rows, cols multiples of 64).
 __global__ __launch_bounds__(256) void transpose2d_kernel(const uint16_t* __restrict__ src, int rows, int cols,
                                                           int batch, uint16_t* __restrict__ dst) {
-  __shared__ uint16_t tile[64][66];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kTrPitch];
   const int rt = rows / 64, ct = cols / 64;
+  const int i = threadIdx.x, a = i >> 3, b8 = (i & 7) * 8;
   const long long total = static_cast<long long>(batch) * rt * ct;
   for (long long it = blockIdx.x; it < total; it += gridDim.x) {
-    const int b = static_cast<int>(it / (rt * ct));
-    const int rem = static_cast<int>(it - static_cast<long long>(b) * rt * ct);
+    const int bt = static_cast<int>(it / (rt * ct));
+    const int rem = static_cast<int>(it - static_cast<long long>(bt) * rt * ct);
     const int r0 = (rem / ct) * 64, c0 = (rem % ct) * 64;
-    const uint16_t* sb = src + static_cast<size_t>(b) * rows * cols;
-    uint16_t* db = dst + static_cast<size_t>(b) * rows * cols;
-    for (int i = threadIdx.x; i < 4096; i += 256) {
-      const int r = i >> 6, c = i & 63;
-      tile[r][c] = sb[static_cast<size_t>(r0 + r) * cols + c0 + c];
-    }
+    const uint16_t* sb = src + static_cast<size_t>(bt) * rows * cols;
+    uint16_t* db = dst + static_cast<size_t>(bt) * rows * cols;
+    const uint4 v0 = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(r0 + a) * cols + c0 + b8);
+    const uint4 v1 = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(r0 + a + 32) * cols + c0 + b8);
+    tile_put8(tile, a, b8, v0);
+    tile_put8(tile, a + 32, b8, v1);
     __syncthreads();
-    for (int i = threadIdx.x; i < 4096; i += 256) {
-      const int c = i >> 6, r = i & 63;
-      db[static_cast<size_t>(c0 + c) * rows + r0 + r] = tile[r][c];
-    }
+    // destination row c0 + a holds source column a: rows r0 + b8 .. + 7
+    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a) * rows + r0 + b8) = tile_col8(tile, b8, a);
+    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a + 32) * rows + r0 + b8) = tile_col8(tile, b8, a + 32);
     __syncthreads();
   }
 }
@@ -562,8 +598,9 @@ __global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t* __r
                                                              const int32_t* __restrict__ row_index,
                                                              const int32_t* __restrict__ rep_offsets, int E, int C,
                                                              uint16_t* __restrict__ dst) {
-  __shared__ uint16_t tile[64][66];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kTrPitch];
   const int lane = threadIdx.x & 63;
+  const int i = threadIdx.x, a = i >> 3, b8 = (i & 7) * 8;
   int kt = 0, lo = 0, hi = 0;
   if (lane < E) {
     lo = rep_offsets[lane];
@@ -585,42 +622,54 @@ __global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t* __r
     const int elo = __shfl(lo, e, 64), ehi = __shfl(hi, e, 64);
     const int kp = (ehi - elo + 63) / 64 * 64;
     const int k0 = (u - excl) * 64;
-    for (int i = threadIdx.x; i < 4096; i += 256) {
-      const int r = i >> 6, c = i & 63;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = a + 32 * h;
       const int row = elo + k0 + r;
-      uint16_t v = 0;
+      uint4 v = make_uint4(0, 0, 0, 0);
       if (row < ehi) {
         const int srow = row_index ? row_index[row] : row;
-        v = src[static_cast<size_t>(srow) * C + c0 + c];
+        v = *reinterpret_cast<const uint4*>(src + static_cast<size_t>(srow) * C + c0 + b8);
         if constexpr (MODE != 0) {
-          const float a = act_fast<MODE == 1 ? LUFFY_ACT_GELU : LUFFY_ACT_SILU>(bf16_to_f32(v));
-          v = static_cast<uint16_t>(pack_bf16x2(a, 0.f) & 0xFFFFu);
+          uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            constexpr int ACT = MODE == 1 ? LUFFY_ACT_GELU : LUFFY_ACT_SILU;
+            wv[q] = pack_bf16x2(act_fast<ACT>(__uint_as_float(wv[q] << 16)),
+                                act_fast<ACT>(__uint_as_float(wv[q] & 0xFFFF0000u)));
+          }
+          v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
         }
       }
-      tile[r][c] = v;
+      tile_put8(tile, r, b8, v);
     }
     __syncthreads();
     uint16_t* db = dst + static_cast<size_t>(C) * (excl * 64);
-    for (int i = threadIdx.x; i < 4096; i += 256) {
-      const int c = i >> 6, r = i & 63;
-      db[static_cast<size_t>(c0 + c) * kp + k0 + r] = tile[r][c];
-    }
+    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a) * kp + k0 + b8) = tile_col8(tile, b8, a);
+    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a + 32) * kp + k0 + b8) = tile_col8(tile, b8, a + 32);
     __syncthreads();
   }
 }
 
-// dZ = dA * act'(Z), in place over the R = rep_offsets[E] rows of [*, d_ff].
+// dZ = dA * act'(Z), in place over the R = rep_offsets[E] rows of [*, d_ff]
+// (8 elements per thread and step).
 template <int ACT>
 __global__ __launch_bounds__(256) void dz_kernel(const int32_t* __restrict__ rep_offsets, int E, int d_ff,
                                                  const uint16_t* __restrict__ z, uint16_t* __restrict__ da) {
-  const long long n2 = static_cast<long long>(rep_offsets[E]) * d_ff / 2;
-  const uint32_t* zz = reinterpret_cast<const uint32_t*>(z);
-  uint32_t* aa = reinterpret_cast<uint32_t*>(da);
-  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n2; i += static_cast<long long>(gridDim.x) * 256) {
-    const uint32_t zw = zz[i], aw = aa[i];
-    const float z0 = __uint_as_float(zw << 16), z1 = __uint_as_float(zw & 0xFFFF0000u);
-    const float a0 = __uint_as_float(aw << 16), a1 = __uint_as_float(aw & 0xFFFF0000u);
-    aa[i] = pack_bf16x2(a0 * act_grad<ACT>(z0), a1 * act_grad<ACT>(z1));
+  const long long n8 = static_cast<long long>(rep_offsets[E]) * d_ff / 8;
+  const uint4* zz = reinterpret_cast<const uint4*>(z);
+  uint4* aa = reinterpret_cast<uint4*>(da);
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n8; i += static_cast<long long>(gridDim.x) * 256) {
+    const uint4 zv = zz[i], av = aa[i];
+    const uint32_t zw[4] = {zv.x, zv.y, zv.z, zv.w}, aw[4] = {av.x, av.y, av.z, av.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float z0 = __uint_as_float(zw[q] << 16), z1 = __uint_as_float(zw[q] & 0xFFFF0000u);
+      const float a0 = __uint_as_float(aw[q] << 16), a1 = __uint_as_float(aw[q] & 0xFFFF0000u);
+      o[q] = pack_bf16x2(a0 * act_grad<ACT>(z0), a1 * act_grad<ACT>(z1));
+    }
+    aa[i] = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
