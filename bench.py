@@ -76,8 +76,6 @@ def kernel_work(name, cfg, counts):
         return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * dff * b + R * d * b))
     if name in ("bwd_dw1", "bwd_dw2"):
         return dict(flops=2.0 * R * d * dff, bytes=float(E * d * dff * 4 + R * (d + dff) * b))
-    if name == "bwd_dz":
-        return dict(flops=0.0, bytes=float(3 * R * dff * b))
     if name == "bwd_tr":       # four launches (R x d, R x d_ff, R x d_ff, R x d): their mean
         return dict(flops=0.0, bytes=float(R * (d + dff) * b))
     if name == "cbwd_rows":
@@ -166,7 +164,7 @@ def cpu_baseline(inp, h, budget_s=15.0):
                 sample=sample)
 
 
-BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_wt", "bwd_z", "bwd_da", "bwd_dz", "bwd_dx",
+BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_wt", "bwd_z", "bwd_da", "bwd_dx",
                     "bwd_dx_reduce", "bwd_tr", "bwd_dw2", "bwd_dw1")
 
 

@@ -266,7 +266,7 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
  * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
  * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
- * bwd_wt, bwd_z, bwd_da, bwd_dz, bwd_dx, bwd_dx_reduce, bwd_tr, bwd_dw2,
+ * bwd_wt, bwd_z, bwd_da, bwd_dx, bwd_dx_reduce, bwd_tr, bwd_dw2,
  * bwd_dw1.
  * ---------------------------------------------------------------------- */
 int luffy_profile_kernel(const char* name);

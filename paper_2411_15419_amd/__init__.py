@@ -355,6 +355,39 @@ class MoELayer:
         b = self.buf
         luffy_combine(b.y_rep, b.rep_row, b.slot_pos, b.topk_gate, b.y, stream)
 
+    def backward(self, x, dy, stream=None):
+        """Gradients of the last call's output for dy = dL/dy [T, d], with its
+        condensation held fixed (bf16 layers): returns (dgate [T, k] float32,
+        dx_rep [T*k, d] with rows 0..R-1 the representatives' input
+        gradients, in the order of rep_token, dw1, dw2 float32).  Buffers
+        are allocated on the first call and reused."""
+        b = self.buf
+        if self.dtype != torch.bfloat16:
+            raise LuffyError("MoELayer.backward: the expert FFN backward is bf16 only")
+        S = self.T * self.k
+        dev = dy.device
+        if getattr(self, "_bwd", None) is None:
+            E, dff, d = self.w1.shape
+            self._bwd = dict(
+                dy_rep=torch.empty_like(b.y_rep),
+                dgate=torch.empty(self.T, self.k, dtype=torch.float32, device=dev),
+                dx_rep=torch.empty(S, d, dtype=self.dtype, device=dev),
+                dw1=torch.empty(E, dff, d, dtype=torch.float32, device=dev),
+                dw2=torch.empty(E, d, dff, dtype=torch.float32, device=dev),
+                ws_c=_workspace(combine_backward_workspace_size(self.T, self.k, S), dev),
+                ws_f=_workspace(expert_ffn_backward_workspace_size(S, E, d, dff, LUFFY_BF16), dev),
+            )
+        g = self._bwd
+        luffy_combine_backward(dy, b.y_rep, b.rep_row, b.perm_token, b.slot_pos, b.topk_gate, b.offsets,
+                               b.rep_offsets, g["dy_rep"], g["dgate"], g["ws_c"], stream)
+        if b.x_rep is not None:
+            src, idx = b.x_rep, None
+        else:
+            src, idx = x, b.rep_token
+        luffy_expert_ffn_backward(src, idx, b.rep_offsets, self.w1, self.w2, self.act, S, g["dy_rep"],
+                                  g["dx_rep"], g["dw1"], g["dw2"], g["ws_f"], stream)
+        return g["dgate"], g["dx_rep"], g["dw1"], g["dw2"]
+
     def __call__(self, x, stream=None, threshold=None):
         if x.shape != (self.T, self.d) or x.dtype != self.dtype:
             raise LuffyError(f"x must be [{self.T}, {self.d}] {self.dtype}")

@@ -63,6 +63,35 @@ __device__ __forceinline__ float act_fast(float z) {
   }
 }
 
+// Derivative of the activation, with the approximations of act_fast (the
+// result is rounded to bf16): GELU'(z) = Phi(z) + z phi(z), Phi from the
+// same Hastings erf (Phi(z) = 1 - q/2 for z >= 0, q/2 below), phi(z) =
+// e^{-z^2/2} / sqrt(2 pi) from the same exp2; SiLU'(z) = s (1 + z (1 - s)).
+template <int ACT>
+__device__ __forceinline__ float act_grad(float z) {
+  if constexpr (ACT == LUFFY_ACT_GELU) {
+    constexpr float kP = 0.3275911f;
+    constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
+    constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
+    constexpr float kInvSqrt2 = 0.70710678118654752f, kInvSqrt2Pi = 0.39894228040143268f;
+    constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
+    const float u = fabsf(z) * kInvSqrt2;
+    const float t = __builtin_amdgcn_rcpf(fmaf(kP, u, 1.0f));
+    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, kA5, kA4), kA3), kA2), kA1);
+    const float e = __builtin_amdgcn_exp2f(z * z * kHalfLog2e);   // e^{-z^2/2}
+    const float hq = 0.5f * poly * e;
+    return (z >= 0.f ? 1.0f - hq : hq) + z * kInvSqrt2Pi * e;
+  } else {
+    constexpr float kNegLog2e = -1.44269504088896341f;
+    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * kNegLog2e));
+    return sg * (1.0f + z * (1.0f - sg));
+  }
+}
+
+// Epilogue codes of the backward's dA product: multiply by act'(Z) read
+// from a second buffer (dZ = dA * act'(Z)).
+constexpr int kActDzGelu = 3, kActDzSilu = 4;
+
 // Row tile q of the ragged row list: expert e, first row row0 and row count.
 // Wave-uniform; lane e handles expert e.  Returns false past the last tile.
 __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_offsets, int E,
@@ -198,7 +227,7 @@ template <class G, int ACT, bool FIRST>
 __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
                                          const uint16_t* __restrict__ We, int K, int N, int k0, int k1, int row0,
                                          int rows, int n0, uint16_t* __restrict__ out, float* __restrict__ slot,
-                                         uint8_t* lds) {
+                                         const uint16_t* __restrict__ aux, uint8_t* lds) {
   static_assert(G::FN <= 5, "ragged dispatch instantiates FN + 1 main loops");
   const int tid = opaque_tid(), lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = G::wave_m(w), wn = G::wave_n(w);
@@ -237,10 +266,20 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
           continue;
         }
         float z[4];
+        if constexpr (ACT == kActDzGelu || ACT == kActDzSilu) {
+          // dZ = dA * act'(Z): the four Z values of this store
+          const uint2 zw = *reinterpret_cast<const uint2*>(aux + static_cast<size_t>(row0 + ml) * N + n);
+          const float zz[4] = {__uint_as_float(zw.x << 16), __uint_as_float(zw.x & 0xFFFF0000u),
+                               __uint_as_float(zw.y << 16), __uint_as_float(zw.y & 0xFFFF0000u)};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          z[q] = acc[fm][fn][4 * g + q];
-          if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
+          for (int q = 0; q < 4; ++q)
+            z[q] = acc[fm][fn][4 * g + q] * act_grad<ACT == kActDzGelu ? LUFFY_ACT_GELU : LUFFY_ACT_SILU>(zz[q]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            z[q] = acc[fm][fn][4 * g + q];
+            if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
+          }
         }
         *reinterpret_cast<uint2*>(orow + n) = make_uint2(pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3]));
       }
@@ -257,7 +296,8 @@ template <int ACT, bool FIRST>
 __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
-    const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots) {
+    const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots,
+    const uint16_t* __restrict__ aux) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kFfnLds];
   const FfnTiles map(rep_offsets, E, N);
   const int nk = K / kFfnKUnit;
@@ -276,9 +316,9 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const int k0 = (part * nk / S) * kFfnKUnit, k1 = ((part + 1) * nk / S) * kFfnKUnit;
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
     if (wide)
-      ffn_tile<FfnGemmWide, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, lds);
+      ffn_tile<FfnGemmWide, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
     else
-      ffn_tile<FfnGemm, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, lds);
+      ffn_tile<FfnGemm, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
   }
 }
 
@@ -473,12 +513,13 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
     {
       launch("ffn1", ffn_kernel_bf16<ACT, true>, grid, FfnGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
              row_index, rep_offsets, E, d, d_ff, static_cast<const uint16_t*>(w1), static_cast<uint16_t*>(hidden),
-             ws.split_slots);
+             ws.split_slots, static_cast<const uint16_t*>(nullptr));
     }
     {
       launch("ffn2", ffn_kernel_bf16<ACT, false>, grid, FfnGemm::THREADS, 0, s,
              static_cast<const uint16_t*>(hidden), nullptr, rep_offsets, E, d_ff, d,
-             static_cast<const uint16_t*>(w2), static_cast<uint16_t*>(y_rep), ws.split_slots);
+             static_cast<const uint16_t*>(w2), static_cast<uint16_t*>(y_rep), ws.split_slots,
+             static_cast<const uint16_t*>(nullptr));
     }
     {
       launch("ffn2_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots,
@@ -500,38 +541,13 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
 
 // ---------------------------------------------------------------- backward
 // Gradients of Y = W2 act(W1 x) on the representatives (bf16):
-//   Z = X W1^T (recomputed), dA = dY W2, dZ = dA * act'(Z),
-//   dX = dZ W1, dW2 = dY^T act(Z), dW1 = dZ^T X.
+//   Z = X W1^T (recomputed), dZ = (dY W2) * act'(Z) (in the product's
+//   epilogue), dX = dZ W1, dW2 = dY^T act(Z), dW1 = dZ^T X.
 // The row products dA and dX run on the forward's grouped kernel with
 // transposed weights; the weight gradients contract over an expert's rows,
 // so those operands are first transposed per expert into [columns, Kp_e]
 // blocks (Kp_e = R_e rounded up to 64, zero-padded) and multiplied by a
 // grouped 256 x 256 tile kernel with float32 output.
-
-// Derivative of the activation, with the approximations of act_fast (the
-// result is rounded to bf16): GELU'(z) = Phi(z) + z phi(z), Phi from the
-// same Hastings erf (Phi(z) = 1 - q/2 for z >= 0, q/2 below), phi(z) =
-// e^{-z^2/2} / sqrt(2 pi) from the same exp2; SiLU'(z) = s (1 + z (1 - s)).
-template <int ACT>
-__device__ __forceinline__ float act_grad(float z) {
-  if constexpr (ACT == LUFFY_ACT_GELU) {
-    constexpr float kP = 0.3275911f;
-    constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
-    constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
-    constexpr float kInvSqrt2 = 0.70710678118654752f, kInvSqrt2Pi = 0.39894228040143268f;
-    constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
-    const float u = fabsf(z) * kInvSqrt2;
-    const float t = __builtin_amdgcn_rcpf(fmaf(kP, u, 1.0f));
-    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, kA5, kA4), kA3), kA2), kA1);
-    const float e = __builtin_amdgcn_exp2f(z * z * kHalfLog2e);   // e^{-z^2/2}
-    const float hq = 0.5f * poly * e;
-    return (z >= 0.f ? 1.0f - hq : hq) + z * kInvSqrt2Pi * e;
-  } else {
-    constexpr float kNegLog2e = -1.44269504088896341f;
-    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * kNegLog2e));
-    return sg * (1.0f + z * (1.0f - sg));
-  }
-}
 
 // 64 x 64 bf16 tile transposes through LDS with 16-byte global accesses:
 // thread i loads 8 consecutive elements of source rows i/8 and i/8 + 32
@@ -557,27 +573,42 @@ __device__ __forceinline__ uint4 tile_col8(const uint16_t (*tile)[kTrPitch], int
 }
 
 // Batched transpose of [batch][rows][cols] bf16 into [batch][cols][rows]
-// (rows, cols multiples of 64).
+// (rows, cols multiples of 64); two tiles per step, so that four 16-byte
+// loads per thread are in flight.
 __global__ __launch_bounds__(256) void transpose2d_kernel(const uint16_t* __restrict__ src, int rows, int cols,
                                                           int batch, uint16_t* __restrict__ dst) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kTrPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][64][kTrPitch];
   const int rt = rows / 64, ct = cols / 64;
   const int i = threadIdx.x, a = i >> 3, b8 = (i & 7) * 8;
   const long long total = static_cast<long long>(batch) * rt * ct;
-  for (long long it = blockIdx.x; it < total; it += gridDim.x) {
-    const int bt = static_cast<int>(it / (rt * ct));
-    const int rem = static_cast<int>(it - static_cast<long long>(bt) * rt * ct);
-    const int r0 = (rem / ct) * 64, c0 = (rem % ct) * 64;
-    const uint16_t* sb = src + static_cast<size_t>(bt) * rows * cols;
-    uint16_t* db = dst + static_cast<size_t>(bt) * rows * cols;
-    const uint4 v0 = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(r0 + a) * cols + c0 + b8);
-    const uint4 v1 = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(r0 + a + 32) * cols + c0 + b8);
-    tile_put8(tile, a, b8, v0);
-    tile_put8(tile, a + 32, b8, v1);
+  for (long long it0 = 2ll * blockIdx.x; it0 < total; it0 += 2ll * gridDim.x) {
+    uint4 v[2][2];
+    size_t sbase[2], dbase[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const long long it = min(it0 + h, total - 1);   // a missing second tile repeats the first
+      const int bt = static_cast<int>(it / (rt * ct));
+      const int rem = static_cast<int>(it - static_cast<long long>(bt) * rt * ct);
+      const int r0 = (rem / ct) * 64, c0 = (rem % ct) * 64;
+      sbase[h] = static_cast<size_t>(bt) * rows * cols + static_cast<size_t>(r0) * cols + c0;
+      dbase[h] = static_cast<size_t>(bt) * rows * cols + static_cast<size_t>(c0) * rows + r0;
+      v[h][0] = *reinterpret_cast<const uint4*>(src + sbase[h] + static_cast<size_t>(a) * cols + b8);
+      v[h][1] = *reinterpret_cast<const uint4*>(src + sbase[h] + static_cast<size_t>(a + 32) * cols + b8);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      tile_put8(tile[h], a, b8, v[h][0]);
+      tile_put8(tile[h], a + 32, b8, v[h][1]);
+    }
     __syncthreads();
-    // destination row c0 + a holds source column a: rows r0 + b8 .. + 7
-    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a) * rows + r0 + b8) = tile_col8(tile, b8, a);
-    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a + 32) * rows + r0 + b8) = tile_col8(tile, b8, a + 32);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (it0 + h >= total) break;
+      // destination row c0 + a holds source column a: rows r0 + b8 .. + 7
+      *reinterpret_cast<uint4*>(dst + dbase[h] + static_cast<size_t>(a) * rows + b8) = tile_col8(tile[h], b8, a);
+      *reinterpret_cast<uint4*>(dst + dbase[h] + static_cast<size_t>(a + 32) * rows + b8) =
+          tile_col8(tile[h], b8, a + 32);
+    }
     __syncthreads();
   }
 }
@@ -648,28 +679,6 @@ __global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t* __r
     *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a) * kp + k0 + b8) = tile_col8(tile, b8, a);
     *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a + 32) * kp + k0 + b8) = tile_col8(tile, b8, a + 32);
     __syncthreads();
-  }
-}
-
-// dZ = dA * act'(Z), in place over the R = rep_offsets[E] rows of [*, d_ff]
-// (8 elements per thread and step).
-template <int ACT>
-__global__ __launch_bounds__(256) void dz_kernel(const int32_t* __restrict__ rep_offsets, int E, int d_ff,
-                                                 const uint16_t* __restrict__ z, uint16_t* __restrict__ da) {
-  const long long n8 = static_cast<long long>(rep_offsets[E]) * d_ff / 8;
-  const uint4* zz = reinterpret_cast<const uint4*>(z);
-  uint4* aa = reinterpret_cast<uint4*>(da);
-  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n8; i += static_cast<long long>(gridDim.x) * 256) {
-    const uint4 zv = zz[i], av = aa[i];
-    const uint32_t zw[4] = {zv.x, zv.y, zv.z, zv.w}, aw[4] = {av.x, av.y, av.z, av.w};
-    uint32_t o[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float z0 = __uint_as_float(zw[q] << 16), z1 = __uint_as_float(zw[q] & 0xFFFF0000u);
-      const float a0 = __uint_as_float(aw[q] << 16), a1 = __uint_as_float(aw[q] & 0xFFFF0000u);
-      o[q] = pack_bf16x2(a0 * act_grad<ACT>(z0), a1 * act_grad<ACT>(z1));
-    }
-    aa[i] = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -749,20 +758,20 @@ void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* 
                     const uint16_t* w1, const uint16_t* w2, int max_rows, const uint16_t* dy, uint16_t* dx,
                     float* dw1, float* dw2, const FfnBwdWs& ws, hipStream_t s) {
   const int grid = persistent_grid();
-  const int tgrid = 4 * grid;
+  const int tgrid = 8 * grid;
   // transposed weights: W1T [E][d][d_ff], W2T [E][d_ff][d]
   launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w1, d_ff, d, E, ws.w1t);
   launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w2, d, d_ff, E, ws.w2t);
   // Z = X W1^T; dA = dY W2 (weights W2T, K = d); dZ = dA act'(Z)
   launch("bwd_z", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, x, row_index, rep_offsets, E, d,
-         d_ff, w1, ws.z, ws.split_slots);
-  launch("bwd_da", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d,
-         d_ff, static_cast<const uint16_t*>(ws.w2t), ws.da, ws.split_slots);
-  launch("bwd_dz", dz_kernel<ACT>, tgrid, 256, 0, s, rep_offsets, E, d_ff, static_cast<const uint16_t*>(ws.z), ws.da);
+         d_ff, w1, ws.z, ws.split_slots, static_cast<const uint16_t*>(nullptr));
+  constexpr int kDz = ACT == LUFFY_ACT_GELU ? kActDzGelu : kActDzSilu;
+  launch("bwd_da", ffn_kernel_bf16<kDz, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d, d_ff,
+         static_cast<const uint16_t*>(ws.w2t), ws.da, ws.split_slots, static_cast<const uint16_t*>(ws.z));
   // dX = dZ W1 (weights W1T, K = d_ff), split over K as in the forward's second product
   launch("bwd_dx", ffn_kernel_bf16<kActNone, false>, grid, FfnGemm::THREADS, 0, s,
          static_cast<const uint16_t*>(ws.da), nullptr, rep_offsets, E, d_ff, d,
-         static_cast<const uint16_t*>(ws.w1t), dx, ws.split_slots);
+         static_cast<const uint16_t*>(ws.w1t), dx, ws.split_slots, static_cast<const uint16_t*>(nullptr));
   launch("bwd_dx_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots, dx,
          grid);
   // dW2 = dY^T act(Z): P = dY^T [d, Kp], Q = act(Z)^T [d_ff, Kp]

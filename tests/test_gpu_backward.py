@@ -146,3 +146,33 @@ def test_expert_ffn_backward(d, d_ff, act):
             assert viol.max() <= 1e-12, \
                 f"{name} expert {e} (rows {hi - lo}): worst entry {np.unravel_index(viol.argmax(), viol.shape)}"
 
+
+
+def test_layer_backward_end_to_end():
+    """MoELayer.backward (both backward entry points in a row) on c2
+    reduced, against the oracle's chain on the GPU forward's condensation:
+    dgate within 1e-4 |dy_t| |y_rep_r|, the representatives' dx rows within
+    the bf16 tolerance, and a second call with a different dy."""
+    import torch
+    print_case("layer_backward", config="c2", **REDUCED["c2"])
+    inp, dev, layer, g = _forward("c2")
+    x = dev["x"]
+    T, d = layer.buf.y.shape
+    R = int(g["rep_offsets"][-1])
+    xr = inp.x.astype(np.float64)[g["rep_token"]]
+    rng = np.random.default_rng(29)
+    for call in range(2):
+        dy_np = _bf16_exact(rng.standard_normal((T, d)))
+        dy = torch.from_numpy(dy_np.astype(np.float32)).to(torch.bfloat16).cuda()
+        dgate, dx_rep, dw1, dw2 = layer.backward(x, dy)
+        torch.cuda.synchronize()
+        ref_rep, ref_gate = O.combine_backward(dy_np, g["y_rep"].astype(np.float64), g["rep_row"],
+                                               g["slot_pos"], g["topk_gate"].astype(np.float64))
+        ref_dx, _, _ = O.expert_ffn_backward(xr, g["rep_offsets"], inp.w1, inp.w2, inp.cfg.act, ref_rep[:R])
+        got_gate = dgate.double().cpu().numpy()
+        kept = g["slot_pos"] >= 0
+        rows = g["rep_row"][g["slot_pos"][kept]]
+        scale = np.linalg.norm(dy_np, axis=1)[np.nonzero(kept)[0]] * np.linalg.norm(g["y_rep"][rows], axis=1)
+        assert np.all(np.abs(got_gate[kept] - ref_gate[kept]) <= 1e-4 * scale), f"call {call}: dgate"
+        err, _ = rel_err_rows(dx_rep[:R].double().cpu().numpy(), ref_dx)
+        assert err.max() <= TOL["bf16"], f"call {call}: dx_rep max row rel err {err.max():.3g}"
