@@ -87,6 +87,23 @@ def test_invalid_arguments_rejected_on_host(lib):
                                 fake, 1 << 30, None) == -2
     # combine: k not 1/2
     assert lib.luffy_combine(fake, fake, fake, fake, 8, 3, 64, 1, fake, None) == -1
+    # combine backward: null pointer, k not 1/2, d not a multiple of 64, workspace too small
+    assert lib.luffy_combine_backward(None, fake, fake, fake, fake, fake, fake, fake, 4, 8, 2, 64, 1, 16,
+                                      fake, fake, fake, 1 << 20, None) == -1
+    assert lib.luffy_combine_backward(fake, fake, fake, fake, fake, fake, fake, fake, 4, 8, 3, 64, 1, 16,
+                                      fake, fake, fake, 1 << 20, None) == -1
+    assert lib.luffy_combine_backward(fake, fake, fake, fake, fake, fake, fake, fake, 4, 8, 2, 96, 1, 16,
+                                      fake, fake, fake, 1 << 20, None) == -2
+    assert lib.luffy_combine_backward(fake, fake, fake, fake, fake, fake, fake, fake, 4, 8, 2, 64, 1, 16,
+                                      fake, fake, fake, 16, None) == -3
+    # expert FFN backward: bf16 only, unknown activation, workspace too small
+    assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 0, fake, fake, 0, 8, fake, fake,
+                                         fake, fake, fake, 1 << 30, None) == -2
+    assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 1, fake, fake, 9, 8, fake, fake,
+                                         fake, fake, fake, 1 << 30, None) == -1
+    assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 1, fake, fake, 0, 8, fake, fake,
+                                         fake, fake, fake, 256, None) == -3
+    assert lib.luffy_expert_ffn_backward_workspace_size(8, 4, 64, 128, 0) == 0   # float32: none
 
 
 def test_binding_refuses_cpu_tensors(lib):
