@@ -43,7 +43,9 @@ namespace {
 
 constexpr int kGreedyGridRounds = 2;
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
-constexpr int kTileF32 = 128;   // similarity tile of the fp32 path
+constexpr int kTileF32 = 64;    // similarity tile of the fp32 path
+constexpr int kGroupsF32 = kTileF32 / 16;   // 16-column bit groups per tile row
+constexpr int kWordsF32 = kTileF32 / 64;    // bitmask words per tile row
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
 
 __device__ __forceinline__ float wave_sum_f32(float v) {
@@ -182,27 +184,29 @@ __device__ __forceinline__ TileCoord decode_tile(int tile, const int32_t* __rest
   return c;
 }
 
-// Writes the tile's adjacency words: rows of tile-row ti at words 2tj, 2tj+1
-// (from dbits) and, off the diagonal, rows of tile-row tj at words 2ti, 2ti+1
-// (from tbits).  dbits/tbits: [128 rows][8 groups of 16 columns].
-__device__ __forceinline__ void write_tile_words(const TileCoord& c, const uint16_t (*dbits)[8],
-                                                 const uint16_t (*tbits)[8],
+// Writes the tile's adjacency words: rows of tile-row ti at words
+// kWordsF32 * tj + w (from dbits) and, off the diagonal, rows of tile-row tj
+// at words kWordsF32 * ti + w (from tbits).  dbits/tbits: [kTileF32 rows]
+// [kGroupsF32 groups of 16 columns].
+__device__ __forceinline__ void write_tile_words(const TileCoord& c, const uint16_t (*dbits)[kGroupsF32],
+                                                 const uint16_t (*tbits)[kGroupsF32],
                                                  uint64_t* __restrict__ bitmask, long long base) {
   const int tid = threadIdx.x;
-  const int rl = tid >> 1, ww = tid & 1;
+  if (tid >= kTileF32 * kWordsF32) return;
+  const int rl = tid / kWordsF32, ww = tid % kWordsF32;
   auto pack = [](const uint16_t* g) {
     return static_cast<uint64_t>(g[0]) | (static_cast<uint64_t>(g[1]) << 16) |
            (static_cast<uint64_t>(g[2]) << 32) | (static_cast<uint64_t>(g[3]) << 48);
   };
   {
     const int a = c.ti * kTileF32 + rl;
-    const int wd = 2 * c.tj + ww;
+    const int wd = kWordsF32 * c.tj + ww;
     if (a < c.n && wd < c.W)
       bitmask[base + static_cast<long long>(a) * c.W + wd] = pack(&dbits[rl][4 * ww]);
   }
   if (c.ti != c.tj) {
     const int b = c.tj * kTileF32 + rl;
-    const int wd = 2 * c.ti + ww;
+    const int wd = kWordsF32 * c.ti + ww;
     if (b < c.n && wd < c.W)
       bitmask[base + static_cast<long long>(b) * c.W + wd] = pack(&tbits[rl][4 * ww]);
   }
@@ -366,8 +370,9 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
   }
 }
 
-// float32 tokens: same tiles and bitmask, plain FMA with an 8x8 micro-tile
-// per thread.
+// float32 tokens: 64-row tiles (small buckets give more tiles than with the
+// bf16 path's 256), same bitmask, plain FMA with a 4x4 micro-tile per
+// thread.
 __global__ __launch_bounds__(256) void gram_kernel_f32(
     const float* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
@@ -376,19 +381,20 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
   constexpr int KC = 16;
   __shared__ float Ps[kTileF32][KC + 1];
   __shared__ float Qs[kTileF32][KC + 1];
+  constexpr int MT = kTileF32 / 16;   // micro-tile edge: 16 x 16 threads cover the tile
   __shared__ uint8_t edge[kTileF32][kTileF32];
-  __shared__ uint16_t dbits[kTileF32][8];
-  __shared__ uint16_t tbits[kTileF32][8];
+  __shared__ uint16_t dbits[kTileF32][kGroupsF32];
+  __shared__ uint16_t tbits[kTileF32][kGroupsF32];
   __shared__ float inv_a[kTileF32], inv_b[kTileF32];
   if (*err) return;
   const int tid = threadIdx.x;
-  const int rb = (tid >> 4) * 8, cb = (tid & 15) * 8;
+  const int rb = (tid >> 4) * MT, cb = (tid & 15) * MT;
   const int total = tile_off[E];
   for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
     const TileCoord c = decode_tile(tile, tile_off, offsets, E);
     const int32_t* pt = perm_token + c.lo;
     if (tid < kTileF32) inv_a[tid] = inv_norm[pt[min(c.ti * kTileF32 + tid, c.n - 1)]];
-    else inv_b[tid - kTileF32] = inv_norm[pt[min(c.tj * kTileF32 + tid - kTileF32, c.n - 1)]];
+    else if (tid < 2 * kTileF32) inv_b[tid - kTileF32] = inv_norm[pt[min(c.tj * kTileF32 + tid - kTileF32, c.n - 1)]];
     // staged element i of this thread: tile row r0 + 16i, column kk; the
     // token rows are looked up once per tile and the next chunk is loaded
     // into registers while the current one is multiplied
@@ -408,11 +414,11 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       vp[i] = pp[i][0];
       vq[i] = qp[i][0];
     }
-    float acc[8][8];
+    float acc[MT][MT];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+      for (int j = 0; j < MT; ++j) acc[i][j] = 0.f;
     for (int k0 = 0; k0 < d; k0 += KC) {
       __syncthreads();
 #pragma unroll
@@ -430,28 +436,28 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       }
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        float pa[8], qb[8];
+        float pa[MT], qb[MT];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) pa[i] = Ps[rb + i][k];
+        for (int i = 0; i < MT; ++i) pa[i] = Ps[rb + i][k];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) qb[j] = Qs[cb + j][k];
+        for (int j = 0; j < MT; ++j) qb[j] = Qs[cb + j][k];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < MT; ++i)
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(pa[i], qb[j], acc[i][j]);
+          for (int j = 0; j < MT; ++j) acc[i][j] = fmaf(pa[i], qb[j], acc[i][j]);
       }
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < MT; ++j) {
         const int a = c.ti * kTileF32 + rb + i, b = c.tj * kTileF32 + cb + j;
         const float cs = acc[i][j] * inv_a[rb + i] * inv_b[cb + j];
         edge[rb + i][cb + j] = (a < c.n && b < c.n && a != b && cs >= h) ? 1 : 0;
       }
     __syncthreads();
-    for (int idx = tid; idx < kTileF32 * 8; idx += 256) {
-      const int r = idx >> 3, g = idx & 7;
+    for (int idx = tid; idx < kTileF32 * kGroupsF32; idx += 256) {
+      const int r = idx / kGroupsF32, g = idx % kGroupsF32;
       uint32_t dv = 0, tv = 0;
       for (int bit = 0; bit < 16; ++bit) {
         dv |= static_cast<uint32_t>(edge[r][16 * g + bit]) << bit;
@@ -461,11 +467,11 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
       tbits[r][g] = static_cast<uint16_t>(tv);
     }
     __syncthreads();
-    {
+    if (tid < 2 * kTileF32) {
       const bool mirror = tid >= kTileF32;
       const int rl = mirror ? tid - kTileF32 : tid;
       int cnt = 0;
-      for (int g = 0; g < 8; ++g) cnt += __popc(mirror ? tbits[rl][g] : dbits[rl][g]);
+      for (int g = 0; g < kGroupsF32; ++g) cnt += __popc(mirror ? tbits[rl][g] : dbits[rl][g]);
       const int r = (mirror ? c.tj : c.ti) * kTileF32 + rl;
       if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
     }
