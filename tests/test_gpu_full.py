@@ -149,3 +149,84 @@ def test_full_size_c4_threshold_sweep():
             tokens = sample_tokens(o, cfg.T, seed=0)
             ref = (tokens,) + sampled_expected(inp, o, tokens)
         assert_sampled_close(g, inp, *ref)
+
+
+@pytest.mark.timeout(300)
+def test_full_size_backward_c2():
+    """The backward at the full c2 size (T = 8192, d = 1024, E = 16,
+    d_ff = 4096), as `bench.py --backward` runs it (MoELayer.backward after
+    one forward whose indices match the oracle's), checked on seeded samples
+    the oracle computes one by one from the GPU's own forward values:
+    dgate of sampled slots, dy_rep of sampled representatives (their member
+    sums), dx_rep of sampled representatives (the FFN gradient of one row),
+    and sampled entries of dW1 and dW2 of two experts (sums over all their
+    representatives, held to 2e-2 of the sum of the terms' magnitudes)."""
+    import torch
+    inp = G.make_inputs("c2", seed=0)
+    print_case("backward c2 full")
+    dev = upload(inp)
+    layer = make_layer(inp, dev)
+    layer(dev["x"])
+    g = fetch(layer)
+    o = O.moe_layer(inp.x.astype(np.float64), inp.w_g, inp.b_g, inp.w1, inp.w2, k=inp.cfg.k, h=inp.cfg.h,
+                    act=inp.cfg.act, capacity_factor=inp.cfg.capacity_factor, with_ffn=False)
+    assert_route_equal(g, o)
+    assert_condense_equal(g, o)
+    T, d = layer.buf.y.shape
+    act = inp.cfg.act
+    rng = np.random.default_rng(31)
+    dy = torch.randn(T, d, generator=torch.Generator().manual_seed(31)).to(torch.bfloat16)
+    dy_np = dy.double().numpy()
+    dgate, dx_rep, dw1, dw2 = layer.backward(dev["x"], dy.cuda())
+    torch.cuda.synchronize()
+    dy_rep = layer._bwd["dy_rep"].double().cpu().numpy()
+    dgate, dx_rep = dgate.double().cpu().numpy(), dx_rep.double().cpu().numpy()
+    y_rep = g["y_rep"].astype(np.float64)
+    R = int(g["rep_offsets"][-1])
+    # dgate of sampled kept slots
+    kept_t, kept_j = np.nonzero(g["slot_pos"] >= 0)
+    for i in rng.choice(kept_t.size, 64, replace=False):
+        t, j = kept_t[i], kept_j[i]
+        r = g["rep_row"][g["slot_pos"][t, j]]
+        ref = dy_np[t] @ y_rep[r]
+        assert abs(dgate[t, j] - ref) <= 1e-4 * np.linalg.norm(dy_np[t]) * np.linalg.norm(y_rep[r]), (t, j)
+    # dy_rep of sampled representatives: the gate-weighted sum of their members' dy
+    S = int(g["offsets"][-1])
+    pos_t = g["perm_token"]
+    pos_gate = np.zeros(S)
+    for j in range(g["slot_pos"].shape[1]):
+        kept = g["slot_pos"][:, j] >= 0
+        pos_gate[g["slot_pos"][kept, j]] = g["topk_gate"][kept, j]
+    reps = rng.choice(R, 32, replace=False)
+    for r in reps:
+        members = np.flatnonzero(g["rep_row"][:S] == r)
+        ref = (pos_gate[members, None] * dy_np[pos_t[members]]).sum(axis=0)
+        err = np.abs(dy_rep[r] - ref).max() / np.abs(ref).max()
+        assert err <= TOL["bf16"], f"dy_rep row {r}: {err:.3g}"
+    # dx_rep of sampled representatives, from the GPU's dy_rep rows
+    ro = g["rep_offsets"]
+    xr = inp.x.astype(np.float64)[g["rep_token"]]
+    for r in reps:
+        e = int(np.searchsorted(ro, r, side="right") - 1)
+        z = xr[r] @ inp.w1[e].T
+        dz = (dy_rep[r] @ inp.w2[e]) * O.activation_grad(z, act)
+        ref = dz @ inp.w1[e]
+        err = np.abs(dx_rep[r] - ref).max() / np.abs(ref).max()
+        assert err <= TOL["bf16"], f"dx_rep row {r}: {err:.3g}"
+    # sampled weight-gradient entries of two experts
+    gw1, gw2 = dw1.double().cpu().numpy(), dw2.double().cpu().numpy()
+    for e in (0, inp.cfg.E - 1):
+        lo, hi = int(ro[e]), int(ro[e + 1])
+        z = xr[lo:hi] @ inp.w1[e].T
+        a = O.activation(z, act)
+        da = dy_rep[lo:hi] @ inp.w2[e]
+        dz = da * O.activation_grad(z, act)
+        for _ in range(16):
+            i, c = rng.integers(inp.cfg.d_ff), rng.integers(d)
+            ref1 = dz[:, i] @ xr[lo:hi, c]
+            b1 = (np.abs(da[:, i]) * (np.abs(O.activation_grad(z[:, i], act)) + np.abs(z[:, i]))) @ np.abs(xr[lo:hi, c])
+            assert abs(gw1[e, i, c] - ref1) <= TOL["bf16"] * b1, ("dW1", e, i, c)
+            ref2 = dy_rep[lo:hi, c] @ a[:, i]
+            b2 = np.abs(dy_rep[lo:hi, c]) @ (np.abs(a[:, i]) + np.abs(z[:, i]) * np.abs(O.activation_grad(z[:, i], act)))
+            assert abs(gw2[e, c, i] - ref2) <= TOL["bf16"] * b2, ("dW2", e, c, i)
+    print(f"[sampled backward] R={R}, 64 gate slots, {reps.size} rows, 64 weight entries ok", flush=True)
