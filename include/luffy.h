@@ -52,7 +52,7 @@ extern "C" {
 typedef enum {
   LUFFY_OK = 0,
   LUFFY_E_INVALID = -1,     /* null pointer, bad size, k > E, k not 1 or 2 */
-  LUFFY_E_UNSUPPORTED = -2, /* a size this build does not handle           */
+  LUFFY_E_UNSUPPORTED = -2, /* a size the library does not handle         */
   LUFFY_E_WORKSPACE = -3,   /* workspace missing, too small or misaligned  */
   LUFFY_E_HIP = -4          /* a HIP runtime call or launch failed         */
 } luffy_status;
