@@ -164,8 +164,8 @@ def cpu_baseline(inp, h, budget_s=15.0):
                 sample=sample)
 
 
-BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_wt", "bwd_z", "bwd_da", "bwd_dx",
-                    "bwd_dx_reduce", "bwd_tr", "bwd_dw2", "bwd_dw1")
+BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_z", "bwd_act", "bwd_da", "bwd_dx",
+                    "bwd_dx_reduce", "bwd_gather", "bwd_dw2", "bwd_dw1")
 
 
 def bench_backward(args, cfg, layer, x, L, torch, np):

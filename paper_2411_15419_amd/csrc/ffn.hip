@@ -12,6 +12,8 @@
 // each as one 8-byte word.  The last row tile of an expert usually holds
 // fewer rows; its waves skip the MFMAs of the missing rows.
 // fp32: 64 x 64 tiles of plain FMA (4 x 4 per thread).
+#include <type_traits>
+
 #include "gemm_core.h"
 #include "luffy_common.h"
 
@@ -131,6 +133,9 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
 // split-K slots.
 using FfnGemm = GemmRagged64;
 using FfnGemmWide = GemmCore<256, 320, 4, 2, true, false>;
+// The backward's row products read the weights transposed: P K-major.
+using FfnGemmT = GemmCore<256, 256, 4, 2, true, false, 64, 2, true, false>;
+using FfnGemmWideT = GemmCore<256, 320, 4, 2, true, false, 64, 2, true, false>;
 static_assert(FfnGemm::BM == FfnGemmWide::BM && FfnGemm::THREADS == FfnGemmWide::THREADS, "shared tile map");
 constexpr int kFfnLds = FfnGemmWide::LDS_BYTES > FfnGemm::LDS_BYTES ? FfnGemmWide::LDS_BYTES : FfnGemm::LDS_BYTES;
 // split-K partial tiles: one slot (the accumulators of a tile in register
@@ -209,12 +214,12 @@ struct FfnTiles {
 template <class G, int N>
 __device__ __forceinline__ void run_nq(int nq, const uint16_t* pbase, const uint32_t (&poff)[G::LP],
                                        const uint16_t* qbase, const uint32_t (&qoff)[G::LQ], int K, int pvalid,
-                                       int qvalid, uint8_t* lds, typename G::Acc& acc) {
+                                       int qvalid, uint8_t* lds, typename G::Acc& acc, int pld) {
   if constexpr (N == 0) {
-    G::template run<0>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
+    G::template run<0>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc, pld);
   } else {
-    if (nq >= N) G::template run<N>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
-    else run_nq<G, N - 1>(nq, pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc);
+    if (nq >= N) G::template run<N>(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc, pld);
+    else run_nq<G, N - 1>(nq, pbase, poff, qbase, qoff, K, pvalid, qvalid, lds, acc, pld);
   }
 }
 
@@ -233,7 +238,11 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
   const int wm = G::wave_m(w), wn = G::wave_n(w);
   uint32_t poff[G::LP], qoff[G::LQ];
 #pragma unroll
-  for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
+  for (int j = 0; j < G::LP; ++j) {
+    // weights [N, K] row-major, or (G::PT) [K, N]: element (k, n) at k * N + n
+    if constexpr (G::PT) poff[j] = G::kmajor_offset(j, N, n0, N - n0);
+    else poff[j] = static_cast<uint32_t>(min(n0 + G::load_row(j), N - 1)) * K;
+  }
 #pragma unroll
   for (int j = 0; j < G::LQ; ++j) {
     const int m = row0 + min(G::load_row(G::LP + j) - G::BM, rows - 1);
@@ -242,8 +251,8 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
   const int nq = G::active_q(wn, rows);
   typename G::Acc acc;
   G::zero(acc);
-  run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + k0, poff, A + k0, qoff, k1 - k0, N - n0, rows, lds,
-                   acc);
+  run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + (G::PT ? static_cast<size_t>(k0) * N : k0), poff,
+                   A + k0, qoff, k1 - k0, N - n0, rows, lds, acc, N);
 #pragma unroll
   for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
@@ -292,7 +301,7 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
 // representatives it can have fewer tiles than CUs, and it then splits K
 // (decided on the device from the actual tile count): parts store float32
 // partial tiles and ffn_split_reduce_kernel finishes them.
-template <int ACT, bool FIRST>
+template <int ACT, bool FIRST, bool WT = false>
 __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
@@ -315,10 +324,12 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     // K range of this part, in whole 64-wide units
     const int k0 = (part * nk / S) * kFfnKUnit, k1 = ((part + 1) * nk / S) * kFfnKUnit;
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
+    using GN = std::conditional_t<WT, FfnGemmT, FfnGemm>;
+    using GW = std::conditional_t<WT, FfnGemmWideT, FfnGemmWide>;
     if (wide)
-      ffn_tile<FfnGemmWide, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
+      ffn_tile<GW, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
     else
-      ffn_tile<FfnGemm, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
+      ffn_tile<GN, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
   }
 }
 
@@ -543,149 +554,55 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
 // Gradients of Y = W2 act(W1 x) on the representatives (bf16):
 //   Z = X W1^T (recomputed), dZ = (dY W2) * act'(Z) (in the product's
 //   epilogue), dX = dZ W1, dW2 = dY^T act(Z), dW1 = dZ^T X.
-// The row products dA and dX run on the forward's grouped kernel with
-// transposed weights; the weight gradients contract over an expert's rows,
-// so those operands are first transposed per expert into [columns, Kp_e]
-// blocks (Kp_e = R_e rounded up to 64, zero-padded) and multiplied by a
-// grouped 256 x 256 tile kernel with float32 output.
+// The row products dZ and dX run on the forward's grouped kernel with the
+// weights read K-major (no transposed copy: the core's transposing LDS
+// reads); the weight gradients contract over an expert's rows, read K-major
+// from the row-major activations, with the rows past the expert's read as
+// zeros up to the next multiple of 64.
 
-// 64 x 64 bf16 tile transposes through LDS with 16-byte global accesses:
-// thread i loads 8 consecutive elements of source rows i/8 and i/8 + 32
-// (uint4), and stores 8 consecutive elements of destination rows i/8 and
-// i/8 + 32, gathered from an LDS column.  The LDS row pitch of 66 elements
-// (33 words) spreads a column over the banks.
-constexpr int kTrPitch = 66;
-
-__device__ __forceinline__ void tile_put8(uint16_t (*tile)[kTrPitch], int r, int c, uint4 v) {
-  uint32_t* row = reinterpret_cast<uint32_t*>(&tile[r][c]);
-  row[0] = v.x;
-  row[1] = v.y;
-  row[2] = v.z;
-  row[3] = v.w;
-}
-
-__device__ __forceinline__ uint4 tile_col8(const uint16_t (*tile)[kTrPitch], int r, int c) {
-  uint32_t w[4];
+// A = act(Z) over the R = rep_offsets[E] rows of [*, d_ff] (8 per step).
+template <int ACT>
+__global__ __launch_bounds__(256) void act_rows_kernel(const int32_t* __restrict__ rep_offsets, int E, int d_ff,
+                                                       const uint16_t* __restrict__ z, uint16_t* __restrict__ a) {
+  const long long n8 = static_cast<long long>(rep_offsets[E]) * d_ff / 8;
+  const uint4* zz = reinterpret_cast<const uint4*>(z);
+  uint4* aa = reinterpret_cast<uint4*>(a);
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n8; i += static_cast<long long>(gridDim.x) * 256) {
+    const uint4 v = zz[i];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    w[q] = static_cast<uint32_t>(tile[r + 2 * q][c]) | (static_cast<uint32_t>(tile[r + 2 * q + 1][c]) << 16);
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-// Batched transpose of [batch][rows][cols] bf16 into [batch][cols][rows]
-// (rows, cols multiples of 64); two tiles per step, so that four 16-byte
-// loads per thread are in flight.
-__global__ __launch_bounds__(256) void transpose2d_kernel(const uint16_t* __restrict__ src, int rows, int cols,
-                                                          int batch, uint16_t* __restrict__ dst) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][64][kTrPitch];
-  const int rt = rows / 64, ct = cols / 64;
-  const int i = threadIdx.x, a = i >> 3, b8 = (i & 7) * 8;
-  const long long total = static_cast<long long>(batch) * rt * ct;
-  for (long long it0 = 2ll * blockIdx.x; it0 < total; it0 += 2ll * gridDim.x) {
-    uint4 v[2][2];
-    size_t sbase[2], dbase[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const long long it = min(it0 + h, total - 1);   // a missing second tile repeats the first
-      const int bt = static_cast<int>(it / (rt * ct));
-      const int rem = static_cast<int>(it - static_cast<long long>(bt) * rt * ct);
-      const int r0 = (rem / ct) * 64, c0 = (rem % ct) * 64;
-      sbase[h] = static_cast<size_t>(bt) * rows * cols + static_cast<size_t>(r0) * cols + c0;
-      dbase[h] = static_cast<size_t>(bt) * rows * cols + static_cast<size_t>(c0) * rows + r0;
-      v[h][0] = *reinterpret_cast<const uint4*>(src + sbase[h] + static_cast<size_t>(a) * cols + b8);
-      v[h][1] = *reinterpret_cast<const uint4*>(src + sbase[h] + static_cast<size_t>(a + 32) * cols + b8);
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      tile_put8(tile[h], a, b8, v[h][0]);
-      tile_put8(tile[h], a + 32, b8, v[h][1]);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (it0 + h >= total) break;
-      // destination row c0 + a holds source column a: rows r0 + b8 .. + 7
-      *reinterpret_cast<uint4*>(dst + dbase[h] + static_cast<size_t>(a) * rows + b8) = tile_col8(tile[h], b8, a);
-      *reinterpret_cast<uint4*>(dst + dbase[h] + static_cast<size_t>(a + 32) * rows + b8) =
-          tile_col8(tile[h], b8, a + 32);
-    }
-    __syncthreads();
+    for (int q = 0; q < 4; ++q)
+      o[q] = pack_bf16x2(act_fast<ACT>(__uint_as_float(w[q] << 16)), act_fast<ACT>(__uint_as_float(w[q] & 0xFFFF0000u)));
+    aa[i] = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
-// Per-expert layout of the transposed activations: expert e's block starts
-// at column offset kbase_e = sum of Kp over the experts before it.
-__device__ __forceinline__ void expert_kblock(const int32_t* __restrict__ rep_offsets, int e, int& kbase, int& kp) {
-  kbase = 0;
-  for (int i = 0; i < e; ++i) kbase += (rep_offsets[i + 1] - rep_offsets[i] + 63) / 64 * 64;
-  kp = (rep_offsets[e + 1] - rep_offsets[e] + 63) / 64 * 64;
-}
-
-// Expert e's rows [lo_e, hi_e) of src [*, C] (read through row_index when
-// given) into dst[C * kbase_e + c * Kp_e + k] = src[lo_e + k][c] for k < R_e,
-// 0 for R_e <= k < Kp_e; MODE applies act to the values (A = act(Z)).
-template <int MODE>
-__global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t* __restrict__ src,
-                                                             const int32_t* __restrict__ row_index,
-                                                             const int32_t* __restrict__ rep_offsets, int E, int C,
-                                                             uint16_t* __restrict__ dst) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][kTrPitch];
+// xg[r] = x[row_index[r]] for the R rows in use (one wave per row).
+__global__ __launch_bounds__(256) void gather_rows_kernel(const int32_t* __restrict__ rep_offsets, int E, int d,
+                                                          const uint16_t* __restrict__ x,
+                                                          const int32_t* __restrict__ row_index,
+                                                          uint16_t* __restrict__ xg) {
+  const int R = rep_offsets[E];
   const int lane = threadIdx.x & 63;
-  const int i = threadIdx.x, a = i >> 3, b8 = (i & 7) * 8;
-  int kt = 0, lo = 0, hi = 0;
-  if (lane < E) {
-    lo = rep_offsets[lane];
-    hi = rep_offsets[lane + 1];
-    kt = (hi - lo + 63) / 64;
-  }
-  int incl = kt;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
-  }
-  const int units = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
-  const int ct = C / 64;
-  for (int it = blockIdx.x; it < units * ct; it += gridDim.x) {
-    const int u = it / ct, c0 = (it - u * ct) * 64;
-    const int e = __popcll(__ballot(lane < E && incl <= u));
-    const int excl = __shfl(incl - kt, e, 64);   // k-tiles of the experts before e
-    const int elo = __shfl(lo, e, 64), ehi = __shfl(hi, e, 64);
-    const int kp = (ehi - elo + 63) / 64 * 64;
-    const int k0 = (u - excl) * 64;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = a + 32 * h;
-      const int row = elo + k0 + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row < ehi) {
-        const int srow = row_index ? row_index[row] : row;
-        v = *reinterpret_cast<const uint4*>(src + static_cast<size_t>(srow) * C + c0 + b8);
-        if constexpr (MODE != 0) {
-          uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            constexpr int ACT = MODE == 1 ? LUFFY_ACT_GELU : LUFFY_ACT_SILU;
-            wv[q] = pack_bf16x2(act_fast<ACT>(__uint_as_float(wv[q] << 16)),
-                                act_fast<ACT>(__uint_as_float(wv[q] & 0xFFFF0000u)));
-          }
-          v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-        }
-      }
-      tile_put8(tile, r, b8, v);
-    }
-    __syncthreads();
-    uint16_t* db = dst + static_cast<size_t>(C) * (excl * 64);
-    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a) * kp + k0 + b8) = tile_col8(tile, b8, a);
-    *reinterpret_cast<uint4*>(db + static_cast<size_t>(c0 + a + 32) * kp + k0 + b8) = tile_col8(tile, b8, a + 32);
-    __syncthreads();
+  for (int r = blockIdx.x * 4 + (threadIdx.x >> 6); r < R; r += gridDim.x * 4) {
+    const uint4* src = reinterpret_cast<const uint4*>(x + static_cast<size_t>(row_index[r]) * d);
+    uint4* dst = reinterpret_cast<uint4*>(xg + static_cast<size_t>(r) * d);
+    for (int c = lane; c < d / 8; c += 64) dst[c] = src[c];
   }
 }
 
-// Weight gradients: out[e][i][j] = sum_k P_e[i][k] Q_e[j][k] over k < Kp_e,
-// P_e = P + M * kbase_e ([M, Kp_e]), Q_e = Q + N * kbase_e ([N, Kp_e]);
-// float32 output [E][M][N]; an expert without rows gets zeros.
-using WgradGemm = GemmBig64;
+// First row and K extent (R_e rounded up to 64) of expert e.
+__device__ __forceinline__ void expert_rows(const int32_t* __restrict__ rep_offsets, int e, int& lo, int& re) {
+  lo = rep_offsets[e];
+  re = rep_offsets[e + 1] - lo;
+}
+
+// Weight gradients: out[e][i][j] = sum over the expert's rows r of
+// P[r][i] Q[r][j], P [*, M] and Q [*, N] row-major token rows (both read
+// K-major: the contraction runs over rows); float32 output [E][M][N]; an
+// expert without rows gets zeros.
+using WgradGemm = GemmCore<256, 256, 2, 4, false, false, 64, 2, true, true>;
 
 __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_t* __restrict__ P,
                                                                    const uint16_t* __restrict__ Q,
@@ -698,21 +615,20 @@ __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_
   for (int t = blockIdx.x; t < E * tpe; t += gridDim.x) {
     const int e = t / tpe, r = t - e * tpe;
     const int m0 = (r / nt) * G::BM, n0 = (r % nt) * G::BN;
-    int kbase, kp;
-    expert_kblock(rep_offsets, e, kbase, kp);
-    kbase = __builtin_amdgcn_readfirstlane(kbase);
-    kp = __builtin_amdgcn_readfirstlane(kp);
+    int lo, re;
+    expert_rows(rep_offsets, e, lo, re);
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    re = __builtin_amdgcn_readfirstlane(re);
     typename G::Acc acc;
     G::zero(acc);
-    if (kp > 0) {
+    if (re > 0) {
       uint32_t poff[G::LP], qoff[G::LQ];
 #pragma unroll
-      for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(min(m0 + G::load_row(j), M - 1)) * kp;
+      for (int j = 0; j < G::LP; ++j) poff[j] = G::kmajor_offset(j, M, m0, M - m0);
 #pragma unroll
-      for (int j = 0; j < G::LQ; ++j)
-        qoff[j] = static_cast<uint32_t>(min(n0 + G::load_row(G::LP + j) - G::BM, N - 1)) * kp;
-      G::template run<G::FN>(P + static_cast<size_t>(M) * kbase, poff, Q + static_cast<size_t>(N) * kbase, qoff, kp,
-                             M - m0, N - n0, lds, acc);
+      for (int j = 0; j < G::LQ; ++j) qoff[j] = G::kmajor_offset(G::LP + j, N, n0, N - n0);
+      G::template run<G::FN>(P + static_cast<size_t>(lo) * M, poff, Q + static_cast<size_t>(lo) * N, qoff,
+                             (re + 63) / 64 * 64, M - m0, N - n0, lds, acc, M, N, re);
     }
     const int tid = opaque_tid(), lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = G::wave_m(w), wn = G::wave_n(w);
@@ -733,22 +649,17 @@ __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_
 }
 
 struct FfnBwdWs {
-  uint16_t *w1t, *w2t, *z, *da, *tp, *tq;
+  uint16_t *z, *a, *dz, *xg;
   float* split_slots;
 };
 
-// Transposed activation blocks hold at most max_rows + 64 E columns.
 FfnBwdWs carve_ffn_bwd(Carver& c, int max_rows, int E, int d, int d_ff) {
+  (void)E;
   FfnBwdWs w;
-  const size_t wsz = static_cast<size_t>(E) * d * d_ff;
-  const size_t kcols = static_cast<size_t>(max_rows) + 64 * static_cast<size_t>(E);
-  const int wide = d > d_ff ? d : d_ff;
-  w.w1t = c.take<uint16_t>(wsz);
-  w.w2t = c.take<uint16_t>(wsz);
   w.z = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
-  w.da = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
-  w.tp = c.take<uint16_t>(kcols * wide);
-  w.tq = c.take<uint16_t>(kcols * wide);
+  w.a = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
+  w.dz = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
+  w.xg = c.take<uint16_t>(static_cast<size_t>(max_rows) * d);
   w.split_slots = c.take<float>(kFfnSlotFloats * kFfnMaxSlots);
   return w;
 }
@@ -757,35 +668,34 @@ template <int ACT>
 void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d, int d_ff,
                     const uint16_t* w1, const uint16_t* w2, int max_rows, const uint16_t* dy, uint16_t* dx,
                     float* dw1, float* dw2, const FfnBwdWs& ws, hipStream_t s) {
+  (void)max_rows;
   const int grid = persistent_grid();
-  const int tgrid = 8 * grid;
-  // transposed weights: W1T [E][d][d_ff], W2T [E][d_ff][d]
-  launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w1, d_ff, d, E, ws.w1t);
-  launch("bwd_wt", transpose2d_kernel, tgrid, 256, 0, s, w2, d, d_ff, E, ws.w2t);
-  // Z = X W1^T; dA = dY W2 (weights W2T, K = d); dZ = dA act'(Z)
+  const int egrid = 4 * grid;
+  // Z = X W1^T, A = act(Z)
   launch("bwd_z", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, x, row_index, rep_offsets, E, d,
          d_ff, w1, ws.z, ws.split_slots, static_cast<const uint16_t*>(nullptr));
+  launch("bwd_act", act_rows_kernel<ACT>, egrid, 256, 0, s, rep_offsets, E, d_ff, static_cast<const uint16_t*>(ws.z),
+         ws.a);
+  // dZ = (dY W2) act'(Z): W2 [E][d][d_ff] read K-major (k = output row o)
   constexpr int kDz = ACT == LUFFY_ACT_GELU ? kActDzGelu : kActDzSilu;
-  launch("bwd_da", ffn_kernel_bf16<kDz, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d, d_ff,
-         static_cast<const uint16_t*>(ws.w2t), ws.da, ws.split_slots, static_cast<const uint16_t*>(ws.z));
-  // dX = dZ W1 (weights W1T, K = d_ff), split over K as in the forward's second product
-  launch("bwd_dx", ffn_kernel_bf16<kActNone, false>, grid, FfnGemm::THREADS, 0, s,
-         static_cast<const uint16_t*>(ws.da), nullptr, rep_offsets, E, d_ff, d,
-         static_cast<const uint16_t*>(ws.w1t), dx, ws.split_slots, static_cast<const uint16_t*>(nullptr));
+  launch("bwd_da", ffn_kernel_bf16<kDz, true, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d,
+         d_ff, w2, ws.dz, ws.split_slots, static_cast<const uint16_t*>(ws.z));
+  // dX = dZ W1: W1 [E][d_ff][d] read K-major, split over K as the forward's second product
+  launch("bwd_dx", ffn_kernel_bf16<kActNone, false, true>, grid, FfnGemm::THREADS, 0, s,
+         static_cast<const uint16_t*>(ws.dz), nullptr, rep_offsets, E, d_ff, d, w1, dx, ws.split_slots,
+         static_cast<const uint16_t*>(nullptr));
   launch("bwd_dx_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots, dx,
          grid);
-  // dW2 = dY^T act(Z): P = dY^T [d, Kp], Q = act(Z)^T [d_ff, Kp]
-  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, dy, nullptr, rep_offsets, E, d, ws.tp);
-  launch("bwd_tr", transpose_rows_kernel<ACT == LUFFY_ACT_GELU ? 1 : 2>, tgrid, 256, 0, s,
-         static_cast<const uint16_t*>(ws.z), nullptr, rep_offsets, E, d_ff, ws.tq);
-  launch("bwd_dw2", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.tp),
-         static_cast<const uint16_t*>(ws.tq), rep_offsets, E, d, d_ff, dw2);
-  // dW1 = dZ^T X: P = dZ^T [d_ff, Kp], Q = X^T [d, Kp]
-  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, static_cast<const uint16_t*>(ws.da), nullptr,
-         rep_offsets, E, d_ff, ws.tp);
-  launch("bwd_tr", transpose_rows_kernel<0>, tgrid, 256, 0, s, x, row_index, rep_offsets, E, d, ws.tq);
-  launch("bwd_dw1", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.tp),
-         static_cast<const uint16_t*>(ws.tq), rep_offsets, E, d_ff, d, dw1);
+  // dW2 = dY^T A, dW1 = dZ^T X (X's rows gathered first)
+  launch("bwd_dw2", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, dy, static_cast<const uint16_t*>(ws.a),
+         rep_offsets, E, d, d_ff, dw2);
+  const uint16_t* xr = x;
+  if (row_index) {
+    launch("bwd_gather", gather_rows_kernel, egrid, 256, 0, s, rep_offsets, E, d, x, row_index, ws.xg);
+    xr = ws.xg;
+  }
+  launch("bwd_dw1", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.dz), xr,
+         rep_offsets, E, d_ff, d, dw1);
 }
 
 }  // namespace
@@ -860,10 +770,11 @@ extern "C" int luffy_expert_ffn_backward(const void* x, const int32_t* row_index
     return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: d=%d d_ff=%d must be multiples of 64", d, d_ff);
   if (d > 32768 || d_ff > 32768)
     return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: d=%d d_ff=%d must be at most 32768", d, d_ff);
-  const long long kcols = static_cast<long long>(max_rows) + 64ll * E;
+  // K-major reads of the activations run up to 63 rows past an expert's last
+  const long long krows = static_cast<long long>(max_rows) + 64;
   if (static_cast<long long>(max_rows) * d_ff * 2 > 0xFFFF0000ll ||
       static_cast<long long>(d) * d_ff * 2 > 0xFFFF0000ll ||
-      kcols * (d > d_ff ? d : d_ff) * 2 > 0xFFFF0000ll)
+      krows * (d > d_ff ? d : d_ff) * 2 > 0xFFFF0000ll)
     return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: an operand exceeds 4 GiB - 64 KiB");
   const size_t need = luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff, dtype);
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))

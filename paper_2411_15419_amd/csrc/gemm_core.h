@@ -71,10 +71,18 @@ __device__ __forceinline__ int opaque_tid() {
 // Result layout of acc[fm][fn][v] in lane l of wave w:
 //   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
 //   Q row  q_row(wave_n(w), fn) + l%32
-template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_, int BK_ = 64, int STAGES_ = 2>
+template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_, int BK_ = 64, int STAGES_ = 2,
+          bool PT_ = false, bool QT_ = false>
 struct GemmCore {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr bool QIL = QIL_;
+  // K-major operands (PT: P, QT: Q): the operand is stored with its rows
+  // along K (element (k, m) at k * ld + m), as a weight read transposed or
+  // the token rows of a product that contracts over tokens.  Its stage holds
+  // BK rows of k, each with the tile's BM (BN) values of m in 16-byte slots
+  // XOR-permuted by swz_t(k); MFMA fragments are read with the transposing
+  // LDS read (ds_read_b64_tr_b16), two per fragment.
+  static constexpr bool PT = PT_, QT = QT_;
   static constexpr int BK = BK_;                     // K per stage
   static constexpr int STAGES = STAGES_;
   static_assert(BK == 32 || BK == 64, "stage width");
@@ -95,11 +103,17 @@ struct GemmCore {
   static_assert(LP * NWAVES * RPI == BM && LQ * NWAVES * RPI == BN, "load plan");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
   static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+  static constexpr int SLOTS_P = BM / 8, SLOTS_Q = BN / 8;   // 16-byte slots per k row (K-major)
+  static_assert(!PT || (BK == 64 && (SLOTS_P == 16 || SLOTS_P == 32 || SLOTS_P == 64)), "K-major P tile");
+  static_assert(!QT || (BK == 64 && (SLOTS_Q == 16 || SLOTS_Q == 32 || SLOTS_Q == 64)), "K-major Q tile");
 
   using Acc = f32x16[FM][FN];
   using lds_ptr = __attribute__((address_space(3))) uint8_t*;
 
   static __device__ __forceinline__ int swz(int r) { return BK == 64 ? (r >> 1) & 7 : (r >> 2) & 3; }
+  // slot permutation of k row k of a K-major operand: the four k rows one
+  // transposing read touches land on different slots
+  static __device__ __forceinline__ int swz_t(int k) { return 2 * (k & 7); }
   static __device__ __forceinline__ int wave_m(int w) { return MFAST_ ? w % WM : w / WN; }
   static __device__ __forceinline__ int wave_n(int w) { return MFAST_ ? w / WM : w % WN; }
   static __device__ __forceinline__ int wave() { return __builtin_amdgcn_readfirstlane(opaque_tid() >> 6); }
@@ -116,6 +130,24 @@ struct GemmCore {
   static __device__ __forceinline__ int load_row(int j) {
     const int w = wave(), lane = opaque_tid() & 63;
     return (w + NWAVES * j) * RPI + lane / CPR;
+  }
+
+  // K-major operand, load j (P: j < LP, Q: j >= LP): the k row (0..BK-1) this
+  // lane fills, and the element offset, at k = 0, of the 8 values it
+  // fetches: k_row * ld + m_first + 8 * (slot ^ swz_t(k_row)); 0xFFFFFFFF
+  // when those columns are at or past m_valid (not fetched).
+  static __device__ __forceinline__ int kmajor_row(int j) {
+    const int w = wave(), lane = opaque_tid() & 63;
+    const bool isp = j < LP;
+    const int slots = isp ? SLOTS_P : SLOTS_Q;
+    return (w + NWAVES * (isp ? j : j - LP)) * (64 / slots) + lane / slots;
+  }
+  static __device__ __forceinline__ uint32_t kmajor_offset(int j, int ld, int m_first, int m_valid) {
+    const int lane = opaque_tid() & 63;
+    const int slots = j < LP ? SLOTS_P : SLOTS_Q;
+    const int kr = kmajor_row(j);
+    const int m = 8 * ((lane % slots) ^ swz_t(kr));
+    return m < m_valid ? static_cast<uint32_t>(kr) * ld + m_first + m : 0xFFFFFFFFu;
   }
 
   static __device__ __forceinline__ void zero(Acc& acc) {
@@ -145,14 +177,27 @@ struct GemmCore {
                                              static_cast<int>(kRange), 0x00020000);
   }
 
+  // Stage kt: a row-major operand advances by the scalar offset kt*BK*2; a
+  // K-major one by kt*BK rows of ld elements in its per-lane offset, and its
+  // rows at or past kvalid are not fetched (they read as zeros).
   static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t prs, __amdgpu_buffer_rsrc_t qrs,
-                                               const uint32_t (&goff)[LOADS], int k0, lds_ptr st, int w) {
+                                               const uint32_t (&goff)[LOADS], int kt, lds_ptr st, int w,
+                                               int pld = 0, int qld = 0, int kvalid = 0x7fffffff) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       lds_ptr dst = st + (w + NWAVES * j) * 1024;
+      const bool kmaj = j < LP ? PT : QT;
+      uint32_t off = goff[j];
+      int soff = kt * BK * 2;
+      if (kmaj) {
+        const int ld = j < LP ? pld : qld;
+        const bool ok = off != kRange && kt * BK + kmajor_row(j) < kvalid;
+        off = ok ? off + static_cast<uint32_t>(kt * BK) * static_cast<uint32_t>(ld) * 2u : kRange;
+        soff = 0;
+      }
       __builtin_amdgcn_raw_ptr_buffer_load_lds(j < LP ? prs : qrs,
                                                reinterpret_cast<__attribute__((address_space(3))) void*>(dst),
-                                               16, goff[j], k0 * 2, 0, 0);
+                                               16, off, soff, 0, 0);
     }
   }
 
@@ -164,6 +209,12 @@ struct GemmCore {
     const int lane = opaque_tid() & 63;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
+      if (j < LP ? PT : QT) {
+        // K-major: the caller's kmajor_offset already places the 8 values
+        const uint32_t o = j < LP ? poff[j] : qoff[j - LP];
+        goff[j] = o == 0xFFFFFFFFu ? kRange : o * 2u;
+        continue;
+      }
       const int r = load_row(j);
       const uint32_t lc = static_cast<uint32_t>((lane % CPR) ^ swz(r));
       const bool valid = j < LP ? r < pvalid : r - BM < qvalid;
@@ -178,19 +229,55 @@ struct GemmCore {
   };
 
   // K step `step` of the stage at S, first NQ Q blocks.
+  // One fragment of a K-major operand whose stage region starts at R (row
+  // pitch PITCH bytes): lane l (group g = l/16, c = l%16) gets m = m_blk +
+  // 16*(g%2) + c and k = 16*step + 8*(g/2) + 0..7, as the row-major read
+  // does.  In each 16-lane group the transposing read hands lane c the
+  // values (k0 + 0..3, m0 + c) when lane c addresses (k0 + c/4, m0 + 4*(c%4)).
+  template <int PITCH>
+  static __device__ __forceinline__ bf16x8 read_kmajor(lds_ptr R, int m_blk, int step) {
+    typedef short v4i16 __attribute__((ext_vector_type(4)));
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const int lane = opaque_tid() & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int m = m_blk + 16 * (g & 1) + 4 * (c & 3);
+    const int k0 = 16 * step + 8 * (g >> 1) + (c >> 2);
+    v4i16 h[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = k0 + 4 * u;
+      lds_ptr a = R + k * PITCH + 16 * ((m >> 3) ^ swz_t(k)) + 2 * (m & 7);
+      h[u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<__attribute__((address_space(3))) v4i16*>(a));
+    }
+    const v8i16 v = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
+  }
+
   template <int NQ>
   static __device__ __forceinline__ void read_step(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
                                                    Frags& f) {
     if constexpr (NQ > 0) {
       const int pc = ((2 * step + half) ^ sw) * 16;
+      if constexpr (PT) {
+        const int wm = wave_m(wave());
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        f.a[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + prow0 + 32 * i * ROW_BYTES +
-                                                                                      pc);
+        for (int i = 0; i < FM; ++i) f.a[i] = read_kmajor<BM * 2>(S, wm * WTM + 32 * i, step);
+      } else {
 #pragma unroll
-      for (int j = 0; j < NQ; ++j)
-        f.b[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + qrow0 +
-                                                                                      QSTEP * j * ROW_BYTES + pc);
+        for (int i = 0; i < FM; ++i)
+          f.a[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + prow0 +
+                                                                                        32 * i * ROW_BYTES + pc);
+      }
+      if constexpr (QT) {
+        const int wn = wave_n(wave());
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) f.b[j] = read_kmajor<BN * 2>(S + BM * ROW_BYTES, q_row(wn, j), step);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NQ; ++j)
+          f.b[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(S + qrow0 +
+                                                                                        QSTEP * j * ROW_BYTES + pc);
+      }
     }
   }
 
@@ -283,10 +370,13 @@ struct GemmCore {
   // kt+STAGES into it and read step 0 of stage kt+1 while the last step is
   // multiplied.  Holding one step per buffer keeps the FFN tile within 256
   // registers per lane without register reuse stalls.
+  // pld, qld: row pitch (elements) of a K-major P / Q; kvalid: K rows of
+  // K-major operands at or past it read as zeros (rows beyond an expert's).
   template <int NQ = FN>
   static __device__ __forceinline__ void run(const uint16_t* __restrict__ pbase, const uint32_t (&poff)[LP],
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
-                                             int K, int pvalid, int qvalid, uint8_t* lds_generic, Acc& acc) {
+                                             int K, int pvalid, int qvalid, uint8_t* lds_generic, Acc& acc,
+                                             int pld = 0, int qld = 0, int kvalid = 0x7fffffff) {
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int lane = opaque_tid() & 63;
     const int w = wave();
@@ -298,7 +388,7 @@ struct GemmCore {
     const int pro = min(nk, STAGES);
 #pragma unroll
     for (int s = 0; s < STAGES; ++s)
-      if (s < pro) issue(prs, qrs, goff, s * BK, lds + s * STAGE_BYTES, w);
+      if (s < pro) issue(prs, qrs, goff, s, lds + s * STAGE_BYTES, w, pld, qld, kvalid);
     wait_stages(pro - 1);
     raw_barrier();
     const int sw = swz(lane & 31);
@@ -319,7 +409,7 @@ struct GemmCore {
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
       raw_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      issue(prs, qrs, goff, (kt + STAGES) * BK, cur, w);
+      issue(prs, qrs, goff, kt + STAGES, cur, w, pld, qld, kvalid);
       read_step<NQ>(nxt, prow0, qrow0, half, sw, 0, f[0]);
       mma_step<NQ>(f[1], acc);
       interleave_loads<NQ>();
