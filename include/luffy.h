@@ -226,10 +226,10 @@ int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep
  *   luffy_expert_ffn (Z is recomputed, nothing of the forward is kept);
  *   dy_rep [max_rows, d] bf16 (rows 0..R-1 used); dx_rep [max_rows, d] bf16
  *   (rows 0..R-1 written); dw1 [E, d_ff, d] and dw2 [E, d, d_ff] float32.
- * bf16 only (LUFFY_E_UNSUPPORTED for float32).  Intermediates (Z, dY W2,
- * dZ and the transposed operands of the weight gradients) are bf16 in the
+ * bf16 only (LUFFY_E_UNSUPPORTED for float32).  Intermediates (Z, act(Z),
+ * dZ and, with row_index, the gathered rows of x) are bf16 in the
  * workspace: luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff,
- * dtype) bytes, which includes transposed copies of both weight tensors.
+ * dtype) bytes (no copy of the weights).
  * ---------------------------------------------------------------------- */
 size_t luffy_expert_ffn_backward_workspace_size(int max_rows, int E, int d, int d_ff, int dtype);
 int luffy_expert_ffn_backward(const void* x, const int32_t* row_index, const int32_t* rep_offsets,
@@ -266,7 +266,7 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
  * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
  * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
- * bwd_wt, bwd_z, bwd_da, bwd_dx, bwd_dx_reduce, bwd_tr, bwd_dw2,
+ * bwd_z, bwd_act, bwd_da, bwd_dx, bwd_dx_reduce, bwd_gather, bwd_dw2,
  * bwd_dw1.
  * ---------------------------------------------------------------------- */
 int luffy_profile_kernel(const char* name);
