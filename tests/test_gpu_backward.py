@@ -148,14 +148,18 @@ def test_expert_ffn_backward(d, d_ff, act):
 
 
 
-def test_layer_backward_end_to_end():
-    """MoELayer.backward (both backward entry points in a row) on c2
-    reduced, against the oracle's chain on the GPU forward's condensation:
-    dgate within 1e-4 |dy_t| |y_rep_r|, the representatives' dx rows within
-    the bf16 tolerance, and a second call with a different dy."""
+@pytest.mark.parametrize("name", ["c2", "c5"])
+def test_layer_backward_end_to_end(name):
+    """MoELayer.backward (both backward entry points in a row) on c2 and c5
+    reduced (top-2; top-1 over 64 experts with dropped slots and experts
+    without representatives), against the oracle's chain on the GPU
+    forward's condensation: dgate within 1e-4 |dy_t| |y_rep_r|, the
+    representatives' dx rows within the bf16 tolerance, the weight
+    gradients of experts without representatives exactly zero, and a second
+    call with a different dy."""
     import torch
-    print_case("layer_backward", config="c2", **REDUCED["c2"])
-    inp, dev, layer, g = _forward("c2")
+    print_case("layer_backward", config=name, **REDUCED[name])
+    inp, dev, layer, g = _forward(name)
     x = dev["x"]
     T, d = layer.buf.y.shape
     R = int(g["rep_offsets"][-1])
@@ -176,3 +180,6 @@ def test_layer_backward_end_to_end():
         assert np.all(np.abs(got_gate[kept] - ref_gate[kept]) <= 1e-4 * scale), f"call {call}: dgate"
         err, _ = rel_err_rows(dx_rep[:R].double().cpu().numpy(), ref_dx)
         assert err.max() <= TOL["bf16"], f"call {call}: dx_rep max row rel err {err.max():.3g}"
+        empty = np.flatnonzero(np.diff(g["rep_offsets"]) == 0)
+        if empty.size:
+            assert not dw1[torch.from_numpy(empty).cuda()].any() and not dw2[torch.from_numpy(empty).cuda()].any()
