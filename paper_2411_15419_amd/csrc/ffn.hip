@@ -37,7 +37,8 @@ __device__ __forceinline__ float act_fn(float z) {
 //   GELU: erf from Abramowitz & Stegun 7.1.26 (Hastings' rational
 //   approximation), erf(u) = 1 - q(u), q(u) = t (a1 + t (a2 + ... + t a5))
 //   e^{-u^2}, t = 1 / (1 + p u), u >= 0, |error| <= 1.5e-7.  With
-//   u = |z| / sqrt(2): GELU(z) = z (1 - q/2) for z >= 0 and z q/2 for z < 0.
+//   u = |z| / sqrt(2): GELU(z) = z (1 - q/2) for z >= 0 and z q/2 for z < 0,
+//   evaluated as |z| (1 - q) / 2 + z / 2.
 //   SiLU: z / (1 + 2^{-z log2 e}).
 // The hardware exp2 and reciprocal are accurate to about 1 ulp.
 // Activation code of a plain product (no activation), used by the backward.
@@ -48,17 +49,21 @@ __device__ __forceinline__ float act_fast(float z) {
   if constexpr (ACT == kActNone) {
     return z;
   } else if constexpr (ACT == LUFFY_ACT_GELU) {
-    constexpr float kP = 0.3275911f;
-    constexpr float kA1 = 0.254829592f, kA2 = -0.284496736f, kA3 = 1.421413741f;
-    constexpr float kA4 = -1.453152027f, kA5 = 1.061405429f;
-    constexpr float kInvSqrt2 = 0.70710678118654752f;
+    // Hastings' erf(u) = 1 - t (a1 + a2 t + ... + a5 t^4) e^{-u^2},
+    // t = 1 / (1 + p u), u = |z| / sqrt(2), with the a_i halved here so
+    // that w = 1/2 - t e P(t) = erf(u) / 2.  Then z Phi(z) = |z| w + z / 2
+    // for either sign of z (Phi(z) = 1/2 + sign(z) erf(u) / 2): 10 vector
+    // operations and two transcendentals per element.
+    constexpr float kPs = 0.3275911f * 0.70710678118654752f;   // p / sqrt(2)
+    constexpr float kB1 = 0.5f * 0.254829592f, kB2 = 0.5f * -0.284496736f, kB3 = 0.5f * 1.421413741f;
+    constexpr float kB4 = 0.5f * -1.453152027f, kB5 = 0.5f * 1.061405429f;
     constexpr float kHalfLog2e = -0.72134752044448170f;   // -log2(e) / 2
-    const float u = fabsf(z) * kInvSqrt2;
-    const float t = __builtin_amdgcn_rcpf(fmaf(kP, u, 1.0f));
-    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, kA5, kA4), kA3), kA2), kA1);
+    const float a = fabsf(z);
+    const float t = __builtin_amdgcn_rcpf(fmaf(kPs, a, 1.0f));
+    const float pt = fmaf(t, fmaf(t, fmaf(t, fmaf(t, kB5, kB4), kB3), kB2), kB1);
     const float e = __builtin_amdgcn_exp2f(z * z * kHalfLog2e);   // e^{-u^2}
-    const float hq = 0.5f * poly * e;
-    return z * (z >= 0.f ? 1.0f - hq : hq);
+    const float w = fmaf(-(t * e), pt, 0.5f);
+    return fmaf(a, w, 0.5f * z);
   } else {
     constexpr float kNegLog2e = -1.44269504088896341f;
     return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z * kNegLog2e));
@@ -199,8 +204,13 @@ struct FfnTiles {
   }
   // Split-K parts per tile (second product only): the largest split of at
   // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
-  // the partial-tile slots and fewer work items than blocks.  Always 1, 2
-  // or 4 (the reduction is instantiated for 2 and 4).
+  // the partial-tile slots, doubling while the current split still has
+  // fewer work items than blocks.  The last doubling may leave more items
+  // than blocks, so that parts run in two rounds: with 140 tiles of K =
+  // 4096, two rounds of half-K parts (the first on every CU) measured
+  // faster than one round of whole tiles on 140 CUs, because the per-CU
+  // operand stream, not HBM, bounds such a product.  Always 1, 2 or 4 (the
+  // reduction is instantiated for 2 and 4).
   __device__ __forceinline__ int parts(int grid, int nk) const {
     if (tiles <= 0) return 1;
     int s = 1;

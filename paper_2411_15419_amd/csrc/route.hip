@@ -345,10 +345,20 @@ __global__ __launch_bounds__(256) void gate_kernel(
   }
   // partial tiles summed in wave order into part[0], one (token, expert)
   // pair per thread at a time
+  // (token tl, expert e) = divmod(i, E), advanced by divmod(256, E) per
+  // step rather than divided out each time
   float (*logit)[kMaxExperts + 1] = part[0];
-  for (int i = threadIdx.x; i < TOK * E; i += 256) {
-    const int tl = i / E, e = i - tl * E;
-    logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
+  {
+    const int dq = 256 / E, dr = 256 - dq * E;
+    int tl = static_cast<int>(threadIdx.x) / E, e = static_cast<int>(threadIdx.x) - tl * E;
+    for (; tl < TOK; tl += dq, e += dr) {
+      if (e >= E) {
+        e -= E;
+        ++tl;
+        if (tl >= TOK) break;
+      }
+      logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
+    }
   }
   __syncthreads();
   gate_select<BF16, TOK>(logit, bias, cnt, choice, xv, wv, T, d, E, k, t0, ch, nchunks, topk_idx, topk_gate,
