@@ -75,9 +75,7 @@ def kernel_work(name, cfg, counts):
     if name == "bwd_dx":
         return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * dff * b + R * d * b))
     if name in ("bwd_dw1", "bwd_dw2"):
-        return dict(flops=2.0 * R * d * dff, bytes=float(E * d * dff * 4 + R * (d + dff) * b))
-    if name == "bwd_tr":       # four launches (R x d, R x d_ff, R x d_ff, R x d): their mean
-        return dict(flops=0.0, bytes=float(R * (d + dff) * b))
+        return dict(flops=2.0 * R * d * dff, bytes=float(E * d * dff * counts.get("dw_bytes", 4) + R * (d + dff) * b))
     if name == "cbwd_rows":
         return dict(flops=2.0 * S * d, bytes=float(S * d * b + R * d * b + 12 * S))
     if name == "cbwd_gate":
@@ -185,8 +183,9 @@ def bench_backward(args, cfg, layer, x, L, torch, np):
     dy_rep = torch.empty_like(b.y_rep)
     dgate = torch.empty(T, k, dtype=torch.float32, device="cuda")
     dx_rep = torch.empty(S, d, dtype=b.y.dtype, device="cuda")
-    dw1 = torch.empty(E, dff, d, dtype=torch.float32, device="cuda")
-    dw2 = torch.empty(E, d, dff, dtype=torch.float32, device="cuda")
+    wdt = torch.bfloat16 if args.dw_dtype == "bf16" else torch.float32
+    dw1 = torch.empty(E, dff, d, dtype=wdt, device="cuda")
+    dw2 = torch.empty(E, d, dff, dtype=wdt, device="cuda")
     ws_c = torch.empty(L.combine_backward_workspace_size(T, k, S), dtype=torch.uint8, device="cuda")
     ws_f = torch.empty(L.expert_ffn_backward_workspace_size(S, E, d, dff, L.LUFFY_BF16), dtype=torch.uint8,
                        device="cuda")
@@ -227,7 +226,7 @@ def bench_backward(args, cfg, layer, x, L, torch, np):
     off = b.offsets.cpu().numpy()
     ro = b.rep_offsets.cpu().numpy()
     counts = dict(S=int(off[-1]), R=int(ro[-1]), bucket_sizes=np.diff(off).tolist(),
-                  used_experts=int((np.diff(ro) > 0).sum()))
+                  used_experts=int((np.diff(ro) > 0).sum()), dw_bytes=2 if args.dw_dtype == "bf16" else 4)
     rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
     rl.update(traffic=None, algorithmic_bytes=kernel_work(dominant, cfg, counts)["bytes"], kernel=dominant,
               us_per_launch=dom_ms / dom_n * 1e3)
@@ -253,7 +252,7 @@ def bench_backward(args, cfg, layer, x, L, torch, np):
         "data": "synthetic (seeded clustered tokens, random-init weights, normal dL/dy)",
         "config": {"workload": WORKLOAD_NAMES[args.config] + ", backward (combine + expert FFN)",
                    "name": args.config, "T": cfg.T, "d_model": cfg.d, "E": cfg.E, "top_k": cfg.k,
-                   "d_ff": cfg.d_ff, "act": cfg.act},
+                   "d_ff": cfg.d_ff, "act": cfg.act, "dw_dtype": args.dw_dtype},
         "condensation": {"slots_kept": counts["S"], "representatives": counts["R"]},
         "roofline": rl,
         "kernels": kernels,
@@ -274,6 +273,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the layer (combine and expert FFN) instead of the forward")
+    ap.add_argument("--dw-dtype", default="f32", choices=("f32", "bf16"),
+                    help="type of the backward's weight gradients: f32, or bf16 (the weights' own type, as "
+                         "a bf16 parameter's gradient)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUFFY_ABI_VERSION 3
+#define LUFFY_ABI_VERSION 4
 
 typedef enum {
   LUFFY_OK = 0,
@@ -225,7 +225,9 @@ int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep
  *   x, row_index, rep_offsets, w1, w2, act, max_rows: as for
  *   luffy_expert_ffn (Z is recomputed, nothing of the forward is kept);
  *   dy_rep [max_rows, d] bf16 (rows 0..R-1 used); dx_rep [max_rows, d] bf16
- *   (rows 0..R-1 written); dw1 [E, d_ff, d] and dw2 [E, d, d_ff] float32.
+ *   (rows 0..R-1 written); dw1 [E, d_ff, d] and dw2 [E, d, d_ff] of type
+ *   dw_dtype: LUFFY_F32, or LUFFY_BF16 (the weights' own type, as a bf16
+ *   parameter's gradient; the float32 sums rounded once, half the bytes).
  * bf16 only (LUFFY_E_UNSUPPORTED for float32).  Intermediates (Z, act(Z),
  * dZ and, with row_index, the gathered rows of x) are bf16 in the
  * workspace: luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff,
@@ -235,8 +237,8 @@ size_t luffy_expert_ffn_backward_workspace_size(int max_rows, int E, int d, int 
 int luffy_expert_ffn_backward(const void* x, const int32_t* row_index, const int32_t* rep_offsets,
                               int E, int d, int d_ff, int dtype, const void* w1, const void* w2,
                               int act, int max_rows, const void* dy_rep, void* dx_rep,
-                              float* dw1, float* dw2, void* workspace, size_t workspace_bytes,
-                              void* stream);
+                              void* dw1, void* dw2, int dw_dtype, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * luffy_adaptive_threshold - the condensation threshold h_t of training

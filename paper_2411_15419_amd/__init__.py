@@ -53,7 +53,7 @@ _SIGS = {
                                         _c_int, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_expert_ffn_backward_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_expert_ffn_backward": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int,
-                                           _c_int, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+                                           _c_int, _vp, _vp, _vp, _vp, _c_int, _vp, _c_size, _vp]),
     "luffy_adaptive_threshold": (_c_int, [ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_double)]),
     "luffy_profile_kernel": (_c_int, [ctypes.c_char_p]),
     "luffy_profile_read": (_c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_c_int)]),
@@ -202,12 +202,15 @@ def expert_ffn_backward_workspace_size(max_rows: int, E: int, d: int, d_ff: int,
 def luffy_expert_ffn_backward(x, row_index, rep_offsets, w1, w2, act, max_rows, dy_rep, dx_rep, dw1, dw2,
                               workspace, stream=None):
     """Gradients of luffy_expert_ffn: dx_rep [max_rows, d] (bf16), dw1
-    [E, d_ff, d] and dw2 [E, d, d_ff] (float32) from dy_rep."""
+    [E, d_ff, d] and dw2 [E, d, d_ff] (float32 or bf16, both the same) from
+    dy_rep."""
     E, d_ff, d = w1.shape
+    if dw1.dtype != dw2.dtype:
+        raise LuffyError("luffy_expert_ffn_backward: dw1 and dw2 must have the same dtype")
     _check(load_library().luffy_expert_ffn_backward(
         _p(x), _p(row_index), _p(rep_offsets), E, d, d_ff, _dtype_code(x), _p(w1), _p(w2), _ACTS[act],
-        max_rows, _p(dy_rep), _p(dx_rep), _p(dw1), _p(dw2), _p(workspace), workspace.numel(), _stream(stream)),
-        "luffy_expert_ffn_backward")
+        max_rows, _p(dy_rep), _p(dx_rep), _p(dw1), _p(dw2), _dtype_code(dw1), _p(workspace), workspace.numel(),
+        _stream(stream)), "luffy_expert_ffn_backward")
 
 
 def adaptive_threshold(l_ini: float, l_prev: float) -> float:
@@ -355,25 +358,26 @@ class MoELayer:
         b = self.buf
         luffy_combine(b.y_rep, b.rep_row, b.slot_pos, b.topk_gate, b.y, stream)
 
-    def backward(self, x, dy, stream=None):
+    def backward(self, x, dy, stream=None, dw_dtype=torch.float32):
         """Gradients of the last call's output for dy = dL/dy [T, d], with its
         condensation held fixed (bf16 layers): returns (dgate [T, k] float32,
         dx_rep [T*k, d] with rows 0..R-1 the representatives' input
-        gradients, in the order of rep_token, dw1, dw2 float32).  Buffers
-        are allocated on the first call and reused."""
+        gradients, in the order of rep_token, dw1, dw2 of dw_dtype: float32,
+        or bfloat16 as the gradient of a bf16 parameter).  Buffers are
+        allocated on the first call and reused."""
         b = self.buf
         if self.dtype != torch.bfloat16:
             raise LuffyError("MoELayer.backward: the expert FFN backward is bf16 only")
         S = self.T * self.k
         dev = dy.device
-        if getattr(self, "_bwd", None) is None:
+        if getattr(self, "_bwd", None) is None or self._bwd["dw1"].dtype != dw_dtype:
             E, dff, d = self.w1.shape
             self._bwd = dict(
                 dy_rep=torch.empty_like(b.y_rep),
                 dgate=torch.empty(self.T, self.k, dtype=torch.float32, device=dev),
                 dx_rep=torch.empty(S, d, dtype=self.dtype, device=dev),
-                dw1=torch.empty(E, dff, d, dtype=torch.float32, device=dev),
-                dw2=torch.empty(E, d, dff, dtype=torch.float32, device=dev),
+                dw1=torch.empty(E, dff, d, dtype=dw_dtype, device=dev),
+                dw2=torch.empty(E, d, dff, dtype=dw_dtype, device=dev),
                 ws_c=_workspace(combine_backward_workspace_size(self.T, self.k, S), dev),
                 ws_f=_workspace(expert_ffn_backward_workspace_size(S, E, d, dff, LUFFY_BF16), dev),
             )

@@ -614,10 +614,15 @@ __device__ __forceinline__ void expert_rows(const int32_t* __restrict__ rep_offs
 // expert without rows gets zeros.
 using WgradGemm = GemmCore<256, 256, 2, 4, false, false, 64, 2, true, true>;
 
+// OUT_BF16: the sums are rounded to bf16 (the weights' own type), stored
+// four bytes at a time: lanes l and l^1 hold neighbouring columns of the
+// same rows and swap one value, so that the even lane stores its row v and
+// the odd lane row v+1, two columns each.
+template <bool OUT_BF16>
 __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_t* __restrict__ P,
                                                                    const uint16_t* __restrict__ Q,
                                                                    const int32_t* __restrict__ rep_offsets, int E,
-                                                                   int M, int N, float* __restrict__ out) {
+                                                                   int M, int N, void* __restrict__ out) {
   using G = WgradGemm;
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
   const int mt = (M + G::BM - 1) / G::BM, nt = (N + G::BN - 1) / G::BN;
@@ -642,19 +647,44 @@ __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_
     }
     const int tid = opaque_tid(), lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = G::wave_m(w), wn = G::wave_n(w);
-    float* oe = out + static_cast<size_t>(e) * M * N;
+    if constexpr (OUT_BF16) {
+      uint16_t* oe = static_cast<uint16_t*>(out) + static_cast<size_t>(e) * M * N;
+      const bool odd = lane & 1;
 #pragma unroll
-    for (int fm = 0; fm < G::FM; ++fm)
+      for (int fm = 0; fm < G::FM; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < G::FN; ++fn) {
-        const int j = n0 + G::q_row(wn, fn) + (lane & 31);
-        if (j >= N) continue;
+        for (int fn = 0; fn < G::FN; ++fn) {
+          // first column of the lane pair; N is a multiple of 64, so both
+          // columns are in range or neither is (same for both lanes)
+          const int jp = (n0 + G::q_row(wn, fn) + (lane & 31)) & ~1;
+          if (jp >= N) continue;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int i = m0 + wm * G::WTM + 32 * fm + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
-          if (i < M) oe[static_cast<size_t>(i) * N + j] = acc[fm][fn][v];
+          for (int v = 0; v < 16; v += 2) {
+            // the even lane needs the odd lane's row-v value, the odd lane
+            // the even lane's row-(v+1) value
+            const float recv = __shfl_xor(odd ? acc[fm][fn][v] : acc[fm][fn][v + 1], 1, 64);
+            const float lo = odd ? recv : acc[fm][fn][v];
+            const float hi = odd ? acc[fm][fn][v + 1] : recv;
+            const int i = m0 + wm * G::WTM + 32 * fm + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4) + (odd ? 1 : 0);
+            if (i < M)
+              *reinterpret_cast<uint32_t*>(oe + static_cast<size_t>(i) * N + jp) = pack_bf16x2(lo, hi);
+          }
         }
-      }
+    } else {
+      float* oe = static_cast<float*>(out) + static_cast<size_t>(e) * M * N;
+#pragma unroll
+      for (int fm = 0; fm < G::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < G::FN; ++fn) {
+          const int j = n0 + G::q_row(wn, fn) + (lane & 31);
+          if (j >= N) continue;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int i = m0 + wm * G::WTM + 32 * fm + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+            if (i < M) oe[static_cast<size_t>(i) * N + j] = acc[fm][fn][v];
+          }
+        }
+    }
   }
 }
 
@@ -677,7 +707,7 @@ FfnBwdWs carve_ffn_bwd(Carver& c, int max_rows, int E, int d, int d_ff) {
 template <int ACT>
 void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* rep_offsets, int E, int d, int d_ff,
                     const uint16_t* w1, const uint16_t* w2, int max_rows, const uint16_t* dy, uint16_t* dx,
-                    float* dw1, float* dw2, const FfnBwdWs& ws, hipStream_t s) {
+                    void* dw1, void* dw2, bool dw_bf16, const FfnBwdWs& ws, hipStream_t s) {
   (void)max_rows;
   const int grid = persistent_grid();
   const int egrid = 4 * grid;
@@ -697,15 +727,16 @@ void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* 
   launch("bwd_dx_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots, dx,
          grid);
   // dW2 = dY^T A, dW1 = dZ^T X (X's rows gathered first)
-  launch("bwd_dw2", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, dy, static_cast<const uint16_t*>(ws.a),
-         rep_offsets, E, d, d_ff, dw2);
+  auto* wgrad = dw_bf16 ? wgrad_kernel<true> : wgrad_kernel<false>;
+  launch("bwd_dw2", wgrad, grid, WgradGemm::THREADS, 0, s, dy, static_cast<const uint16_t*>(ws.a), rep_offsets, E, d,
+         d_ff, dw2);
   const uint16_t* xr = x;
   if (row_index) {
     launch("bwd_gather", gather_rows_kernel, egrid, 256, 0, s, rep_offsets, E, d, x, row_index, ws.xg);
     xr = ws.xg;
   }
-  launch("bwd_dw1", wgrad_kernel, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.dz), xr,
-         rep_offsets, E, d_ff, d, dw1);
+  launch("bwd_dw1", wgrad, grid, WgradGemm::THREADS, 0, s, static_cast<const uint16_t*>(ws.dz), xr, rep_offsets, E,
+         d_ff, d, dw1);
 }
 
 }  // namespace
@@ -764,8 +795,8 @@ extern "C" size_t luffy_expert_ffn_backward_workspace_size(int max_rows, int E, 
 
 extern "C" int luffy_expert_ffn_backward(const void* x, const int32_t* row_index, const int32_t* rep_offsets, int E,
                                          int d, int d_ff, int dtype, const void* w1, const void* w2, int act,
-                                         int max_rows, const void* dy_rep, void* dx_rep, float* dw1, float* dw2,
-                                         void* workspace, size_t workspace_bytes, void* stream) {
+                                         int max_rows, const void* dy_rep, void* dx_rep, void* dw1, void* dw2,
+                                         int dw_dtype, void* workspace, size_t workspace_bytes, void* stream) {
   if (!x || !rep_offsets || !w1 || !w2 || !dy_rep || !dx_rep || !dw1 || !dw2)
     return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: null pointer argument");
   if (E <= 0 || d <= 0 || d_ff <= 0 || max_rows <= 0)
@@ -774,6 +805,8 @@ extern "C" int luffy_expert_ffn_backward(const void* x, const int32_t* row_index
     return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: unknown dtype %d", dtype);
   if (act != LUFFY_ACT_GELU && act != LUFFY_ACT_SILU)
     return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: unknown activation %d", act);
+  if (dw_dtype != LUFFY_F32 && dw_dtype != LUFFY_BF16)
+    return fail(LUFFY_E_INVALID, "luffy_expert_ffn_backward: unknown weight-gradient dtype %d", dw_dtype);
   if (dtype != LUFFY_BF16) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: bf16 only");
   if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_expert_ffn_backward: E=%d > %d", E, kMaxExperts);
   if (d % 64 != 0 || d_ff % 64 != 0)
@@ -798,9 +831,11 @@ extern "C" int luffy_expert_ffn_backward(const void* x, const int32_t* row_index
   const auto* dyb = static_cast<const uint16_t*>(dy_rep);
   auto* dxb = static_cast<uint16_t*>(dx_rep);
   if (act == LUFFY_ACT_GELU)
-    launch_ffn_bwd<LUFFY_ACT_GELU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2, ws, s);
+    launch_ffn_bwd<LUFFY_ACT_GELU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2,
+                                   dw_dtype == LUFFY_BF16, ws, s);
   else
-    launch_ffn_bwd<LUFFY_ACT_SILU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2, ws, s);
+    launch_ffn_bwd<LUFFY_ACT_SILU>(xb, row_index, rep_offsets, E, d, d_ff, w1b, w2b, max_rows, dyb, dxb, dw1, dw2,
+                                   dw_dtype == LUFFY_BF16, ws, s);
   return check_launch("luffy_expert_ffn_backward");
 }
 

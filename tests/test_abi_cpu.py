@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.luffy_abi_version() == 3
+    assert lib.luffy_abi_version() == 4
     assert lib.luffy_status_string(0) == b"ok"
     assert lib.luffy_status_string(-3).startswith(b"workspace")
 
@@ -96,13 +96,17 @@ def test_invalid_arguments_rejected_on_host(lib):
                                       fake, fake, fake, 1 << 20, None) == -2
     assert lib.luffy_combine_backward(fake, fake, fake, fake, fake, fake, fake, fake, 4, 8, 2, 64, 1, 16,
                                       fake, fake, fake, 16, None) == -3
-    # expert FFN backward: bf16 only, unknown activation, workspace too small
+    # expert FFN backward: bf16 only, unknown activation, unknown weight-
+    # gradient dtype, workspace too small (with either gradient dtype)
     assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 0, fake, fake, 0, 8, fake, fake,
-                                         fake, fake, fake, 1 << 30, None) == -2
+                                         fake, fake, 0, fake, 1 << 30, None) == -2
     assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 1, fake, fake, 9, 8, fake, fake,
-                                         fake, fake, fake, 1 << 30, None) == -1
+                                         fake, fake, 0, fake, 1 << 30, None) == -1
     assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 1, fake, fake, 0, 8, fake, fake,
-                                         fake, fake, fake, 256, None) == -3
+                                         fake, fake, 2, fake, 1 << 30, None) == -1
+    for dw in (0, 1):
+        assert lib.luffy_expert_ffn_backward(fake, None, fake, 4, 64, 128, 1, fake, fake, 0, 8, fake, fake,
+                                             fake, fake, dw, fake, 256, None) == -3
     assert lib.luffy_expert_ffn_backward_workspace_size(8, 4, 64, 128, 0) == 0   # float32: none
 
 

@@ -83,18 +83,22 @@ def test_combine_backward(name):
         assert np.all(gerr <= 1e-4 * scale + 1e-30), f"call {rep}: dgate max err / scale {(gerr / scale).max():.3g}"
 
 
-@pytest.mark.parametrize("d,d_ff,act", [(256, 512, "gelu"), (256, 1024, "silu"), (128, 192, "gelu")])
-def test_expert_ffn_backward(d, d_ff, act):
+@pytest.mark.parametrize("d,d_ff,act,dw", [(256, 512, "gelu", "f32"), (256, 1024, "silu", "f32"),
+                                            (128, 192, "gelu", "f32"), (256, 512, "gelu", "bf16"),
+                                            (192, 320, "silu", "bf16")])
+def test_expert_ffn_backward(d, d_ff, act, dw):
     """luffy_expert_ffn_backward on the expert sizes of the forward tile
     test (empty, 1 row, 255-257, 300, 320, 321, 600, 700: every tile shape,
     split second products, Kp padding of the weight gradients), rows
     gathered through a permuted index, against the oracle's fp64 gradients
     on the same bf16 inputs: dx_rep per row within the bf16 tolerance, each
-    row of dW1 and dW2 within it too, and exact zeros for the empty expert."""
+    entry of dW1 and dW2 (float32, or rounded to bf16: one more relative
+    2^-9, well inside the bound) within it too, and exact zeros for the
+    empty expert."""
     import torch
     import paper_2411_15419_amd as L
     sizes = [0, 1, 255, 256, 257, 300, 320, 321, 600, 700]
-    print_case("expert_ffn_backward", d=d, d_ff=d_ff, act=act, sizes=sizes)
+    print_case("expert_ffn_backward", d=d, d_ff=d_ff, act=act, dw=dw, sizes=sizes)
     E = len(sizes)
     R = sum(sizes)
     rng = np.random.default_rng(23)
@@ -107,13 +111,25 @@ def test_expert_ffn_backward(d, d_ff, act):
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).astype(np.float32)).to(torch.bfloat16).cuda()
     i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(torch.int32).cuda()
     dx = torch.full((R, d), float("nan"), dtype=torch.bfloat16, device="cuda")
-    dw1 = torch.full((E, d_ff, d), float("nan"), dtype=torch.float32, device="cuda")
-    dw2 = torch.full((E, d, d_ff), float("nan"), dtype=torch.float32, device="cuda")
+    wdt = torch.float32 if dw == "f32" else torch.bfloat16
+    dw1 = torch.full((E, d_ff, d), float("nan"), dtype=wdt, device="cuda")
+    dw2 = torch.full((E, d, d_ff), float("nan"), dtype=wdt, device="cuda")
     ws = torch.empty(L.expert_ffn_backward_workspace_size(R, E, d, d_ff, L.LUFFY_BF16), dtype=torch.uint8,
                      device="cuda")
     L.luffy_expert_ffn_backward(bf(x_all), i32(row_index), i32(offsets), bf(w1), bf(w2), act, R, bf(dy), dx, dw1,
                                 dw2, ws)
     torch.cuda.synchronize()
+    if dw == "bf16":
+        # same call with float32 gradients: the bf16 ones are those rounded
+        # to nearest even, bit for bit (same sums in the same order)
+        f1 = torch.empty((E, d_ff, d), dtype=torch.float32, device="cuda")
+        f2 = torch.empty((E, d, d_ff), dtype=torch.float32, device="cuda")
+        dx32 = torch.empty_like(dx)
+        L.luffy_expert_ffn_backward(bf(x_all), i32(row_index), i32(offsets), bf(w1), bf(w2), act, R, bf(dy), dx32,
+                                    f1, f2, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(dw1, f1.to(torch.bfloat16)) and torch.equal(dw2, f2.to(torch.bfloat16))
+        assert torch.equal(dx, dx32)
     rdx, rdw1, rdw2 = O.expert_ffn_backward(x_all[row_index], offsets, w1, w2, act, dy)
     tol = TOL["bf16"]
     err, _ = rel_err_rows(dx.double().cpu().numpy(), rdx)
@@ -148,8 +164,8 @@ def test_expert_ffn_backward(d, d_ff, act):
 
 
 
-@pytest.mark.parametrize("name", ["c2", "c5"])
-def test_layer_backward_end_to_end(name):
+@pytest.mark.parametrize("name,dw", [("c2", "f32"), ("c5", "f32"), ("c2", "bf16")])
+def test_layer_backward_end_to_end(name, dw):
     """MoELayer.backward (both backward entry points in a row) on c2 and c5
     reduced (top-2; top-1 over 64 experts with dropped slots and experts
     without representatives), against the oracle's chain on the GPU
@@ -158,7 +174,7 @@ def test_layer_backward_end_to_end(name):
     gradients of experts without representatives exactly zero, and a second
     call with a different dy."""
     import torch
-    print_case("layer_backward", config=name, **REDUCED[name])
+    print_case("layer_backward", config=name, dw=dw, **REDUCED[name])
     inp, dev, layer, g = _forward(name)
     x = dev["x"]
     T, d = layer.buf.y.shape
@@ -168,7 +184,7 @@ def test_layer_backward_end_to_end(name):
     for call in range(2):
         dy_np = _bf16_exact(rng.standard_normal((T, d)))
         dy = torch.from_numpy(dy_np.astype(np.float32)).to(torch.bfloat16).cuda()
-        dgate, dx_rep, dw1, dw2 = layer.backward(x, dy)
+        dgate, dx_rep, dw1, dw2 = layer.backward(x, dy, dw_dtype=torch.float32 if dw == "f32" else torch.bfloat16)
         torch.cuda.synchronize()
         ref_rep, ref_gate = O.combine_backward(dy_np, g["y_rep"].astype(np.float64), g["rep_row"],
                                                g["slot_pos"], g["topk_gate"].astype(np.float64))
@@ -183,3 +199,17 @@ def test_layer_backward_end_to_end(name):
         empty = np.flatnonzero(np.diff(g["rep_offsets"]) == 0)
         if empty.size:
             assert not dw1[torch.from_numpy(empty).cuda()].any() and not dw2[torch.from_numpy(empty).cuda()].any()
+        if dw == "bf16":
+            # the FFN backward again on the same dy_rep (the layer's own
+            # buffer: a second combine backward may differ in its last bits)
+            # with float32 gradients: the bf16 ones are those rounded to
+            # nearest even, bit for bit
+            import paper_2411_15419_amd as L
+            b, bw = layer.buf, layer._bwd
+            src, idx = (b.x_rep, None) if b.x_rep is not None else (x, b.rep_token)
+            f1 = torch.empty(dw1.shape, dtype=torch.float32, device="cuda")
+            f2 = torch.empty(dw2.shape, dtype=torch.float32, device="cuda")
+            L.luffy_expert_ffn_backward(src, idx, b.rep_offsets, layer.w1, layer.w2, layer.act, layer.T * layer.k,
+                                        bw["dy_rep"], torch.empty_like(dx_rep), f1, f2, bw["ws_f"])
+            torch.cuda.synchronize()
+            assert torch.equal(dw1, f1.to(torch.bfloat16)) and torch.equal(dw2, f2.to(torch.bfloat16))
