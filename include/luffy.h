@@ -227,7 +227,8 @@ int luffy_combine_backward(const void* dy, const void* y_rep, const int32_t* rep
  *   dy_rep [max_rows, d] bf16 (rows 0..R-1 used); dx_rep [max_rows, d] bf16
  *   (rows 0..R-1 written); dw1 [E, d_ff, d] and dw2 [E, d, d_ff] of type
  *   dw_dtype: LUFFY_F32, or LUFFY_BF16 (the weights' own type, as a bf16
- *   parameter's gradient; the float32 sums rounded once, half the bytes).
+ *   parameter's gradient; the float32 sums rounded once, half the bytes);
+ *   another dw_dtype is LUFFY_E_INVALID.
  * bf16 only (LUFFY_E_UNSUPPORTED for float32).  Intermediates (Z, act(Z),
  * dZ and, with row_index, the gathered rows of x) are bf16 in the
  * workspace: luffy_expert_ffn_backward_workspace_size(max_rows, E, d, d_ff,
