@@ -16,6 +16,10 @@ per step, in the paper's order:
             similar -> similarity only inside a bucket) and step 3 (true
             cosine for the remaining pairs); Sec. 5.2: edges whose weight is
             below the threshold are deleted.
+  historical_weights, historical_record
+            Sec. 5.1 step 2 (a NEXT piece with no GPU path): pairs whose
+            previous-block similarity is above S1 / below S2 take weight
+            1 / 0 without a cosine; condense(history=...) uses them.
   greedy    Sec. 5.2: in the thresholded graph keep the highest-degree token,
             condense its neighbours, repeat until every token is decided.
   ffn       Sec. 2.1: an expert is an FFN; Sec. 3: only the kept token of a
@@ -205,8 +209,51 @@ def greedy(adj, degree_mode="static"):
     return rep, deg
 
 
-def condense(x, perm_token, offsets, h, sim_mode="raw", degree_mode="static"):
+def historical_weights(x, tokens, prev_sim, S1, S2, sim_mode="raw"):
+    """Edge weights of one bucket under the fast similarity measurement of
+    Sec. 5.1 (NEXT piece; no GPU path).  Step 1 is the bucketing itself
+    (tokens of different experts get weight 0, so only a bucket's pairs
+    exist); step 2: a pair whose similarity in the previous block exceeds S1
+    gets weight 1, one below S2 gets weight 0, neither computed; step 3: the
+    remaining pairs (no previous value, NaN, or one in [S2, S1]) get their
+    cosine.  prev_sim is a [T, T] record indexed by token id.
+
+    Returns (weights [n, n], computed bool [n, n]); the diagonal is not a
+    pair (computed False)."""
+    tokens = np.asarray(tokens, np.int64)
+    prev = np.asarray(prev_sim, np.float64)[np.ix_(tokens, tokens)]
+    with np.errstate(invalid="ignore"):
+        one, zero = prev > S1, prev < S2
+    computed = ~(one | zero)
+    np.fill_diagonal(computed, False)
+    w = np.where(one, 1.0, np.where(zero, 0.0, cosine(np.asarray(x, np.float64)[tokens], sim_mode)))
+    return w, computed
+
+
+def historical_record(x, perm_token, offsets, prev_sim, S1, S2, sim_mode="raw"):
+    """The similarity record this block leaves for the next one: the weight
+    of every pair that shares a bucket (decided or computed), NaN for every
+    other pair and the diagonal; and the number of distinct pairs (a < b)
+    whose cosine was computed, the cost Sec. 7 reports against S1 and S2.
+    Reading: a pair decided by history passes on its weight (1 or 0)."""
+    T = np.asarray(prev_sim).shape[0]
+    rec = np.full((T, T), np.nan)
+    done = np.zeros((T, T), bool)
+    for e in range(len(offsets) - 1):
+        tok = np.asarray(perm_token[offsets[e]:offsets[e + 1]], np.int64)
+        if tok.size == 0:
+            continue
+        w, comp = historical_weights(x, tok, prev_sim, S1, S2, sim_mode)
+        rec[np.ix_(tok, tok)] = w
+        done[np.ix_(tok, tok)] |= comp
+    np.fill_diagonal(rec, np.nan)
+    return rec, int(np.triu(done, 1).sum())
+
+
+def condense(x, perm_token, offsets, h, sim_mode="raw", degree_mode="static", history=None):
     """Per-bucket similarity + greedy, then compaction of the kept tokens.
+    history = (prev_sim, S1, S2) takes the edge weights of
+    historical_weights (Sec. 5.1 step 2) instead of the cosine of every pair.
 
     Returns a namespace with
       rep_of_pos  int32 [S]  bucket position of the representative of each
@@ -228,7 +275,12 @@ def condense(x, perm_token, offsets, h, sim_mode="raw", degree_mode="static"):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         if hi == lo:
             continue
-        adj = adjacency(x[perm_token[lo:hi]], h, sim_mode)
+        if history is None:
+            adj = adjacency(x[perm_token[lo:hi]], h, sim_mode)
+        else:                          # (prev_sim, S1, S2): Sec. 5.1 step 2
+            w, _ = historical_weights(x, perm_token[lo:hi], *history, sim_mode=sim_mode)
+            adj = w >= h
+            np.fill_diagonal(adj, False)
         rep, deg = greedy(adj, degree_mode)
         rep_of_pos[lo:hi] = rep + lo
         degree[lo:hi] = deg
