@@ -5,7 +5,7 @@ over one batch of synthetic tokens already resident in HBM.  Prints one JSON
 line with tokens/s, the roofline of the dominant kernel (timed live with HIP
 events on the stream it runs on) and the CPU oracle timed on the host cores.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config c2]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config c3] [--extras c2,c4,c5]
     python bench.py --copy-calibration      # plain 1 GiB device copies, for
                                             # scaling the HBM byte counters
 
@@ -45,56 +45,76 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_work(name, cfg, counts):
-    """Algorithmic flops and HBM bytes of one launch of a kernel."""
+def kernel_work(name, cfg, counts, norms_from_route=True):
+    """Work of one launch of a kernel: flops, the algorithmic HBM bytes of the
+    measurement plan ("bytes": the FFN counts only its weights, d*d_ff*b per
+    used expert and product; combine 8 bytes of indices per slot), and the
+    bytes with the activation rows the kernel also moves ("bytes_act")."""
     b = 2 if cfg.dtype == "bf16" else 4
     T, d, E, k, dff = cfg.T, cfg.d, cfg.E, cfg.k, cfg.d_ff
     S, R = counts["S"], counts["R"]
     used = counts["used_experts"]
+
+    def w(flops, nbytes, nbytes_act=None):
+        return dict(flops=float(flops), bytes=float(nbytes),
+                    bytes_act=float(nbytes if nbytes_act is None else nbytes_act))
+
     if name == "gram":
         n = counts["bucket_sizes"]
-        return dict(flops=2.0 * d * sum(x * (x + 1) / 2 for x in n),
-                    bytes=float(S * d * b))
-    if name == "ffn1":
-        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * d * b + R * dff * b))
-    if name == "ffn2":
-        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * dff * b + R * d * b))
+        return w(2.0 * d * sum(x * (x + 1) / 2 for x in n), S * d * b)
+    if name in ("ffn1", "ffn2"):
+        wb = used * d * dff * b
+        return w(2.0 * R * d * dff, wb, wb + R * d * b + R * dff * b)
     if name == "gate":
-        return dict(flops=2.0 * T * d * E, bytes=float(T * d * b + E * d * b + 12 * T * k))
+        return w(2.0 * T * d * E, T * d * b + E * d * b + 12 * T * k)
     if name == "norm":
-        return dict(flops=2.0 * T * d, bytes=float(T * d * b))
+        # with the norms from the gate pass it only clears the per-position
+        # state (degree, walk state, claim key: 16 bytes a position)
+        return w(0.0, 16 * S) if norms_from_route else w(2.0 * T * d, T * d * b + 16 * S)
     if name == "combine":
-        return dict(flops=2.0 * S * d, bytes=float(R * d * b + 12 * T * k + T * d * b))
+        return w(2.0 * S * d, R * d * b + 8 * T * k + T * d * b, R * d * b + 12 * T * k + T * d * b)
     if name == "gather":
-        return dict(flops=0.0, bytes=float(2 * R * d * b + 8 * S))
+        return w(0.0, 2 * R * d * b + 8 * S)
     # backward (per launch)
-    if name == "bwd_wt":       # one weight tensor read and written transposed
-        return dict(flops=0.0, bytes=float(2 * E * d * dff * b))
-    if name in ("bwd_z", "bwd_da"):
-        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * d * b + R * dff * b))
-    if name == "bwd_dx":
-        return dict(flops=2.0 * R * d * dff, bytes=float(used * d * dff * b + R * dff * b + R * d * b))
+    if name in ("bwd_z", "bwd_da", "bwd_dx"):
+        wb = used * d * dff * b
+        return w(2.0 * R * d * dff, wb, wb + R * d * b + R * dff * b)
     if name in ("bwd_dw1", "bwd_dw2"):
-        return dict(flops=2.0 * R * d * dff, bytes=float(E * d * dff * counts.get("dw_bytes", 4) + R * (d + dff) * b))
+        ob = E * d * dff * counts.get("dw_bytes", 4)
+        return w(2.0 * R * d * dff, ob, ob + R * (d + dff) * b)
     if name == "cbwd_rows":
-        return dict(flops=2.0 * S * d, bytes=float(S * d * b + R * d * b + 12 * S))
+        return w(2.0 * S * d, S * d * b + R * d * b + 12 * S)
     if name == "cbwd_gate":
-        return dict(flops=2.0 * S * d, bytes=float(T * d * b + S * d * b + 12 * T * k))
-    return dict(flops=0.0, bytes=0.0)
+        return w(2.0 * S * d, T * d * b + S * d * b + 12 * T * k)
+    return w(0.0, 0.0)
 
 
-def roofline(name, cfg, counts, sec_per_launch):
-    w = kernel_work(name, cfg, counts)
+MFMA_KERNELS = ("gram", "ffn1", "ffn2", "bwd_z", "bwd_da", "bwd_dx", "bwd_dw1", "bwd_dw2")
+
+
+def roofline(name, cfg, counts, sec_per_launch, norms_from_route=True):
+    """Roofline of one kernel: MFMA kernels whose flops per algorithmic byte
+    reach the ridge (peak flops / 8 TB/s) are bound by the MFMA peak, every
+    other kernel by HBM.  `attainable` = min(MFMA peak, intensity x 8 TB/s)
+    in the kernel's unit; `frac_attainable` = achieved / attainable."""
+    wk = kernel_work(name, cfg, counts, norms_from_route)
     mfma_peak = MFMA_PEAK_TFLOPS[cfg.dtype]
     ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-    mfma_kernel = name in ("gram", "ffn1", "ffn2", "bwd_z", "bwd_da", "bwd_dx", "bwd_dw1", "bwd_dw2")
-    if mfma_kernel and (w["bytes"] == 0 or w["flops"] / w["bytes"] >= ridge):
-        ach = w["flops"] / sec_per_launch / 1e12
-        return dict(bound="mfma", achieved=ach, peak=mfma_peak, unit="TFLOP/s",
-                    frac=ach / mfma_peak, traffic=None)
-    ach = w["bytes"] / sec_per_launch / 1e9
-    return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=ach / HBM_PEAK_GBS, traffic=None)
+    tflops = wk["flops"] / sec_per_launch / 1e12
+    gbs = wk["bytes"] / sec_per_launch / 1e9
+    gbs_act = wk["bytes_act"] / sec_per_launch / 1e9
+    extra = dict(tflops=tflops, mfma_frac=tflops / mfma_peak, hbm_gbs=gbs, hbm_frac=gbs / HBM_PEAK_GBS,
+                 hbm_gbs_with_activations=gbs_act)
+    if name in MFMA_KERNELS and wk["bytes"] > 0:
+        intensity = wk["flops"] / wk["bytes"]
+        att = min(mfma_peak, intensity * HBM_PEAK_GBS / 1e3)
+        if intensity >= ridge:
+            return dict(bound="mfma", achieved=tflops, peak=mfma_peak, unit="TFLOP/s", frac=tflops / mfma_peak,
+                        traffic=None, attainable=att, frac_attainable=tflops / att, intensity=intensity, **extra)
+        return dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s", frac=gbs / HBM_PEAK_GBS,
+                    traffic=None, attainable=att, frac_attainable=tflops / att, intensity=intensity, **extra)
+    return dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s", frac=gbs / HBM_PEAK_GBS,
+                traffic=None, attainable=HBM_PEAK_GBS, frac_attainable=gbs / HBM_PEAK_GBS, **extra)
 
 
 def source_digest():
@@ -135,31 +155,61 @@ def copy_calibration(n_bytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes_read": n_bytes, "copy_bytes_written": n_bytes, "reps": reps}))
 
 
-def cpu_baseline(inp, h, budget_s=15.0):
-    """The oracle as it stands, on the host cores, on a bounded sample."""
+def cpu_baseline(inp, h, full_bucket_sizes, budget_s=15.0):
+    """The oracle as it stands, on the host cores, on a bounded sample: the
+    whole layer (its steps called in order, each timed) on the first T' tokens
+    of the batch (all of them when T <= 8192), repeated for about budget_s.
+
+    The similarity step costs the square of a bucket's size, so a sample of
+    T/8 tokens does about 1/64 of the full batch's similarity work per bucket;
+    `full_layer_estimate` scales the sample's similarity time by the ratio of
+    sum(n_e^2) over the full batch's buckets to the sample's, and the other
+    steps by T/T'."""
     import numpy as np
     from oracle import luffy_oracle as O
+    affinity = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
-        threads = len(os.sched_getaffinity(0))
+        blas = None
     cfg = inp.cfg
-    # sample: the first T' tokens of the batch (all of it when it fits the budget)
     T_s = cfg.T if cfg.T <= 8192 else max(1024, cfg.T // 8)
     x = inp.x[:T_s].astype(np.float64)
-    runs, t0 = 0, time.perf_counter()
+    E = cfg.E
+    t_sim = t_other = 0.0
+    runs = 0
+    sizes = None
+    t_start = time.perf_counter()
     while True:
-        O.moe_layer(x, inp.w_g, inp.b_g, inp.w1, inp.w2, k=cfg.k, h=h, act=cfg.act,
-                    capacity_factor=cfg.capacity_factor)
+        t0 = time.perf_counter()
+        idx, gates, _ = O.gate(x, inp.w_g, inp.b_g, cfg.k)
+        C = O.capacity_of(T_s, cfg.k, E, cfg.capacity_factor)
+        offsets, perm_token, slot_pos = O.dispatch(idx, E, C)
+        t1 = time.perf_counter()
+        cz = O.condense(x, perm_token, offsets, h)
+        t2 = time.perf_counter()
+        y_rep = O.expert_ffn(x[cz.rep_token], cz.rep_offsets, inp.w1, inp.w2, cfg.act)
+        O.combine(y_rep, cz.rep_row, slot_pos, gates)
+        t3 = time.perf_counter()
+        t_other += (t1 - t0) + (t3 - t2)
+        t_sim += t2 - t1
+        sizes = np.diff(offsets)
         runs += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
+        if time.perf_counter() - t_start >= budget_s:
             break
+    el = t_sim + t_other
+    sq_s = float((sizes.astype(np.float64) ** 2).sum())
+    sq_f = float((np.asarray(full_bucket_sizes, np.float64) ** 2).sum())
+    est = (t_other / runs) * (cfg.T / T_s) + (t_sim / runs) * (sq_f / max(sq_s, 1.0))
     sample = (f"whole layer on the first {T_s} of {cfg.T} tokens" if T_s < cfg.T
               else f"whole layer on all {cfg.T} tokens") + f", {runs} run(s), {el:.1f} s"
-    return dict(value=T_s * runs / el, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=sample)
+    return dict(value=T_s * runs / el, unit="tokens/s", cores=int(blas or affinity), kind="oracle",
+                sample=sample, affinity_cores=affinity, blas_threads=blas,
+                similarity_share=t_sim / el,
+                full_layer_estimate=dict(value=cfg.T / est, unit="tokens/s", seconds=est,
+                                         note="sample similarity time x sum(n_e^2) full/sample, "
+                                              "other steps x T/T'"))
 
 
 BACKWARD_KERNELS = ("cbwd_group", "cbwd_rows", "cbwd_gate", "bwd_z", "bwd_act", "bwd_da", "bwd_dx",
@@ -230,12 +280,7 @@ def bench_backward(args, cfg, layer, x, L, torch, np):
     rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
     rl.update(traffic=None, algorithmic_bytes=kernel_work(dominant, cfg, counts)["bytes"], kernel=dominant,
               us_per_launch=dom_ms / dom_n * 1e3)
-    kernels = {}
-    for name, v in per_kernel.items():
-        r = roofline(name, cfg, counts, v["ms_per_launch"] / 1e3)
-        kernels[name] = dict(us_per_launch=round(v["ms_per_launch"] * 1e3, 2),
-                             launches_per_step=v["launches_per_step"], bound=r["bound"],
-                             achieved=round(r["achieved"], 1), unit=r["unit"], frac=round(r["frac"], 4))
+    kernels = kernel_table(per_kernel, cfg, counts)
     out = {
         "metric": "condensed MoE-layer backward tokens/s on 1 MI355X",
         "value": cfg.T / (ms_per_step / 1e3),
@@ -261,12 +306,122 @@ def bench_backward(args, cfg, layer, x, L, torch, np):
     print(json.dumps(out), flush=True)
 
 
+def kernel_table(per_kernel, cfg, counts, norms_from_route=True):
+    out = {}
+    for name, v in per_kernel.items():
+        r = roofline(name, cfg, counts, v["ms_per_launch"] / 1e3, norms_from_route)
+        out[name] = dict(us_per_launch=round(v["ms_per_launch"] * 1e3, 2), launches_per_step=v["launches_per_step"],
+                         bound=r["bound"], achieved=round(r["achieved"], 1), unit=r["unit"], frac=round(r["frac"], 4),
+                         tflops=round(r["tflops"], 1), mfma_frac=round(r["mfma_frac"], 4),
+                         hbm_gbs=round(r["hbm_gbs"], 1), hbm_frac=round(r["hbm_frac"], 4))
+    return out
+
+
+def measure_forward(name, thresholds, args, torch, np, G, L, with_cpu):
+    """Times the forward step of workload `name` at each threshold (the
+    inputs are drawn and uploaded once).  Returns one record per threshold."""
+    cfg = G.config(name)
+    log(f"generating {name} (seed {args.seed})")
+    inp = G.make_inputs(cfg, seed=args.seed)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+    def dev(a, dtype=dt):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        return t.to(dtype).to("cuda")
+
+    x = dev(inp.x)
+    weights = (dev(inp.w_g), dev(inp.b_g, torch.float32), dev(inp.w1), dev(inp.w2))
+    records = []
+    for h in thresholds:
+        layer = L.MoELayer(*weights, k=cfg.k, act=cfg.act, threshold=h, capacity_factor=cfg.capacity_factor,
+                           T=cfg.T)
+        torch.cuda.synchronize()
+        log(f"{name} h={h}: warmup")
+        for _ in range(max(args.warmup, 1)):
+            layer(x)
+        torch.cuda.synchronize()
+        if args.backward:
+            bench_backward(args, cfg, layer, x, L, torch, np)
+            return None
+        # per-kernel breakdown (untimed passes) to find the dominant kernel
+        per_kernel = {}
+        for kname in L.KERNELS:
+            L.profile_kernel(kname)
+            for _ in range(3):
+                layer(x)
+            ms, n = L.profile_read()
+            if n:
+                per_kernel[kname] = dict(ms_per_step=ms / 3, launches_per_step=n / 3, ms_per_launch=ms / n)
+        L.profile_kernel(None)
+        dominant = max(per_kernel, key=lambda kk: per_kernel[kk]["ms_per_step"])
+        log(f"{name} h={h}: dominant kernel {dominant}; timing {args.steps} steps")
+        # timed region: K steps, only the dominant kernel bracketed by events
+        L.profile_kernel(dominant)
+        L.profile_read()
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        w0 = time.perf_counter()
+        start.record()
+        for _ in range(args.steps):
+            layer(x)
+        stop.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        ms_total = start.elapsed_time(stop)
+        dom_ms, dom_n = L.profile_read()
+        L.profile_kernel(None)
+        ms_per_step = ms_total / args.steps
+        b = layer.buf
+        off = b.offsets.cpu().numpy()
+        ro = b.rep_offsets.cpu().numpy()
+        counts = dict(S=int(off[-1]), R=int(ro[-1]), bucket_sizes=np.diff(off).tolist(),
+                      used_experts=int((np.diff(ro) > 0).sum()))
+        rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
+        wk = kernel_work(dominant, cfg, counts)
+        rl.update(traffic=recorded_traffic(name, dominant),
+                  traffic_unit="HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+                  algorithmic_flops=wk["flops"], algorithmic_bytes=wk["bytes"],
+                  algorithmic_bytes_with_activations=wk["bytes_act"], kernel=dominant,
+                  us_per_launch=dom_ms / dom_n * 1e3, launches_timed=dom_n)
+        rec = dict(name=name, threshold=h, cfg=cfg, value=cfg.T / (ms_per_step / 1e3), ms_per_step=ms_per_step,
+                   wall_s=wall,
+                   condensation={"slots_kept": counts["S"], "representatives": counts["R"],
+                                 "ratio": counts["R"] / max(counts["S"], 1),
+                                 "dropped_slots": cfg.T * cfg.k - counts["S"],
+                                 "largest_bucket": int(max(counts["bucket_sizes"])),
+                                 "used_experts": counts["used_experts"]},
+                   roofline=rl, kernels=kernel_table(per_kernel, cfg, counts), cpu_baseline=None)
+        if with_cpu and h == thresholds[0]:
+            log(f"{name}: cpu baseline (oracle)")
+            rec["cpu_baseline"] = cpu_baseline(inp, h, counts["bucket_sizes"])
+        records.append(rec)
+        del layer
+    del x, weights, inp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return records
+
+
+def compact(rec):
+    """Summary of a workload measured beside the headline one."""
+    rl = rec["roofline"]
+    return {"workload": WORKLOAD_NAMES[rec["name"]], "threshold": rec["threshold"],
+            "tokens_per_s": rec["value"], "ms_per_step": rec["ms_per_step"], "condensation": rec["condensation"],
+            "dominant": {k: rl[k] for k in ("kernel", "bound", "achieved", "unit", "frac", "tflops", "mfma_frac",
+                                            "hbm_gbs", "hbm_frac", "us_per_launch")},
+            "kernels_us": {k: v["us_per_launch"] for k, v in rec["kernels"].items()}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="c2", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--config", default="c3", choices=sorted(WORKLOAD_NAMES),
+                    help="headline workload (default c3: one GPU's share of an expert-parallel layer)")
+    ap.add_argument("--extras", default="c2,c4,c5",
+                    help="workloads measured beside the headline one, reported under 'workloads' "
+                         "(c4 at each of its four thresholds); 'none' for none")
     ap.add_argument("--threshold", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -297,96 +452,28 @@ def main():
     torch.cuda.set_device(0)
     cfg = G.config(args.config)
     h = cfg.h if args.threshold is None else args.threshold
-    log(f"generating {args.config} (seed {args.seed})")
-    inp = G.make_inputs(cfg, seed=args.seed)
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-
-    def dev(a, dtype=dt):
-        t = torch.from_numpy(np.ascontiguousarray(a))
-        return t.to(dtype).to("cuda")
-
-    x = dev(inp.x)
-    layer = L.MoELayer(dev(inp.w_g), dev(inp.b_g, torch.float32), dev(inp.w1), dev(inp.w2),
-                       k=cfg.k, act=cfg.act, threshold=h, capacity_factor=cfg.capacity_factor,
-                       T=cfg.T)
-    torch.cuda.synchronize()
-    log("warmup")
-    for _ in range(max(args.warmup, 1)):
-        layer(x)
-    torch.cuda.synchronize()
-
-    if args.backward:
-        bench_backward(args, cfg, layer, x, L, torch, np)
+    recs = measure_forward(args.config, [h], args, torch, np, G, L, with_cpu=not args.no_cpu_baseline)
+    if recs is None:      # --backward printed its own line
         return
-
-    # per-kernel breakdown (untimed pass) to find the dominant kernel
-    per_kernel = {}
-    for name in L.KERNELS:
-        L.profile_kernel(name)
-        for _ in range(3):
-            layer(x)
-        ms, n = L.profile_read()
-        if n:
-            per_kernel[name] = dict(ms_per_step=ms / 3, launches_per_step=n / 3, ms_per_launch=ms / n)
-    L.profile_kernel(None)
-    dominant = max(per_kernel, key=lambda kname: per_kernel[kname]["ms_per_step"])
-    log(f"dominant kernel: {dominant}")
-
-    # timed region: K steps, only the dominant kernel bracketed by events
-    L.profile_kernel(dominant)
-    L.profile_read()
-    torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    w0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        layer(x)
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms_total = start.elapsed_time(stop)
-    dom_ms, dom_n = L.profile_read()
-    L.profile_kernel(None)
-    ms_per_step = ms_total / args.steps
-    tokens_per_s = cfg.T / (ms_per_step / 1e3)
-
-    b = layer.buf
-    off = b.offsets.cpu().numpy()
-    ro = b.rep_offsets.cpu().numpy()
-    sizes = np.diff(off).tolist()
-    counts = dict(S=int(off[-1]), R=int(ro[-1]), bucket_sizes=sizes,
-                  used_experts=int((np.diff(ro) > 0).sum()))
-    dropped = cfg.T * cfg.k - counts["S"]
-
-    rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
-    traffic = recorded_traffic(args.config, dominant)
-    rl["traffic"] = traffic
-    rl["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)"
-    rl["algorithmic_bytes"] = kernel_work(dominant, cfg, counts)["bytes"]
-    rl["kernel"] = dominant
-    rl["us_per_launch"] = dom_ms / dom_n * 1e3
-    kernels = {}
-    for name, v in per_kernel.items():
-        r = roofline(name, cfg, counts, v["ms_per_launch"] / 1e3)
-        kernels[name] = dict(us_per_launch=round(v["ms_per_launch"] * 1e3, 2),
-                             launches_per_step=v["launches_per_step"],
-                             bound=r["bound"], achieved=round(r["achieved"], 1), unit=r["unit"],
-                             frac=round(r["frac"], 4))
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        log("cpu baseline (oracle)")
-        cpu = cpu_baseline(inp, h)
-
+    head = recs[0]
+    extras = {}
+    if not args.backward and args.extras and args.extras != "none":
+        for name in [n.strip() for n in args.extras.split(",") if n.strip()]:
+            if name == args.config or name not in WORKLOAD_NAMES:
+                continue
+            ecfg = G.config(name)
+            for r in measure_forward(name, list(ecfg.thresholds), args, torch, np, G, L, with_cpu=False):
+                key = name if len(ecfg.thresholds) == 1 else f"{name}_h{r['threshold']:.2f}"
+                extras[key] = compact(r)
     out = {
         "metric": "condensed MoE-layer tokens/s on 1 MI355X",
-        "value": tokens_per_s,
+        "value": head["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "wall_s": wall,
+        "ms_per_step": head["ms_per_step"],
+        "wall_s": head["wall_s"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -396,11 +483,11 @@ def main():
                    "d_model": cfg.d, "E": cfg.E, "top_k": cfg.k, "d_ff": cfg.d_ff,
                    "act": cfg.act, "threshold": h, "capacity_factor": cfg.capacity_factor,
                    "seed": args.seed},
-        "condensation": {"slots_kept": counts["S"], "representatives": counts["R"],
-                         "ratio": counts["R"] / max(counts["S"], 1), "dropped_slots": dropped},
-        "roofline": rl,
-        "kernels": kernels,
-        "cpu_baseline": cpu,
+        "condensation": head["condensation"],
+        "roofline": head["roofline"],
+        "kernels": head["kernels"],
+        "cpu_baseline": head["cpu_baseline"],
+        "workloads": extras,
     }
     print(json.dumps(out), flush=True)
 

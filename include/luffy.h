@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUFFY_ABI_VERSION 4
+#define LUFFY_ABI_VERSION 5
 
 typedef enum {
   LUFFY_OK = 0,
@@ -74,8 +74,8 @@ const char* luffy_last_error(void);
  *   x          [T, d] dtype, device          token embeddings
  *   w_gate     [E, d] dtype, device          gate weights
  *   b_gate     [E] float, device, or NULL    gate bias
- *   capacity_factor  > 0: each expert keeps at most C = ceil(cf*k*T/E)
- *                    slots; <= 0: no limit
+ *   capacity_factor  > 0: each expert keeps at most C slots, C =
+ *                    luffy_capacity(T, k, E, capacity_factor); <= 0: no limit
  * Outputs (device):
  *   topk_idx   [T, k] int32   experts by descending logit, ties to the lower
  *                             id; logits are float32 sums, and a choice
@@ -99,10 +99,18 @@ const char* luffy_last_error(void);
 size_t luffy_route_workspace_size(int T, int E, int k);
 int luffy_route(const void* x, int T, int d, int dtype,
                 const void* w_gate, const float* b_gate, int E, int k,
-                float capacity_factor,
+                double capacity_factor,
                 int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
                 int32_t* perm_token, int32_t* offsets, float* inv_norm,
                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Per-expert slot capacity used by luffy_route: ceil(cf*k*T/E - 1e-9),
+ * evaluated in double precision left to right (the 1e-9 keeps a product that
+ * is an integer but for the binary rounding of a decimal factor, such as
+ * 1.1*2*4000/8, at that integer).  0 (no limit) for cf <= 0 or a
+ * non-positive size; at most INT_MAX.  Host arithmetic.  A caller sizing
+ * luffy_condense's max_bucket as min(T, C) gets the same C as the routing. */
+int luffy_capacity(int T, int k, int E, double capacity_factor);
 
 /* ------------------------------------------------------------------------
  * luffy_condense - per-bucket similarity, representative selection and
@@ -120,9 +128,11 @@ int luffy_route(const void* x, int T, int d, int dtype,
  *   x            [T, d] dtype, device     embeddings (same as luffy_route)
  *   perm_token, offsets                   as written by luffy_route
  *   max_bucket   upper bound on any bucket size (min(T, C) for outputs of
- *                luffy_route); sizes the workspace.  Buckets larger than it
- *                make the call write nothing past the workspace and leave the
- *                outputs undefined.
+ *                luffy_route, C from luffy_capacity); sizes the workspace.
+ *                If a bucket is larger (the bound was wrong), the call still
+ *                writes nothing past the workspace: no position is condensed
+ *                (every position is its own representative, degrees are not
+ *                written) and the compaction below runs as usual.
  *   threshold    cosine threshold h (a value > 1 disables condensation)
  *   inv_norm     [T] float, device, or NULL: 1/|x_t| as written by
  *                luffy_route for the same x; NULL computes the norms here

@@ -47,7 +47,7 @@ import numpy as np
 
 __all__ = [
     "LayerConfig", "CONFIGS", "config", "Inputs", "make_inputs",
-    "round_bf16", "bf16_bits", "gate_bias", "capacity",
+    "round_bf16", "bf16_bits", "gate_bias",
 ]
 
 
@@ -101,14 +101,6 @@ def config(name: str, **overrides) -> LayerConfig:
     if overrides:
         cfg = cfg.replace(**overrides)
     return cfg
-
-
-def capacity(T: int, k: int, E: int, cf: float) -> int:
-    """Per-expert slot capacity ceil(cf*k*T/E); 0 means unlimited."""
-    if cf <= 0:
-        return 0
-    # exact for the listed configurations (1.25*2*8192/16 and 1.0*65536/64)
-    return int(math.ceil(cf * k * T / E - 1e-9))
 
 
 def round_bf16(a: np.ndarray, inplace: bool = False) -> np.ndarray:

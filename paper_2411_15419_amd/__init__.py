@@ -9,7 +9,6 @@ fallback: without the built library every call raises.
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 from dataclasses import dataclass
 from typing import Optional
@@ -39,7 +38,8 @@ _SIGS = {
     "luffy_status_string": (ctypes.c_char_p, [_c_int]),
     "luffy_last_error": (ctypes.c_char_p, []),
     "luffy_route_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
-    "luffy_route": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_float,
+    "luffy_capacity": (_c_int, [_c_int, _c_int, _c_int, ctypes.c_double]),
+    "luffy_route": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, ctypes.c_double,
                              _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
     "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
@@ -114,10 +114,8 @@ def _stream(stream) -> Optional[int]:
 
 
 def capacity(T: int, k: int, E: int, cf: float) -> int:
-    """Per-expert capacity ceil(cf*k*T/E) (0 = unlimited)."""
-    if cf <= 0:
-        return 0
-    return int(math.ceil(cf * k * T / E - 1e-9))
+    """Per-expert capacity of luffy_route (luffy_capacity; 0 = unlimited)."""
+    return int(load_library().luffy_capacity(int(T), int(k), int(E), float(cf)))
 
 
 def route_workspace_size(T: int, E: int, k: int) -> int:

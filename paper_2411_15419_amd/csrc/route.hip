@@ -459,9 +459,13 @@ RouteWs carve_route(Carver& c, int T, int E, int k) {
 
 }  // namespace
 
-int capacity_slots(int T, int k, int E, float cf) {
-  if (!(cf > 0.f)) return 0;
-  return static_cast<int>(std::ceil(static_cast<double>(cf) * k * T / E - 1e-9));
+// ceil(cf*k*T/E - 1e-9) in double precision, evaluated left to right; the
+// 1e-9 keeps a product that is an integer up to the rounding of a decimal
+// factor (cf = 1.1, k*T/E = 1000) at that integer.
+int capacity_slots(int T, int k, int E, double cf) {
+  if (!(cf > 0.0)) return 0;
+  const double c = std::ceil(cf * k * T / E - 1e-9);
+  return c >= 2147483647.0 ? 2147483647 : static_cast<int>(c);
 }
 
 }  // namespace luffy
@@ -475,34 +479,33 @@ extern "C" size_t luffy_route_workspace_size(int T, int E, int k) {
   return c.size();
 }
 
-extern "C" int luffy_route(const void* x, int T, int d, int dtype,
-                           const void* w_gate, const float* b_gate, int E, int k,
-                           float capacity_factor,
-                           int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
-                           int32_t* perm_token, int32_t* offsets, float* inv_norm,
-                           void* workspace, size_t workspace_bytes, void* stream) {
-  if (!x || !w_gate || !topk_idx || !topk_gate || !slot_pos || !perm_token || !offsets)
-    return fail(LUFFY_E_INVALID, "luffy_route: null pointer argument");
-  if (T <= 0 || d <= 0 || E <= 0)
-    return fail(LUFFY_E_INVALID, "luffy_route: T=%d d=%d E=%d must be positive", T, d, E);
-  if (k != 1 && k != 2)
-    return fail(LUFFY_E_INVALID, "luffy_route: k=%d must be 1 or 2", k);
-  if (k > E) return fail(LUFFY_E_INVALID, "luffy_route: k=%d > E=%d", k, E);
-  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
-    return fail(LUFFY_E_INVALID, "luffy_route: unknown dtype %d", dtype);
-  if (E > kMaxExperts)
-    return fail(LUFFY_E_UNSUPPORTED, "luffy_route: E=%d > %d", E, kMaxExperts);
-  if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_route: d=%d not a multiple of 64", d);
-  if (static_cast<long long>(T) * k >= (1ll << 31))
-    return fail(LUFFY_E_UNSUPPORTED, "luffy_route: T*k too large");
-  const size_t need = luffy_route_workspace_size(T, E, k);
-  if (workspace_bytes < need || (need && !workspace) ||
-      (reinterpret_cast<uintptr_t>(workspace) & 255u))
-    return fail(LUFFY_E_WORKSPACE, "luffy_route: workspace needs %zu bytes, 256-aligned", need);
+namespace {
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  Carver c(workspace);
-  RouteWs ws = carve_route(c, T, E, k);
+// Host checks shared by both route entry points.
+int route_check(const char* fn, const void* x, int T, int d, int dtype, const void* w_gate, int E, int k,
+                const int32_t* topk_idx, const float* topk_gate, const int32_t* slot_pos, const int32_t* perm_token,
+                const int32_t* offsets) {
+  if (!x || !w_gate || !topk_idx || !topk_gate || !slot_pos || !perm_token || !offsets)
+    return fail(LUFFY_E_INVALID, "%s: null pointer argument", fn);
+  if (T <= 0 || d <= 0 || E <= 0)
+    return fail(LUFFY_E_INVALID, "%s: T=%d d=%d E=%d must be positive", fn, T, d, E);
+  if (k != 1 && k != 2)
+    return fail(LUFFY_E_INVALID, "%s: k=%d must be 1 or 2", fn, k);
+  if (k > E) return fail(LUFFY_E_INVALID, "%s: k=%d > E=%d", fn, k, E);
+  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
+    return fail(LUFFY_E_INVALID, "%s: unknown dtype %d", fn, dtype);
+  if (E > kMaxExperts)
+    return fail(LUFFY_E_UNSUPPORTED, "%s: E=%d > %d", fn, E, kMaxExperts);
+  if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "%s: d=%d not a multiple of 64", fn, d);
+  if (static_cast<long long>(T) * k >= (1ll << 31))
+    return fail(LUFFY_E_UNSUPPORTED, "%s: T*k too large", fn);
+  return LUFFY_OK;
+}
+
+// The three launches of a route call on scratch `ws`.
+void route_enqueue(const void* x, int T, int d, int dtype, const void* w_gate, const float* b_gate, int E, int k,
+                   double capacity_factor, int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
+                   int32_t* perm_token, int32_t* offsets, float* inv_norm, const RouteWs& ws, hipStream_t s) {
   const int C = capacity_slots(T, k, E, capacity_factor);
   const long long S = static_cast<long long>(T) * k;
   const int tok = gate_tokens(T);
@@ -519,12 +522,34 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
     }
 #undef LUFFY_GATE_ARGS
   }
-  {
-    launch("slot_scan", slot_scan_kernel, E, 1024, 0, s, ws.hist, nch, E, C, offsets, ws.totals, ws.done);
-  }
-  {
-    launch("slot_scatter", slot_scatter_kernel, static_cast<int>((S + 255) / 256), 256, 0, s, topk_idx, ws.hist,
-           offsets, T, k, E, C, tok, slot_pos, perm_token);
-  }
+  launch("slot_scan", slot_scan_kernel, E, 1024, 0, s, ws.hist, nch, E, C, offsets, ws.totals, ws.done);
+  launch("slot_scatter", slot_scatter_kernel, static_cast<int>((S + 255) / 256), 256, 0, s, topk_idx, ws.hist,
+         offsets, T, k, E, C, tok, slot_pos, perm_token);
+}
+
+}  // namespace
+
+extern "C" int luffy_capacity(int T, int k, int E, double capacity_factor) {
+  if (T <= 0 || k <= 0 || E <= 0) return 0;
+  return capacity_slots(T, k, E, capacity_factor);
+}
+
+extern "C" int luffy_route(const void* x, int T, int d, int dtype,
+                           const void* w_gate, const float* b_gate, int E, int k,
+                           double capacity_factor,
+                           int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
+                           int32_t* perm_token, int32_t* offsets, float* inv_norm,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  const int st = route_check("luffy_route", x, T, d, dtype, w_gate, E, k, topk_idx, topk_gate, slot_pos, perm_token,
+                             offsets);
+  if (st != LUFFY_OK) return st;
+  const size_t need = luffy_route_workspace_size(T, E, k);
+  if (workspace_bytes < need || (need && !workspace) ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LUFFY_E_WORKSPACE, "luffy_route: workspace needs %zu bytes, 256-aligned", need);
+  Carver c(workspace);
+  const RouteWs ws = carve_route(c, T, E, k);
+  route_enqueue(x, T, d, dtype, w_gate, b_gate, E, k, capacity_factor, topk_idx, topk_gate, slot_pos, perm_token,
+                offsets, inv_norm, ws, static_cast<hipStream_t>(stream));
   return check_launch("luffy_route");
 }

@@ -38,9 +38,26 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.luffy_abi_version() == 4
+    assert lib.luffy_abi_version() == 5
     assert lib.luffy_status_string(0) == b"ok"
     assert lib.luffy_status_string(-3).startswith(b"workspace")
+
+
+def test_capacity_agrees_with_the_oracle(lib):
+    """luffy_capacity (what luffy_route drops at, and what MoELayer sizes
+    max_bucket from) equals the oracle's capacity_of on a grid that includes
+    decimal factors whose product with k*T/E is an integer (cf = 1.1 with
+    k*T/E = 1000: a float32 factor would give 1101)."""
+    from oracle import luffy_oracle as O
+    import paper_2411_15419_amd as L
+    assert lib.luffy_capacity(4000, 2, 8, 1.1) == 1100
+    assert O.capacity_of(4000, 2, 8, 1.1) == 1100
+    for T in (1, 7, 1000, 4000, 8192, 32768, 65536):
+        for k in (1, 2):
+            for E in (1, 3, 8, 16, 64):
+                for cf in (0.0, -1.0, 0.1, 0.3, 0.75, 1.0, 1.1, 1.2, 1.25, 1.3, 2.0, 2.5):
+                    assert lib.luffy_capacity(T, k, E, cf) == O.capacity_of(T, k, E, cf), (T, k, E, cf)
+                    assert L.capacity(T, k, E, cf) == O.capacity_of(T, k, E, cf)
 
 
 def test_workspace_sizes(lib):

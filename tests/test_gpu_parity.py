@@ -111,6 +111,27 @@ def test_empty_buckets_and_full_drop():
     assert_output_close(g, o, "bf16")
 
 
+def test_decimal_capacity_factor():
+    """cf = 1.1 with k*T/E = 500: the capacity is exactly 550 on both sides
+    (a float32 factor made it 551 on the device); the four hot buckets are
+    larger, so each keeps exactly its first 550 slots, and the layer's
+    max_bucket (sized from the same capacity) holds every bucket, so
+    condensation still runs."""
+    cfg = G.config("c2", T=2000, d=256, d_ff=256, E=8, n_centres=64, capacity_factor=1.1)
+    inp = G.make_inputs(cfg, seed=4)
+    assert O.capacity_of(2000, 2, 8, 1.1) == 550
+    inp.b_g[:] = 0.0
+    inp.b_g[:4] = 3.0          # four hot experts overflow the capacity
+    print_case("capacity 1.1", T=2000, E=8, k=2)
+    g = run_gpu(inp)
+    o = run_oracle(inp)
+    assert_route_equal(g, o)
+    assert np.diff(g["offsets"]).max() == 550
+    assert_condense_equal(g, o)
+    assert g["rep_offsets"][-1] < g["offsets"][-1]
+    assert_output_close(g, o, "bf16")
+
+
 def test_identical_tokens_one_group():
     # every token identical: one clique per bucket, dense adjacency words
     inp = G.make_inputs("c2", seed=4, T=2048, d=256, d_ff=256, n_centres=1,
