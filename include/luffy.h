@@ -104,6 +104,26 @@ int luffy_route(const void* x, int T, int d, int dtype,
                 int32_t* perm_token, int32_t* offsets, float* inv_norm,
                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* luffy_route_noalloc - luffy_route for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments and results without the workspace, whose
+ * role is taken by a scratch array the library holds in device memory, one
+ * per GPU, for the life of the process (luffy_route_noalloc_max_bytes()
+ * bytes, 1 MiB).  Calls whose luffy_route_workspace_size(T, E, k) exceeds it
+ * return LUFFY_E_UNSUPPORTED and enqueue nothing (at E = 64, k = 2 that is
+ * T above 131008).  It allocates nothing on any call.  Every call on a GPU
+ * uses that GPU's one array, so calls that can overlap on one GPU (several
+ * streams, several host threads) race and must be ordered by the caller.  On
+ * its first call on a device (the current device) it looks up the array's
+ * address there, which can fail with LUFFY_E_HIP. */
+size_t luffy_route_noalloc_max_bytes(void);
+int luffy_route_noalloc(const void* x, int T, int d, int dtype,
+                        const void* w_gate, const float* b_gate, int E, int k,
+                        double capacity_factor,
+                        int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
+                        int32_t* perm_token, int32_t* offsets, float* inv_norm,
+                        void* stream);
+
 /* Per-expert slot capacity used by luffy_route: ceil(cf*k*T/E - 1e-9),
  * evaluated in double precision left to right (the 1e-9 keeps a product that
  * is an integer but for the binary rounding of a decimal factor, such as

@@ -17,7 +17,7 @@ import torch
 
 __all__ = [
     "LuffyError", "load_library", "LUFFY_F32", "LUFFY_BF16", "LUFFY_ACT_GELU",
-    "LUFFY_ACT_SILU", "luffy_route", "luffy_condense", "luffy_expert_ffn",
+    "LUFFY_ACT_SILU", "luffy_route", "luffy_route_noalloc", "luffy_condense", "luffy_expert_ffn",
     "luffy_combine", "route_workspace_size", "condense_workspace_size",
     "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
     "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
@@ -41,6 +41,9 @@ _SIGS = {
     "luffy_capacity": (_c_int, [_c_int, _c_int, _c_int, ctypes.c_double]),
     "luffy_route": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, ctypes.c_double,
                              _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "luffy_route_noalloc_max_bytes": (_c_size, []),
+    "luffy_route_noalloc": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, ctypes.c_double,
+                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
                                 _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
@@ -139,6 +142,19 @@ def luffy_route(x, w_gate, b_gate, k, capacity_factor, topk_idx, topk_gate, slot
                            float(capacity_factor), _p(topk_idx), _p(topk_gate), _p(slot_pos),
                            _p(perm_token), _p(offsets), _p(inv_norm), _p(workspace),
                            workspace.numel(), _stream(stream)), "luffy_route")
+
+
+def luffy_route_noalloc(x, w_gate, b_gate, k, capacity_factor, topk_idx, topk_gate, slot_pos,
+                        perm_token, offsets, stream=None, inv_norm=None):
+    """luffy_route without a workspace (the library's own scratch array;
+    calls that may overlap on one GPU must be ordered by the caller)."""
+    T, d = x.shape
+    E = w_gate.shape[0]
+    lib = load_library()
+    _check(lib.luffy_route_noalloc(_p(x), T, d, _dtype_code(x), _p(w_gate), _p(b_gate), E, k,
+                                   float(capacity_factor), _p(topk_idx), _p(topk_gate), _p(slot_pos),
+                                   _p(perm_token), _p(offsets), _p(inv_norm), _stream(stream)),
+           "luffy_route_noalloc")
 
 
 def luffy_condense(x, perm_token, offsets, k, max_bucket, threshold, rep_of_pos, rep_row,

@@ -15,8 +15,16 @@
 //   slot_scatter_kernel  bucket position of every slot, capacity drop,
 //                    perm_token.
 #include <cmath>
+#include <mutex>
 
 #include "luffy_common.h"
+
+// Scratch of luffy_route_noalloc (the per-chunk slot counts of one call):
+// one copy per GPU for the life of the process.  In host code the name only
+// stands for the symbol; kernels get the device address that
+// hipGetSymbolAddress returns for the current device.
+static constexpr size_t kRouteScratchBytes = 1u << 20;
+static __device__ __align__(256) uint8_t route_scratch[kRouteScratchBytes];
 
 namespace luffy {
 namespace {
@@ -527,6 +535,27 @@ void route_enqueue(const void* x, int T, int d, int dtype, const void* w_gate, c
          offsets, T, k, E, C, tok, slot_pos, perm_token);
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this GPU's route_scratch, looked up once per device.
+int route_scratch_ptr(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(LUFFY_E_HIP, "luffy_route_noalloc: no current device (or device id >= %d)", kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(route_scratch));
+    if (e != hipSuccess || !p)
+      return fail(LUFFY_E_HIP, "luffy_route_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LUFFY_OK;
+}
+
 }  // namespace
 
 extern "C" int luffy_capacity(int T, int k, int E, double capacity_factor) {
@@ -552,4 +581,29 @@ extern "C" int luffy_route(const void* x, int T, int d, int dtype,
   route_enqueue(x, T, d, dtype, w_gate, b_gate, E, k, capacity_factor, topk_idx, topk_gate, slot_pos, perm_token,
                 offsets, inv_norm, ws, static_cast<hipStream_t>(stream));
   return check_launch("luffy_route");
+}
+
+extern "C" size_t luffy_route_noalloc_max_bytes(void) { return kRouteScratchBytes; }
+
+extern "C" int luffy_route_noalloc(const void* x, int T, int d, int dtype,
+                                   const void* w_gate, const float* b_gate, int E, int k,
+                                   double capacity_factor,
+                                   int32_t* topk_idx, float* topk_gate, int32_t* slot_pos,
+                                   int32_t* perm_token, int32_t* offsets, float* inv_norm, void* stream) {
+  const int st = route_check("luffy_route_noalloc", x, T, d, dtype, w_gate, E, k, topk_idx, topk_gate, slot_pos,
+                             perm_token, offsets);
+  if (st != LUFFY_OK) return st;
+  const size_t need = luffy_route_workspace_size(T, E, k);
+  if (need > kRouteScratchBytes)
+    return fail(LUFFY_E_UNSUPPORTED,
+                "luffy_route_noalloc: T=%d E=%d k=%d needs %zu bytes of scratch, more than its %zu", T, E, k, need,
+                kRouteScratchBytes);
+  void* scratch = nullptr;
+  const int sp = route_scratch_ptr(&scratch);
+  if (sp != LUFFY_OK) return sp;
+  Carver c(scratch);
+  const RouteWs ws = carve_route(c, T, E, k);
+  route_enqueue(x, T, d, dtype, w_gate, b_gate, E, k, capacity_factor, topk_idx, topk_gate, slot_pos, perm_token,
+                offsets, inv_norm, ws, static_cast<hipStream_t>(stream));
+  return check_launch("luffy_route_noalloc");
 }
