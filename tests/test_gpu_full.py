@@ -3,20 +3,22 @@ throughput benchmark times (one MoELayer call on inputs resident in HBM).
 
 Indices (routing, buckets, degrees, representatives, compaction) are compared
 bit-exactly with the oracle over the whole batch.  Layer outputs are compared
-on a seeded sample of tokens: the oracle evaluates the expert FFN in fp64 for
-just the representatives those tokens use (the index maps having been found
-identical first), then gate-weights them as its combine does."""
+on every row: the oracle evaluates the expert FFN in fp64 on every
+representative (the index maps having been found identical first) and
+combines as the layer does; Y_rep and y are held to the per-row relative
+tolerance.  The generator's margins (similarity 0.01 from every threshold,
+routing gaps) are asserted on the same oracle buckets."""
 import numpy as np
 import pytest
 
 import luffy_gen as G
 from oracle import luffy_oracle as O
 from tests.layer_runner import (TOL, assert_condense_equal, assert_route_equal, fetch,
-                                make_layer, upload)
+                                make_layer, rel_err_rows, upload)
+from tests.test_generator_margins import check_margins
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-N_SAMPLE = 96
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -38,56 +40,29 @@ def run_layer(inp, dev, h):
     return fetch(layer)
 
 
-def sample_tokens(o, T, seed):
-    """Seeded token sample that always includes condensed (non-representative)
-    slots, multi-slot tokens and, where they exist, fully dropped tokens."""
-    rng = np.random.default_rng([seed, 17])
-    picks = set(rng.choice(T, size=min(N_SAMPLE // 2, T), replace=False).tolist())
-    kept = o.slot_pos >= 0
-    dup = np.zeros(T, bool)
-    for j in range(o.slot_pos.shape[1]):
-        pos = o.slot_pos[kept[:, j], j]
-        dup[np.flatnonzero(kept[:, j])] |= o.rep_of_pos[pos] != pos
-    for mask in (dup, ~kept.any(axis=1), kept.all(axis=1)):
-        cand = np.flatnonzero(mask)
-        if cand.size:
-            picks.update(rng.choice(cand, size=min(N_SAMPLE // 6, cand.size),
-                                    replace=False).tolist())
-    return np.array(sorted(picks))
+def full_expected(inp, o):
+    """fp64 Y_rep of every representative and y of every token, from the
+    oracle's own indices (found identical to the GPU's first)."""
+    cfg = inp.cfg
+    y_rep = O.expert_ffn(inp.x[o.rep_token].astype(np.float64), o.rep_offsets, inp.w1, inp.w2, cfg.act)
+    y = O.combine(y_rep, o.rep_row, o.slot_pos, o.topk_gate)
+    return y_rep, y
 
 
-def sampled_expected(inp, o, tokens):
-    """fp64 y_t for the sampled tokens and Y_rep for the rows they read."""
-    rows = sorted({int(o.rep_row[p]) for t in tokens for p in o.slot_pos[t] if p >= 0})
-    rows = np.array(rows, np.int64)
-    expert = np.searchsorted(o.rep_offsets, rows, side="right") - 1
-    E = inp.cfg.E
-    sub_off = np.zeros(E + 1, np.int64)
-    np.add.at(sub_off, expert + 1, 1)
-    sub_off = np.cumsum(sub_off)
-    x_sub = inp.x[o.rep_token[rows]].astype(np.float64)   # rows ascend, so experts do too
-    y_sub = O.expert_ffn(x_sub, sub_off, inp.w1, inp.w2, inp.cfg.act)
-    where = {int(r): i for i, r in enumerate(rows)}
-    y = np.zeros((tokens.size, inp.cfg.d), np.float64)
-    for i, t in enumerate(tokens):
-        for j, p in enumerate(o.slot_pos[t]):
-            if p >= 0:
-                y[i] += float(o.topk_gate[t, j]) * y_sub[where[int(o.rep_row[p])]]
-    return rows, y_sub, y
-
-
-def assert_sampled_close(g, inp, tokens, rows, y_sub, y_ref):
+def assert_all_rows_close(g, inp, o, y_rep_ref, y_ref):
+    """Every row of Y_rep and of y within the dtype's per-row relative
+    tolerance; fully dropped tokens exactly zero."""
     tol = TOL[inp.cfg.dtype]
-    den = np.abs(y_sub).max(axis=1)
-    err_rep = np.abs(g["y_rep"][rows] - y_sub).max(axis=1) / den
-    assert err_rep.max() <= tol, f"Y_rep max row rel err {err_rep.max():.3g}"
-    gy = g["y"][tokens]
-    dropped = np.abs(y_ref).max(axis=1) == 0
-    assert np.all(gy[dropped] == 0), "fully dropped tokens must be zero"
-    err = np.abs(gy[~dropped] - y_ref[~dropped]).max(axis=1) / np.abs(y_ref[~dropped]).max(axis=1)
-    assert err.size == 0 or err.max() <= tol, f"y max row rel err {err.max():.3g}"
-    print(f"[sampled] {tokens.size} tokens, {rows.size} rows, y err {err.max():.3g}, "
-          f"Y_rep err {err_rep.max():.3g}", flush=True)
+    R = y_rep_ref.shape[0]
+    err_rep, _ = rel_err_rows(g["y_rep"][:R], y_rep_ref)
+    assert err_rep.max() <= tol, f"Y_rep max row rel err {err_rep.max():.3g} (row {int(err_rep.argmax())})"
+    dropped = (o.slot_pos < 0).all(axis=1)
+    assert np.all(g["y"][dropped] == 0), "fully dropped tokens must be zero"
+    err, _ = rel_err_rows(g["y"], y_ref)
+    assert err.max() <= tol, f"y max row rel err {err.max():.3g}"
+    print(f"[all rows] {R} representatives, {int((~dropped).sum())} tokens with a kept slot, "
+          f"{int(dropped.sum())} fully dropped; max row rel err Y_rep {err_rep.max():.3g}, y {err.max():.3g}",
+          flush=True)
 
 
 def assert_clique_union(inp, o):
@@ -104,8 +79,8 @@ def assert_clique_union(inp, o):
         assert np.array_equal(o.rep_of_pos[lo:hi], want), f"bucket {e} is not a clique union"
 
 
-# The fp64 oracle's Gram over the largest workload takes tens of seconds on
-# the host, so these tests get longer limits than the per-test default.
+# The fp64 oracle's Gram and expert FFN over the largest workloads take tens
+# of seconds on the host, so these tests get longer limits than the default.
 @pytest.mark.parametrize("name", [
     pytest.param("c2", marks=pytest.mark.timeout(300)),
     pytest.param("c3", marks=pytest.mark.timeout(600)),
@@ -118,12 +93,12 @@ def test_full_size_layer(name):
     dev = upload(inp)
     g = run_layer(inp, dev, cfg.h)
     o = run_oracle_indices(inp, cfg.h)
+    check_margins(inp, o.logits, o.perm_token, o.offsets)
     assert_route_equal(g, o)
     assert_condense_equal(g, o)
     assert_clique_union(inp, o)
-    tokens = sample_tokens(o, cfg.T, seed=0)
-    rows, y_sub, y_ref = sampled_expected(inp, o, tokens)
-    assert_sampled_close(g, inp, tokens, rows, y_sub, y_ref)
+    y_rep_ref, y_ref = full_expected(inp, o)
+    assert_all_rows_close(g, inp, o, y_rep_ref, y_ref)
 
 
 def run_oracle_indices(inp, h):
@@ -132,7 +107,7 @@ def run_oracle_indices(inp, h):
                        capacity_factor=cfg.capacity_factor, with_ffn=False)
 
 
-@pytest.mark.timeout(400)
+@pytest.mark.timeout(900)
 def test_full_size_c4_threshold_sweep():
     inp = G.make_inputs("c4", seed=0)
     cfg = inp.cfg
@@ -146,9 +121,9 @@ def test_full_size_c4_threshold_sweep():
         assert_condense_equal(g, o)
         assert o.rep_offsets[-1] == o.offsets[-1], "i.i.d. tokens should not merge"
         if ref is None:
-            tokens = sample_tokens(o, cfg.T, seed=0)
-            ref = (tokens,) + sampled_expected(inp, o, tokens)
-        assert_sampled_close(g, inp, *ref)
+            check_margins(inp, o.logits, o.perm_token, o.offsets)
+            ref = full_expected(inp, o)     # nothing merges: the same at every threshold
+        assert_all_rows_close(g, inp, o, *ref)
 
 
 @pytest.mark.timeout(300)
