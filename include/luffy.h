@@ -179,6 +179,58 @@ int luffy_condense(const void* x, int T, int d, int dtype,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * luffy_condense_history - luffy_condense with the historical similarity of
+ * Sec. 5.1 step 2, for a stack of MoE blocks over the same tokens.
+ *
+ * The weight of a pair of tokens in one bucket is 1 when the pair's weight in
+ * the previous block was above S1, 0 when it was below S2 (S1 first when both
+ * hold), and the cosine otherwise (in particular when the two tokens did not
+ * share a bucket in the previous block, or there is no previous block).  An
+ * edge joins the pair when its weight is >= threshold; selection and
+ * compaction are those of luffy_condense.
+ *
+ *   x ... inv_norm, max_bucket, threshold  as for luffy_condense
+ *   slot_pos   [T, k] int32, device (luffy_route's): needed with hist_out
+ *   hist_in    record left by the previous block (a luffy_condense_history
+ *              call with the same T, E, k and max_bucket), or NULL for the
+ *              first block (every pair computed).  A record from another
+ *              shape, or one whose writer hit an oversized bucket, counts as
+ *              empty.
+ *   hist_out   record this block leaves for the next one, or NULL; it holds
+ *              this block's weight classes (w > S1, w < S2) of every pair of
+ *              every bucket, so the next block must use the same S1 and S2.
+ *              Must not alias hist_in.  Records are luffy_history_size(T, E,
+ *              k, max_bucket) bytes of device memory, 256-byte aligned,
+ *              written entirely by the call.
+ *   S1, S2     the two thresholds of the rule above (not NaN)
+ *   stats      [4] uint64, device, or NULL: pairs (a < b of one bucket) the
+ *              record left undecided, pairs it decided, 256 x 256 similarity
+ *              tiles computed and tiles skipped because every pair in them
+ *              was decided (bf16; float32 computes every tile)
+ *   workspace  luffy_condense_history_workspace_size(T, d, E, k, max_bucket)
+ * Record layout (for inspection; sections in this order, each starting at a
+ * multiple of 256 bytes): int32 info[8] (a format tag, T, E, k, max_bucket);
+ * int32 slot_pos[T*k]; int32 offsets[E+1]; int64 word_off[E+1]; uint64
+ * hi[W]; uint64 lo[W], W = T*k*ceil(max_bucket/64).  Bit c % 64 of word
+ * word_off[e] + a*ceil(n_e/64) + c/64 of hi (lo) is the class w > S1
+ * (w < S2) of positions a and c of bucket e, n_e its size.
+ * With a hist_in, returns LUFFY_E_UNSUPPORTED for max_bucket above 131072
+ * (k = 2) or 262144 (k = 1).
+ * ---------------------------------------------------------------------- */
+size_t luffy_history_size(int T, int E, int k, int max_bucket);
+size_t luffy_condense_history_workspace_size(int T, int d, int E, int k, int max_bucket);
+int luffy_condense_history(const void* x, int T, int d, int dtype,
+                           const int32_t* perm_token, const int32_t* offsets,
+                           const int32_t* slot_pos, int E, int k, int max_bucket,
+                           float threshold, const void* hist_in, void* hist_out,
+                           float S1, float S2,
+                           int32_t* rep_of_pos, int32_t* rep_row,
+                           int32_t* rep_offsets, int32_t* rep_token,
+                           void* x_rep, int32_t* degree, const float* inv_norm,
+                           unsigned long long* stats,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * luffy_expert_ffn - expert FFN on the representatives only (Sec. 2.1: an
  * expert is an FFN; Sec. 3: only one token of a similar group goes through
  * the expert).
@@ -296,8 +348,9 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
- * Kernel names: gate, slot_scan, slot_scatter, norm, gram,
- * greedy_round, greedy_finish, claim, rep_local, rep_finalize, gather,
+ * Kernel names: gate, slot_scan, slot_scatter, norm, gram, hist_gather,
+ * hist_header, greedy_round, greedy_finish, claim, rep_local, rep_finalize,
+ * gather,
  * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
  * bwd_z, bwd_act, bwd_da, bwd_dx, bwd_dx_reduce, bwd_gather, bwd_dw2,
  * bwd_dw1.

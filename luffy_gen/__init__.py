@@ -47,7 +47,7 @@ import numpy as np
 
 __all__ = [
     "LayerConfig", "CONFIGS", "config", "Inputs", "make_inputs",
-    "round_bf16", "bf16_bits", "gate_bias",
+    "round_bf16", "bf16_bits", "gate_bias", "make_stack",
 ]
 
 
@@ -272,3 +272,72 @@ def make_inputs(cfg, seed: int = 0, *, weights: bool = True,
             w2 = round_bf16(w2, inplace=True)
     return Inputs(cfg=cfg, seed=seed, x=x, w_g=w_g, b_g=gate_bias(cfg),
                   w1=w1, w2=w2, centre_id=cid, planted=planted)
+
+
+def make_stack(cfg, blocks: int, seed: int = 0, *, token_drift: float = 1.0, gate_drift: float = 0.0,
+               mix_fraction: float = 0.0, weights: bool = False, **overrides) -> list:
+    """Inputs of a stack of MoE blocks over the same tokens (token ids are
+    shared by every block), for the historical similarity of Sec. 5.1 step 2.
+
+    The paper observes that pairs that are very similar or very dissimilar in
+    one block stay so in the next; these inputs keep each token's centre for
+    the whole stack and redraw what varies from block to block.
+
+    Draw order (numpy PCG64 seeded with [seed, 7]):
+      1. centres ~ N(0,1) [n_c, d], centre ids ~ U{0..n_c-1} [T]
+      2. mixed tokens: each token is mixed with probability mix_fraction
+         (U[0,1) [T] < mix_fraction), second centre ids ~ U{0..n_c-1} [T];
+         a mixed token's base is (c_id + c_id2) / sqrt(2) (cosine about
+         0.71 with a plain token of either centre), a plain token's c_id
+      3. gate weights of block 0: w_scale * N(0,1) [E, d]
+      4. per block b: noise N(0,1) [T, d]; x_b = base + sigma * noise for
+         b = 0, x_b = x_{b-1} + token_drift * sigma * noise after it
+         (token_drift = 1: a fresh draw of the same size each block);
+         gate weights W_b = W_{b-1} + gate_drift * w_scale * N(0,1) [E, d]
+         for b >= 1
+      5. with weights: W1, W2 per block as in make_inputs
+    bf16 workloads round x_b and the weights to bf16 after the draws (the
+    drift is applied to the unrounded values).  The gate bias is the
+    configuration's.  Returns one Inputs per block."""
+    if isinstance(cfg, str):
+        cfg = config(cfg)
+    if overrides:
+        cfg = cfg.replace(**overrides)
+    if cfg.n_centres <= 0:
+        raise ValueError("make_stack needs a clustered workload (n_centres > 0)")
+    rng = np.random.default_rng([seed, 7])
+    T, d, E = cfg.T, cfg.d, cfg.E
+    centres = _normal(rng, (cfg.n_centres, d), 1.0)
+    cid = rng.integers(0, cfg.n_centres, size=T, dtype=np.int64)
+    mixed = rng.random(T) < mix_fraction
+    cid2 = rng.integers(0, cfg.n_centres, size=T, dtype=np.int64)
+    base = centres[cid]
+    base[mixed] = (centres[cid[mixed]] + centres[cid2[mixed]]) * np.float32(1.0 / math.sqrt(2.0))
+    del centres
+    w_scale = cfg.w_scale if cfg.w_scale > 0 else 1.0 / math.sqrt(d)
+    w_g = _normal(rng, (E, d), w_scale)
+    bias = gate_bias(cfg)
+    out = []
+    x = None
+    for b in range(blocks):
+        noise = _normal(rng, (T, d), cfg.sigma)
+        if b == 0:
+            x = base + noise
+        else:
+            x = x + np.float32(token_drift) * noise
+            w_g = w_g + _normal(rng, (E, d), gate_drift * w_scale)
+        w1 = w2 = None
+        if weights:
+            w1 = _normal(rng, (E, cfg.d_ff, d), 0.02)
+            w2 = _normal(rng, (E, d, cfg.d_ff), 0.02)
+        xb, wgb = x.copy(), w_g.copy()
+        if cfg.dtype == "bf16":
+            xb = round_bf16(xb, inplace=True)
+            wgb = round_bf16(wgb, inplace=True)
+            if weights:
+                w1 = round_bf16(w1, inplace=True)
+                w2 = round_bf16(w2, inplace=True)
+        cid_b = np.where(mixed, -1, cid)     # centre of plain tokens, -1 for mixed ones
+        out.append(Inputs(cfg=cfg, seed=seed, x=xb, w_g=wgb, b_g=bias, w1=w1, w2=w2, centre_id=cid_b,
+                          planted=None))
+    return out

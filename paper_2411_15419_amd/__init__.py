@@ -22,7 +22,8 @@ __all__ = [
     "expert_ffn_workspace_size", "capacity", "MoELayer", "LIB_PATH", "profile_kernel",
     "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
     "luffy_combine_backward", "combine_backward_workspace_size", "luffy_expert_ffn_backward",
-    "expert_ffn_backward_workspace_size",
+    "expert_ffn_backward_workspace_size", "luffy_condense_history", "history_size",
+    "condense_history_workspace_size", "MoEStack",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
@@ -47,6 +48,11 @@ _SIGS = {
     "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
                                 _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "luffy_history_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
+    "luffy_condense_history_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
+    "luffy_condense_history": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                        _c_float, _vp, _vp, _c_float, _c_float, _vp, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, _vp, _vp, _c_size, _vp]),
     "luffy_expert_ffn_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "luffy_expert_ffn": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                                   _c_int, _c_int, _vp, _vp, _c_size, _vp]),
@@ -167,6 +173,30 @@ def luffy_condense(x, perm_token, offsets, k, max_bucket, threshold, rep_of_pos,
                               _p(rep_offsets), _p(rep_token), _p(x_rep), _p(degree),
                               _p(inv_norm), _p(workspace), workspace.numel(), _stream(stream)),
            "luffy_condense")
+
+
+def history_size(T: int, E: int, k: int, max_bucket: int) -> int:
+    return int(load_library().luffy_history_size(T, E, k, max_bucket))
+
+
+def condense_history_workspace_size(T: int, d: int, E: int, k: int, max_bucket: int) -> int:
+    return int(load_library().luffy_condense_history_workspace_size(T, d, E, k, max_bucket))
+
+
+def luffy_condense_history(x, perm_token, offsets, slot_pos, k, max_bucket, threshold, hist_in, hist_out, S1, S2,
+                           rep_of_pos, rep_row, rep_offsets, rep_token, x_rep, degree, stats, workspace,
+                           stream=None, inv_norm=None):
+    """luffy_condense with the historical similarity of Sec. 5.1 step 2:
+    hist_in is the previous block's record (or None), hist_out receives this
+    block's (or None); stats (4 int64 or None) receives undecided pairs,
+    decided pairs, tiles computed and tiles skipped."""
+    T, d = x.shape
+    E = offsets.numel() - 1
+    _check(load_library().luffy_condense_history(
+        _p(x), T, d, _dtype_code(x), _p(perm_token), _p(offsets), _p(slot_pos), E, k, max_bucket,
+        float(threshold), _p(hist_in), _p(hist_out), float(S1), float(S2), _p(rep_of_pos), _p(rep_row),
+        _p(rep_offsets), _p(rep_token), _p(x_rep), _p(degree), _p(inv_norm), _p(stats), _p(workspace),
+        workspace.numel(), _stream(stream)), "luffy_condense_history")
 
 
 def luffy_expert_ffn(x, row_index, rep_offsets, w1, w2, act, max_rows, y_rep, workspace,
@@ -312,7 +342,8 @@ class MoELayer:
 
     def __init__(self, w_gate, b_gate, w1, w2, *, k: int, act: str, threshold: float,
                  capacity_factor: float = 0.0, T: int, keep_degree: bool = True,
-                 gather_x_rep: bool = False, norms_from_route: bool = True):
+                 gather_x_rep: bool = False, norms_from_route: bool = True,
+                 history: Optional[tuple] = None):
         self.w_gate, self.b_gate, self.w1, self.w2 = w_gate, b_gate, w1, w2
         self.k, self.act, self.h, self.cf = k, act, threshold, capacity_factor
         self.E, self.d_ff, self.d = w1.shape
@@ -323,6 +354,9 @@ class MoELayer:
         S = T * k
         C = capacity(T, k, self.E, capacity_factor)
         self.max_bucket = min(T, C) if C > 0 else T
+        # history = (S1, S2): condense with the historical similarity of the
+        # previous block's record and leave this block's in self.record
+        self.history = history
         i32 = dict(dtype=torch.int32, device=dev)
         self.buf = LayerBuffers(
             topk_idx=torch.empty(T, k, **i32),
@@ -340,24 +374,36 @@ class MoELayer:
             y=torch.empty(T, self.d, dtype=self.dtype, device=dev),
             inv_norm=torch.empty(T, dtype=torch.float32, device=dev),
             ws_route=_workspace(route_workspace_size(T, self.E, k), dev),
-            ws_condense=_workspace(condense_workspace_size(T, self.d, self.E, k,
-                                                           self.max_bucket), dev),
+            ws_condense=_workspace((condense_history_workspace_size if history else condense_workspace_size)(
+                T, self.d, self.E, k, self.max_bucket), dev),
             ws_ffn=_workspace(expert_ffn_workspace_size(
                 S, self.E, self.d_ff, LUFFY_BF16 if self.dtype == torch.bfloat16 else LUFFY_F32),
                 dev),
         )
+        if history:
+            self.record = _workspace(history_size(T, self.E, k, self.max_bucket), dev)
+            self.hist_stats = torch.zeros(4, dtype=torch.int64, device=dev)
 
     def route(self, x, stream=None):
         b = self.buf
         luffy_route(x, self.w_gate, self.b_gate, self.k, self.cf, b.topk_idx, b.topk_gate,
                     b.slot_pos, b.perm_token, b.offsets, b.ws_route, stream, inv_norm=b.inv_norm)
 
-    def condense(self, x, stream=None, threshold=None):
+    def condense(self, x, stream=None, threshold=None, hist_in=None):
         b = self.buf
         h = self.h if threshold is None else threshold
-        luffy_condense(x, b.perm_token, b.offsets, self.k, self.max_bucket, h, b.rep_of_pos,
-                       b.rep_row, b.rep_offsets, b.rep_token, b.x_rep, b.degree, b.ws_condense,
-                       stream, inv_norm=b.inv_norm if self.norms_from_route else None)
+        inv = b.inv_norm if self.norms_from_route else None
+        if self.history:
+            S1, S2 = self.history
+            luffy_condense_history(x, b.perm_token, b.offsets, b.slot_pos, self.k, self.max_bucket, h, hist_in,
+                                   self.record, S1, S2, b.rep_of_pos, b.rep_row, b.rep_offsets, b.rep_token,
+                                   b.x_rep, b.degree, self.hist_stats, b.ws_condense, stream, inv_norm=inv)
+        else:
+            if hist_in is not None:
+                raise LuffyError("MoELayer: hist_in needs a layer built with history=(S1, S2)")
+            luffy_condense(x, b.perm_token, b.offsets, self.k, self.max_bucket, h, b.rep_of_pos,
+                           b.rep_row, b.rep_offsets, b.rep_token, b.x_rep, b.degree, b.ws_condense,
+                           stream, inv_norm=inv)
 
     def expert_ffn(self, x, stream=None):
         b = self.buf
@@ -406,11 +452,40 @@ class MoELayer:
                                   g["dx_rep"], g["dw1"], g["dw2"], g["ws_f"], stream)
         return g["dgate"], g["dx_rep"], g["dw1"], g["dw2"]
 
-    def __call__(self, x, stream=None, threshold=None):
+    def __call__(self, x, stream=None, threshold=None, hist_in=None):
         if x.shape != (self.T, self.d) or x.dtype != self.dtype:
             raise LuffyError(f"x must be [{self.T}, {self.d}] {self.dtype}")
         self.route(x, stream)
-        self.condense(x, stream, threshold)
+        self.condense(x, stream, threshold, hist_in)
         self.expert_ffn(x, stream)
         self.combine(stream)
         return self.buf.y
+
+
+class MoEStack:
+    """Consecutive MoE blocks over the same tokens, each condensing with the
+    historical similarity of the block before it (Sec. 5.1 step 2): block b
+    reads block b-1's record (block 0 computes every pair) and leaves its
+    own.  Each block takes its own input (the caller's model computes block
+    b's input from block b-1's output)."""
+
+    def __init__(self, layers):
+        if not layers or any(not L.history for L in layers):
+            raise LuffyError("MoEStack: every layer needs history=(S1, S2)")
+        self.layers = list(layers)
+
+    def __call__(self, xs, stream=None, threshold=None, ffn=True):
+        """Runs every block on its input xs[b]; returns the blocks' outputs
+        (with ffn=False only route and condense run, and nothing is
+        returned)."""
+        prev = None
+        outs = []
+        for layer, x in zip(self.layers, xs):
+            layer.route(x, stream)
+            layer.condense(x, stream, threshold, prev)
+            if ffn:
+                layer.expert_ffn(x, stream)
+                layer.combine(stream)
+                outs.append(layer.buf.y)
+            prev = layer.record
+        return outs if ffn else None

@@ -108,9 +108,11 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
                                                    unsigned long long* __restrict__ claim,
                                                    const int32_t* __restrict__ offsets, int E, int max_bucket,
                                                    int tile, long long cap_words, int32_t* __restrict__ tile_off,
-                                                   long long* __restrict__ bm_off, int* __restrict__ err) {
+                                                   long long* __restrict__ bm_off, int* __restrict__ err,
+                                                   unsigned long long* __restrict__ stats) {
   if (blockIdx.x == 0 && threadIdx.x < 64)
     gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
+  if (stats && blockIdx.x == 0 && threadIdx.x >= 64 && threadIdx.x < 68) stats[threadIdx.x - 64] = 0ull;
   // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
@@ -479,6 +481,590 @@ __global__ __launch_bounds__(256) void gram_kernel_f32(
   }
 }
 
+// ------------------------------------------------------------ history
+// Historical similarity (Sec. 5.1 step 2): a pair of tokens whose weight in
+// the previous block was above S1 takes weight 1 here, one below S2 takes
+// weight 0, and only the other pairs use their cosine.  A block leaves the
+// next one a record of its own weights as two bit classes per pair of
+// positions of one bucket, in the layout of the adjacency bitmask:
+// hi (weight > S1) and lo (weight < S2), with hi taking precedence.  The
+// record also keeps the block's token -> position map and bucket layout, so
+// the next block, whose buckets differ, can find a pair (t, u) in it: the
+// pair is decided when t and u shared a bucket there.
+constexpr int kHistMagic = 0x4C594831;   // record format tag
+
+struct HistRec {
+  int32_t* info;        // magic, T, E, k, max_bucket
+  int32_t* slot_pos;    // [T*k] position of slot (t, j) in the writing block, -1 if dropped
+  int32_t* offsets;     // [E+1] its buckets
+  long long* word_off;  // [E+1] first word of bucket e in hi and lo
+  uint64_t* hi;         // [cap_words]
+  uint64_t* lo;         // [cap_words]
+};
+
+HistRec carve_hist(Carver& c, int T, int E, int k, int max_bucket) {
+  HistRec h;
+  const long long S = static_cast<long long>(T) * k;
+  const long long cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
+  h.info = c.take<int32_t>(8);
+  h.slot_pos = c.take<int32_t>(static_cast<size_t>(S));
+  h.offsets = c.take<int32_t>(E + 1);
+  h.word_off = c.take<long long>(E + 1);
+  h.hi = c.take<uint64_t>(static_cast<size_t>(cap_words));
+  h.lo = c.take<uint64_t>(static_cast<size_t>(cap_words));
+  return h;
+}
+
+// Rows of one bucket per gather block (at most; fewer when a previous
+// block's rows do not fit the 64 KB of row images).
+constexpr int kGatherRowsMax = 4;
+constexpr int kGatherLdsBytes = 64 * 1024;
+
+// Header of the record a block leaves: format, sizes, the token -> position
+// map, bucket offsets and word offsets (after the layout).  A layout error
+// (a bucket larger than max_bucket) leaves the record marked invalid, which
+// makes the next block compute every pair.
+__global__ __launch_bounds__(256) void hist_header_kernel(const int32_t* __restrict__ slot_pos, int T, int k,
+                                                          const int32_t* __restrict__ offsets, int E, int max_bucket,
+                                                          const long long* __restrict__ bm_off,
+                                                          const int* __restrict__ err, HistRec out) {
+  const long long S = static_cast<long long>(T) * k;
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < S; i += gridDim.x * 256ll) out.slot_pos[i] = slot_pos[i];
+  if (blockIdx.x == 0) {
+    if (threadIdx.x <= static_cast<unsigned>(E)) {
+      out.offsets[threadIdx.x] = offsets[threadIdx.x];
+      out.word_off[threadIdx.x] = bm_off[threadIdx.x];
+    }
+    if (threadIdx.x == 0) {
+      out.info[0] = *err ? 0 : kHistMagic;
+      out.info[1] = T;
+      out.info[2] = E;
+      out.info[3] = k;
+      out.info[4] = max_bucket;
+    }
+  }
+}
+
+// The previous block's classes of every pair of this block's buckets, in
+// this block's bitmask layout: rb_hi / rb_lo bit c of row a of bucket e is
+// set when tokens perm_token[lo+a] and perm_token[lo+c] shared a bucket in
+// the previous block with class hi / lo there.  One block per G rows of one
+// bucket (G = rows): it copies the previous rows of its G tokens (one per
+// kept slot, hi and lo words interleaved) into LDS, then walks the bucket's
+// columns, one per lane, looking each column token's previous positions up.
+// A record that does not match (T, E, k, max_bucket) counts as empty.
+template <int K>
+__global__ __launch_bounds__(256) void hist_gather_kernel(const int32_t* __restrict__ offsets, int E,
+                                                          const int32_t* __restrict__ perm_token,
+                                                          const long long* __restrict__ bm_off,
+                                                          const int* __restrict__ err, HistRec in, int T,
+                                                          int max_bucket, int G, uint64_t* __restrict__ rb_hi,
+                                                          uint64_t* __restrict__ rb_lo) {
+  extern __shared__ uint64_t img[];                 // [G][K][Wp][2]
+  __shared__ int poff[kMaxExperts + 1];              // previous block's bucket offsets
+  __shared__ int rinfo[kGatherRowsMax][K][2];        // previous bucket, local row (-1: none)
+  __shared__ int tile_e, tile_a0, tile_rows, rec_ok;
+  if (*err) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int Wp = (max_bucket + 63) / 64;
+  if (w == 0) {
+    // this block's bucket and first row: lane e holds bucket e's row groups
+    const int n = lane < E ? offsets[lane + 1] - offsets[lane] : 0;
+    const int g = (n + G - 1) / G;
+    int incl = g;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += v;
+    }
+    const int b = blockIdx.x;
+    const int e = __popcll(__ballot(lane < E && incl <= b));
+    const int es = e < E ? e : 0;
+    const int excl = __shfl(incl - g, es, 64);
+    const int ne = __shfl(n, es, 64);
+    if (lane == 0) {
+      tile_e = e < E ? e : -1;
+      tile_a0 = (b - excl) * G;
+      tile_rows = min(G, ne - tile_a0);
+      rec_ok = in.info[0] == kHistMagic && in.info[1] == T && in.info[2] == E && in.info[3] == K &&
+               in.info[4] == max_bucket;
+    }
+  }
+  __syncthreads();
+  const int e = tile_e;
+  if (e < 0) return;
+  const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
+  const int a0 = tile_a0, rows = tile_rows;
+  const bool ok = rec_ok;
+  if (ok && tid <= E) poff[tid] = in.offsets[tid];
+  __syncthreads();
+  if (tid < kGatherRowsMax * K) {
+    const int i = tid / K, j = tid % K;
+    int pe = -1, pl = 0;
+    if (ok && i < rows) {
+      const int t = perm_token[lo + a0 + i];
+      const int p = in.slot_pos[static_cast<size_t>(t) * K + j];
+      if (p >= 0) {
+        pe = bucket_of(poff, E, p);
+        pl = p - poff[pe];
+      }
+    }
+    rinfo[i][j][0] = pe;
+    rinfo[i][j][1] = pl;
+  }
+  __syncthreads();
+  // row images: previous row (hi, lo) of every kept slot of the G tokens
+  for (int i = 0; i < rows; ++i)
+    for (int j = 0; j < K; ++j) {
+      const int pe = rinfo[i][j][0];
+      if (pe < 0) continue;
+      const int np = poff[pe + 1] - poff[pe], Wq = (np + 63) / 64;
+      const long long base = in.word_off[pe] + static_cast<long long>(rinfo[i][j][1]) * Wq;
+      uint64_t* dst = img + (static_cast<size_t>(i) * K + j) * Wp * 2;
+      for (int q = tid; q < Wq; q += 256) {
+        dst[2 * q] = in.hi[base + q];
+        dst[2 * q + 1] = in.lo[base + q];
+      }
+    }
+  __syncthreads();
+  // columns, one per lane, 256 at a time; wave w owns words (c0 + 64 w) / 64
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    const int c = c0 + tid;
+    int qe[K], ql[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      qe[j] = -1;
+      ql[j] = 0;
+    }
+    if (ok && c < n) {
+      const int u = perm_token[lo + c];
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        const int q = in.slot_pos[static_cast<size_t>(u) * K + j];
+        if (q >= 0) {
+          qe[j] = bucket_of(poff, E, q);
+          ql[j] = q - poff[qe[j]];
+        }
+      }
+    }
+    for (int i = 0; i < rows; ++i) {
+      bool bh = false, bl = false, found = false;
+#pragma unroll
+      for (int jr = 0; jr < K; ++jr) {
+        const int pe = rinfo[i][jr][0];
+#pragma unroll
+        for (int jc = 0; jc < K; ++jc) {
+          if (!found && pe >= 0 && qe[jc] == pe) {
+            const uint64_t* im = img + (static_cast<size_t>(i) * K + jr) * Wp * 2;
+            const int q = ql[jc];
+            bh = (im[2 * (q >> 6)] >> (q & 63)) & 1ull;
+            bl = (im[2 * (q >> 6) + 1] >> (q & 63)) & 1ull;
+            found = true;
+          }
+        }
+      }
+      const uint64_t mh = __ballot(bh), ml = __ballot(bl);
+      const int wd = (c0 >> 6) + w;
+      if (lane == 0 && wd < W) {
+        const long long o = bm_off[e] + static_cast<long long>(a0 + i) * W + wd;
+        rb_hi[o] = mh;
+        rb_lo[o] = ml;
+      }
+    }
+  }
+}
+
+// Constants of a block's pair weights: a decided pair's weight is 1 or 0,
+// which gives its edge (w >= h) and its classes for the next block
+// (w > S1, w < S2) without a cosine.
+struct HistParams {
+  float h, S1, S2;
+  uint64_t* out_hi;   // record words of this block (nullptr: no record)
+  uint64_t* out_lo;
+  const uint64_t* rb_hi;   // previous classes in this block's layout (nullptr: none)
+  const uint64_t* rb_lo;
+  unsigned long long* stats;   // undecided pairs, decided pairs, tiles computed, tiles skipped
+};
+
+// Words of one row piece from its (hi, lo) previous classes, for a tile
+// whose pairs are all decided: edge, class hi and class lo of every pair
+// under the valid mask vm.
+__device__ __forceinline__ void decided_words(uint64_t hi, uint64_t lo, uint64_t vm, const HistParams& hp,
+                                              uint64_t& edge, uint64_t& rh, uint64_t& rl) {
+  const uint64_t one = hi & vm, zero = lo & ~hi & vm;
+  edge = (1.0f >= hp.h ? one : 0ull) | (0.0f >= hp.h ? zero : 0ull);
+  rh = (1.0f > hp.S1 ? one : 0ull) | (0.0f > hp.S1 ? zero : 0ull);
+  rl = (1.0f < hp.S2 ? one : 0ull) | (0.0f < hp.S2 ? zero : 0ull);
+}
+
+// Columns of word wd (global word index) of a row that are pairs inside the
+// bucket: columns < n, the row's own position excluded.
+__device__ __forceinline__ uint64_t pair_mask(int row, int wd, int n) {
+  const int c0 = wd * 64;
+  uint64_t m = n - c0 >= 64 ? ~0ull : (n - c0 <= 0 ? 0ull : (1ull << (n - c0)) - 1);
+  if (row >= c0 && row < c0 + 64) m &= ~(1ull << (row - c0));
+  return m;
+}
+
+// bf16 similarity with history.  Per tile: the previous classes of its pairs
+// (rows of tile-row ti, words of tile-column tj) are read into LDS; the
+// undecided and decided pairs above the diagonal are counted; a tile whose
+// pairs are all decided skips the product and derives its words from the
+// classes alone (its mirror from the mirrored classes, which are the same
+// pairs); any other tile runs the product and takes, pair by pair, weight 1
+// or 0 where the previous block decided it and the cosine elsewhere.  The
+// record of this block (classes of every weight) is written beside the
+// adjacency words, direct and mirrored.
+template <bool HIN, bool HOUT>
+__global__ __launch_bounds__(GramGemm::THREADS) void gram_hist_kernel_bf16(
+    const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
+    const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, HistParams hp,
+    const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
+    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
+  using G = GramGemm;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
+  __shared__ __attribute__((aligned(16))) float inv_a[kTile];
+  __shared__ float inv_b[kTile];
+  __shared__ __attribute__((aligned(16))) uint64_t rbw[2][kTile][4];   // previous classes of the tile's pairs
+  __shared__ unsigned long long cnt_s[2];
+  constexpr int NM = HOUT ? 3 : 1;   // masks built per tile: edge, then class hi and class lo
+  // after the K loop the operand buffers hold the masks' pieces:
+  // dbits[m][row][32-column group], tbits[m][column][32-row group]
+  auto dbits = reinterpret_cast<uint32_t (*)[kTile][kTile / 32]>(lds);
+  auto tbits = reinterpret_cast<uint32_t (*)[kTile][kTile / 32]>(lds + NM * kTile * kTile / 8);
+  static_assert(2 * NM * kTile * kTile / 8 <= G::LDS_BYTES, "mask pieces fit the operand buffer");
+  if (*err) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = G::wave_m(w), wn = G::wave_n(w);
+  const int total = tile_off[E];
+  for (int tile = xcd_virtual_block(); tile < total; tile += gridDim.x) {
+    const TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
+    const int32_t* pt = perm_token + c.lo;
+    const long long bmo = bm_off[c.e];
+    const int nrow_a = c.n - c.ti * kTile, nrow_b = c.n - c.tj * kTile;
+    const bool same_tile = c.ti == c.tj;
+    // previous classes of the tile's pairs; count undecided / decided pairs
+    // above the diagonal
+    if (tid < 2) cnt_s[tid] = 0;
+    __syncthreads();
+    int undecided = 0;
+    {
+      unsigned long long nu = 0, nd = 0;
+      for (int i = tid; i < kTile * 4; i += G::THREADS) {
+        const int rl = i >> 2, ww = i & 3;
+        const int a = c.ti * kTile + rl, wd = 4 * c.tj + ww;
+        uint64_t h1 = 0, l1 = 0, vm = 0;
+        if (a < c.n && wd < c.W) {
+          vm = pair_mask(a, wd, c.n);
+          if constexpr (HIN) {
+            h1 = hp.rb_hi[bmo + static_cast<long long>(a) * c.W + wd];
+            l1 = hp.rb_lo[bmo + static_cast<long long>(a) * c.W + wd];
+          }
+        }
+        rbw[0][rl][ww] = h1;
+        rbw[1][rl][ww] = l1;
+        const uint64_t und = ~(h1 | l1) & vm;
+        undecided |= und != 0;
+        // pairs above the diagonal only (columns > row) on a diagonal tile
+        uint64_t up = ~0ull;
+        if (same_tile) {
+          const int c0 = wd * 64;
+          up = a < c0 ? ~0ull : (a >= c0 + 63 ? 0ull : ~((2ull << (a - c0)) - 1));
+        }
+        nu += __popcll(und & up);
+        nd += __popcll(vm & ~und & up);
+      }
+      if (nu) atomicAdd(&cnt_s[0], nu);
+      if (nd) atomicAdd(&cnt_s[1], nd);
+    }
+    undecided = __syncthreads_or(undecided);
+    if (tid == 0) {
+      atomicAdd(&hp.stats[0], cnt_s[0]);
+      atomicAdd(&hp.stats[1], cnt_s[1]);
+      atomicAdd(&hp.stats[undecided ? 2 : 3], 1ull);
+    }
+    if (!undecided) {
+      // every pair decided: no product; direct words from rbw, mirrored
+      // words from the mirrored classes (same pairs, read from rb)
+      for (int i = tid; i < 2 * kTile * 4; i += G::THREADS) {
+        const bool mirror = i >= kTile * 4;
+        if (mirror && same_tile) continue;
+        const int j = mirror ? i - kTile * 4 : i;
+        const int rl = j >> 2, ww = j & 3;
+        const int a = (mirror ? c.tj : c.ti) * kTile + rl, wd = 4 * (mirror ? c.ti : c.tj) + ww;
+        if (a >= c.n || wd >= c.W) continue;
+        const long long o = bmo + static_cast<long long>(a) * c.W + wd;
+        const uint64_t h1 = mirror ? hp.rb_hi[o] : rbw[0][rl][ww];
+        const uint64_t l1 = mirror ? hp.rb_lo[o] : rbw[1][rl][ww];
+        uint64_t edge, rh, rlw;
+        decided_words(h1, l1, pair_mask(a, wd, c.n), hp, edge, rh, rlw);
+        bitmask[o] = edge;
+        if constexpr (HOUT) {
+          hp.out_hi[o] = rh;
+          hp.out_lo[o] = rlw;
+        }
+        if (edge) atomicAdd(&deg[c.lo + a], __popcll(edge));
+      }
+      __syncthreads();
+      continue;
+    }
+    uint32_t poff[G::LP], qoff[G::LQ];
+#pragma unroll
+    for (int j = 0; j < G::LP; ++j)
+      poff[j] = static_cast<uint32_t>(pt[min(c.ti * kTile + G::load_row(j), c.n - 1)]) * d;
+#pragma unroll
+    for (int j = 0; j < G::LQ; ++j)
+      qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)]) * d;
+    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
+      if (i < kTile) inv_a[i] = inv_norm[pt[min(c.ti * kTile + i, c.n - 1)]];
+      else inv_b[i - kTile] = inv_norm[pt[min(c.tj * kTile + i - kTile, c.n - 1)]];
+    }
+    G::Acc acc;
+    G::zero(acc);
+    G::run(X, poff, X, qoff, d, nrow_a, nrow_b, lds, acc);  // ends with a barrier
+
+    // Epilogue as in gram_kernel_bf16, for NM predicates per pair:
+    //   weight w = 1 (class hi), 0 (class lo) or the cosine;
+    //   edge = w >= h; next classes w > S1, w < S2.
+    const int l31 = lane & 31, hi = lane >> 5;
+    const uint32_t* rbh32 = reinterpret_cast<const uint32_t*>(&rbw[0][0][0]);
+    const uint32_t* rbl32 = reinterpret_cast<const uint32_t*>(&rbw[1][0][0]);
+    const bool e1 = 1.0f >= hp.h, e0 = 0.0f >= hp.h;
+    const bool h1c = 1.0f > hp.S1, h0c = 0.0f > hp.S1, l1c = 1.0f < hp.S2, l0c = 0.0f < hp.S2;
+#pragma unroll
+    for (int fm = 0; fm < G::FM; ++fm) {
+      const int abase = wm * G::WTM + 32 * fm;
+      const float nan = __builtin_nanf("");
+      float ia[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int al0 = abase + 8 * q + 4 * hi;
+        const float4 f = *reinterpret_cast<const float4*>(&inv_a[al0]);
+        const float fv[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ia[4 * q + r] = al0 + r < nrow_a ? fv[r] : nan;
+      }
+#pragma unroll
+      for (int fn = 0; fn < G::FN; ++fn) {
+        const int bbase = wn * G::WTN + 32 * fn;
+        const int bl = bbase + l31;
+        const float ib = bl < nrow_b ? inv_b[bl] : nan;
+        const bool diag = same_tile && abase == bbase;   // wave-uniform
+        uint32_t colbits[NM], piece[NM];
+#pragma unroll
+        for (int m = 0; m < NM; ++m) colbits[m] = piece[m] = 0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int rv = 8 * (v >> 2) + (v & 3);
+          const int row = abase + rv + 4 * hi;
+          const bool hb = (rbh32[row * 8 + (bbase >> 5)] >> l31) & 1u;
+          const bool lb = (rbl32[row * 8 + (bbase >> 5)] >> l31) & 1u;
+          const float cs = acc[fm][fn][v] * ia[v] * ib;
+          const bool self = diag && rv + 4 * hi == l31;
+          bool pr[NM];
+          pr[0] = !self && (hb ? e1 : (lb ? e0 : cs >= hp.h));
+          if constexpr (HOUT) {
+            pr[1] = !self && (hb ? h1c : (lb ? h0c : cs > hp.S1));
+            pr[2] = !self && (hb ? l1c : (lb ? l0c : cs < hp.S2));
+          }
+#pragma unroll
+          for (int m = 0; m < NM; ++m) {
+            const uint64_t bm = __ballot(pr[m]);
+            piece[m] = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(bm)), rv, piece[m]);
+            piece[m] = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(bm >> 32)), rv + 4, piece[m]);
+            colbits[m] |= pr[m] ? 1u << rv : 0u;
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          colbits[m] <<= 4 * hi;
+          const uint32_t tv = colbits[m] | static_cast<uint32_t>(__shfl_xor(static_cast<int>(colbits[m]), 32, 64));
+          if (lane < 32) {
+            dbits[m][abase + l31][bbase >> 5] = piece[m];
+            tbits[m][bl][abase >> 5] = tv;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
+      const bool mirror = i >= kTile;
+      const int rl = mirror ? i - kTile : i;
+      const uint32_t* pcs = mirror ? tbits[0][rl] : dbits[0][rl];
+      int cnt = 0;
+#pragma unroll
+      for (int g = 0; g < kTile / 32; ++g) cnt += __popc(pcs[g]);
+      const int r = (mirror ? c.tj : c.ti) * kTile + rl;
+      if (cnt && r < c.n && (!mirror || !same_tile)) atomicAdd(&deg[c.lo + r], cnt);
+    }
+    for (int i = tid; i < kTile * 4; i += G::THREADS) {
+      const int rl = i >> 2, ww = i & 3;
+      const int a = c.ti * kTile + rl, wd = 4 * c.tj + ww;
+      const int bb = c.tj * kTile + rl, wt = 4 * c.ti + ww;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        uint64_t* dst = m == 0 ? bitmask : (m == 1 ? hp.out_hi : hp.out_lo);
+        const uint64_t dv = static_cast<uint64_t>(dbits[m][rl][2 * ww]) |
+                            (static_cast<uint64_t>(dbits[m][rl][2 * ww + 1]) << 32);
+        if (a < c.n && wd < c.W) dst[bmo + static_cast<long long>(a) * c.W + wd] = dv;
+        if (!same_tile) {
+          const uint64_t tv = static_cast<uint64_t>(tbits[m][rl][2 * ww]) |
+                              (static_cast<uint64_t>(tbits[m][rl][2 * ww + 1]) << 32);
+          if (bb < c.n && wt < c.W) dst[bmo + static_cast<long long>(bb) * c.W + wt] = tv;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// float32 similarity with history: the 64-row tiles of gram_kernel_f32, every
+// tile computed; each pair takes weight 1 or 0 where the previous block
+// decided it and its cosine elsewhere; the record words are written beside
+// the adjacency words.
+template <bool HIN, bool HOUT>
+__global__ __launch_bounds__(256) void gram_hist_kernel_f32(
+    const float* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
+    const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, HistParams hp,
+    const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
+    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
+  constexpr int KC = 16;
+  constexpr int NM = HOUT ? 3 : 1;
+  __shared__ float Ps[kTileF32][KC + 1];
+  __shared__ float Qs[kTileF32][KC + 1];
+  constexpr int MT = kTileF32 / 16;
+  __shared__ uint8_t pred[kTileF32][kTileF32];   // bit m: predicate m of the pair
+  __shared__ uint16_t dbits[NM][kTileF32][kGroupsF32];
+  __shared__ uint16_t tbits[NM][kTileF32][kGroupsF32];
+  __shared__ float inv_a[kTileF32], inv_b[kTileF32];
+  __shared__ uint64_t rbw[2][kTileF32];
+  if (*err) return;
+  const int tid = threadIdx.x;
+  const int rb = (tid >> 4) * MT, cb = (tid & 15) * MT;
+  const int total = tile_off[E];
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    const TileCoord c = decode_tile(tile, tile_off, offsets, E);
+    const int32_t* pt = perm_token + c.lo;
+    const long long bmo = bm_off[c.e];
+    if (tid < kTileF32) inv_a[tid] = inv_norm[pt[min(c.ti * kTileF32 + tid, c.n - 1)]];
+    else if (tid < 2 * kTileF32) inv_b[tid - kTileF32] = inv_norm[pt[min(c.tj * kTileF32 + tid - kTileF32, c.n - 1)]];
+    else if (tid < 3 * kTileF32) {
+      // previous classes: tile-row rows, word tj (64-column tiles are one word)
+      const int rl = tid - 2 * kTileF32, a = c.ti * kTileF32 + rl;
+      uint64_t h1 = 0, l1 = 0;
+      if constexpr (HIN) {
+        if (a < c.n) {
+          h1 = hp.rb_hi[bmo + static_cast<long long>(a) * c.W + c.tj];
+          l1 = hp.rb_lo[bmo + static_cast<long long>(a) * c.W + c.tj];
+        }
+      }
+      rbw[0][rl] = h1;
+      rbw[1][rl] = l1;
+    }
+    constexpr int PER = kTileF32 * KC / 256;
+    const int kk = tid % KC, r0 = tid / KC;
+    const float* pp[PER];
+    const float* qp[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int r = r0 + (256 / KC) * i;
+      pp[i] = X + static_cast<size_t>(pt[min(c.ti * kTileF32 + r, c.n - 1)]) * d + kk;
+      qp[i] = X + static_cast<size_t>(pt[min(c.tj * kTileF32 + r, c.n - 1)]) * d + kk;
+    }
+    float vp[PER], vq[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      vp[i] = pp[i][0];
+      vq[i] = qp[i][0];
+    }
+    float acc[MT][MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < MT; ++j) acc[i][j] = 0.f;
+    for (int k0 = 0; k0 < d; k0 += KC) {
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        Ps[r0 + (256 / KC) * i][kk] = vp[i];
+        Qs[r0 + (256 / KC) * i][kk] = vq[i];
+      }
+      __syncthreads();
+      if (k0 + KC < d) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          vp[i] = pp[i][k0 + KC];
+          vq[i] = qp[i][k0 + KC];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        float pa[MT], qb[MT];
+#pragma unroll
+        for (int i = 0; i < MT; ++i) pa[i] = Ps[rb + i][k];
+#pragma unroll
+        for (int j = 0; j < MT; ++j) qb[j] = Qs[cb + j][k];
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < MT; ++j) acc[i][j] = fmaf(pa[i], qb[j], acc[i][j]);
+      }
+    }
+    unsigned long long nu = 0, nd = 0;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < MT; ++j) {
+        const int a = c.ti * kTileF32 + rb + i, b = c.tj * kTileF32 + cb + j;
+        const bool pair = a < c.n && b < c.n && a != b;
+        const bool hb = (rbw[0][rb + i] >> (cb + j)) & 1ull, lb = (rbw[1][rb + i] >> (cb + j)) & 1ull;
+        const float cs = acc[i][j] * inv_a[rb + i] * inv_b[cb + j];
+        const float wv = hb ? 1.0f : (lb ? 0.0f : cs);
+        uint8_t p = 0;
+        if (pair) {
+          p |= wv >= hp.h ? 1 : 0;
+          p |= wv > hp.S1 ? 2 : 0;
+          p |= wv < hp.S2 ? 4 : 0;
+          if (a < b) {
+            if (hb || lb) ++nd;
+            else ++nu;
+          }
+        }
+        pred[rb + i][cb + j] = p;
+      }
+    if (nu) atomicAdd(&hp.stats[0], nu);
+    if (nd) atomicAdd(&hp.stats[1], nd);
+    if (tid == 0) atomicAdd(&hp.stats[2], 1ull);
+    __syncthreads();
+    for (int idx = tid; idx < NM * kTileF32 * kGroupsF32; idx += 256) {
+      const int m = idx / (kTileF32 * kGroupsF32), rem = idx % (kTileF32 * kGroupsF32);
+      const int r = rem / kGroupsF32, g = rem % kGroupsF32;
+      uint32_t dv = 0, tv = 0;
+      for (int bit = 0; bit < 16; ++bit) {
+        dv |= static_cast<uint32_t>((pred[r][16 * g + bit] >> m) & 1) << bit;
+        tv |= static_cast<uint32_t>((pred[16 * g + bit][r] >> m) & 1) << bit;
+      }
+      dbits[m][r][g] = static_cast<uint16_t>(dv);
+      tbits[m][r][g] = static_cast<uint16_t>(tv);
+    }
+    __syncthreads();
+    if (tid < 2 * kTileF32) {
+      const bool mirror = tid >= kTileF32;
+      const int rl = mirror ? tid - kTileF32 : tid;
+      int cnt = 0;
+      for (int g = 0; g < kGroupsF32; ++g) cnt += __popc(mirror ? tbits[0][rl][g] : dbits[0][rl][g]);
+      const int r = (mirror ? c.tj : c.ti) * kTileF32 + rl;
+      if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
+    }
+    write_tile_words(c, dbits[0], tbits[0], bitmask, bmo);
+    if constexpr (HOUT) {
+      write_tile_words(c, dbits[1], tbits[1], hp.out_hi, bmo);
+      write_tile_words(c, dbits[2], tbits[2], hp.out_lo, bmo);
+    }
+    __syncthreads();
+  }
+}
+
 // Decides position p if its neighbours allow it; returns true when p is
 // still undecided afterwards (uniform over the GW-lane group that visits p,
 // GW = 16 or 64, aligned inside the wave).  The group walks the adjacency
@@ -770,9 +1356,14 @@ struct CondenseWs {
   int32_t* bsum;
   uint64_t* bitmask;
   long long cap_words;
+  // history calls only: the previous block's classes in this block's
+  // layout, and the pair / tile counters when the caller passes none
+  uint64_t* rb_hi = nullptr;
+  uint64_t* rb_lo = nullptr;
+  unsigned long long* stats = nullptr;
 };
 
-CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket) {
+CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool history = false) {
   CondenseWs w;
   const long long S = static_cast<long long>(T) * k;
   w.inv_norm = c.take<float>(T);
@@ -786,7 +1377,27 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket) {
   w.bsum = c.take<int32_t>((S + 1023) / 1024 + 1);
   w.cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
   w.bitmask = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
+  if (history) {
+    w.rb_hi = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
+    w.rb_lo = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
+    w.stats = c.take<unsigned long long>(4);
+  }
   return w;
+}
+
+// Arguments of a call with historical similarity.
+struct HistCall {
+  const int32_t* slot_pos;   // this block's slot positions (for its record)
+  const void* in;            // previous block's record or nullptr
+  void* out;                 // this block's record or nullptr
+  float S1, S2;
+  unsigned long long* stats;
+};
+
+// Rows per gather block for a record of max_bucket (0: too large).
+int gather_rows(int k, int max_bucket) {
+  const long long per_row = static_cast<long long>(k) * ((max_bucket + 63) / 64) * 16;
+  return static_cast<int>(std::min<long long>(kGatherRowsMax, kGatherLdsBytes / std::max(per_row, 1ll)));
 }
 
 
@@ -794,6 +1405,129 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket) {
 }  // namespace luffy
 
 using namespace luffy;
+
+namespace {
+
+int condense_check(const char* fn, const void* x, int T, int d, int dtype, const int32_t* perm_token,
+                   const int32_t* offsets, int E, int k, int max_bucket, float threshold, const int32_t* rep_of_pos,
+                   const int32_t* rep_row, const int32_t* rep_offsets, const int32_t* rep_token) {
+  if (!x || !perm_token || !offsets || !rep_of_pos || !rep_row || !rep_offsets || !rep_token)
+    return fail(LUFFY_E_INVALID, "%s: null pointer argument", fn);
+  if (T <= 0 || d <= 0 || E <= 0 || max_bucket < 0)
+    return fail(LUFFY_E_INVALID, "%s: T=%d d=%d E=%d max_bucket=%d", fn, T, d, E, max_bucket);
+  if (k != 1 && k != 2) return fail(LUFFY_E_INVALID, "%s: k=%d must be 1 or 2", fn, k);
+  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16) return fail(LUFFY_E_INVALID, "%s: unknown dtype %d", fn, dtype);
+  if (threshold != threshold) return fail(LUFFY_E_INVALID, "%s: threshold is NaN", fn);
+  if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "%s: E=%d > %d", fn, E, kMaxExperts);
+  if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "%s: d=%d not a multiple of 64", fn, d);
+  if (d > 32768) return fail(LUFFY_E_UNSUPPORTED, "%s: d=%d > 32768", fn, d);
+  if (static_cast<long long>(T) * d * elem_bytes(dtype) > 0xFFFF0000ll)
+    return fail(LUFFY_E_UNSUPPORTED, "%s: x exceeds 4 GiB - 64 KiB", fn);
+  if (static_cast<long long>(T) * k > (1ll << 24)) return fail(LUFFY_E_UNSUPPORTED, "%s: T*k > 2^24", fn);
+  return LUFFY_OK;
+}
+
+// Every launch of a condense call; hc is null for a call without history.
+void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* perm_token, const int32_t* offsets,
+                      int E, int k, int max_bucket, float threshold, int32_t* rep_of_pos, int32_t* rep_row,
+                      int32_t* rep_offsets, int32_t* rep_token, void* x_rep, int32_t* degree,
+                      const float* inv_norm, const CondenseWs& ws, const HistCall* hc, hipStream_t s) {
+  const int S = T * k;
+  const bool bf16 = dtype == LUFFY_BF16;
+  unsigned long long* stats = hc ? (hc->stats ? hc->stats : ws.stats) : nullptr;
+  // norms from the caller when given (the gate pass already read x)
+  const float* inv_norm_use = inv_norm ? inv_norm : ws.inv_norm;
+  const int norm_blocks = inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
+  {
+    const int tile = bf16 ? kTile : kTileF32;
+#define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
+                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats
+    if (bf16) {
+      if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+      else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+    } else {
+      if (inv_norm) launch("norm", norm_kernel<false, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+      else launch("norm", norm_kernel<false, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+    }
+#undef LUFFY_NORM_ARGS
+  }
+  if (!hc) {
+    if (bf16)
+      launch("gram", gram_kernel_bf16, persistent_grid(), GramGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
+             d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask,
+             ws.deg);
+    else
+      launch("gram", gram_kernel_f32, 2 * persistent_grid(), 256, 0, s, static_cast<const float*>(x), d, perm_token,
+             offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg);
+  } else {
+    Carver cin(const_cast<void*>(hc->in)), cout(hc->out);
+    const HistRec rin = carve_hist(cin, T, E, k, max_bucket);
+    const HistRec rout = carve_hist(cout, T, E, k, max_bucket);
+    if (hc->in) {
+      const int G = gather_rows(k, max_bucket);
+      const size_t lds = static_cast<size_t>(G) * k * ((max_bucket + 63) / 64) * 16;
+      const int blocks = (S + G - 1) / G + E;
+      if (k == 1)
+        launch("hist_gather", hist_gather_kernel<1>, blocks, 256, lds, s, offsets, E, perm_token, ws.bm_off, ws.err,
+               rin, T, max_bucket, G, ws.rb_hi, ws.rb_lo);
+      else
+        launch("hist_gather", hist_gather_kernel<2>, blocks, 256, lds, s, offsets, E, perm_token, ws.bm_off, ws.err,
+               rin, T, max_bucket, G, ws.rb_hi, ws.rb_lo);
+    }
+    if (hc->out)
+      launch("hist_header", hist_header_kernel, std::max(1, std::min(1024, (S + 255) / 256)), 256, 0, s,
+             hc->slot_pos, T, k, offsets, E, max_bucket, ws.bm_off, ws.err, rout);
+    HistParams hp;
+    hp.h = threshold;
+    hp.S1 = hc->S1;
+    hp.S2 = hc->S2;
+    hp.out_hi = hc->out ? rout.hi : nullptr;
+    hp.out_lo = hc->out ? rout.lo : nullptr;
+    hp.rb_hi = hc->in ? ws.rb_hi : nullptr;
+    hp.rb_lo = hc->in ? ws.rb_lo : nullptr;
+    hp.stats = stats;
+    const bool hin = hc->in != nullptr, hout = hc->out != nullptr;
+#define LUFFY_GH_ARGS d, perm_token, offsets, E, inv_norm_use, hp, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg
+    if (bf16) {
+      const uint16_t* xb = static_cast<const uint16_t*>(x);
+      const int g = persistent_grid();
+      const int th = GramGemm::THREADS;
+      if (hin && hout) launch("gram", gram_hist_kernel_bf16<true, true>, g, th, 0, s, xb, LUFFY_GH_ARGS);
+      else if (hin) launch("gram", gram_hist_kernel_bf16<true, false>, g, th, 0, s, xb, LUFFY_GH_ARGS);
+      else if (hout) launch("gram", gram_hist_kernel_bf16<false, true>, g, th, 0, s, xb, LUFFY_GH_ARGS);
+      else launch("gram", gram_hist_kernel_bf16<false, false>, g, th, 0, s, xb, LUFFY_GH_ARGS);
+    } else {
+      const float* xf = static_cast<const float*>(x);
+      const int g = 2 * persistent_grid();
+      if (hin && hout) launch("gram", gram_hist_kernel_f32<true, true>, g, 256, 0, s, xf, LUFFY_GH_ARGS);
+      else if (hin) launch("gram", gram_hist_kernel_f32<true, false>, g, 256, 0, s, xf, LUFFY_GH_ARGS);
+      else if (hout) launch("gram", gram_hist_kernel_f32<false, true>, g, 256, 0, s, xf, LUFFY_GH_ARGS);
+      else launch("gram", gram_hist_kernel_f32<false, false>, g, 256, 0, s, xf, LUFFY_GH_ARGS);
+    }
+#undef LUFFY_GH_ARGS
+  }
+  const int wave_blocks = (S + 3) / 4;
+  const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
+  for (int r = 0; r < kGreedyGridRounds; ++r) {
+    launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
+           ws.deg, ws.state, r, degree);
+  }
+  launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+         ws.state);
+  launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+         ws.state, ws.claim);
+  const int pos_blocks = (S + 1023) / 1024;
+  launch("rep_local", rep_local_kernel, pos_blocks, 1024, 0, s, offsets, E, ws.err, ws.state, ws.claim, rep_of_pos,
+         ws.local, ws.bsum, S);
+  launch("rep_finalize", rep_finalize_kernel, pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s, offsets, E,
+         rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, S);
+  if (x_rep) {
+    launch("gather", gather_kernel, wave_blocks, 256, 0, s, static_cast<const uint8_t*>(x),
+           static_cast<size_t>(d) * elem_bytes(dtype), rep_offsets, E, rep_token, static_cast<uint8_t*>(x_rep));
+  }
+}
+
+}  // namespace
 
 extern "C" size_t luffy_condense_workspace_size(int T, int d, int E, int k, int max_bucket) {
   (void)d;
@@ -810,82 +1544,62 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
                               int32_t* rep_offsets, int32_t* rep_token,
                               void* x_rep, int32_t* degree, const float* inv_norm,
                               void* workspace, size_t workspace_bytes, void* stream) {
-  if (!x || !perm_token || !offsets || !rep_of_pos || !rep_row || !rep_offsets || !rep_token)
-    return fail(LUFFY_E_INVALID, "luffy_condense: null pointer argument");
-  if (T <= 0 || d <= 0 || E <= 0 || max_bucket < 0)
-    return fail(LUFFY_E_INVALID, "luffy_condense: T=%d d=%d E=%d max_bucket=%d", T, d, E, max_bucket);
-  if (k != 1 && k != 2) return fail(LUFFY_E_INVALID, "luffy_condense: k=%d must be 1 or 2", k);
-  if (dtype != LUFFY_F32 && dtype != LUFFY_BF16)
-    return fail(LUFFY_E_INVALID, "luffy_condense: unknown dtype %d", dtype);
-  if (threshold != threshold) return fail(LUFFY_E_INVALID, "luffy_condense: threshold is NaN");
-  if (E > kMaxExperts) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: E=%d > %d", E, kMaxExperts);
-  if (d % 64 != 0) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: d=%d not a multiple of 64", d);
-  if (d > 32768) return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: d=%d > 32768", d);
-  if (static_cast<long long>(T) * d * elem_bytes(dtype) > 0xFFFF0000ll)
-    return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: x exceeds 4 GiB - 64 KiB");
-  if (static_cast<long long>(T) * k > (1ll << 24))
-    return fail(LUFFY_E_UNSUPPORTED, "luffy_condense: T*k > 2^24");
+  const int st = condense_check("luffy_condense", x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold,
+                                rep_of_pos, rep_row, rep_offsets, rep_token);
+  if (st != LUFFY_OK) return st;
   const size_t need = luffy_condense_workspace_size(T, d, E, k, max_bucket);
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "luffy_condense: workspace needs %zu bytes, 256-aligned", need);
-
-  hipStream_t s = static_cast<hipStream_t>(stream);
   Carver c(workspace);
-  CondenseWs ws = carve_condense(c, T, E, k, max_bucket);
-  const int S = T * k;
-  const bool bf16 = dtype == LUFFY_BF16;
-
-  // norms from the caller when given (the gate pass already read x)
-  const float* inv_norm_use = inv_norm ? inv_norm : ws.inv_norm;
-  const int norm_blocks = inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
-  {
-    const int tile = bf16 ? kTile : kTileF32;
-#define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
-                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err
-    if (bf16) {
-      if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
-      else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
-    } else {
-      if (inv_norm) launch("norm", norm_kernel<false, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
-      else launch("norm", norm_kernel<false, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
-    }
-#undef LUFFY_NORM_ARGS
-  }
-  {
-    if (bf16)
-      launch("gram", gram_kernel_bf16, persistent_grid(), GramGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
-             d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask,
-             ws.deg);
-    else
-      launch("gram", gram_kernel_f32, 2 * persistent_grid(), 256, 0, s, static_cast<const float*>(x), d, perm_token,
-             offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg);
-  }
-  const int wave_blocks = (S + 3) / 4;
-  const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
-  for (int r = 0; r < kGreedyGridRounds; ++r) {
-    launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-           ws.deg, ws.state, r, degree);
-  }
-  {
-    launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-           ws.state);
-  }
-  {
-    launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-           ws.state, ws.claim);
-  }
-  const int pos_blocks = (S + 1023) / 1024;
-  {
-    launch("rep_local", rep_local_kernel, pos_blocks, 1024, 0, s, offsets, E, ws.err, ws.state, ws.claim,
-           rep_of_pos, ws.local, ws.bsum, S);
-  }
-  {
-    launch("rep_finalize", rep_finalize_kernel, pos_blocks, 1024, (pos_blocks + 1) * sizeof(int), s, offsets, E,
-           rep_of_pos, perm_token, ws.local, ws.bsum, rep_row, rep_token, rep_offsets, S);
-  }
-  if (x_rep) {
-    launch("gather", gather_kernel, wave_blocks, 256, 0, s, static_cast<const uint8_t*>(x),
-           static_cast<size_t>(d) * elem_bytes(dtype), rep_offsets, E, rep_token, static_cast<uint8_t*>(x_rep));
-  }
+  const CondenseWs ws = carve_condense(c, T, E, k, max_bucket);
+  condense_enqueue(x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold, rep_of_pos, rep_row,
+                   rep_offsets, rep_token, x_rep, degree, inv_norm, ws, nullptr, static_cast<hipStream_t>(stream));
   return check_launch("luffy_condense");
+}
+
+extern "C" size_t luffy_history_size(int T, int E, int k, int max_bucket) {
+  if (T <= 0 || E <= 0 || k <= 0 || max_bucket < 0) return 0;
+  Carver c(nullptr);
+  carve_hist(c, T, E, k, max_bucket);
+  return c.size();
+}
+
+extern "C" size_t luffy_condense_history_workspace_size(int T, int d, int E, int k, int max_bucket) {
+  (void)d;
+  if (T <= 0 || E <= 0 || k <= 0 || max_bucket < 0) return 0;
+  Carver c(nullptr);
+  carve_condense(c, T, E, k, max_bucket, true);
+  return c.size();
+}
+
+extern "C" int luffy_condense_history(const void* x, int T, int d, int dtype,
+                                      const int32_t* perm_token, const int32_t* offsets,
+                                      const int32_t* slot_pos, int E, int k, int max_bucket,
+                                      float threshold, const void* hist_in, void* hist_out,
+                                      float S1, float S2,
+                                      int32_t* rep_of_pos, int32_t* rep_row,
+                                      int32_t* rep_offsets, int32_t* rep_token,
+                                      void* x_rep, int32_t* degree, const float* inv_norm,
+                                      unsigned long long* stats,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  const char* fn = "luffy_condense_history";
+  const int st = condense_check(fn, x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold, rep_of_pos,
+                                rep_row, rep_offsets, rep_token);
+  if (st != LUFFY_OK) return st;
+  if (hist_out && !slot_pos) return fail(LUFFY_E_INVALID, "%s: hist_out needs slot_pos", fn);
+  if (S1 != S1 || S2 != S2) return fail(LUFFY_E_INVALID, "%s: S1 or S2 is NaN", fn);
+  if (hist_in && hist_in == hist_out) return fail(LUFFY_E_INVALID, "%s: hist_in and hist_out alias", fn);
+  if ((reinterpret_cast<uintptr_t>(hist_in) & 255u) || (reinterpret_cast<uintptr_t>(hist_out) & 255u))
+    return fail(LUFFY_E_INVALID, "%s: records must be 256-byte aligned", fn);
+  if (hist_in && gather_rows(k, max_bucket) < 1)
+    return fail(LUFFY_E_UNSUPPORTED, "%s: max_bucket=%d too large for a record", fn, max_bucket);
+  const size_t need = luffy_condense_history_workspace_size(T, d, E, k, max_bucket);
+  if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(LUFFY_E_WORKSPACE, "%s: workspace needs %zu bytes, 256-aligned", fn, need);
+  Carver c(workspace);
+  const CondenseWs ws = carve_condense(c, T, E, k, max_bucket, true);
+  HistCall hc{slot_pos, hist_in, hist_out, S1, S2, stats};
+  condense_enqueue(x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold, rep_of_pos, rep_row,
+                   rep_offsets, rep_token, x_rep, degree, inv_norm, ws, &hc, static_cast<hipStream_t>(stream));
+  return check_launch(fn);
 }

@@ -127,6 +127,46 @@ def test_invalid_arguments_rejected_on_host(lib):
     assert lib.luffy_expert_ffn_backward_workspace_size(8, 4, 64, 128, 0) == 0   # float32: none
 
 
+def test_history_record_layout(lib):
+    """luffy_history_size is the record layout the header documents:
+    sections info[8] int32, slot_pos[T*k] int32, offsets[E+1] int32,
+    word_off[E+1] int64, hi[W] and lo[W] uint64 with W = T*k*ceil(max_bucket/64),
+    each starting at a multiple of 256 bytes."""
+    def up(v):
+        return (v + 255) // 256 * 256
+    for T, E, k, mb in ((2048, 8, 2, 2048), (512, 4, 1, 512), (65536, 64, 1, 1024), (32768, 32, 2, 32768)):
+        W = T * k * ((mb + 63) // 64)
+        size = 0
+        for nbytes in (32, 4 * T * k, 4 * (E + 1), 8 * (E + 1), 8 * W, 8 * W):
+            size = up(size) + nbytes
+        assert lib.luffy_history_size(T, E, k, mb) == up(size), (T, E, k, mb)
+    assert lib.luffy_condense_history_workspace_size(2048, 256, 8, 2, 2048) > \
+        lib.luffy_condense_workspace_size(2048, 256, 8, 2, 2048)
+
+
+def test_history_arguments_rejected_on_host(lib):
+    fake = ctypes.c_void_p(256)
+    args = [fake, 8, 64, 1, fake, fake, fake, 4, 1, 8, 0.9, None, None, 0.8, 0.2, fake, fake, fake, fake,
+            None, None, None, None, fake, 1 << 30, None]
+    ok_ws = lib.luffy_condense_history_workspace_size(8, 64, 4, 1, 8)
+    assert ok_ws > 0
+    def call(**kw):
+        a = list(args)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return lib.luffy_condense_history(*a)
+    assert call(a0=None) == -1                       # null x
+    assert call(a13=float("nan")) == -1              # S1 NaN
+    assert call(a12=fake, a6=None) == -1             # hist_out without slot_pos
+    assert call(a11=fake, a12=fake) == -1            # hist_in aliases hist_out
+    assert call(a11=ctypes.c_void_p(260)) == -1      # misaligned record
+    assert call(a24=16) == -3                        # workspace too small
+    a = list(args)
+    a[8], a[9], a[11], a[24] = 2, 200000, fake, 1 << 62
+    assert lib.luffy_condense_history(*a) == -2      # record of that bucket size does not fit the gather
+    assert b"max_bucket" in lib.luffy_last_error()
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
     import paper_2411_15419_amd as L
