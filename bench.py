@@ -402,6 +402,81 @@ def measure_forward(name, thresholds, args, torch, np, G, L, with_cpu):
     return records
 
 
+HISTORY_SETTINGS = ((0.8, 0.2), (0.7, 0.3), (0.6, 0.4), (0.5, 0.5))
+HISTORY_DRIFTS = {"stable routing": dict(token_drift=0.1, gate_drift=0.0),
+                  "drifting routing": dict(token_drift=1.0, gate_drift=0.05)}
+
+
+def measure_history(name, args, torch, np, G, L):
+    """Historical similarity (Sec. 5.1 step 2) on a two-block stack at the
+    workload's shape (block 1 reads block 0's record): the condense call of
+    block 1 with history against the plain condense call on the same input,
+    per (S1, S2) and per drift of the tokens and router between the blocks
+    (one token in twenty a mixture of two centres, whose pairs fall between
+    S2 and S1)."""
+    cfg = G.config(name)
+    h = cfg.h
+    out = {}
+    for label, drift in HISTORY_DRIFTS.items():
+        log(f"history {name} ({label}): generating a two-block stack")
+        stack = G.make_stack(cfg, 2, seed=args.seed, mix_fraction=0.05, **drift)
+        dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        xs = [torch.from_numpy(b.x).to(dt).cuda() for b in stack]
+        wg = [torch.from_numpy(b.w_g).to(dt).cuda() for b in stack]
+        bg = torch.from_numpy(stack[0].b_g).cuda()
+        w1 = torch.zeros(cfg.E, 64, cfg.d, dtype=dt, device="cuda")
+        w2 = torch.zeros(cfg.E, cfg.d, 64, dtype=dt, device="cuda")
+        mk = lambda b, hist: L.MoELayer(wg[b], bg, w1, w2, k=cfg.k, act=cfg.act, threshold=h,  # noqa: E731
+                                        capacity_factor=cfg.capacity_factor, T=cfg.T, history=hist)
+
+        def timed(fn, kernel="gram"):
+            for _ in range(2):
+                fn()
+            L.profile_kernel(kernel)
+            L.profile_read()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(args.steps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            kms, kn = L.profile_read()
+            L.profile_kernel(None)
+            return a.elapsed_time(b) / args.steps * 1e3, kms / max(kn, 1) * 1e3
+
+        plain = mk(1, None)
+        plain.route(xs[1])
+        plain_us, plain_gram = timed(lambda: plain.condense(xs[1]))
+        runs = []
+        for S1, S2 in HISTORY_SETTINGS:
+            b0, b1 = mk(0, (S1, S2)), mk(1, (S1, S2))
+            b0.route(xs[0])
+            b0.condense(xs[0])
+            b1.route(xs[1])
+            us, gram_us = timed(lambda: b1.condense(xs[1], hist_in=b0.record))
+            _, gather_us = timed(lambda: b1.condense(xs[1], hist_in=b0.record), "hist_gather")
+            breakdown = {}
+            for kname in ("hist_cols", "norm", "hist_header", "greedy_round", "greedy_finish", "claim",
+                          "rep_local", "rep_finalize"):
+                breakdown[kname] = round(timed(lambda: b1.condense(xs[1], hist_in=b0.record), kname)[1], 1)
+            st = b1.hist_stats.cpu().numpy().tolist()
+            same = bool(torch.equal(b1.buf.rep_offsets, plain.buf.rep_offsets))
+            runs.append(dict(S1=S1, S2=S2, condense_us=us, gram_us=gram_us, gather_us=gather_us,
+                             saved_us=plain_us - us, undecided_pairs=st[0], decided_pairs=st[1],
+                             undecided_frac=st[0] / max(st[0] + st[1], 1), tiles_computed=st[2],
+                             tiles_skipped=st[3], same_representative_counts_as_plain=same,
+                             other_kernels_us=breakdown))
+            log(f"history {name} {label} S1={S1} S2={S2}: {us:.1f} us (plain {plain_us:.1f}), "
+                f"undecided {st[0] / max(st[0] + st[1], 1):.3f}, tiles {st[2]} computed {st[3]} skipped")
+            del b0, b1
+        out[label] = dict(drift=drift, plain_condense_us=plain_us, plain_gram_us=plain_gram, settings=runs)
+        del plain, xs, wg, stack
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
+
+
 def compact(rec):
     """Summary of a workload measured beside the headline one."""
     rl = rec["roofline"]
@@ -422,6 +497,9 @@ def main():
     ap.add_argument("--extras", default="c2,c4,c5",
                     help="workloads measured beside the headline one, reported under 'workloads' "
                          "(c4 at each of its four thresholds); 'none' for none")
+    ap.add_argument("--history", default="c3",
+                    help="workload whose two-block stack times the historical similarity beside the headline "
+                         "(reported under 'history'); 'none' for none")
     ap.add_argument("--threshold", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -465,6 +543,9 @@ def main():
             for r in measure_forward(name, list(ecfg.thresholds), args, torch, np, G, L, with_cpu=False):
                 key = name if len(ecfg.thresholds) == 1 else f"{name}_h{r['threshold']:.2f}"
                 extras[key] = compact(r)
+    history = None
+    if args.history and args.history != "none" and args.history in WORKLOAD_NAMES:
+        history = measure_history(args.history, args, torch, np, G, L)
     out = {
         "metric": "condensed MoE-layer tokens/s on 1 MI355X",
         "value": head["value"],
@@ -488,6 +569,7 @@ def main():
         "kernels": head["kernels"],
         "cpu_baseline": head["cpu_baseline"],
         "workloads": extras,
+        "history": history,
     }
     print(json.dumps(out), flush=True)
 

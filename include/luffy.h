@@ -214,8 +214,6 @@ int luffy_condense(const void* x, int T, int d, int dtype,
  * hi[W]; uint64 lo[W], W = T*k*ceil(max_bucket/64).  Bit c % 64 of word
  * word_off[e] + a*ceil(n_e/64) + c/64 of hi (lo) is the class w > S1
  * (w < S2) of positions a and c of bucket e, n_e its size.
- * With a hist_in, returns LUFFY_E_UNSUPPORTED for max_bucket above 131072
- * (k = 2) or 262144 (k = 1).
  * ---------------------------------------------------------------------- */
 size_t luffy_history_size(int T, int E, int k, int max_bucket);
 size_t luffy_condense_history_workspace_size(int T, int d, int E, int k, int max_bucket);
@@ -348,8 +346,8 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
- * Kernel names: gate, slot_scan, slot_scatter, norm, gram, hist_gather,
- * hist_header, greedy_round, greedy_finish, claim, rep_local, rep_finalize,
+ * Kernel names: gate, slot_scan, slot_scatter, norm, gram, hist_cols,
+ * hist_gather, hist_header, greedy_round, greedy_finish, claim, rep_local, rep_finalize,
  * gather,
  * ffn1, ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
  * bwd_z, bwd_act, bwd_da, bwd_dx, bwd_dx_reduce, bwd_gather, bwd_dw2,

@@ -41,12 +41,14 @@
 namespace luffy {
 namespace {
 
-constexpr int kGreedyGridRounds = 2;
+constexpr int kGreedyGridRounds = 4;   // the rounds after the second run only when the previous left work
+constexpr int kGreedyPasses = 32;      // visits of a blocked position in those later rounds
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
 constexpr int kTileF32 = 64;    // similarity tile of the fp32 path
 constexpr int kGroupsF32 = kTileF32 / 16;   // 16-column bit groups per tile row
 constexpr int kWordsF32 = kTileF32 / 64;    // bitmask words per tile row
 constexpr int kStateUndecided = 0, kStateKept = 1, kStateAbsorbed = 2;
+constexpr int kTileQueues = 8;  // tile queues of the history similarity kernel, one per XCD
 
 __device__ __forceinline__ float wave_sum_f32(float v) {
 #pragma unroll
@@ -109,10 +111,13 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
                                                    const int32_t* __restrict__ offsets, int E, int max_bucket,
                                                    int tile, long long cap_words, int32_t* __restrict__ tile_off,
                                                    long long* __restrict__ bm_off, int* __restrict__ err,
-                                                   unsigned long long* __restrict__ stats) {
+                                                   unsigned long long* __restrict__ stats, int* __restrict__ queue,
+                                                   int* __restrict__ left) {
   if (blockIdx.x == 0 && threadIdx.x < 64)
     gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
   if (stats && blockIdx.x == 0 && threadIdx.x >= 64 && threadIdx.x < 68) stats[threadIdx.x - 64] = 0ull;
+  if (queue && blockIdx.x == 0 && threadIdx.x >= 128 && threadIdx.x < 128 + kTileQueues) queue[threadIdx.x - 128] = 0;
+  if (blockIdx.x == 0 && threadIdx.x >= 192 && threadIdx.x < 192 + kGreedyGridRounds) left[threadIdx.x - 192] = 0;
   // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
@@ -515,10 +520,6 @@ HistRec carve_hist(Carver& c, int T, int E, int k, int max_bucket) {
   return h;
 }
 
-// Rows of one bucket per gather block (at most; fewer when a previous
-// block's rows do not fit the 64 KB of row images).
-constexpr int kGatherRowsMax = 4;
-constexpr int kGatherLdsBytes = 64 * 1024;
 
 // Header of the record a block leaves: format, sizes, the token -> position
 // map, bucket offsets and word offsets (after the layout).  A layout error
@@ -545,28 +546,65 @@ __global__ __launch_bounds__(256) void hist_header_kernel(const int32_t* __restr
   }
 }
 
+// Previous position of every slot of every position of this block, as
+// (previous bucket << 24) | position inside it, -1 where the token had no
+// kept slot there; every entry -1 when the record does not match (T, E, k,
+// max_bucket) or is marked invalid.  One thread per position.
+template <int K>
+__global__ __launch_bounds__(256) void hist_cols_kernel(const int32_t* __restrict__ offsets, int E,
+                                                        const int32_t* __restrict__ perm_token,
+                                                        const int* __restrict__ err, HistRec in, int T,
+                                                        int max_bucket, int32_t* __restrict__ colinfo) {
+  __shared__ int poff[kMaxExperts + 1];
+  __shared__ int rec_ok;
+  if (*err) return;
+  if (threadIdx.x == 0)
+    rec_ok = in.info[0] == kHistMagic && in.info[1] == T && in.info[2] == E && in.info[3] == K &&
+             in.info[4] == max_bucket;
+  __syncthreads();
+  const bool ok = rec_ok;
+  if (ok && threadIdx.x <= static_cast<unsigned>(E)) poff[threadIdx.x] = in.offsets[threadIdx.x];
+  __syncthreads();
+  const int S = offsets[E];
+  for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
+    const int u = perm_token[p];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      int v = -1;
+      if (ok) {
+        const int q = in.slot_pos[static_cast<size_t>(u) * K + j];
+        if (q >= 0) {
+          const int pe = bucket_of(poff, E, q);
+          v = (pe << 24) | (q - poff[pe]);
+        }
+      }
+      colinfo[static_cast<size_t>(p) * K + j] = v;
+    }
+  }
+}
+
 // The previous block's classes of every pair of this block's buckets, in
 // this block's bitmask layout: rb_hi / rb_lo bit c of row a of bucket e is
 // set when tokens perm_token[lo+a] and perm_token[lo+c] shared a bucket in
-// the previous block with class hi / lo there.  One block per G rows of one
-// bucket (G = rows): it copies the previous rows of its G tokens (one per
-// kept slot, hi and lo words interleaved) into LDS, then walks the bucket's
-// columns, one per lane, looking each column token's previous positions up.
-// A record that does not match (T, E, k, max_bucket) counts as empty.
+// the previous block with class hi / lo there.  One block per kGatherRows
+// rows of one bucket; each wave walks 64 columns of a 256-column chunk (the
+// columns' previous positions from colinfo), and for each row reads the
+// previous row's word of each matching column straight from memory (a row is
+// a few KB, so its words stay in L1 / L2 while the block walks it).
+constexpr int kGatherRows = 8;
+
 template <int K>
 __global__ __launch_bounds__(256) void hist_gather_kernel(const int32_t* __restrict__ offsets, int E,
-                                                          const int32_t* __restrict__ perm_token,
                                                           const long long* __restrict__ bm_off,
-                                                          const int* __restrict__ err, HistRec in, int T,
-                                                          int max_bucket, int G, uint64_t* __restrict__ rb_hi,
-                                                          uint64_t* __restrict__ rb_lo) {
-  extern __shared__ uint64_t img[];                 // [G][K][Wp][2]
-  __shared__ int poff[kMaxExperts + 1];              // previous block's bucket offsets
-  __shared__ int rinfo[kGatherRowsMax][K][2];        // previous bucket, local row (-1: none)
-  __shared__ int tile_e, tile_a0, tile_rows, rec_ok;
+                                                          const int* __restrict__ err, HistRec in,
+                                                          const int32_t* __restrict__ colinfo,
+                                                          uint64_t* __restrict__ rb_hi, uint64_t* __restrict__ rb_lo) {
+  __shared__ int rinfo[kGatherRows][K];        // previous bucket of the rows' slots (-1: none)
+  __shared__ long long rbase[kGatherRows][K];  // first word of that previous row
+  __shared__ int tile_e, tile_a0, tile_rows;
   if (*err) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int Wp = (max_bucket + 63) / 64;
+  constexpr int G = kGatherRows;
   if (w == 0) {
     // this block's bucket and first row: lane e holds bucket e's row groups
     const int n = lane < E ? offsets[lane + 1] - offsets[lane] : 0;
@@ -586,8 +624,6 @@ __global__ __launch_bounds__(256) void hist_gather_kernel(const int32_t* __restr
       tile_e = e < E ? e : -1;
       tile_a0 = (b - excl) * G;
       tile_rows = min(G, ne - tile_a0);
-      rec_ok = in.info[0] == kHistMagic && in.info[1] == T && in.info[2] == E && in.info[3] == K &&
-               in.info[4] == max_bucket;
     }
   }
   __syncthreads();
@@ -595,76 +631,56 @@ __global__ __launch_bounds__(256) void hist_gather_kernel(const int32_t* __restr
   if (e < 0) return;
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   const int a0 = tile_a0, rows = tile_rows;
-  const bool ok = rec_ok;
-  if (ok && tid <= E) poff[tid] = in.offsets[tid];
-  __syncthreads();
-  if (tid < kGatherRowsMax * K) {
+  if (tid < G * K) {
     const int i = tid / K, j = tid % K;
-    int pe = -1, pl = 0;
-    if (ok && i < rows) {
-      const int t = perm_token[lo + a0 + i];
-      const int p = in.slot_pos[static_cast<size_t>(t) * K + j];
-      if (p >= 0) {
-        pe = bucket_of(poff, E, p);
-        pl = p - poff[pe];
-      }
+    const int ri = i < rows ? colinfo[static_cast<size_t>(lo + a0 + i) * K + j] : -1;
+    long long base = 0;
+    if (ri >= 0) {
+      const int pe = ri >> 24, pl = ri & 0xFFFFFF;
+      const int wq = (in.offsets[pe + 1] - in.offsets[pe] + 63) / 64;
+      base = in.word_off[pe] + static_cast<long long>(pl) * wq;
     }
-    rinfo[i][j][0] = pe;
-    rinfo[i][j][1] = pl;
+    rinfo[i][j] = ri < 0 ? -1 : (ri >> 24);
+    rbase[i][j] = base;
   }
   __syncthreads();
-  // row images: previous row (hi, lo) of every kept slot of the G tokens
-  for (int i = 0; i < rows; ++i)
-    for (int j = 0; j < K; ++j) {
-      const int pe = rinfo[i][j][0];
-      if (pe < 0) continue;
-      const int np = poff[pe + 1] - poff[pe], Wq = (np + 63) / 64;
-      const long long base = in.word_off[pe] + static_cast<long long>(rinfo[i][j][1]) * Wq;
-      uint64_t* dst = img + (static_cast<size_t>(i) * K + j) * Wp * 2;
-      for (int q = tid; q < Wq; q += 256) {
-        dst[2 * q] = in.hi[base + q];
-        dst[2 * q + 1] = in.lo[base + q];
-      }
-    }
-  __syncthreads();
-  // columns, one per lane, 256 at a time; wave w owns words (c0 + 64 w) / 64
   for (int c0 = 0; c0 < n; c0 += 256) {
     const int c = c0 + tid;
-    int qe[K], ql[K];
+    int qv[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-      qe[j] = -1;
-      ql[j] = 0;
-    }
-    if (ok && c < n) {
-      const int u = perm_token[lo + c];
+    for (int j = 0; j < K; ++j) qv[j] = c < n ? colinfo[static_cast<size_t>(lo + c) * K + j] : -1;
+    const int wd = (c0 >> 6) + w;
+    // the words of all G rows are loaded before any is used, so their
+    // latencies overlap
+    long long widx[G];
+    int bit[G];
 #pragma unroll
-      for (int j = 0; j < K; ++j) {
-        const int q = in.slot_pos[static_cast<size_t>(u) * K + j];
-        if (q >= 0) {
-          qe[j] = bucket_of(poff, E, q);
-          ql[j] = q - poff[qe[j]];
-        }
-      }
-    }
-    for (int i = 0; i < rows; ++i) {
-      bool bh = false, bl = false, found = false;
+    for (int i = 0; i < G; ++i) {
+      widx[i] = -1;
+      bit[i] = 0;
 #pragma unroll
-      for (int jr = 0; jr < K; ++jr) {
-        const int pe = rinfo[i][jr][0];
+      for (int jr = K - 1; jr >= 0; --jr) {
+        const int pe = i < rows ? rinfo[i][jr] : -1;
 #pragma unroll
-        for (int jc = 0; jc < K; ++jc) {
-          if (!found && pe >= 0 && qe[jc] == pe) {
-            const uint64_t* im = img + (static_cast<size_t>(i) * K + jr) * Wp * 2;
-            const int q = ql[jc];
-            bh = (im[2 * (q >> 6)] >> (q & 63)) & 1ull;
-            bl = (im[2 * (q >> 6) + 1] >> (q & 63)) & 1ull;
-            found = true;
+        for (int jc = K - 1; jc >= 0; --jc) {
+          if (pe >= 0 && qv[jc] >= 0 && (qv[jc] >> 24) == pe) {
+            const int q = qv[jc] & 0xFFFFFF;
+            widx[i] = rbase[i][jr] + (q >> 6);
+            bit[i] = q & 63;
           }
         }
       }
-      const uint64_t mh = __ballot(bh), ml = __ballot(bl);
-      const int wd = (c0 >> 6) + w;
+    }
+    uint64_t vh[G], vl[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      vh[i] = widx[i] >= 0 ? in.hi[widx[i]] : 0ull;
+      vl[i] = widx[i] >= 0 ? in.lo[widx[i]] : 0ull;
+    }
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      if (i >= rows) break;
+      const uint64_t mh = __ballot((vh[i] >> bit[i]) & 1ull), ml = __ballot((vl[i] >> bit[i]) & 1ull);
       if (lane == 0 && wd < W) {
         const long long o = bm_off[e] + static_cast<long long>(a0 + i) * W + wd;
         rb_hi[o] = mh;
@@ -684,6 +700,7 @@ struct HistParams {
   const uint64_t* rb_hi;   // previous classes in this block's layout (nullptr: none)
   const uint64_t* rb_lo;
   unsigned long long* stats;   // undecided pairs, decided pairs, tiles computed, tiles skipped
+  int* queue;                  // kTileQueues tile counters, zero at launch
 };
 
 // Words of one row piece from its (hi, lo) previous classes, for a tile
@@ -737,7 +754,32 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_hist_kernel_bf16(
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = G::wave_m(w), wn = G::wave_n(w);
   const int total = tile_off[E];
-  for (int tile = xcd_virtual_block(); tile < total; tile += gridDim.x) {
+  // Tiles cost very different times (skipped or computed), so blocks take
+  // them from queues: queue x holds the x-th eighth of the tile order, a
+  // block first drains the queue of its own XCD (blocks are dealt to the
+  // XCDs round-robin), then the others'.
+  __shared__ int next_tile;
+  const int home = blockIdx.x % kTileQueues;
+  int qi = 0;
+  for (;;) {
+    if (tid == 0) {
+      int t = -1;
+      while (qi < kTileQueues) {
+        const int x = (home + qi) % kTileQueues;
+        const int t0 = static_cast<int>(static_cast<long long>(total) * x / kTileQueues);
+        const int t1 = static_cast<int>(static_cast<long long>(total) * (x + 1) / kTileQueues);
+        const int v = atomicAdd(&hp.queue[x], 1);
+        if (t0 + v < t1) {
+          t = t0 + v;
+          break;
+        }
+        ++qi;
+      }
+      next_tile = t;
+    }
+    __syncthreads();
+    const int tile = next_tile;
+    if (tile < 0) break;
     const TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
     const int32_t* pt = perm_token + c.lo;
     const long long bmo = bm_off[c.e];
@@ -1152,9 +1194,12 @@ __device__ __forceinline__ void load_offsets(const int32_t* __restrict__ offsets
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out) {
+    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out,
+    int* __restrict__ left) {
   __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
+  // left[r]: some position was still undecided after a visit in round r
+  if (r >= 2 && load_flag(&left[r - 1]) == 0) return;
   load_offsets(offsets, E, soff);
   const int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
   const int gl = threadIdx.x & (kVisitLanes - 1);
@@ -1163,33 +1208,83 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
   if (state[p] != kStateUndecided) return;
   const int e = bucket_of(soff, E, p);
   const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
-  greedy_visit<false, kVisitLanes>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg,
-                                   state);
+  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
+  bool still = greedy_visit<false, kVisitLanes>(p, lo, n, W, row, deg, state);
+  // The later rounds (run only when the earlier ones left work, as on graphs
+  // with long dependency chains) revisit a blocked position a bounded number
+  // of times, reading the states coherently: a chain of length L resolves in
+  // about L visits inside one launch instead of L launches.
+  for (int pass = 1; r >= 2 && still && pass < kGreedyPasses; ++pass) {
+    __builtin_amdgcn_s_sleep(32);
+    still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+  }
+  if (still && gl == 0 && load_flag(&left[r]) == 0) store_flag(&left[r], 1);
 }
 
-// One workgroup per bucket: rounds until every position is decided.  Each
-// round decides at least the highest-priority undecided position, so at most
-// n rounds run.
+// One workgroup per bucket: rounds until every position is decided.  The
+// undecided positions left by the grid rounds are gathered once into a list
+// in LDS (a coalesced pass over the bucket's states); each round then visits
+// only the listed positions, 16 lanes each (64 at a time), and keeps those
+// still undecided for the next round.  Each round decides at least the
+// highest-priority undecided position, so rounds <= the list's length; a
+// bucket with more undecided positions than the list holds takes the
+// original path, a pass over all its positions per round.
+constexpr int kFinishList = 16384;
+
 __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state) {
+    const int32_t* __restrict__ deg, int32_t* state, const int* __restrict__ left) {
+  __shared__ int list[2][kFinishList];
+  __shared__ int cnt[2];
   if (*err) return;
+  if (load_flag(&left[kGreedyGridRounds - 1]) == 0) return;   // the grid rounds decided every position
   const int e = blockIdx.x;
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   if (n == 0) return;
-  // coalesced check first: most buckets are fully decided by the grid rounds
-  int any = 0;
-  for (int i = threadIdx.x; i < n; i += 1024) any |= state[lo + i] == kStateUndecided;
-  if (!__syncthreads_or(any)) return;
-  const int wv = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  if (tid < 2) cnt[tid] = 0;
+  __syncthreads();
+  for (int i = tid; i < n; i += 1024) {
+    if (load_flag(&state[lo + i]) == kStateUndecided) {
+      const int slot = atomicAdd(&cnt[0], 1);
+      if (slot < kFinishList) list[0][slot] = i;
+    }
+  }
+  __syncthreads();
+  int m = cnt[0];
+  if (m == 0) return;
+  const uint64_t* rows = bitmask + bm_off[e];
+  if (m <= kFinishList) {
+    const int grp = tid / kVisitLanes;
+    constexpr int kGroups = 1024 / kVisitLanes;
+    int cur = 0;
+    const int m0 = m;
+    for (int it = 0; it <= m0 && m > 0; ++it) {
+      for (int idx = grp; idx < m; idx += kGroups) {
+        const int pl = list[cur][idx];
+        greedy_visit<true, kVisitLanes>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
+      }
+      if (tid == 0) cnt[cur ^ 1] = 0;
+      __syncthreads();
+      for (int idx = tid; idx < m; idx += 1024) {
+        const int pl = list[cur][idx];
+        if (load_flag(&state[lo + pl]) == kStateUndecided) list[cur ^ 1][atomicAdd(&cnt[cur ^ 1], 1)] = pl;
+      }
+      __syncthreads();
+      cur ^= 1;
+      m = cnt[cur];
+      __syncthreads();
+    }
+    return;
+  }
+  const int wv = tid >> 6;
   for (int it = 0; it <= n; ++it) {
     int undecided = 0;
     for (int pl = wv; pl < n; pl += 16) {
       const int p = lo + pl;
       if (load_flag(&state[p]) != kStateUndecided) continue;
-      if (greedy_visit<true, 64>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(pl) * W, deg, state))
-        undecided = 1;
+      if (greedy_visit<true, 64>(p, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state)) undecided = 1;
     }
     if (!__syncthreads_or(undecided)) break;
   }
@@ -1361,6 +1456,9 @@ struct CondenseWs {
   uint64_t* rb_hi = nullptr;
   uint64_t* rb_lo = nullptr;
   unsigned long long* stats = nullptr;
+  int* left;                    // per greedy grid round: a position stayed undecided
+  int32_t* colinfo = nullptr;   // previous positions of every slot of every position
+  int* queue = nullptr;         // tile queues of the similarity kernel
 };
 
 CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool history = false) {
@@ -1375,12 +1473,15 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool h
   w.claim = c.take<unsigned long long>(S);
   w.local = c.take<int32_t>(S);
   w.bsum = c.take<int32_t>((S + 1023) / 1024 + 1);
+  w.left = c.take<int>(kGreedyGridRounds);
   w.cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
   w.bitmask = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
   if (history) {
     w.rb_hi = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
     w.rb_lo = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
     w.stats = c.take<unsigned long long>(4);
+    w.colinfo = c.take<int32_t>(static_cast<size_t>(S) * k);
+    w.queue = c.take<int>(kTileQueues);
   }
   return w;
 }
@@ -1393,13 +1494,6 @@ struct HistCall {
   float S1, S2;
   unsigned long long* stats;
 };
-
-// Rows per gather block for a record of max_bucket (0: too large).
-int gather_rows(int k, int max_bucket) {
-  const long long per_row = static_cast<long long>(k) * ((max_bucket + 63) / 64) * 16;
-  return static_cast<int>(std::min<long long>(kGatherRowsMax, kGatherLdsBytes / std::max(per_row, 1ll)));
-}
-
 
 }  // namespace
 }  // namespace luffy
@@ -1441,7 +1535,7 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   {
     const int tile = bf16 ? kTile : kTileF32;
 #define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
-                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats
+                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats, ws.queue, ws.left
     if (bf16) {
       if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
       else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
@@ -1464,15 +1558,19 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
     const HistRec rin = carve_hist(cin, T, E, k, max_bucket);
     const HistRec rout = carve_hist(cout, T, E, k, max_bucket);
     if (hc->in) {
-      const int G = gather_rows(k, max_bucket);
-      const size_t lds = static_cast<size_t>(G) * k * ((max_bucket + 63) / 64) * 16;
-      const int blocks = (S + G - 1) / G + E;
-      if (k == 1)
-        launch("hist_gather", hist_gather_kernel<1>, blocks, 256, lds, s, offsets, E, perm_token, ws.bm_off, ws.err,
-               rin, T, max_bucket, G, ws.rb_hi, ws.rb_lo);
-      else
-        launch("hist_gather", hist_gather_kernel<2>, blocks, 256, lds, s, offsets, E, perm_token, ws.bm_off, ws.err,
-               rin, T, max_bucket, G, ws.rb_hi, ws.rb_lo);
+      const int blocks = (S + kGatherRows - 1) / kGatherRows + E;
+      const int cblocks = std::max(1, std::min(1024, (S + 255) / 256));
+      if (k == 1) {
+        launch("hist_cols", hist_cols_kernel<1>, cblocks, 256, 0, s, offsets, E, perm_token, ws.err, rin, T,
+               max_bucket, ws.colinfo);
+        launch("hist_gather", hist_gather_kernel<1>, blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, rin,
+               ws.colinfo, ws.rb_hi, ws.rb_lo);
+      } else {
+        launch("hist_cols", hist_cols_kernel<2>, cblocks, 256, 0, s, offsets, E, perm_token, ws.err, rin, T,
+               max_bucket, ws.colinfo);
+        launch("hist_gather", hist_gather_kernel<2>, blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, rin,
+               ws.colinfo, ws.rb_hi, ws.rb_lo);
+      }
     }
     if (hc->out)
       launch("hist_header", hist_header_kernel, std::max(1, std::min(1024, (S + 255) / 256)), 256, 0, s,
@@ -1486,6 +1584,7 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
     hp.rb_hi = hc->in ? ws.rb_hi : nullptr;
     hp.rb_lo = hc->in ? ws.rb_lo : nullptr;
     hp.stats = stats;
+    hp.queue = ws.queue;
     const bool hin = hc->in != nullptr, hout = hc->out != nullptr;
 #define LUFFY_GH_ARGS d, perm_token, offsets, E, inv_norm_use, hp, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg
     if (bf16) {
@@ -1510,10 +1609,10 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
   for (int r = 0; r < kGreedyGridRounds; ++r) {
     launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-           ws.deg, ws.state, r, degree);
+           ws.deg, ws.state, r, degree, ws.left);
   }
   launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-         ws.state);
+         ws.state, ws.left);
   launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
          ws.state, ws.claim);
   const int pos_blocks = (S + 1023) / 1024;
@@ -1591,8 +1690,6 @@ extern "C" int luffy_condense_history(const void* x, int T, int d, int dtype,
   if (hist_in && hist_in == hist_out) return fail(LUFFY_E_INVALID, "%s: hist_in and hist_out alias", fn);
   if ((reinterpret_cast<uintptr_t>(hist_in) & 255u) || (reinterpret_cast<uintptr_t>(hist_out) & 255u))
     return fail(LUFFY_E_INVALID, "%s: records must be 256-byte aligned", fn);
-  if (hist_in && gather_rows(k, max_bucket) < 1)
-    return fail(LUFFY_E_UNSUPPORTED, "%s: max_bucket=%d too large for a record", fn, max_bucket);
   const size_t need = luffy_condense_history_workspace_size(T, d, E, k, max_bucket);
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "%s: workspace needs %zu bytes, 256-aligned", fn, need);
