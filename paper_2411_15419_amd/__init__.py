@@ -23,7 +23,7 @@ __all__ = [
     "profile_read", "KERNELS", "adaptive_threshold", "AdaptiveThreshold",
     "luffy_combine_backward", "combine_backward_workspace_size", "luffy_expert_ffn_backward",
     "expert_ffn_backward_workspace_size", "luffy_condense_history", "history_size",
-    "condense_history_workspace_size", "MoEStack",
+    "condense_history_workspace_size", "MoEStack", "CondensationDriver",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libluffy.so")
@@ -489,3 +489,38 @@ class MoEStack:
                 outs.append(layer.buf.y)
             prev = layer.record
         return outs if ffn else None
+
+
+class CondensationDriver:
+    """Training iterations over a stack of condensed MoE blocks with the
+    adaptive threshold of Sec. 5.2 (Eq. 2): before an iteration, h_t comes
+    from the first and the previous iteration's loss (AdaptiveThreshold; 1/2
+    until a loss is recorded, as Eq. 2 gives for an unmoved loss); every
+    block of the iteration condenses at h_t, each with the historical
+    similarity of the block before it (Sec. 5.1 step 2); after it, the
+    iteration's loss is recorded.  Eq. 2 as printed keeps h_t in
+    (1/(1+e), 1/2] while the loss falls.
+
+    stack: an MoEStack (or a single MoELayer, run alone)."""
+
+    def __init__(self, stack, schedule: Optional[AdaptiveThreshold] = None):
+        self.stack = stack
+        self.schedule = schedule if schedule is not None else AdaptiveThreshold()
+        self.thresholds = []
+        self.losses = []
+
+    def step(self, xs, loss, stream=None, ffn=True):
+        """One iteration on the blocks' inputs xs (a list, one per block, or
+        one tensor for a single layer).  loss: a number, or a callable that
+        takes the outputs and returns this iteration's loss.  Returns
+        (h_t, outputs)."""
+        h = self.schedule.threshold()
+        if isinstance(self.stack, MoEStack):
+            outs = self.stack(xs, stream, threshold=h, ffn=ffn)
+        else:
+            outs = self.stack(xs, stream, threshold=h)
+        value = float(loss(outs) if callable(loss) else loss)
+        self.schedule.record(value)
+        self.thresholds.append(h)
+        self.losses.append(value)
+        return h, outs
