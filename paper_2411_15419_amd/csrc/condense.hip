@@ -41,8 +41,8 @@
 namespace luffy {
 namespace {
 
-constexpr int kGreedyGridRounds = 4;   // the rounds after the second run only when the previous left work
-constexpr int kGreedyPasses = 32;      // visits of a blocked position in those later rounds
+constexpr int kGreedyGridRounds = 2;
+constexpr int kGreedyPasses = 32;   // visits of a blocked position in the round after the grid rounds
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
 constexpr int kTileF32 = 64;    // similarity tile of the fp32 path
 constexpr int kGroupsF32 = kTileF32 / 16;   // 16-column bit groups per tile row
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
     gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
   if (stats && blockIdx.x == 0 && threadIdx.x >= 64 && threadIdx.x < 68) stats[threadIdx.x - 64] = 0ull;
   if (queue && blockIdx.x == 0 && threadIdx.x >= 128 && threadIdx.x < 128 + kTileQueues) queue[threadIdx.x - 128] = 0;
-  if (blockIdx.x == 0 && threadIdx.x >= 192 && threadIdx.x < 192 + kGreedyGridRounds) left[threadIdx.x - 192] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 192) *left = 0;
   // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
@@ -1194,12 +1194,9 @@ __device__ __forceinline__ void load_offsets(const int32_t* __restrict__ offsets
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out,
-    int* __restrict__ left) {
+    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out) {
   __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
-  // left[r]: some position was still undecided after a visit in round r
-  if (r >= 2 && load_flag(&left[r - 1]) == 0) return;
   load_offsets(offsets, E, soff);
   const int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
   const int gl = threadIdx.x & (kVisitLanes - 1);
@@ -1208,17 +1205,39 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
   if (state[p] != kStateUndecided) return;
   const int e = bucket_of(soff, E, p);
   const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
-  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
-  bool still = greedy_visit<false, kVisitLanes>(p, lo, n, W, row, deg, state);
-  // The later rounds (run only when the earlier ones left work, as on graphs
-  // with long dependency chains) revisit a blocked position a bounded number
-  // of times, reading the states coherently: a chain of length L resolves in
-  // about L visits inside one launch instead of L launches.
-  for (int pass = 1; r >= 2 && still && pass < kGreedyPasses; ++pass) {
-    __builtin_amdgcn_s_sleep(32);
-    still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+  greedy_visit<false, kVisitLanes>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg,
+                                   state);
+}
+
+// The round after the grid rounds: a persistent grid, 16 lanes per
+// position, that passes over every position (those already decided cost a
+// state read) and revisits a blocked one a bounded number of times, reading
+// the states coherently, so a dependency chain of length L resolves in
+// about L visits inside one launch instead of L launches (graphs whose
+// chains the grid rounds leave unfinished).  left[0] records that a
+// position is still undecided after it, for the finishing pass.
+__global__ __launch_bounds__(256) void greedy_more_kernel(
+    const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
+    const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
+    const int32_t* __restrict__ deg, int32_t* state, int* __restrict__ left) {
+  __shared__ int soff[kMaxExperts + 1];
+  if (*err) return;
+  load_offsets(offsets, E, soff);
+  const int gl = threadIdx.x & (kVisitLanes - 1);
+  const int S = soff[E];
+  for (int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes); p < S;
+       p += gridDim.x * kVisitPerBlock) {
+    if (load_flag(&state[p]) != kStateUndecided) continue;
+    const int e = bucket_of(soff, E, p);
+    const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
+    const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
+    bool still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+    for (int pass = 1; still && pass < kGreedyPasses; ++pass) {
+      __builtin_amdgcn_s_sleep(32);
+      still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+    }
+    if (still && gl == 0) store_flag(&left[0], 1);
   }
-  if (still && gl == 0 && load_flag(&left[r]) == 0) store_flag(&left[r], 1);
 }
 
 // One workgroup per bucket: rounds until every position is decided.  The
@@ -1238,7 +1257,7 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
   __shared__ int list[2][kFinishList];
   __shared__ int cnt[2];
   if (*err) return;
-  if (load_flag(&left[kGreedyGridRounds - 1]) == 0) return;   // the grid rounds decided every position
+  if (load_flag(&left[0]) == 0) return;   // the grid rounds decided every position
   const int e = blockIdx.x;
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   if (n == 0) return;
@@ -1456,7 +1475,7 @@ struct CondenseWs {
   uint64_t* rb_hi = nullptr;
   uint64_t* rb_lo = nullptr;
   unsigned long long* stats = nullptr;
-  int* left;                    // per greedy grid round: a position stayed undecided
+  int* left;                    // a position stayed undecided after the greedy rounds
   int32_t* colinfo = nullptr;   // previous positions of every slot of every position
   int* queue = nullptr;         // tile queues of the similarity kernel
 };
@@ -1473,7 +1492,7 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool h
   w.claim = c.take<unsigned long long>(S);
   w.local = c.take<int32_t>(S);
   w.bsum = c.take<int32_t>((S + 1023) / 1024 + 1);
-  w.left = c.take<int>(kGreedyGridRounds);
+  w.left = c.take<int>(1);
   w.cap_words = S * ((static_cast<long long>(max_bucket) + 63) / 64);
   w.bitmask = c.take<uint64_t>(static_cast<size_t>(w.cap_words));
   if (history) {
@@ -1607,10 +1626,11 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   }
   const int wave_blocks = (S + 3) / 4;
   const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
-  for (int r = 0; r < kGreedyGridRounds; ++r) {
+  for (int r = 0; r < kGreedyGridRounds; ++r)
     launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-           ws.deg, ws.state, r, degree, ws.left);
-  }
+           ws.deg, ws.state, r, degree);
+  launch("greedy_more", greedy_more_kernel, std::min(visit_blocks, persistent_grid()), 256, 0, s, offsets, E,
+         ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, ws.left);
   launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
          ws.state, ws.left);
   launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,

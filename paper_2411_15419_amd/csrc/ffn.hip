@@ -145,7 +145,7 @@ static_assert(FfnGemm::BM == FfnGemmWide::BM && FfnGemm::THREADS == FfnGemmWide:
 constexpr int kFfnLds = FfnGemmWide::LDS_BYTES > FfnGemm::LDS_BYTES ? FfnGemmWide::LDS_BYTES : FfnGemm::LDS_BYTES;
 // split-K partial tiles: one slot (the accumulators of a tile in register
 // layout) per work item, at most kFfnMaxSlots (>= CUs) work items
-constexpr int kFfnMaxSlots = 512;
+constexpr int kFfnMaxSlots = 1536;
 constexpr size_t kFfnSlotFloats = static_cast<size_t>(FfnGemm::BM) * FfnGemmWide::BN;
 // split-K parts cut K at multiples of this (a multiple of both stage widths)
 constexpr int kFfnKUnit = 64;
@@ -202,20 +202,29 @@ struct FfnTiles {
     n0 = __builtin_amdgcn_readfirstlane(nt * FfnGemm::BM);
     wide = rte == FfnGemmWide::BN;
   }
-  // Split-K parts per tile (second product only): the largest split of at
-  // most 4 (each part >= 4 K-stages) that keeps every tile's parts within
-  // the partial-tile slots, doubling while the current split still has
-  // fewer work items than blocks.  The last doubling may leave more items
-  // than blocks, so that parts run in two rounds: with 140 tiles of K =
-  // 4096, two rounds of half-K parts (the first on every CU) measured
-  // faster than one round of whole tiles on 140 CUs, because the per-CU
-  // operand stream, not HBM, bounds such a product.  Always 1, 2 or 4 (the
-  // reduction is instantiated for 2 and 4).
+  // Split-K parts per tile (second product only).  Only a product with
+  // fewer tiles than blocks splits (with more, every CU already has a tile
+  // and the partial tiles' round trip costs more than the balance gains:
+  // measured on 424 tiles of K = 8192).  It takes the split s in 2..4 (each
+  // part at least 4 K-units, every part's partial tile within the slots)
+  // with the fewest rounds times part length, ceil(tiles*s/grid)/s in units
+  // of a whole tile; ties keep the smaller split.  The per-CU operand
+  // stream, not HBM, bounds these products, so rounds of shorter parts on
+  // more CUs win even when a round is not full: 140 tiles of K = 4096 take
+  // 2 rounds of thirds instead of 2 rounds of halves.
   __device__ __forceinline__ int parts(int grid, int nk) const {
-    if (tiles <= 0) return 1;
-    int s = 1;
-    while (s < 4 && 2 * s <= nk / 4 && tiles * 2 * s <= kFfnMaxSlots && tiles * s < grid) s *= 2;
-    return s;
+    if (tiles <= 0 || tiles >= grid) return 1;
+    int best = 1;
+    long long best_cost = 12ll * ((tiles + grid - 1) / grid);
+    for (int sp = 2; sp <= 4; ++sp) {
+      if (nk / sp < 4 || static_cast<long long>(tiles) * sp > kFfnMaxSlots) break;
+      const long long cost = (12 / sp) * ((static_cast<long long>(tiles) * sp + grid - 1) / grid);
+      if (cost < best_cost) {
+        best_cost = cost;
+        best = sp;
+      }
+    }
+    return best;
   }
 };
 
@@ -420,6 +429,9 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
     if (S == 4) {
       if (wide) reduce_unit<FfnGemmWide, 4>(slots, q, row0, rows, n0, N, out);
       else if (narrow_unit) reduce_unit<FfnGemm, 4>(slots, q, row0, rows, n0, N, out);
+    } else if (S == 3) {
+      if (wide) reduce_unit<FfnGemmWide, 3>(slots, q, row0, rows, n0, N, out);
+      else if (narrow_unit) reduce_unit<FfnGemm, 3>(slots, q, row0, rows, n0, N, out);
     } else {
       if (wide) reduce_unit<FfnGemmWide, 2>(slots, q, row0, rows, n0, N, out);
       else if (narrow_unit) reduce_unit<FfnGemm, 2>(slots, q, row0, rows, n0, N, out);

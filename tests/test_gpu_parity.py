@@ -241,17 +241,22 @@ def test_activation_values_bf16(act):
     assert np.mean(got[core] == ref[core]) > 0.99
 
 
-@pytest.mark.parametrize("d,d_ff", [(256, 512), (256, 1024), (64, 64), (128, 192), (192, 576), (64, 2048)])
+@pytest.mark.parametrize("d,d_ff", [(256, 512), (256, 1024), (64, 64), (128, 192), (192, 576), (64, 2048),
+                                   (1280, 768)])
 def test_expert_ffn_tile_shapes(d, d_ff):
     """The bf16 expert FFN on expert sizes that pick every tile shape: empty,
     1 row, 255-257 rows (narrow tiles, one of them partial), 300 and 320
     (one 320-row tile instead of 256 + rest), 321 (narrow again), 600 (two
     320-row tiles instead of three) and 700 (narrow); representative rows
-    gathered through a permuted row index.  d_ff = 512 splits the second
-    product in 2, 1024 and 2048 in 4, 576 in 2 parts of 4 and 5 64-wide
-    K stages; d and d_ff of 64 to 192 give products of 1 to 3 stages (the
-    pipeline's prologue and tail only).  Each output row within the bf16
-    tolerance of the oracle's fp64 product on the same bf16 inputs."""
+    gathered through a permuted row index.  On 256 CUs the second product
+    (14 token tiles times d/256 column tiles) splits K in 2 at d_ff = 512,
+    in 4 at 1024 and 2048, in 2 parts of 4 and 5 64-wide K stages at 576,
+    and in 3 parts of 4 stages at d = 1280, d_ff = 768 (70 tiles).  d and
+    d_ff of 64 to 192
+    give products of 1 to 3 stages (the pipeline's prologue and tail only).
+    Each output row within the bf16 tolerance of the oracle's fp64 product
+    on the same bf16 inputs; run twice, bit-identical (the parts are summed
+    in a fixed order)."""
     import torch
     import paper_2411_15419_amd as L
     from tests.layer_runner import TOL, rel_err_rows
@@ -268,12 +273,19 @@ def test_expert_ffn_tile_shapes(d, d_ff):
     dev = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
     y = torch.empty(R, d, dtype=torch.bfloat16, device="cuda")
     ws = torch.empty(L.expert_ffn_workspace_size(R, E, d_ff, L.LUFFY_BF16), dtype=torch.uint8, device="cuda")
-    L.luffy_expert_ffn(dev(x_all), dev(row_index, torch.int32), dev(offsets, torch.int32), dev(w1), dev(w2),
-                       "gelu", R, y, ws)
-    got = y.double().cpu().numpy()
+    args = (dev(x_all), dev(row_index, torch.int32), dev(offsets, torch.int32), dev(w1), dev(w2))
     ref = O.expert_ffn(x_all[row_index], offsets, w1, w2, "gelu")
-    err, _ = rel_err_rows(got, ref)
-    assert err.max() <= TOL["bf16"], f"max row rel err {err.max():.3g}"
+    first = None
+    for call in range(2):
+        y.fill_(float("nan"))
+        L.luffy_expert_ffn(*args, "gelu", R, y, ws)
+        got = y.double().cpu().numpy()
+        err, _ = rel_err_rows(got, ref)
+        assert err.max() <= TOL["bf16"], f"call {call}: max row rel err {err.max():.3g}"
+        if first is None:
+            first = got
+        else:
+            assert np.array_equal(first, got), "the split sum differs between calls"
 
 
 @pytest.mark.parametrize("d", [256, 2560])
