@@ -43,13 +43,13 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// Epilogue of a gate chunk of TOK tokens starting at t0, once logit[tl][e]
-// (bias included) is in LDS for every token: top-k, gates, the float64
+// Epilogue of a gate chunk of TOK tokens starting at t0, once the logit of
+// token tl and expert e (bias included) is in LDS at lg[e * (TOK + 4) + tl]: top-k, gates, the float64
 // re-decision of close calls; then wave 0 ranks every slot among the chunk's
 // slots of the same expert and writes the chunk's per-expert counts.  Called
 // by all four waves of the block; ends with the ranking done (no barrier).
 template <bool BF16, int TOK>
-__device__ __forceinline__ void gate_select(float (*logit)[kMaxExperts + 1], const float* bias, int* cnt,
+__device__ __forceinline__ void gate_select(const float* lg, const float* bias, int* cnt,
                                             int (*choice)[2], const void* __restrict__ xv,
                                             const void* __restrict__ wv, int T, int d, int E, int k, int t0,
                                             int ch, int nchunks, int32_t* __restrict__ topk_idx,
@@ -71,7 +71,7 @@ __device__ __forceinline__ void gate_select(float (*logit)[kMaxExperts + 1], con
     int i0 = kMaxExperts, i1 = kMaxExperts, i2 = kMaxExperts;
     if (valid) {
       for (int e = sub; e < E; e += 4) {
-        const float v = logit[tl_][e];
+        const float v = lg[e * (TOK + 4) + tl_];
         if (v > v0) { v2 = v1; i2 = i1; v1 = v0; i1 = i0; v0 = v; i0 = e; }
         else if (v > v1) { v2 = v1; i2 = i1; v1 = v; i1 = e; }
         else if (v > v2) { v2 = v; i2 = e; }
@@ -113,7 +113,7 @@ __device__ __forceinline__ void gate_select(float (*logit)[kMaxExperts + 1], con
     uint64_t cand = 0;
     if (amb)
       for (int e = sub; e < E; e += 4)
-        if (logit[tl_][e] >= vk1 - delta) cand |= 1ull << e;
+        if (lg[e * (TOK + 4) + tl_] >= vk1 - delta) cand |= 1ull << e;
     cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 1, 64));
     cand |= static_cast<uint64_t>(__shfl_xor(static_cast<long long>(cand), 2, 64));
     uint64_t ambmask = __ballot(amb && sub == 0);
@@ -160,16 +160,16 @@ __device__ __forceinline__ void gate_select(float (*logit)[kMaxExperts + 1], con
       // each lane over its quarter of the experts, then summed over the four
       constexpr float kLog2e = 1.44269504088896341f;
       float den = 0.f;
-      for (int e = sub; e < E; e += 4) den += __builtin_amdgcn_exp2f((logit[tl_][e] - v0) * kLog2e);
+      for (int e = sub; e < E; e += 4) den += __builtin_amdgcn_exp2f((lg[e * (TOK + 4) + tl_] - v0) * kLog2e);
       den += __shfl_xor(den, 1, 64);
       den += __shfl_xor(den, 2, 64);
       if (sub == 0) {
         if (k == 1) {
           topk_idx[t] = i0;
-          topk_gate[t] = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e) / den;
+          topk_gate[t] = __builtin_amdgcn_exp2f((lg[i0 * (TOK + 4) + tl_] - v0) * kLog2e) / den;
         } else {
-          const float ga = __builtin_amdgcn_exp2f((logit[tl_][i0] - v0) * kLog2e);
-          const float gb = __builtin_amdgcn_exp2f((logit[tl_][i1] - v0) * kLog2e);
+          const float ga = __builtin_amdgcn_exp2f((lg[i0 * (TOK + 4) + tl_] - v0) * kLog2e);
+          const float gb = __builtin_amdgcn_exp2f((lg[i1 * (TOK + 4) + tl_] - v0) * kLog2e);
           topk_idx[2 * t] = i0;
           topk_idx[2 * t + 1] = i1;
           topk_gate[2 * t] = ga / (ga + gb);
@@ -230,7 +230,10 @@ __global__ __launch_bounds__(256) void gate_kernel(
     int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done,
     float* __restrict__ inv_norm) {
   constexpr int kGateA = TOK / 16;   // 16-token MFMA row blocks
-  __shared__ float part[4][TOK][kMaxExperts + 1];
+  // partial logits of the four waves, expert-major: part[w][e][tl] (the four
+  // consecutive tokens an MFMA lane holds are one 16-byte store)
+  constexpr int LD = TOK + 4;
+  __shared__ __attribute__((aligned(16))) float part[4][kMaxExperts][LD];
   __shared__ float sumsq[4][TOK];
   __shared__ float bias[kMaxExperts];
   __shared__ int cnt[kMaxExperts];
@@ -264,7 +267,11 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const int q = (nsteps + 3) / 4;
     const int s_lo = w * q, s_hi = min(nsteps, s_lo + q);
     constexpr int B = 2;   // K steps per batch; the next batch is loaded while one is multiplied
-    float sq[kGateA] = {};   // sum of squares of this lane's token columns
+    // sums of squares of the token rows on MFMA: the Gram of a 16-token
+    // block with itself, whose diagonal is the rows' squared norms
+    f32x4 accsq[kGateA];
+#pragma unroll
+    for (int i = 0; i < kGateA; ++i) accsq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     Pack16 a[2][B][kGateA], b[2][B][4];
     auto load = [&](int s0, Pack16 (&aa)[B][kGateA], Pack16 (&bb)[B][4]) {
 #pragma unroll
@@ -292,12 +299,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
 #pragma unroll
         for (int u = 0; u < B; ++u)
 #pragma unroll
-          for (int i = 0; i < kGateA; ++i)
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-              const float f = bf16_to_f32(aa[u][i].h[c]);
-              sq[i] = fmaf(f, f, sq[i]);
-            }
+          for (int i = 0; i < kGateA; ++i) accsq[i] = mfma16x16x32(aa[u][i].v, aa[u][i].v, accsq[i]);
       }
     };
     if (s_lo < s_hi) load(s_lo, a[0], b[0]);
@@ -310,12 +312,16 @@ __global__ __launch_bounds__(256) void gate_kernel(
       compute(a[1], b[1]);
     }
     if (inv_norm) {
-      // the four 8-column pieces of a token row sit in lanes l, l+16, l+32, l+48
+      // element (m, m) of the 16 x 16 Gram sits in lane 16 (m / 4) + m,
+      // register m % 4
+      const int m = lane & 15;
+      if ((m >> 2) == (lane >> 4)) {
 #pragma unroll
-      for (int i = 0; i < kGateA; ++i) {
-        sq[i] += __shfl_xor(sq[i], 16, 64);
-        sq[i] += __shfl_xor(sq[i], 32, 64);
-        if (lane < 16) sumsq[w][16 * i + lane] = sq[i];
+        for (int i = 0; i < kGateA; ++i) {
+          const int r = m & 3;
+          const float v = r == 0 ? accsq[i][0] : (r == 1 ? accsq[i][1] : (r == 2 ? accsq[i][2] : accsq[i][3]));
+          sumsq[w][16 * i + m] = v;
+        }
       }
     }
     // lane holds logits of tokens 16i + 4(lane/16) + r, expert 16j + lane%16
@@ -324,8 +330,7 @@ __global__ __launch_bounds__(256) void gate_kernel(
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (j < nE16)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) part[w][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
+          *reinterpret_cast<f32x4*>(&part[w][16 * j + (lane & 15)][16 * i + 4 * (lane >> 4)]) = acc[i][j];
   } else {
     // float32 inputs: lane = token (lanes past TOK have none), experts
     // strided over the four waves
@@ -335,10 +340,10 @@ __global__ __launch_bounds__(256) void gate_kernel(
     for (int e = w; e < E && lane < TOK; e += 4) {
       float s = 0.f;
       for (int i = 0; i < d; ++i) s = fmaf(X[static_cast<size_t>(t) * d + i], W[static_cast<size_t>(e) * d + i], s);
-      part[0][lane][e] = s;
-      part[1][lane][e] = 0.f;
-      part[2][lane][e] = 0.f;
-      part[3][lane][e] = 0.f;
+      part[0][e][lane] = s;
+      part[1][e][lane] = 0.f;
+      part[2][e][lane] = 0.f;
+      part[3][e][lane] = 0.f;
     }
     if (inv_norm && lane < TOK) {
       float s = 0.f;
@@ -351,26 +356,17 @@ __global__ __launch_bounds__(256) void gate_kernel(
     const float ss = ((sumsq[0][threadIdx.x] + sumsq[1][threadIdx.x]) + sumsq[2][threadIdx.x]) + sumsq[3][threadIdx.x];
     inv_norm[t0 + threadIdx.x] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
   }
-  // partial tiles summed in wave order into part[0], one (token, expert)
+  // partial tiles summed in wave order into part[0], one (expert, token)
   // pair per thread at a time
-  // (token tl, expert e) = divmod(i, E), advanced by divmod(256, E) per
-  // step rather than divided out each time
-  float (*logit)[kMaxExperts + 1] = part[0];
   {
-    const int dq = 256 / E, dr = 256 - dq * E;
-    int tl = static_cast<int>(threadIdx.x) / E, e = static_cast<int>(threadIdx.x) - tl * E;
-    for (; tl < TOK; tl += dq, e += dr) {
-      if (e >= E) {
-        e -= E;
-        ++tl;
-        if (tl >= TOK) break;
-      }
-      logit[tl][e] = ((part[0][tl][e] + part[1][tl][e]) + part[2][tl][e]) + part[3][tl][e] + bias[e];
-    }
+    constexpr int kPerStep = 256 / TOK;
+    const int tl = static_cast<int>(threadIdx.x) % TOK;
+    for (int e = static_cast<int>(threadIdx.x) / TOK; e < E; e += kPerStep)
+      part[0][e][tl] = ((part[0][e][tl] + part[1][e][tl]) + part[2][e][tl]) + part[3][e][tl] + bias[e];
   }
   __syncthreads();
-  gate_select<BF16, TOK>(logit, bias, cnt, choice, xv, wv, T, d, E, k, t0, ch, nchunks, topk_idx, topk_gate,
-                         slot_rank, hist);
+  gate_select<BF16, TOK>(&part[0][0][0], bias, cnt, choice, xv, wv, T, d, E, k, t0, ch, nchunks, topk_idx,
+                         topk_gate, slot_rank, hist);
 }
 
 // One block per expert: exclusive scan of that expert's chunk counts (in
