@@ -161,19 +161,34 @@ struct TileCoord {
 // Bucket of tile `tile` (the last e with tile_off[e] <= tile, skipping
 // empty buckets), its first tile, first slot and size.  One load per lane
 // (lane e holds bucket e, E <= 64) and a ballot: a single round trip instead
-// of a walk of dependent loads.  Called by whole waves.
-__device__ __forceinline__ void locate_bucket(int tile, const int32_t* __restrict__ tile_off,
-                                              const int32_t* __restrict__ offsets, int E, int& e, int& tbase,
-                                              int& lo, int& n) {
+// of a walk of dependent loads.  Called by whole waves.  The _from form
+// takes the three per-lane values already loaded (bucket_lookup_loads).
+__device__ __forceinline__ void bucket_lookup_loads(const int32_t* __restrict__ tile_off,
+                                                    const int32_t* __restrict__ offsets, int E, int& to, int& o0,
+                                                    int& o1) {
   const int lane = threadIdx.x & 63;
   const bool in = lane < E;
-  const int to = in ? tile_off[lane] : 0;
-  const int o0 = in ? offsets[lane] : 0;
-  const int o1 = in ? offsets[lane + 1] : 0;
+  to = in ? tile_off[lane] : 0;
+  o0 = in ? offsets[lane] : 0;
+  o1 = in ? offsets[lane + 1] : 0;
+}
+
+__device__ __forceinline__ void locate_bucket_from(int tile, int to, int o0, int o1, int E, int& e, int& tbase,
+                                                   int& lo, int& n) {
+  const int lane = threadIdx.x & 63;
+  const bool in = lane < E;
   e = __popcll(__ballot(in && lane >= 1 && to <= tile));
   tbase = __builtin_amdgcn_readfirstlane(__shfl(to, e, 64));
   lo = __builtin_amdgcn_readfirstlane(__shfl(o0, e, 64));
   n = __builtin_amdgcn_readfirstlane(__shfl(o1, e, 64)) - lo;
+}
+
+__device__ __forceinline__ void locate_bucket(int tile, const int32_t* __restrict__ tile_off,
+                                              const int32_t* __restrict__ offsets, int E, int& e, int& tbase,
+                                              int& lo, int& n) {
+  int to, o0, o1;
+  bucket_lookup_loads(tile_off, offsets, E, to, o0, o1);
+  locate_bucket_from(tile, to, o0, o1, E, e, tbase, lo, n);
 }
 
 __device__ __forceinline__ TileCoord decode_tile(int tile, const int32_t* __restrict__ tile_off,
@@ -224,11 +239,10 @@ __device__ __forceinline__ void write_tile_words(const TileCoord& c, const uint1
 // full rows above the group's diagonal block, then its upper triangle.  Any
 // 32 consecutive tiles then cover about 8 row blocks x 4 column blocks, so
 // the blocks of one XCD that run them together share operand rows in L2.
-__device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t* __restrict__ tile_off,
-                                                         const int32_t* __restrict__ offsets, int E) {
+__device__ __forceinline__ TileCoord decode_tile_grouped_from(int tile, int to, int o0, int o1, int E) {
   TileCoord c;
   int tbase;
-  locate_bucket(tile, tile_off, offsets, E, c.e, tbase, c.lo, c.n);
+  locate_bucket_from(tile, to, o0, o1, E, c.e, tbase, c.lo, c.n);
   c.W = (c.n + 63) / 64;
   const int nt = (c.n + kTile - 1) / kTile;
   const int q = tile - tbase;
@@ -250,6 +264,13 @@ __device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t
   return c;
 }
 
+__device__ __forceinline__ TileCoord decode_tile_grouped(int tile, const int32_t* __restrict__ tile_off,
+                                                         const int32_t* __restrict__ offsets, int E) {
+  int to, o0, o1;
+  bucket_lookup_loads(tile_off, offsets, E, to, o0, o1);
+  return decode_tile_grouped_from(tile, to, o0, o1, E);
+}
+
 // v_writelane_b32: `old` with lane `lane` replaced by the wave-uniform
 // `value` (the LLVM intrinsic, which clang does not expose as a builtin).
 __device__ int amdgcn_writelane(int value, int lane, int old) __asm("llvm.amdgcn.writelane");
@@ -257,99 +278,217 @@ __device__ int amdgcn_writelane(int value, int lane, int old) __asm("llvm.amdgcn
 using GramGemm = GemmBig64;
 static_assert(GramGemm::BM == kTile && GramGemm::BN == kTile, "similarity tile");
 
+// Tokens of a tile's DMA rows (P rows of tile-row ti, Q rows of tile-row
+// tj; rows past the bucket repeat its last row and are not fetched) and the
+// token whose inverse norm this thread stages for the epilogue: thread
+// i < kTile P row i's, thread kTile + i Q row i's.
+__device__ __forceinline__ void gram_tile_tokens(const TileCoord& c, const int32_t* __restrict__ perm_token,
+                                                 int32_t (&ptok)[GramGemm::LP], int32_t (&qtok)[GramGemm::LQ],
+                                                 int32_t& itok) {
+  using G = GramGemm;
+  static_assert(G::THREADS == 2 * kTile, "one inverse norm per thread");
+  const int32_t* pt = perm_token + c.lo;
+#pragma unroll
+  for (int j = 0; j < G::LP; ++j) ptok[j] = pt[min(c.ti * kTile + G::load_row(j), c.n - 1)];
+#pragma unroll
+  for (int j = 0; j < G::LQ; ++j) qtok[j] = pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)];
+  const int i = threadIdx.x;
+  const int r = i < kTile ? c.ti * kTile + i : c.tj * kTile + i - kTile;
+  itok = r < c.n ? pt[r] : -1;
+}
+
+// Inverse norm staged for the epilogue: NaN for a row outside the bucket,
+// which fails every comparison.
+__device__ __forceinline__ float gram_stage_inv(const float* __restrict__ inv_norm, int32_t itok) {
+  return itok >= 0 ? inv_norm[itok] : __builtin_nanf("");
+}
+
+// bits * 2 + (p >= h): the comparison's bit shifted in through the carry
+// (an ordered compare: a NaN p shifts in 0).  A VALU read of VCC needs two
+// wait states after the VALU write of it: the _next form fills them with the
+// next element's product q = (a * b) * c, the last form with a nop.
+__device__ __forceinline__ uint32_t shift_in_ge_next(uint32_t bits, float p, float h, float a, float b, float c,
+                                                     float& q) {
+  asm("v_cmp_le_f32 vcc, %3, %2\n\t"
+      "v_mul_f32 %1, %4, %5\n\t"
+      "v_mul_f32 %1, %6, %1\n\t"
+      "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+      : "+v"(bits), "=&v"(q)
+      : "v"(p), "s"(h), "v"(a), "v"(b), "v"(c)
+      : "vcc");
+  return bits;
+}
+
+__device__ __forceinline__ uint32_t shift_in_ge_last(uint32_t bits, float p, float h) {
+  asm("v_cmp_le_f32 vcc, %2, %1\n\t"
+      "s_nop 1\n\t"
+      "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+      : "+v"(bits)
+      : "v"(p), "s"(h)
+      : "vcc");
+  return bits;
+}
+
+// One step of the 32 x 32 bit transpose below: lanes i and i ^ S of a
+// half-wave trade the S-bit fields in which bit S of the lane index and of
+// the bit index differ.
+template <int S>
+__device__ __forceinline__ uint32_t transpose_step(uint32_t x, int i) {
+  constexpr uint32_t m0 = S == 16 ? 0x0000FFFFu : S == 8 ? 0x00FF00FFu : S == 4 ? 0x0F0F0F0Fu
+                        : S == 2 ? 0x33333333u : 0x55555555u;   // bits j with bit S of j clear
+  // ds_swizzle bit mode within 32 lanes: and-mask 31, xor-mask S
+  const uint32_t y = static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x1F | (S << 10)));
+  const bool up = (i & S) != 0;
+  // lower lane: the partner's m0 fields move up by S; upper lane: its ~m0 fields move down by S
+  const uint32_t t = __builtin_amdgcn_alignbit(y, y, up ? S : 32 - S);
+  const uint32_t keep = up ? ~m0 : m0;
+  return (x & keep) | (t & ~keep);
+}
+
+// 32 x 32 bit transpose within each half-wave: lane c holds word c of a
+// square bit matrix (bit j: entry (j, c)); afterwards lane j holds the word
+// with bit c = entry (j, c).
+__device__ __forceinline__ uint32_t transpose32_bits(uint32_t x) {
+  const int i = opaque_tid() & 31;   // per-lane masks recomputed here, not hoisted out of the tile loop
+  x = transpose_step<16>(x, i);
+  x = transpose_step<8>(x, i);
+  x = transpose_step<4>(x, i);
+  x = transpose_step<2>(x, i);
+  return transpose_step<1>(x, i);
+}
+
+// Persistent over the upper-triangle tiles of every bucket.  The loop is
+// software-pipelined across tiles: the next tile's bucket lookup is loaded
+// before the current tile's K loop (nothing waits on it until the loop is
+// over, so it does not hold up the loop's first stages, which the in-order
+// load counter would otherwise tie to it); right after the K loop the next
+// tile's row tokens are loaded, their latency hidden by this tile's
+// compares, and its first DMA stages are issued before the rest of this
+// tile's epilogue, which therefore keeps its bit pieces outside the operand
+// ring.
 __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
   using G = GramGemm;
+  static_assert(G::FN % 2 == 0, "column blocks are transposed in pairs");
   __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
-  __shared__ __attribute__((aligned(16))) float inv_a[kTile];
-  __shared__ float inv_b[kTile];
-  // after the K loop the operand buffers hold the tile's adjacency pieces:
-  // dbits[row][32-column group], tbits[column][32-row group]
-  uint32_t (*dbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds);
-  uint32_t (*tbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kTile * kTile / 8);
+  // inverse norms of the tile's P rows (0..kTile-1) and Q rows (kTile..)
+  __shared__ __attribute__((aligned(16))) float inv_ab[2 * kTile];
+  // the tile's adjacency pieces: dbits[row][32-column group], tbits[column][32-row group]
+  __shared__ uint32_t dbits[kTile][kTile / 32];
+  __shared__ uint32_t tbits[kTile][kTile / 32];
+  const float* inv_a = inv_ab;
+  const float* inv_b = inv_ab + kTile;
   if (*err) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int w = G::wave();
   const int wm = G::wave_m(w), wn = G::wave_n(w);
   const int total = tile_off[E];
-  for (int tile = xcd_virtual_block(); tile < total; tile += gridDim.x) {
-    const TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
-    const int32_t* pt = perm_token + c.lo;
-    uint32_t poff[G::LP], qoff[G::LQ];
+  int tile = xcd_virtual_block();
+  if (tile >= total) return;   // block-uniform, before any barrier
+  TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
+  int32_t ptok[G::LP], qtok[G::LQ], itok;
+  uint32_t poff[G::LP], qoff[G::LQ];
+  gram_tile_tokens(c, perm_token, ptok, qtok, itok);
 #pragma unroll
-    for (int j = 0; j < G::LP; ++j)
-      poff[j] = static_cast<uint32_t>(pt[min(c.ti * kTile + G::load_row(j), c.n - 1)]) * d;
+  for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
 #pragma unroll
-    for (int j = 0; j < G::LQ; ++j)
-      qoff[j] = static_cast<uint32_t>(pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)]) * d;
-    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
-      if (i < kTile) inv_a[i] = inv_norm[pt[min(c.ti * kTile + i, c.n - 1)]];
-      else inv_b[i - kTile] = inv_norm[pt[min(c.tj * kTile + i - kTile, c.n - 1)]];
-    }
+  for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
+  float inv = gram_stage_inv(inv_norm, itok);
+  G::Pipe pipe;
+  G::prefetch(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, pipe);
+  for (;;) {
+    inv_ab[opaque_tid()] = inv;   // visible after the K loop's first barrier
+    const int next = tile + gridDim.x;
+    int nto = 0, no0 = 0, no1 = 0;
+    if (next < total) bucket_lookup_loads(tile_off, offsets, E, nto, no0, no1);
     G::Acc acc;
     G::zero(acc);
-    G::run(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, acc);  // ends with a barrier
+    G::resume(pipe, lds, acc);   // ends with a barrier: the ring is free
+    TileCoord cn = c;
+    if (next < total) {
+      cn = decode_tile_grouped_from(next, nto, no0, no1, E);
+      gram_tile_tokens(cn, perm_token, ptok, qtok, itok);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 
     // Each (fm, fn) block is 32 x 32.  Lane l holds column bbase + l%32 and,
     // in accumulator v, row abase + rv(v) + 4*(l/32), rv(v) = 8(v/4) + v%4.
-    // Ballot v is then two row pieces: bits 0..31 are the columns of row
-    // abase + rv(v), bits 32..63 those of row abase + rv(v) + 4; lane r < 32
-    // receives row r's piece by writelane.  The column piece of column
-    // bbase + c has bit rv(v) (+4 in the upper half-wave) from accumulator v:
-    // each lane assembles its 16 bits with selects on its own compares, and
-    // lanes c and c+32 merge theirs with one cross-half exchange.  Every piece
-    // of the tile is written exactly once.  Edge test:
-    // dot * (1/|a|) * (1/|b|) >= h, for rows and columns inside the bucket,
-    // never a token with itself.
-    const int l31 = lane & 31, hi = lane >> 5;
+    // Each lane shifts its 16 compare bits into a word (accumulator v at bit
+    // v) and spreads them to bits rv(v); lanes c and c+32 merge theirs with
+    // one cross-half exchange, which gives the column pieces (the mirrored
+    // tile's row words).  The row pieces are the bit transposes of the
+    // column pieces: the two column blocks of a wave are transposed
+    // together, one per half-wave.  Edge test: dot * (1/|a|) * (1/|b|) >= h
+    // (rows outside the bucket carry a NaN scale), never a token with
+    // itself.
+    // lane values recomputed from the opaque thread index: hoisted out of
+    // the tile loop they would stay live across the K loop
+    const int el = opaque_tid() & 63;
+    const int l31 = el & 31, hi = el >> 5;
     const bool same_tile = c.ti == c.tj;
-    const int nrow_a = c.n - c.ti * kTile, nrow_b = c.n - c.tj * kTile;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
       const int abase = wm * G::WTM + 32 * fm;
-      // this lane's 16 rows: abase + 8q + 4hi + r, as 4 runs of 4.  Rows
-      // (and columns) outside the bucket get a NaN scale, which fails every
-      // comparison.
-      const float nan = __builtin_nanf("");
+      // this lane's 16 rows: abase + 8q + 4hi + r, as 4 runs of 4
       float ia[16];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int al0 = abase + 8 * q + 4 * hi;
-        const float4 f = *reinterpret_cast<const float4*>(&inv_a[al0]);
-        const float fv[4] = {f.x, f.y, f.z, f.w};
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ia[4 * q + r] = al0 + r < nrow_a ? fv[r] : nan;
+        const float4 f = *reinterpret_cast<const float4*>(&inv_a[abase + 8 * q + 4 * hi]);
+        ia[4 * q] = f.x;
+        ia[4 * q + 1] = f.y;
+        ia[4 * q + 2] = f.z;
+        ia[4 * q + 3] = f.w;
       }
+      uint32_t col[G::FN];
 #pragma unroll
       for (int fn = 0; fn < G::FN; ++fn) {
         const int bbase = wn * G::WTN + 32 * fn;
         const int bl = bbase + l31;
-        const float ib = bl < nrow_b ? inv_b[bl] : nan;
-        const bool diag = same_tile && abase == bbase;   // wave-uniform
-        uint32_t colbits = 0, piece = 0;
+        const float ib = inv_b[bl];
+        uint32_t bits = 0;
+        float p = acc[fm][fn][15] * ia[15] * ib;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int rv = 8 * (v >> 2) + (v & 3);
-          bool e = acc[fm][fn][v] * ia[v] * ib >= h;
-          if (diag) e = e && rv + 4 * hi != l31;
-          const uint64_t m = __ballot(e);
-          piece = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(m)), rv, piece);
-          piece = amdgcn_writelane(static_cast<int>(static_cast<uint32_t>(m >> 32)), rv + 4, piece);
-          colbits |= e ? 1u << rv : 0u;
+        for (int v = 15; v >= 1; --v) {
+          float q;
+          bits = shift_in_ge_next(bits, p, h, acc[fm][fn][v - 1], ia[v - 1], ib, q);
+          p = q;
         }
-        colbits <<= 4 * hi;
-        const uint32_t tv = colbits | static_cast<uint32_t>(__shfl_xor(static_cast<int>(colbits), 32, 64));
-        if (lane < 32) {
-          dbits[abase + l31][bbase >> 5] = piece;
-          tbits[bl][abase >> 5] = tv;
-        }
+        bits = shift_in_ge_last(bits, p, h);
+        // nibble k (accumulators 4k..4k+3) to bits 8k..8k+3, then this half's rows
+        bits = (bits & 0xFFu) | ((bits & 0xFF00u) << 8);
+        bits = (bits & 0x000F000Fu) | ((bits & 0x00F000F0u) << 4);
+        bits <<= 4 * hi;
+        uint32_t cw = bits | static_cast<uint32_t>(__shfl_xor(static_cast<int>(bits), 32, 64));
+        if (same_tile && abase == bbase) cw &= ~(1u << l31);   // the token with itself
+        col[fn] = cw;
+        if (hi == 0) tbits[bl][abase >> 5] = cw;
+      }
+#pragma unroll
+      for (int p = 0; p < G::FN / 2; ++p) {
+        // lower half-wave: block 2p, upper: block 2p + 1 (a select, not an
+        // indexed read, which would put col in memory)
+        const uint32_t sel = col[2 * p] ^ ((col[2 * p] ^ col[2 * p + 1]) & (0u - static_cast<uint32_t>(hi)));
+        const uint32_t rowbits = transpose32_bits(sel);
+        dbits[abase + l31][(wn * G::WTN + 32 * (2 * p + hi)) >> 5] = rowbits;
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    if (next < total) {
+#pragma unroll
+      for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
+#pragma unroll
+      for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
+      inv = gram_stage_inv(inv_norm, itok);   // before the DMA: waiting for it then does not wait for the DMA
+      G::prefetch(X, poff, X, qoff, d, cn.n - cn.ti * kTile, cn.n - cn.tj * kTile, lds, pipe);
+    }
+    // LDS-only barriers from here on: a full __syncthreads() would also wait
+    // for the next tile's DMA
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's pieces are in LDS
+    raw_barrier();
     // degree: edges of each tile row (and, off the diagonal, of each mirrored row)
-    for (int i = tid; i < 2 * kTile; i += G::THREADS) {
+    for (int i = opaque_tid(); i < 2 * kTile; i += G::THREADS) {
       const bool mirror = i >= kTile;
       const int rl = mirror ? i - kTile : i;
       const uint32_t* pcs = mirror ? tbits[rl] : dbits[rl];
@@ -360,7 +499,7 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
       if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
     }
     // write the words: 4 per row of the tile, direct and (off-diagonal) mirrored
-    for (int i = tid; i < kTile * 4; i += G::THREADS) {
+    for (int i = opaque_tid(); i < kTile * 4; i += G::THREADS) {
       const int rl = i >> 2, ww = i & 3;
       const uint64_t dv = static_cast<uint64_t>(dbits[rl][2 * ww]) |
                           (static_cast<uint64_t>(dbits[rl][2 * ww + 1]) << 32);
@@ -373,7 +512,13 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
         if (bb < c.n && wt < c.W) bitmask[bm_off[c.e] + static_cast<long long>(bb) * c.W + wt] = tv;
       }
     }
-    __syncthreads();
+    if (next >= total) break;
+    // every wave's reads of the pieces and of inv_ab are done before the
+    // next tile overwrites them
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    raw_barrier();
+    tile = next;
+    c = cn;
   }
 }
 

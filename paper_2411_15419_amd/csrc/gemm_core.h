@@ -354,6 +354,38 @@ struct GemmCore {
     }
   }
 
+  // DMA state of a tile between prefetch() and resume().
+  struct Pipe {
+    __amdgpu_buffer_rsrc_t prs, qrs;
+    uint32_t goff[LOADS];
+    int nk, pld, qld, kvalid;
+  };
+
+  // First half of run(): issues the DMA of the tile's first min(K/BK,
+  // STAGES) stages into the LDS ring (every stage buffer must be free: after
+  // a run()/resume() of the previous tile, whose closing barrier
+  // guarantees it).  A persistent kernel calls it before the previous
+  // tile's epilogue so that the epilogue hides the fetch latency; the
+  // epilogue must then keep out of the ring's LDS.
+  static __device__ __forceinline__ void prefetch(const uint16_t* __restrict__ pbase, const uint32_t (&poff)[LP],
+                                                  const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
+                                                  int K, int pvalid, int qvalid, uint8_t* lds_generic, Pipe& p,
+                                                  int pld = 0, int qld = 0, int kvalid = 0x7fffffff) {
+    const lds_ptr lds = (lds_ptr)lds_generic;
+    const int w = wave();
+    p.prs = rsrc(pbase);
+    p.qrs = rsrc(qbase);
+    p.pld = pld;
+    p.qld = qld;
+    p.kvalid = kvalid;
+    dma_offsets(poff, qoff, pvalid, qvalid, p.goff);
+    p.nk = __builtin_amdgcn_readfirstlane(K / BK);
+    const int pro = min(p.nk, STAGES);
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+      if (s < pro) issue(p.prs, p.qrs, p.goff, s, lds + s * STAGE_BYTES, w, pld, qld, kvalid);
+  }
+
   // poff[j] (j < LP): element offset of P row load_row(j);
   // qoff[j] (j < LQ): element offset of Q row load_row(LP + j) - BM.
   // Only the first pvalid P rows and qvalid Q rows are fetched; the LDS
@@ -377,18 +409,26 @@ struct GemmCore {
                                              const uint16_t* __restrict__ qbase, const uint32_t (&qoff)[LQ],
                                              int K, int pvalid, int qvalid, uint8_t* lds_generic, Acc& acc,
                                              int pld = 0, int qld = 0, int kvalid = 0x7fffffff) {
+    Pipe p;
+    prefetch(pbase, poff, qbase, qoff, K, pvalid, qvalid, lds_generic, p, pld, qld, kvalid);
+    resume<NQ>(p, lds_generic, acc);
+  }
+
+  // Second half of run(): waits for the prefetched stages and runs the K
+  // loop; ends with a barrier after which the LDS may be reused.
+  template <int NQ = FN>
+  static __device__ __forceinline__ void resume(const Pipe& p, uint8_t* lds_generic, Acc& acc) {
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int lane = opaque_tid() & 63;
     const int w = wave();
     const int wm = wave_m(w), wn = wave_n(w);
-    const __amdgpu_buffer_rsrc_t prs = rsrc(pbase), qrs = rsrc(qbase);
+    const __amdgpu_buffer_rsrc_t prs = p.prs, qrs = p.qrs;
+    const int pld = p.pld, qld = p.qld, kvalid = p.kvalid;
     uint32_t goff[LOADS];
-    dma_offsets(poff, qoff, pvalid, qvalid, goff);
-    const int nk = __builtin_amdgcn_readfirstlane(K / BK);
-    const int pro = min(nk, STAGES);
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-      if (s < pro) issue(prs, qrs, goff, s, lds + s * STAGE_BYTES, w, pld, qld, kvalid);
+    for (int j = 0; j < LOADS; ++j) goff[j] = p.goff[j];
+    const int nk = p.nk;
+    const int pro = min(nk, STAGES);
     wait_stages(pro - 1);
     raw_barrier();
     const int sw = swz(lane & 31);
