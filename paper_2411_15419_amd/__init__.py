@@ -301,7 +301,7 @@ def profile_read():
     return ms.value, n.value
 
 
-KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram", "greedy_round", "greedy_more",
+KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram", "greedy_round", "greedy_push", "greedy_more",
            "greedy_finish", "claim", "rep_local", "rep_finalize", "gather", "ffn1", "ffn2",
            "ffn2_reduce", "combine")
 

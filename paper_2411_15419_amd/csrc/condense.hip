@@ -6,22 +6,27 @@
 //                        degree counters and walk states; its first wave
 //                        lays out every bucket's tiles and bitmask.
 //   gram_kernel_{bf16,f32}  persistent loop over the upper-triangle tiles
-//                        (256 rows bf16, 128 rows fp32) of every bucket's Gram
+//                        (256 rows bf16, 64 rows fp32) of every bucket's Gram
 //                        matrix.  The epilogue turns cos >= h into adjacency
 //                        bits, writes both the tile and its transpose (every
 //                        bitmask word is written exactly once) and adds each
 //                        row's edge count to its degree.
-//   greedy_round_kernel  one round of the parallel form of the greedy walk,
-//                        16 lanes per position (launched twice, which
-//                        decides every position of a union of cliques;
-//                        decided positions return at once).
+//   greedy_round_kernel  first round of the parallel form of the greedy
+//                        walk, 16 lanes per position: keeps every position
+//                        with no undecided neighbour of higher priority.
+//   greedy_push_kernel   second round, from the kept side: each position
+//                        kept so far absorbs its neighbours and makes its
+//                        claims on them (with the first round, this decides
+//                        every position of a union of cliques).
+//   greedy_more_kernel   persistent pass with bounded coherent revisits of
+//                        positions still undecided (dependency chains).
 //   greedy_finish_kernel one workgroup per bucket repeats rounds until the
-//                        bucket is fully decided (after a coalesced check
-//                        that anything is left).
-//   claim_kernel         every kept position offers itself to its
-//                        neighbours (64-bit atomic max of degree, ~position):
-//                        an absorbed position ends with its first-visited
-//                        kept neighbour.
+//                        bucket is fully decided (only when the pass before
+//                        left a position undecided).
+//   claim_kernel         every kept position not yet pushed offers itself to
+//                        its neighbours (64-bit atomic max of degree,
+//                        ~position): an absorbed position ends with its
+//                        first-visited kept neighbour.
 //   rep_local_kernel, rep_finalize_kernel  representative rows by a two-pass
 //                        scan: rep_row, rep_token, rep_offsets.
 //   gather_kernel        optional copy of the representative rows.
@@ -41,7 +46,8 @@
 namespace luffy {
 namespace {
 
-constexpr int kGreedyGridRounds = 2;
+// claim word of a kept position whose claims the push round has made
+constexpr unsigned long long kClaimPushed = ~0ull;
 constexpr int kGreedyPasses = 32;   // visits of a blocked position in the round after the grid rounds
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
 constexpr int kTileF32 = 64;    // similarity tile of the fp32 path
@@ -1265,6 +1271,55 @@ __global__ __launch_bounds__(256) void gram_hist_kernel_f32(
 // change once, from undecided to final).  The single-workgroup finishing
 // pass, which relies on seeing the previous iteration's decisions, reads
 // the states with coherent atomic loads (FRESH = true).
+// U words a lane of a GW-lane group, from word b0 of a row on: looks up the
+// state and degree of every neighbour they hold and notes a kept
+// neighbour or an undecided one of higher priority.
+template <bool FRESH, int GW, int U>
+__device__ __forceinline__ void greedy_scan(int b0, int p, int dp, int lo, int n, int W,
+                                            const uint64_t* __restrict__ row, const int32_t* __restrict__ deg,
+                                            const int32_t* state, bool& kept_nb, bool& blocked) {
+  const int gl = threadIdx.x & (GW - 1);
+  const int wd0 = b0 + gl;
+  uint64_t wv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) wv[u] = wd0 + GW * u < W ? row[wd0 + GW * u] : 0ull;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    uint64_t bits = wv[u];
+    const int cbase = (wd0 + GW * u) * 64;
+    while (bits) {
+      int q[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        q[i] = -1;
+        if (bits) {
+          const int b = __ffsll(static_cast<long long>(bits)) - 1;
+          bits &= bits - 1;
+          if (cbase + b < n) q[i] = lo + cbase + b;   // no bit lies past the bucket
+        }
+      }
+      int st[8], dq[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        st[i] = q[i] >= 0 ? (FRESH ? load_flag(&state[q[i]]) : state[q[i]]) : kStateAbsorbed;
+        dq[i] = q[i] >= 0 ? deg[q[i]] : 0;
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (st[i] == kStateKept) kept_nb = true;
+        else if (st[i] == kStateUndecided && (dq[i] > dp || (dq[i] == dp && q[i] < p))) blocked = true;
+      }
+    }
+  }
+}
+
+// Visit of undecided position p by a GW-lane group: kept if no neighbour is
+// kept or undecided with higher priority, absorbed if a neighbour is kept,
+// else left undecided (returns true).  The row is scanned in chunks and the
+// group stops at its first kept or blocking neighbour: the first chunk has
+// 4 words a lane (most rows stop there), later ones 8, so that a row
+// scanned to its end (every neighbour of lower priority) takes half the
+// dependent round trips.
 template <bool FRESH, int GW>
 __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
                                              const uint64_t* __restrict__ row,
@@ -1275,43 +1330,9 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
   const uint64_t gmask = GW == 64 ? ~0ull : ((1ull << (GW & 63)) - 1);
   const int dp = deg[p];
   bool kept_nb = false, blocked = false;
-  for (int b0 = 0; b0 < W; b0 += 4 * GW) {
-    const int wd0 = b0 + gl;
-    uint64_t wv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = wd0 + GW * u < W ? row[wd0 + GW * u] : 0ull;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      uint64_t bits = wv[u];
-      const int cbase = (wd0 + GW * u) * 64;
-      while (bits) {
-        int q[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          q[i] = -1;
-          if (bits) {
-            const int b = __ffsll(static_cast<long long>(bits)) - 1;
-            bits &= bits - 1;
-            if (cbase + b < n) q[i] = lo + cbase + b;   // no bit lies past the bucket
-          }
-        }
-        int st[8], dq[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          st[i] = q[i] >= 0 ? (FRESH ? load_flag(&state[q[i]]) : state[q[i]]) : kStateAbsorbed;
-          dq[i] = q[i] >= 0 ? deg[q[i]] : 0;
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          if (st[i] == kStateKept) kept_nb = true;
-          else if (st[i] == kStateUndecided && (dq[i] > dp || (dq[i] == dp && q[i] < p))) blocked = true;
-        }
-      }
-    }
-    // the group stops at its first kept or blocking neighbour: either way p
-    // cannot be kept now, and a position left undecided is decided later
-    if ((__ballot(kept_nb || blocked) >> gshift) & gmask) break;
-  }
+  greedy_scan<FRESH, GW, 4>(0, p, dp, lo, n, W, row, deg, state, kept_nb, blocked);
+  for (int b0 = 4 * GW; b0 < W && !((__ballot(kept_nb || blocked) >> gshift) & gmask); b0 += 8 * GW)
+    greedy_scan<FRESH, GW, 8>(b0, p, dp, lo, n, W, row, deg, state, kept_nb, blocked);
   const bool any_kept = ((__ballot(kept_nb) >> gshift) & gmask) != 0;
   const bool any_blocked = ((__ballot(blocked) >> gshift) & gmask) != 0;
   if (any_kept) {
@@ -1334,24 +1355,71 @@ __device__ __forceinline__ void load_offsets(const int32_t* __restrict__ offsets
   __syncthreads();
 }
 
-// One round over all positions (16 lanes each); decided positions return
-// at once.  Round 0 also publishes the degrees.
+// The first round over all positions (16 lanes each); also publishes the
+// degrees.
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int r, int32_t* __restrict__ degree_out) {
+    const int32_t* __restrict__ deg, int32_t* state, int32_t* __restrict__ degree_out) {
   __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
   load_offsets(offsets, E, soff);
   const int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
   const int gl = threadIdx.x & (kVisitLanes - 1);
   if (p >= soff[E]) return;
-  if (r == 0 && degree_out && gl == 0) degree_out[p] = deg[p];
-  if (state[p] != kStateUndecided) return;
+  if (degree_out && gl == 0) degree_out[p] = deg[p];
+  // every state starts undecided and only p's own visit writes state[p] in
+  // this round: it need not be read
   const int e = bucket_of(soff, E, p);
   const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
   greedy_visit<false, kVisitLanes>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg,
                                    state);
+}
+
+// Second round, pushed from the kept side.  Every position kept by the
+// first round marks each neighbour absorbed (kept positions are never
+// adjacent, so a neighbour of one is absorbed or undecided, and absorbed
+// for good) and offers itself as the neighbour's representative, as
+// claim_kernel does; its own claim word (unused for a kept position) then
+// tells claim_kernel to skip it.  Only kept rows are read, each once,
+// instead of every undecided row and then the kept rows again for the
+// claims.  Positions left undecided (no kept neighbour yet) go to the
+// passes after it.
+__global__ __launch_bounds__(256) void greedy_push_kernel(
+    const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
+    const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
+    const int32_t* __restrict__ deg, int32_t* state, unsigned long long* __restrict__ claim) {
+  __shared__ int soff[kMaxExperts + 1];
+  if (*err) return;
+  load_offsets(offsets, E, soff);
+  const int q = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
+  const int gl = threadIdx.x & (kVisitLanes - 1);
+  if (q >= soff[E] || state[q] != kStateKept) return;
+  const int e = bucket_of(soff, E, q);
+  const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
+  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
+  const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
+                                 static_cast<unsigned int>(~static_cast<unsigned int>(q));
+  constexpr int U = 8;
+  for (int wd0 = gl; wd0 < W; wd0 += U * kVisitLanes) {
+    uint64_t wv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) wv[u] = wd0 + kVisitLanes * u < W ? row[wd0 + kVisitLanes * u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint64_t bits = wv[u];
+      const int cbase = (wd0 + kVisitLanes * u) * 64;
+      while (bits) {
+        const int b = __ffsll(static_cast<long long>(bits)) - 1;
+        bits &= bits - 1;
+        if (cbase + b < n) {
+          state[lo + cbase + b] = kStateAbsorbed;
+          atomicMax(&claim[lo + cbase + b], key);
+        }
+      }
+    }
+  }
+  if (gl == 0) claim[q] = kClaimPushed;
 }
 
 // The round after the grid rounds: a persistent grid, 16 lanes per
@@ -1468,7 +1536,7 @@ __global__ __launch_bounds__(256) void claim_kernel(
   load_offsets(offsets, E, soff);
   const int q = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
   const int gl = threadIdx.x & (kVisitLanes - 1);
-  if (q >= soff[E] || state[q] != kStateKept) return;
+  if (q >= soff[E] || state[q] != kStateKept || claim[q] == kClaimPushed) return;
   const int e = bucket_of(soff, E, q);
   const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
   const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
@@ -1771,9 +1839,10 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   }
   const int wave_blocks = (S + 3) / 4;
   const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
-  for (int r = 0; r < kGreedyGridRounds; ++r)
-    launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-           ws.deg, ws.state, r, degree);
+  launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
+         ws.deg, ws.state, degree);
+  launch("greedy_push", greedy_push_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
+         ws.deg, ws.state, ws.claim);
   launch("greedy_more", greedy_more_kernel, std::min(visit_blocks, persistent_grid()), 256, 0, s, offsets, E,
          ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, ws.left);
   launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
