@@ -284,23 +284,28 @@ __device__ int amdgcn_writelane(int value, int lane, int old) __asm("llvm.amdgcn
 using GramGemm = GemmBig64;
 static_assert(GramGemm::BM == kTile && GramGemm::BN == kTile, "similarity tile");
 
+
 // Tokens of a tile's DMA rows (P rows of tile-row ti, Q rows of tile-row
 // tj; rows past the bucket repeat its last row and are not fetched) and the
-// token whose inverse norm this thread stages for the epilogue: thread
-// i < kTile P row i's, thread kTile + i Q row i's.
+// tokens whose inverse norms this thread stages for the epilogue: entry i
+// of the tile's 2*kTile (P rows, then Q rows) goes to thread i % THREADS,
+// as its (i / THREADS)-th (-1 past the bucket).
+template <class G>
 __device__ __forceinline__ void gram_tile_tokens(const TileCoord& c, const int32_t* __restrict__ perm_token,
-                                                 int32_t (&ptok)[GramGemm::LP], int32_t (&qtok)[GramGemm::LQ],
-                                                 int32_t& itok) {
-  using G = GramGemm;
-  static_assert(G::THREADS == 2 * kTile, "one inverse norm per thread");
+                                                 int32_t (&ptok)[G::LP], int32_t (&qtok)[G::LQ],
+                                                 int32_t (&itok)[2 * kTile / G::THREADS]) {
+  static_assert((2 * kTile) % G::THREADS == 0, "inverse norms per thread");
   const int32_t* pt = perm_token + c.lo;
 #pragma unroll
   for (int j = 0; j < G::LP; ++j) ptok[j] = pt[min(c.ti * kTile + G::load_row(j), c.n - 1)];
 #pragma unroll
   for (int j = 0; j < G::LQ; ++j) qtok[j] = pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)];
-  const int i = threadIdx.x;
-  const int r = i < kTile ? c.ti * kTile + i : c.tj * kTile + i - kTile;
-  itok = r < c.n ? pt[r] : -1;
+#pragma unroll
+  for (int u = 0; u < 2 * kTile / G::THREADS; ++u) {
+    const int i = static_cast<int>(threadIdx.x) + u * G::THREADS;
+    const int r = i < kTile ? c.ti * kTile + i : c.tj * kTile + i - kTile;
+    itok[u] = r < c.n ? pt[r] : -1;
+  }
 }
 
 // Inverse norm staged for the epilogue: NaN for a row outside the bucket,
@@ -378,13 +383,19 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
   using G = GramGemm;
+  constexpr int NI = 2 * kTile / G::THREADS;   // inverse norms staged per thread
   static_assert(G::FN % 2 == 0, "column blocks are transposed in pairs");
-  __shared__ __attribute__((aligned(16))) uint8_t lds[G::LDS_BYTES];
-  // inverse norms of the tile's P rows (0..kTile-1) and Q rows (kTile..)
-  __shared__ __attribute__((aligned(16))) float inv_ab[2 * kTile];
-  // the tile's adjacency pieces: dbits[row][32-column group], tbits[column][32-row group]
-  __shared__ uint32_t dbits[kTile][kTile / 32];
-  __shared__ uint32_t tbits[kTile][kTile / 32];
+  // One LDS array: the operand ring, then the inverse norms of the tile's P
+  // rows (0..kTile-1) and Q rows (kTile..), then the tile's adjacency
+  // pieces, dbits[row][32-column group] and tbits[column][32-row group].
+  // With separate LDS variables the compiler loses the alias scopes that
+  // tell a stage's fragment reads from the DMA into the other stage, and
+  // waits for each stage's DMA right after issuing it (no overlap).
+  constexpr int kInvOff = G::LDS_BYTES, kBitsOff = kInvOff + 2 * kTile * 4;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kBitsOff + 2 * kTile * (kTile / 32) * 4];
+  float* inv_ab = reinterpret_cast<float*>(lds + kInvOff);
+  uint32_t (*dbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kBitsOff);
+  uint32_t (*tbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kBitsOff + kTile * (kTile / 32) * 4);
   const float* inv_a = inv_ab;
   const float* inv_b = inv_ab + kTile;
   if (*err) return;
@@ -394,18 +405,21 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
   int tile = xcd_virtual_block();
   if (tile >= total) return;   // block-uniform, before any barrier
   TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
-  int32_t ptok[G::LP], qtok[G::LQ], itok;
+  int32_t ptok[G::LP], qtok[G::LQ], itok[NI];
   uint32_t poff[G::LP], qoff[G::LQ];
-  gram_tile_tokens(c, perm_token, ptok, qtok, itok);
+  gram_tile_tokens<G>(c, perm_token, ptok, qtok, itok);
 #pragma unroll
   for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
 #pragma unroll
   for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
-  float inv = gram_stage_inv(inv_norm, itok);
+  float inv[NI];
+#pragma unroll
+  for (int u = 0; u < NI; ++u) inv[u] = gram_stage_inv(inv_norm, itok[u]);
   G::Pipe pipe;
   G::prefetch(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, pipe);
   for (;;) {
-    inv_ab[opaque_tid()] = inv;   // visible after the K loop's first barrier
+#pragma unroll
+    for (int u = 0; u < NI; ++u) inv_ab[opaque_tid() + u * G::THREADS] = inv[u];   // visible after the K loop's first barrier
     const int next = tile + gridDim.x;
     int nto = 0, no0 = 0, no1 = 0;
     if (next < total) bucket_lookup_loads(tile_off, offsets, E, nto, no0, no1);
@@ -415,7 +429,7 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     TileCoord cn = c;
     if (next < total) {
       cn = decode_tile_grouped_from(next, nto, no0, no1, E);
-      gram_tile_tokens(cn, perm_token, ptok, qtok, itok);
+      gram_tile_tokens<G>(cn, perm_token, ptok, qtok, itok);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -486,7 +500,9 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
       for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
 #pragma unroll
       for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
-      inv = gram_stage_inv(inv_norm, itok);   // before the DMA: waiting for it then does not wait for the DMA
+      // before the DMA: waiting for them then does not wait for the DMA
+#pragma unroll
+      for (int u = 0; u < NI; ++u) inv[u] = gram_stage_inv(inv_norm, itok[u]);
       G::prefetch(X, poff, X, qoff, d, cn.n - cn.ti * kTile, cn.n - cn.tj * kTile, lds, pipe);
     }
     // LDS-only barriers from here on: a full __syncthreads() would also wait
