@@ -348,8 +348,8 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * milliseconds and the number of launches since the previous read.
  * Kernel names: gate, slot_scan, slot_scatter, norm, gram, hist_cols,
  * hist_gather, hist_header, greedy_round, greedy_push, greedy_more,
- * greedy_finish, claim, rep_local, rep_finalize, gather, ffn1, ffn2,
- * ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
+ * greedy_finish, claim, rep_local, rep_finalize, gather, ffn_queue, ffn1,
+ * ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
  * bwd_z, bwd_act, bwd_da, bwd_dx, bwd_dx_reduce, bwd_gather, bwd_dw2,
  * bwd_dw1.
  * ---------------------------------------------------------------------- */

@@ -150,6 +150,14 @@ constexpr size_t kFfnSlotFloats = static_cast<size_t>(FfnGemm::BM) * FfnGemmWide
 // split-K parts cut K at multiples of this (a multiple of both stage widths)
 constexpr int kFfnKUnit = 64;
 static_assert(kFfnKUnit % FfnGemm::BK == 0 && kFfnKUnit % FfnGemmWide::BK == 0, "K unit");
+// Tail counters of the grouped products of one call (forward 2, backward 3).
+constexpr int kFfnQueueSets = 3;
+
+// Clears the tail counters of the call's products (a kernel, not a memset,
+// so that the call can be captured in a graph).
+__global__ __launch_bounds__(64) void ffn_queue_clear_kernel(int* __restrict__ queue, int n) {
+  if (static_cast<int>(threadIdx.x) < n) queue[threadIdx.x] = 0;
+}
 
 // Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
 // expert per lane, E <= 64).  Expert e's rows are cut into tiles of rt_e
@@ -315,26 +323,46 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
   }
 }
 
-// One product of the FFN for every tile of every expert (persistent).
-// The second product (FIRST = false) has few output columns (d); with few
-// representatives it can have fewer tiles than CUs, and it then splits K
-// (decided on the device from the actual tile count): parts store float32
-// partial tiles and ffn_split_reduce_kernel finishes them.
+// One product of the FFN for every tile of every expert (persistent).  The
+// whole rounds of work items are dealt statically (serpentine, XCD-aware
+// block order: consecutive items share weight and token rows in an XCD's
+// L2); the items left over, the last ones in the order (the smallest
+// experts' tiles), go one at a time through a counter (*tail, zero at
+// launch) to the blocks that finish first.  The second product (FIRST =
+// false) has few output columns (d); with few representatives it can have
+// fewer tiles than CUs, and it then splits K (decided on the device from the
+// actual tile count): parts store float32 partial tiles and
+// ffn_split_reduce_kernel finishes them.
 template <int ACT, bool FIRST, bool WT = false>
 __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
     const uint16_t* __restrict__ A, const int32_t* __restrict__ row_index,
     const int32_t* __restrict__ rep_offsets, int E, int K, int N,
     const uint16_t* __restrict__ W, uint16_t* __restrict__ out, float* __restrict__ split_slots,
-    const uint16_t* __restrict__ aux) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kFfnLds];
+    const uint16_t* __restrict__ aux, int* __restrict__ tail) {
+  // one LDS array: the operand ring, then the block's current tail item (a
+  // second LDS variable would cost the K loop its DMA overlap)
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kFfnLds + 16];
+  int& item_s = *reinterpret_cast<int*>(lds + kFfnLds);
   const FfnTiles map(rep_offsets, E, N);
   const int nk = K / kFfnKUnit;
   const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
   const int total = map.tiles * S;
+  const int g = gridDim.x, rounds = total / g;
   const int vb = xcd_virtual_block();
-  for (int round = 0; round * static_cast<int>(gridDim.x) < total; ++round) {
-    const int tt = serpentine_item(round, vb);
-    if (tt >= total) continue;
+  for (int round = 0;; ++round) {
+    int tt;
+    if (round < rounds) {
+      tt = serpentine_item(round, vb);
+    } else {
+      if (rounds * g == total) break;   // no tail
+      if (threadIdx.x == 0) item_s = rounds * g + atomicAdd(tail, 1);
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the item is in LDS
+      raw_barrier();
+      // read before the tile's barriers: thread 0 writes the next item only
+      // after every thread has passed them
+      tt = item_s;
+      if (tt >= total) break;
+    }
     const int t = tt / S, part = tt - t * S;
     int e, row0, rows, n0;
     bool wide;
@@ -523,14 +551,17 @@ __global__ __launch_bounds__(256) void ffn_kernel_f32(
 struct FfnWs {
   void* hidden;
   float* split_slots;
+  int* queue;   // kFfnQueueSets tail counters
 };
 
 FfnWs carve_ffn(Carver& c, int max_rows, int d_ff, int dtype) {
   FfnWs w;
   w.hidden = c.take<uint8_t>(static_cast<size_t>(max_rows) * d_ff * elem_bytes(dtype));
   w.split_slots = nullptr;
+  w.queue = nullptr;
   if (dtype == LUFFY_BF16) {
     w.split_slots = c.take<float>(kFfnSlotFloats * kFfnMaxSlots);
+    w.queue = c.take<int>(kFfnQueueSets);
   }
   return w;
 }
@@ -543,16 +574,17 @@ void launch_ffn(const void* x, const int32_t* row_index, const int32_t* rep_offs
   void* hidden = ws.hidden;
   if (dtype == LUFFY_BF16) {
     const int grid = persistent_grid();
+    launch("ffn_queue", ffn_queue_clear_kernel, 1, 64, 0, s, ws.queue, 2);
     {
       launch("ffn1", ffn_kernel_bf16<ACT, true>, grid, FfnGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
              row_index, rep_offsets, E, d, d_ff, static_cast<const uint16_t*>(w1), static_cast<uint16_t*>(hidden),
-             ws.split_slots, static_cast<const uint16_t*>(nullptr));
+             ws.split_slots, static_cast<const uint16_t*>(nullptr), ws.queue);
     }
     {
       launch("ffn2", ffn_kernel_bf16<ACT, false>, grid, FfnGemm::THREADS, 0, s,
              static_cast<const uint16_t*>(hidden), nullptr, rep_offsets, E, d_ff, d,
              static_cast<const uint16_t*>(w2), static_cast<uint16_t*>(y_rep), ws.split_slots,
-             static_cast<const uint16_t*>(nullptr));
+             static_cast<const uint16_t*>(nullptr), ws.queue + 1);
     }
     {
       launch("ffn2_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots,
@@ -703,6 +735,7 @@ __global__ __launch_bounds__(WgradGemm::THREADS) void wgrad_kernel(const uint16_
 struct FfnBwdWs {
   uint16_t *z, *a, *dz, *xg;
   float* split_slots;
+  int* queue;   // kFfnQueueSets tail counters
 };
 
 FfnBwdWs carve_ffn_bwd(Carver& c, int max_rows, int E, int d, int d_ff) {
@@ -713,6 +746,7 @@ FfnBwdWs carve_ffn_bwd(Carver& c, int max_rows, int E, int d, int d_ff) {
   w.dz = c.take<uint16_t>(static_cast<size_t>(max_rows) * d_ff);
   w.xg = c.take<uint16_t>(static_cast<size_t>(max_rows) * d);
   w.split_slots = c.take<float>(kFfnSlotFloats * kFfnMaxSlots);
+  w.queue = c.take<int>(kFfnQueueSets);
   return w;
 }
 
@@ -723,19 +757,20 @@ void launch_ffn_bwd(const uint16_t* x, const int32_t* row_index, const int32_t* 
   (void)max_rows;
   const int grid = persistent_grid();
   const int egrid = 4 * grid;
+  launch("ffn_queue", ffn_queue_clear_kernel, 1, 64, 0, s, ws.queue, 3);
   // Z = X W1^T, A = act(Z)
   launch("bwd_z", ffn_kernel_bf16<kActNone, true>, grid, FfnGemm::THREADS, 0, s, x, row_index, rep_offsets, E, d,
-         d_ff, w1, ws.z, ws.split_slots, static_cast<const uint16_t*>(nullptr));
+         d_ff, w1, ws.z, ws.split_slots, static_cast<const uint16_t*>(nullptr), ws.queue);
   launch("bwd_act", act_rows_kernel<ACT>, egrid, 256, 0, s, rep_offsets, E, d_ff, static_cast<const uint16_t*>(ws.z),
          ws.a);
   // dZ = (dY W2) act'(Z): W2 [E][d][d_ff] read K-major (k = output row o)
   constexpr int kDz = ACT == LUFFY_ACT_GELU ? kActDzGelu : kActDzSilu;
   launch("bwd_da", ffn_kernel_bf16<kDz, true, true>, grid, FfnGemm::THREADS, 0, s, dy, nullptr, rep_offsets, E, d,
-         d_ff, w2, ws.dz, ws.split_slots, static_cast<const uint16_t*>(ws.z));
+         d_ff, w2, ws.dz, ws.split_slots, static_cast<const uint16_t*>(ws.z), ws.queue + 1);
   // dX = dZ W1: W1 [E][d_ff][d] read K-major, split over K as the forward's second product
   launch("bwd_dx", ffn_kernel_bf16<kActNone, false, true>, grid, FfnGemm::THREADS, 0, s,
          static_cast<const uint16_t*>(ws.dz), nullptr, rep_offsets, E, d_ff, d, w1, dx, ws.split_slots,
-         static_cast<const uint16_t*>(nullptr));
+         static_cast<const uint16_t*>(nullptr), ws.queue + 2);
   launch("bwd_dx_reduce", ffn_split_reduce_kernel, 8 * grid, 256, 0, s, rep_offsets, E, d_ff, d, ws.split_slots, dx,
          grid);
   // dW2 = dY^T A, dW1 = dZ^T X (X's rows gathered first)
