@@ -138,11 +138,22 @@ __device__ __forceinline__ bool locate_row_tile(const int32_t* __restrict__ rep_
 // split-K slots.
 using FfnGemm = GemmRagged64;
 using FfnGemmWide = GemmCore<256, 320, 4, 2, true, false>;
+// An expert with at most 128 rows (one token tile of 128) streams its weight
+// panels from HBM for little MFMA work, so its tiles are bound by how much
+// of the stream one CU has in flight: the 256 x 128 shape takes a ring of
+// three 64-wide stages in the same LDS (two in flight while one is
+// multiplied, against one for the 256 x 256 shape).
+using FfnGemmSmall = GemmCore<256, 128, 4, 2, true, false, 64, 3>;
 // The backward's row products read the weights transposed: P K-major.
 using FfnGemmT = GemmCore<256, 256, 4, 2, true, false, 64, 2, true, false>;
 using FfnGemmWideT = GemmCore<256, 320, 4, 2, true, false, 64, 2, true, false>;
+using FfnGemmSmallT = GemmCore<256, 128, 4, 2, true, false, 64, 3, true, false>;
 static_assert(FfnGemm::BM == FfnGemmWide::BM && FfnGemm::THREADS == FfnGemmWide::THREADS, "shared tile map");
+static_assert(FfnGemm::BM == FfnGemmSmall::BM && FfnGemm::THREADS == FfnGemmSmall::THREADS, "shared tile map");
 constexpr int kFfnLds = FfnGemmWide::LDS_BYTES > FfnGemm::LDS_BYTES ? FfnGemmWide::LDS_BYTES : FfnGemm::LDS_BYTES;
+static_assert(FfnGemmSmall::LDS_BYTES <= kFfnLds && FfnGemmSmallT::LDS_BYTES <= kFfnLds, "small shape's ring");
+// tile shapes of the tile map
+constexpr int kShapeNarrow = 0, kShapeWide = 1, kShapeSmall = 2;
 // split-K partial tiles: one slot (the accumulators of a tile in register
 // layout) per work item, at most kFfnMaxSlots (>= CUs) work items
 constexpr int kFfnMaxSlots = 1536;
@@ -161,8 +172,8 @@ __global__ __launch_bounds__(64) void ffn_queue_clear_kernel(int* __restrict__ q
 
 // Tile map of the grouped GEMM (persistent kernels; rep_offsets held one
 // expert per lane, E <= 64).  Expert e's rows are cut into tiles of rt_e
-// rows (256, or 320 where that takes fewer tiles); the last one is usually
-// partial.  Tiles are numbered expert by expert; inside an expert,
+// rows (128 for an expert of at most 128 rows, else 256, or 320 where that
+// takes fewer tiles); the last one is usually partial.  Tiles are numbered expert by expert; inside an expert,
 // output-column tiles come in groups of 4 with the row tiles fastest inside
 // a group, so the tiles that share a weight tile run side by side and ~32
 // consecutive tiles (one XCD's share of a round, with the XCD-aware block
@@ -178,8 +189,8 @@ struct FfnTiles {
       elo = rep_offsets[lane];
       ehi = rep_offsets[lane + 1];
       const int n = ehi - elo;
-      constexpr int NB = FfnGemm::BN, WB = FfnGemmWide::BN;
-      rt = (n + WB - 1) / WB < (n + NB - 1) / NB ? WB : NB;
+      constexpr int NB = FfnGemm::BN, WB = FfnGemmWide::BN, SB = FfnGemmSmall::BN;
+      rt = n <= SB ? SB : ((n + WB - 1) / WB < (n + NB - 1) / NB ? WB : NB);
       mt = (n + rt - 1) / rt;
     }
     incl = mt * NT;
@@ -191,8 +202,8 @@ struct FfnTiles {
     tiles = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
   }
   // Tile t -> expert e, first token row row0, row count, first output n0,
-  // and whether it is a wide tile.
-  __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0, bool& wide) const {
+  // and its shape (kShape*).
+  __device__ __forceinline__ void decode(int t, int E, int& e, int& row0, int& rows, int& n0, int& shape) const {
     const int lane = threadIdx.x & 63;
     e = __popcll(__ballot(lane < E && incl <= t));
     const int me = __shfl(mt, e, 64);
@@ -208,7 +219,7 @@ struct FfnTiles {
     row0 = __builtin_amdgcn_readfirstlane(__shfl(elo, e, 64) + ms * rte);
     rows = __builtin_amdgcn_readfirstlane(min(rte, __shfl(ehi, e, 64) - row0));
     n0 = __builtin_amdgcn_readfirstlane(nt * FfnGemm::BM);
-    wide = rte == FfnGemmWide::BN;
+    shape = rte == FfnGemmWide::BN ? kShapeWide : (rte == FfnGemmSmall::BN ? kShapeSmall : kShapeNarrow);
   }
   // Split-K parts per tile (second product only).  Only a product with
   // fewer tiles than blocks splits (with more, every CU already has a tile
@@ -364,17 +375,19 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
       if (tt >= total) break;
     }
     const int t = tt / S, part = tt - t * S;
-    int e, row0, rows, n0;
-    bool wide;
-    map.decode(t, E, e, row0, rows, n0, wide);
+    int e, row0, rows, n0, shape;
+    map.decode(t, E, e, row0, rows, n0, shape);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
     // K range of this part, in whole 64-wide units
     const int k0 = (part * nk / S) * kFfnKUnit, k1 = ((part + 1) * nk / S) * kFfnKUnit;
     float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
     using GN = std::conditional_t<WT, FfnGemmT, FfnGemm>;
     using GW = std::conditional_t<WT, FfnGemmWideT, FfnGemmWide>;
-    if (wide)
+    using GS = std::conditional_t<WT, FfnGemmSmallT, FfnGemmSmall>;
+    if (shape == kShapeWide)
       ffn_tile<GW, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
+    else if (shape == kShapeSmall)
+      ffn_tile<GS, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
     else
       ffn_tile<GN, ACT, FIRST>(A, row_index, We, K, N, k0, k1, row0, rows, n0, out, slot, aux, lds);
   }
@@ -449,19 +462,22 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
   for (int b = blockIdx.x; b < map.tiles * PER_TILE; b += gridDim.x) {
     const int t = b / PER_TILE;
     const int q = ((b - t * PER_TILE) * 256 + threadIdx.x) >> 6;   // (w*FM + fm)*FN + fn
-    int e, row0, rows, n0;
-    bool wide;
-    map.decode(t, E, e, row0, rows, n0, wide);
+    int e, row0, rows, n0, shape;
+    map.decode(t, E, e, row0, rows, n0, shape);
     const float* slots = split_slots + static_cast<size_t>(t) * S * kFfnSlotFloats;
     const bool narrow_unit = q < FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN;
+    const bool small_unit = q < FfnGemmSmall::NWAVES * FfnGemmSmall::FM * FfnGemmSmall::FN;
     if (S == 4) {
-      if (wide) reduce_unit<FfnGemmWide, 4>(slots, q, row0, rows, n0, N, out);
+      if (shape == kShapeWide) reduce_unit<FfnGemmWide, 4>(slots, q, row0, rows, n0, N, out);
+      else if (shape == kShapeSmall) { if (small_unit) reduce_unit<FfnGemmSmall, 4>(slots, q, row0, rows, n0, N, out); }
       else if (narrow_unit) reduce_unit<FfnGemm, 4>(slots, q, row0, rows, n0, N, out);
     } else if (S == 3) {
-      if (wide) reduce_unit<FfnGemmWide, 3>(slots, q, row0, rows, n0, N, out);
+      if (shape == kShapeWide) reduce_unit<FfnGemmWide, 3>(slots, q, row0, rows, n0, N, out);
+      else if (shape == kShapeSmall) { if (small_unit) reduce_unit<FfnGemmSmall, 3>(slots, q, row0, rows, n0, N, out); }
       else if (narrow_unit) reduce_unit<FfnGemm, 3>(slots, q, row0, rows, n0, N, out);
     } else {
-      if (wide) reduce_unit<FfnGemmWide, 2>(slots, q, row0, rows, n0, N, out);
+      if (shape == kShapeWide) reduce_unit<FfnGemmWide, 2>(slots, q, row0, rows, n0, N, out);
+      else if (shape == kShapeSmall) { if (small_unit) reduce_unit<FfnGemmSmall, 2>(slots, q, row0, rows, n0, N, out); }
       else if (narrow_unit) reduce_unit<FfnGemm, 2>(slots, q, row0, rows, n0, N, out);
     }
   }
