@@ -109,9 +109,9 @@ int luffy_route(const void* x, int T, int d, int dtype,
  * hipMalloc): the same arguments and results without the workspace, whose
  * role is taken by a scratch array the library holds in device memory, one
  * per GPU, for the life of the process (luffy_route_noalloc_max_bytes()
- * bytes, 1 MiB).  Calls whose luffy_route_workspace_size(T, E, k) exceeds it
+ * bytes, 4 MiB).  Calls whose luffy_route_workspace_size(T, E, k) exceeds it
  * return LUFFY_E_UNSUPPORTED and enqueue nothing (at E = 64, k = 2 that is
- * T above 131008).  It allocates nothing on any call.  Every call on a GPU
+ * T above 131056).  It allocates nothing on any call.  Every call on a GPU
  * uses that GPU's one array, so calls that can overlap on one GPU (several
  * streams, several host threads) race and must be ordered by the caller.  On
  * its first call on a device (the current device) it looks up the array's

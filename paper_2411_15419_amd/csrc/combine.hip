@@ -92,6 +92,97 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
 }
 
 
+// Column-sliced form: the eight XCDs each take one eighth of every row.
+// Workgroups are dispatched to the XCDs in turn (block b runs on XCD b % 8),
+// so block b covers column slice b % 8 of a run of consecutive tokens, and
+// each XCD's L2 only ever holds its slice of y_rep: a representative row
+// that several slots use (the condensed duplicates) is fetched from HBM
+// about once per slice instead of once per slot.  LPT lanes (a power of two,
+// at most 64) share a token's slice, each with CPL 16-byte chunks; a thread
+// takes U tokens, tokens_per_pass = 256 / LPT apart, so that U * K * CPL
+// loads per lane are in flight before the first is used.
+template <bool BF16, int K, int U>
+__global__ __launch_bounds__(256) void combine_sliced_kernel(const void* __restrict__ y_rep,
+                                                             const int32_t* __restrict__ rep_row,
+                                                             const int32_t* __restrict__ slot_pos,
+                                                             const float* __restrict__ gate, int T, int d,
+                                                             int lpt_log2, int cpl, void* __restrict__ y) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int ES = BF16 ? 2 : 4;          // bytes per element
+  constexpr int EPC = 16 / ES;              // elements per 16-byte chunk
+  const int slice = blockIdx.x & 7;
+  const int tb = blockIdx.x >> 3;
+  const int lpt = 1 << lpt_log2;
+  const int sub = threadIdx.x & (lpt - 1);
+  const int tl = threadIdx.x >> lpt_log2;
+  const int tpp = 256 >> lpt_log2;          // tokens per pass of the block
+  const int slice_chunks = lpt * cpl;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(y_rep),
+                                                                       static_cast<short>(0),
+                                                                       static_cast<int>(kRange), 0x00020000);
+  int tok[U];
+  uint32_t rbase[U][K];
+  float g[U][K];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = (tb * U + u) * tpp + tl;
+    tok[u] = t;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      rbase[u][j] = kRange;
+      g[u][j] = 0.f;
+      const int p = t < T ? slot_pos[static_cast<size_t>(t) * K + j] : -1;
+      if (p >= 0) {
+        rbase[u][j] = static_cast<uint32_t>(rep_row[p]) * static_cast<uint32_t>(d) * ES;
+        g[u][j] = gate[static_cast<size_t>(t) * K + j];
+      }
+    }
+  }
+  for (int cc = 0; cc < cpl; ++cc) {
+    const int c = (slice * slice_chunks + cc * lpt + sub) * EPC;   // first element of this lane's chunk
+    u32x4 v[U][K];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        const uint32_t off = rbase[u][j] == kRange ? kRange : rbase[u][j] + static_cast<uint32_t>(c) * ES;
+        v[u][j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (tok[u] >= T) continue;
+      if constexpr (BF16) {
+        float a[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          a[i] = 0.f;
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            const uint32_t word = v[u][j][i >> 1];
+            const float f = __uint_as_float((i & 1) ? (word & 0xFFFF0000u) : (word << 16));
+            a[i] = fmaf(g[u][j], f, a[i]);
+          }
+        }
+        uint16_t* dst = static_cast<uint16_t*>(y) + static_cast<size_t>(tok[u]) * d;
+        *reinterpret_cast<uint4*>(dst + c) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
+                                                        pack_bf16x2(a[4], a[5]), pack_bf16x2(a[6], a[7]));
+      } else {
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          a.x = fmaf(g[u][j], __uint_as_float(v[u][j][0]), a.x);
+          a.y = fmaf(g[u][j], __uint_as_float(v[u][j][1]), a.y);
+          a.z = fmaf(g[u][j], __uint_as_float(v[u][j][2]), a.z);
+          a.w = fmaf(g[u][j], __uint_as_float(v[u][j][3]), a.w);
+        }
+        float* dst = static_cast<float*>(y) + static_cast<size_t>(tok[u]) * d;
+        *reinterpret_cast<float4*>(dst + c) = a;
+      }
+    }
+  }
+}
+
+
 // ---------------------------------------------------------------- backward
 // Transpose of combine (the condensation held fixed): every kept slot adds
 // gate * dy[t] to its representative's row, and takes <dy[t], y_rep[r]> as
@@ -300,6 +391,27 @@ extern "C" int luffy_combine(const void* y_rep, const int32_t* rep_row,
     return fail(LUFFY_E_UNSUPPORTED, "luffy_combine: y_rep of up to T*k=%lld rows of d=%d must span < 4 GiB - 64 KiB",
                 static_cast<long long>(T) * k, d);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // Top-2 (two source rows a token) takes the column-sliced kernel when a
+  // row's 16-byte chunks split into eight slices of 2^n (n <= 6) or of a
+  // multiple of 64 chunks; top-1, or other widths, one wave per token.
+  // Measured on the expert-parallel share (T = 32768, d = 2048, top-2):
+  // HBM reads 252 -> 136 MB and 57.7 -> 53.3 us; on a top-1 layer of
+  // 65536 tokens (d = 1024) the sliced form ran 30.5 -> 32.5 us.
+  const int chunks = d * (dtype == LUFFY_BF16 ? 2 : 4) / 16;
+  const int sc = chunks / 8;
+  if (k == 2 && chunks % 8 == 0 && ((sc & (sc - 1)) == 0 || sc % 64 == 0)) {
+    const int lpt = std::min(sc, 64);
+    const int lpt_log2 = __builtin_ctz(static_cast<unsigned>(lpt));
+    const int cpl = sc / lpt;
+    const long long tok_per_block = static_cast<long long>(256 / lpt) * 4;
+    const int sblocks = static_cast<int>(8 * ((T + tok_per_block - 1) / tok_per_block));
+#define LUFFY_COMBINE_S(BF, K_, U_) launch("combine", combine_sliced_kernel<BF, K_, U_>, sblocks, 256, 0, s, y_rep, \
+                                           rep_row, slot_pos, topk_gate, T, d, lpt_log2, cpl, y)
+    if (dtype == LUFFY_BF16) LUFFY_COMBINE_S(true, 2, 4);
+    else LUFFY_COMBINE_S(false, 2, 4);
+#undef LUFFY_COMBINE_S
+    return check_launch("luffy_combine");
+  }
   const int blocks = (T + 3) / 4;
   const bool two = d * (dtype == LUFFY_BF16 ? 2 : 4) <= 2 * 64 * 16;   // two chunks per lane cover a row
 #define LUFFY_COMBINE(BF, K_, U_) launch("combine", combine_kernel<BF, K_, U_>, blocks, 256, 0, s, y_rep, rep_row, \

@@ -14,6 +14,7 @@
 //                    capacity-clamped bucket offsets.
 //   slot_scatter_kernel  bucket position of every slot, capacity drop,
 //                    perm_token.
+#include <algorithm>
 #include <cmath>
 #include <mutex>
 
@@ -23,7 +24,7 @@
 // one copy per GPU for the life of the process.  In host code the name only
 // stands for the symbol; kernels get the device address that
 // hipGetSymbolAddress returns for the current device.
-static constexpr size_t kRouteScratchBytes = 1u << 20;
+static constexpr size_t kRouteScratchBytes = 4u << 20;
 static __device__ __align__(256) uint8_t route_scratch[kRouteScratchBytes];
 
 namespace luffy {
@@ -203,7 +204,7 @@ __device__ __forceinline__ void gate_select(const float* lg, const float* bias, 
       __builtin_amdgcn_wave_barrier();
       if (e >= 0 && rank == 0) cw[e] = __popcll(same);
       __builtin_amdgcn_wave_barrier();
-      if (lane < E) hist[(static_cast<size_t>(j) * nchunks + ch) * E + lane] = cw[lane];
+      if (lane < E) hist[static_cast<size_t>(lane) * k * nchunks + static_cast<size_t>(j) * nchunks + ch] = cw[lane];
       if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
       __builtin_amdgcn_wave_barrier();
     }
@@ -369,6 +370,292 @@ __global__ __launch_bounds__(256) void gate_kernel(
                          topk_gate, slot_rank, hist);
 }
 
+// ------------------------------------------------------------ streaming gate
+// bf16 gate for a weight matrix of at most kGateLdsW bytes (E <= 64): one
+// persistent block of 16 waves per CU stages W in LDS once, and every wave
+// then takes chunks of 16 tokens over the whole of d.  A wave keeps eight
+// K steps of token loads (8 KB) in flight while it multiplies the previous
+// eight, so a CU has ~128 KB of its token stream in flight; the logits stay
+// in the MFMA accumulators (lane = expert 16j + lane%16 of tokens
+// 4(lane/16) .. +3) and top-k runs on them in place, with row-wide DPP
+// reductions over the 16 lanes that hold one token's experts, so nothing
+// but the per-chunk slot counts passes through LDS.  A chunk of the slot
+// histogram is one wave's 16 tokens.
+constexpr int kGateLdsW = 128 * 1024;            // bytes of W held in LDS
+constexpr int kGateStreamWaves = 16;
+constexpr int kGateStreamTok = 16;               // tokens per chunk (one wave)
+constexpr int kGateStreamNB = 4;                 // K steps (of 32) per load batch
+
+inline bool gate_stream_ok(int dtype, int E, int d) {
+  return dtype == LUFFY_BF16 && E <= kMaxExperts && static_cast<long long>(E) * d * 2 <= kGateLdsW && d % 64 == 0;
+}
+
+// rotation by N lanes inside each row of 16 lanes (DPP row_ror)
+template <int N>
+__device__ __forceinline__ uint32_t row_ror(uint32_t x) {
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x120 + N, 0xF, 0xF, false));
+}
+// every lane of a row ends with the maximum (or sum) of the row's 16 values
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t x) {
+  x = max(x, row_ror<8>(x));
+  x = max(x, row_ror<4>(x));
+  x = max(x, row_ror<2>(x));
+  return max(x, row_ror<1>(x));
+}
+__device__ __forceinline__ float row_max_f32(float x) {
+  x = fmaxf(x, __uint_as_float(row_ror<8>(__float_as_uint(x))));
+  x = fmaxf(x, __uint_as_float(row_ror<4>(__float_as_uint(x))));
+  x = fmaxf(x, __uint_as_float(row_ror<2>(__float_as_uint(x))));
+  return fmaxf(x, __uint_as_float(row_ror<1>(__float_as_uint(x))));
+}
+__device__ __forceinline__ float row_sum_f32(float x) {
+  x += __uint_as_float(row_ror<8>(__float_as_uint(x)));
+  x += __uint_as_float(row_ror<4>(__float_as_uint(x)));
+  x += __uint_as_float(row_ror<2>(__float_as_uint(x)));
+  return x + __uint_as_float(row_ror<1>(__float_as_uint(x)));
+}
+
+// Order-preserving key of a logit with the expert in its low six bits: a
+// larger key is a larger logit, and among logits equal in their top 26 bits
+// the lower expert.  Dropping the low six mantissa bits moves a value by
+// less than 2^-17 of itself; every decision closer than the float64
+// re-decision margin (2^-11 (1 + |max|), far wider) goes to float64 anyway.
+__device__ __forceinline__ uint32_t logit_key(float v, int e) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (o & ~63u) | static_cast<uint32_t>(63 - e);
+}
+__device__ __forceinline__ float key_value(uint32_t key) {
+  if (key == 0u) return -INFINITY;                  // no such expert
+  const uint32_t o = key & ~63u;
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+__device__ __forceinline__ int key_expert(uint32_t key) { return 63 - static_cast<int>(key & 63u); }
+
+// Float64 re-decision of one token's close call (called by the whole wave;
+// rare): the
+// two largest of the exact logits over the candidate experts cm, in
+// expert order (the lower expert first among equals).
+__device__ __forceinline__ int2 redecide_f64(const uint16_t* __restrict__ xr,
+                                                       const uint16_t* __restrict__ W,
+                                                       const float* __restrict__ bias_g, int d, int E, uint64_t cm) {
+  const int lane = threadIdx.x & 63;
+  double b0 = -INFINITY, b1 = -INFINITY;
+  int j0 = 0, j1 = 0;
+  for (int e = 0; e < E; ++e) {
+    if (!((cm >> e) & 1ull)) continue;
+    double sacc = 0.0;
+    const uint16_t* wr = W + static_cast<size_t>(e) * d;
+    for (int c = lane * 8; c < d; c += 512) {
+      Pack16 xa, wa;
+      xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
+      wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        sacc += static_cast<double>(bf16_to_f32(xa.h[u])) * static_cast<double>(bf16_to_f32(wa.h[u]));
+    }
+    sacc = wave_sum_f64(sacc);
+    sacc += static_cast<double>(bias_g ? bias_g[e] : 0.f);
+    if (sacc > b0) { b1 = b0; j1 = j0; b0 = sacc; j0 = e; }
+    else if (sacc > b1) { b1 = sacc; j1 = e; }
+  }
+  return make_int2(j0, j1);
+}
+
+template <int NEB>
+__global__ __launch_bounds__(kGateStreamWaves * 64) void gate_stream_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, const float* __restrict__ bias_g, int T, int d,
+    int E, int k, int nchunks, int32_t* __restrict__ topk_idx, float* __restrict__ topk_gate,
+    int32_t* __restrict__ slot_rank, int32_t* __restrict__ hist, int* __restrict__ scan_done,
+    float* __restrict__ inv_norm) {
+  // W (row e, 16-byte chunk c at e * d/8 + (c ^ (e & 7)): the 16 rows one
+  // fragment read touches fall on distinct banks), then 64 slot counts a wave
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kGateLdsW + kGateStreamWaves * kMaxExperts * 4];
+  uint4* wl = reinterpret_cast<uint4*>(lds);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int m = lane & 15, q = lane >> 4;
+  const int cpr = d >> 3;                          // 16-byte chunks per W row
+  if (blockIdx.x == 0 && tid == 0) *scan_done = 0;   // armed for slot_scan_kernel
+  for (int i = tid; i < E * cpr; i += kGateStreamWaves * 64) {
+    const int e = i / cpr, c = i - e * cpr;
+    wl[e * cpr + (c ^ (e & 7))] = reinterpret_cast<const uint4*>(W)[i];
+  }
+  // per expert block j: this lane's W row base, its chunk swizzle folded
+  // with the lane's K group, and the expert's bias (-inf past E)
+  int brow[NEB], bsw[NEB];
+  float bias[NEB];
+#pragma unroll
+  for (int j = 0; j < NEB; ++j) {
+    const int e = 16 * j + m;
+    const int er = min(e, E - 1);
+    brow[j] = er * cpr;
+    bsw[j] = q ^ (er & 7);
+    bias[j] = e < E ? (bias_g ? bias_g[e] : 0.f) : -INFINITY;
+  }
+  int* cw = reinterpret_cast<int*>(lds + kGateLdsW) + w * kMaxExperts;
+  __syncthreads();
+
+  const int nsteps = d >> 5;
+  constexpr int NB = kGateStreamNB;
+  for (int ch = blockIdx.x * kGateStreamWaves + w; ch < nchunks; ch += gridDim.x * kGateStreamWaves) {
+    const int t0 = ch * kGateStreamTok;
+    const uint16_t* arow = X + static_cast<size_t>(min(t0 + m, T - 1)) * d + 8 * q;
+    Pack16 a[2][NB];
+    auto load = [&](int s0, Pack16 (&aa)[NB]) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        aa[u].u4 = s0 + u < nsteps ? *reinterpret_cast<const uint4*>(arow + 32 * (s0 + u)) : make_uint4(0, 0, 0, 0);
+    };
+    f32x4 acc[NEB];
+#pragma unroll
+    for (int j = 0; j < NEB; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 accsq = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](int s0, const Pack16 (&aa)[NB]) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        if (s0 + u >= nsteps) break;
+        const int c4 = 4 * (s0 + u);
+#pragma unroll
+        for (int j = 0; j < NEB; ++j) {
+          Pack16 b;
+          b.u4 = wl[brow[j] + (c4 ^ bsw[j])];
+          acc[j] = mfma16x16x32(aa[u].v, b.v, acc[j]);
+        }
+        if (inv_norm) accsq = mfma16x16x32(aa[u].v, aa[u].v, accsq);
+      }
+    };
+    load(0, a[0]);
+    for (int s0 = 0; s0 < nsteps; s0 += 2 * NB) {
+      if (s0 + NB < nsteps) load(s0 + NB, a[1]);
+      compute(s0, a[0]);
+      if (s0 + NB >= nsteps) break;
+      if (s0 + 2 * NB < nsteps) load(s0 + 2 * NB, a[0]);
+      compute(s0 + NB, a[1]);
+    }
+
+    // ---- epilogue.  Register i of acc[j] holds token 4q + i, expert
+    // 16j + m; the 16 lanes of row q hold all experts of tokens 4q .. 4q+3.
+    // Token 4q + i is decided on row q's lanes, then kept by lane 16q + i
+    // (lanes in token order).
+    const int r = m & 3;
+    int c0 = 0, c1 = 0;
+    float h0 = 0.f, h1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t key[NEB];
+#pragma unroll
+      for (int j = 0; j < NEB; ++j) {
+        const float v = acc[j][i] + bias[j];
+        acc[j][i] = v;
+        key[j] = 16 * j + m < E ? logit_key(v, 16 * j + m) : 0u;
+      }
+      uint32_t m1 = 0, m2 = 0, m3 = 0;
+#pragma unroll
+      for (int j = 0; j < NEB; ++j) m1 = max(m1, key[j]);
+      m1 = row_max_u32(m1);
+#pragma unroll
+      for (int j = 0; j < NEB; ++j) m2 = max(m2, key[j] < m1 ? key[j] : 0u);
+      m2 = row_max_u32(m2);
+      if (k == 2) {
+#pragma unroll
+        for (int j = 0; j < NEB; ++j) m3 = max(m3, key[j] < m2 ? key[j] : 0u);
+        m3 = row_max_u32(m3);
+      }
+      const float v0 = key_value(m1), v1 = key_value(m2), v2 = key_value(m3);
+      // v0 is within 2^-17 of the largest logit: the softmax shift and the
+      // scale of the margin
+      const float vm = v0;
+      const float delta = ldexpf(1.0f + fabsf(vm), -11);
+      const bool amb = (v0 - v1 <= delta) || (k == 2 && v1 - v2 <= delta);
+      const float thr = (k == 1 ? v0 : v1) - delta;
+      int e0 = key_expert(m1), e1 = key_expert(m2);
+      // close calls re-decided in float64 from the exact bf16 products over
+      // the experts within the margin of the k-th logit (rare; a
+      // wave-uniform loop over the row leaders, bit 16q = row q)
+      uint64_t ambmask = __ballot(amb && m == 0 && t0 + 4 * q + i < T);
+      while (ambmask) {
+        const int b = __ffsll(static_cast<long long>(ambmask)) - 1;
+        ambmask &= ambmask - 1;
+        const int qq = b >> 4;
+        uint64_t cm = 0;
+#pragma unroll
+        for (int j = 0; j < NEB; ++j) {
+          const uint64_t bl = __ballot(16 * j + m < E && acc[j][i] >= thr);
+          cm |= ((bl >> (16 * qq)) & 0xFFFFull) << (16 * j);
+        }
+        const int2 jj = redecide_f64(X + static_cast<size_t>(t0 + 4 * qq + i) * d, W, bias_g, d, E, cm);
+        const int j0 = jj.x, j1 = jj.y;
+        if (q == qq) { e0 = j0; e1 = j1; }
+      }
+      // gates from the float32 logits of the chosen experts
+      constexpr float kLog2e = 1.44269504088896341f;
+      float l0 = -INFINITY, l1 = -INFINITY, den = 0.f;
+#pragma unroll
+      for (int j = 0; j < NEB; ++j) {
+        const int e = 16 * j + m;
+        l0 = e == e0 ? acc[j][i] : l0;
+        l1 = e == e1 ? acc[j][i] : l1;
+        if (k == 1) den += __builtin_amdgcn_exp2f((acc[j][i] - vm) * kLog2e);
+      }
+      l0 = row_max_f32(l0);
+      float g0, g1 = 0.f;
+      if (k == 1) {
+        den = row_sum_f32(den);
+        g0 = __builtin_amdgcn_exp2f((l0 - vm) * kLog2e) / den;
+      } else {
+        l1 = row_max_f32(l1);
+        const float ga = __builtin_amdgcn_exp2f((l0 - vm) * kLog2e);
+        const float gb = __builtin_amdgcn_exp2f((l1 - vm) * kLog2e);
+        g0 = ga / (ga + gb);
+        g1 = gb / (ga + gb);
+      }
+      if (r == i) { c0 = e0; c1 = e1; h0 = g0; h1 = g1; }
+    }
+    const int tl = 4 * q + m;
+    const int t = t0 + tl;
+    const bool valid = m < 4 && t < T;
+    if (valid) {
+      if (k == 1) {
+        topk_idx[t] = c0;
+        topk_gate[t] = h0;
+      } else {
+        topk_idx[2 * t] = c0;
+        topk_idx[2 * t + 1] = c1;
+        topk_gate[2 * t] = h0;
+        topk_gate[2 * t + 1] = h1;
+      }
+    }
+    if (inv_norm) {
+      // element (mm, mm) of the 16 x 16 Gram: lane 16 (mm / 4) + mm, register mm % 4
+      if ((m >> 2) == q && t0 + m < T) {
+        const float ss = r == 0 ? accsq[0] : (r == 1 ? accsq[1] : (r == 2 ? accsq[2] : accsq[3]));
+        inv_norm[t0 + m] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
+      }
+    }
+    // stable rank of each slot among the chunk's slots of the same expert
+    // (7 ballots on the expert bits) and the chunk's per-expert counts
+    for (int j = 0; j < k; ++j) {
+      const int e = valid ? (j == 0 ? c0 : c1) : -1;
+      const int key = e < 0 ? 127 : e;
+      uint64_t same = ~0ull;
+#pragma unroll
+      for (int b = 0; b < 7; ++b) {
+        const bool bit = (key >> b) & 1;
+        const uint64_t bb = __ballot(bit);
+        same &= bit ? bb : ~bb;
+      }
+      const int rank = __popcll(same & lanemask_lt());
+      if (lane < E) cw[lane] = 0;
+      __builtin_amdgcn_wave_barrier();
+      if (e >= 0 && rank == 0) cw[e] = __popcll(same);
+      __builtin_amdgcn_wave_barrier();
+      if (lane < E) hist[static_cast<size_t>(lane) * k * nchunks + static_cast<size_t>(j) * nchunks + ch] = cw[lane];
+      if (e >= 0) slot_rank[static_cast<size_t>(t) * k + j] = rank;
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
 // One block per expert: exclusive scan of that expert's chunk counts (in
 // place, they become chunk bases) and its total.  The last block to finish
 // (a counter, no waiting) turns the totals into capacity-clamped bucket
@@ -380,12 +667,17 @@ __global__ __launch_bounds__(1024) void slot_scan_kernel(
   __shared__ bool last;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int e = blockIdx.x;
+  // the expert's counts are contiguous (expert-major layout); each thread
+  // takes four consecutive chunks per pass of 4096
+  int32_t* h = hist + static_cast<size_t>(e) * nch;
   int carry = 0;
-  for (int c0 = 0; c0 < nch; c0 += 1024) {
-    const int c = c0 + tid;
-    const size_t o = static_cast<size_t>(c) * E + e;
-    const int v = c < nch ? hist[o] : 0;
-    int incl = v;
+  for (int c0 = 0; c0 < nch; c0 += 4096) {
+    const int c = c0 + 4 * tid;
+    int v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = c + u < nch ? h[c + u] : 0;
+    const int own = (v[0] + v[1]) + (v[2] + v[3]);
+    int incl = own;
 #pragma unroll
     for (int sh = 1; sh < 64; sh <<= 1) {
       const int u = __shfl_up(incl, sh, 64);
@@ -398,7 +690,12 @@ __global__ __launch_bounds__(1024) void slot_scan_kernel(
       wb += i < wv ? wsum[i] : 0;
       tot += wsum[i];
     }
-    if (c < nch) hist[o] = carry + wb + incl - v;
+    int run = carry + wb + incl - own;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (c + u < nch) h[c + u] = run;
+      run += v[u];
+    }
     carry += tot;
     __syncthreads();
   }
@@ -436,7 +733,7 @@ __global__ __launch_bounds__(256) void slot_scatter_kernel(
   const size_t o = static_cast<size_t>(t) * k + j;
   const int e = topk_idx[o];
   const int nblk = (T + tok - 1) / tok;
-  const int pos = base[(static_cast<size_t>(j) * nblk + t / tok) * E + e] + slot_pos[o];
+  const int pos = base[static_cast<size_t>(e) * k * nblk + static_cast<size_t>(j) * nblk + t / tok] + slot_pos[o];
   if (C > 0 && pos >= C) {
     slot_pos[o] = -1;
   } else {
@@ -454,7 +751,8 @@ struct RouteWs {
 
 RouteWs carve_route(Carver& c, int T, int E, int k) {
   RouteWs w;
-  const long long nch = static_cast<long long>(k) * ((T + gate_tokens(T) - 1) / gate_tokens(T));
+  // sized for the smallest chunk of either gate kernel
+  const long long nch = static_cast<long long>(k) * ((T + kGateStreamTok - 1) / kGateStreamTok);
   w.hist = c.take<int32_t>(static_cast<size_t>(nch) * E);
   w.totals = c.take<int>(E);
   w.done = c.take<int>(1);
@@ -512,10 +810,23 @@ void route_enqueue(const void* x, int T, int d, int dtype, const void* w_gate, c
                    int32_t* perm_token, int32_t* offsets, float* inv_norm, const RouteWs& ws, hipStream_t s) {
   const int C = capacity_slots(T, k, E, capacity_factor);
   const long long S = static_cast<long long>(T) * k;
-  const int tok = gate_tokens(T);
+  // the streaming gate when every wave of its persistent grid has a chunk
+  const bool stream = gate_stream_ok(dtype, E, d) &&
+                      (T + kGateStreamTok - 1) / kGateStreamTok >= kGateStreamWaves * persistent_grid();
+  const int tok = stream ? kGateStreamTok : gate_tokens(T);
   const int gblocks = (T + tok - 1) / tok;
   const int nch = k * gblocks;
-  {
+  if (stream) {
+    const int grid = std::max(1, std::min(persistent_grid(), (gblocks + kGateStreamWaves - 1) / kGateStreamWaves));
+#define LUFFY_GATE_S(NEB) launch("gate", gate_stream_kernel<NEB>, grid, kGateStreamWaves * 64, 0, s,                  \
+                                 static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gate), b_gate, T, d, \
+                                 E, k, gblocks, topk_idx, topk_gate, slot_pos, ws.hist, ws.done, inv_norm)
+    if (E <= 16) LUFFY_GATE_S(1);
+    else if (E <= 32) LUFFY_GATE_S(2);
+    else if (E <= 48) LUFFY_GATE_S(3);
+    else LUFFY_GATE_S(4);
+#undef LUFFY_GATE_S
+  } else {
 #define LUFFY_GATE_ARGS x, w_gate, b_gate, T, d, E, k, topk_idx, topk_gate, slot_pos, ws.hist, ws.done, inv_norm
     if (dtype == LUFFY_BF16) {
       if (tok == 32) launch("gate", gate_kernel<true, 32>, gblocks, 256, 0, s, LUFFY_GATE_ARGS);

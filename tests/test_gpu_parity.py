@@ -288,16 +288,21 @@ def test_expert_ffn_tile_shapes(d, d_ff):
             assert np.array_equal(first, got), "the split sum differs between calls"
 
 
-@pytest.mark.parametrize("d", [256, 2560])
-def test_route_large_batch(d):
-    """luffy_route at T = 32768, where the gate takes 64-token chunks (the
-    reduced layer tests use 32): top-k, gates, dispatch with capacity, and
-    1/|x_t| against the oracle.  E = 24 leaves half of the second 16-expert
-    MFMA block unused; d = 2560 is not a power of two."""
+@pytest.mark.parametrize("T,d,E,k", [(32768, 256, 24, 2), (32768, 2560, 24, 2), (70001, 2560, 24, 2),
+                                     (66000, 1024, 40, 1), (5000, 3072, 48, 2), (80000, 2048, 64, 1)])
+def test_route_large_batch(T, d, E, k):
+    """luffy_route on a large batch: top-k, gates, dispatch with capacity,
+    and 1/|x_t| against the oracle.  With a weight matrix of at most 128 KB
+    and at least one 16-token chunk per wave of its grid (T >= 65536 on 256
+    CUs) the streaming gate runs (T = 70001 ragged; E = 24 or 40 leave part
+    of the last 16-expert MFMA block unused; d = 2560 is not a power of
+    two); otherwise the blocked gate, with 64-token chunks at T >= 32768 and
+    32-token ones below, and for weights of 288 KB (48 x 3072) or 256 KB
+    (64 x 2048) at any T."""
     import torch
     import paper_2411_15419_amd as L
-    T, E, k, cf = 32768, 24, 2, 1.25
-    print_case("route", T=T, d=d, E=E)
+    cf = 1.25
+    print_case("route", T=T, d=d, E=E, k=k)
     rng = np.random.default_rng(13)
     x = _bf16(rng.standard_normal((T, d)))
     wg = _bf16(rng.standard_normal((E, d)) / np.sqrt(d))
@@ -320,6 +325,48 @@ def test_route_large_batch(d):
     assert np.array_equal(pt.cpu().numpy()[:o_off[-1]], o_perm), "perm_token differs"
     ref = 1.0 / np.sqrt((x.astype(np.float64) ** 2).sum(axis=1))
     assert np.allclose(nrm.cpu().numpy(), ref, rtol=2e-6, atol=0)
+
+
+@pytest.mark.parametrize("dtype,k,d", [("bf16", 2, 2048), ("bf16", 1, 1024), ("bf16", 1, 4096),
+                                       ("bf16", 2, 8192), ("bf16", 2, 64), ("f32", 1, 256), ("f32", 2, 64),
+                                       ("f32", 2, 256), ("bf16", 2, 192), ("f32", 1, 192)])
+def test_combine_shapes(dtype, k, d):
+    """luffy_combine alone against the oracle's combine on synthetic rows:
+    top-2 on the column-sliced kernel (a row's 16-byte chunks split into
+    eight slices of 1, 2, 32 and 2 x 64 chunks), top-1 and d = 192 (slices
+    of 3 chunks) on the one-wave-per-token kernel.  About a
+    sixth of the slots are dropped, some tokens lose every slot (their rows
+    must be exactly zero), and T is not a multiple of any block's tokens."""
+    import torch
+    import paper_2411_15419_amd as L
+    T, R = 3001, 517
+    print_case("combine", dtype=dtype, k=k, d=d, T=T, R=R)
+    rng = np.random.default_rng(100 + d + k)
+    y_rep = rng.standard_normal((R, d))
+    if dtype == "bf16":
+        y_rep = _bf16(y_rep)
+    S = T * k
+    rep_row = rng.integers(0, R, size=S).astype(np.int32)
+    slot_pos = rng.permutation(S).astype(np.int32).reshape(T, k)
+    slot_pos[rng.random((T, k)) < 0.17] = -1
+    slot_pos[:7] = -1                                  # tokens with no kept slot
+    gate = rng.random((T, k)).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    y = torch.full((T, d), float("nan"), dtype=tdt, device="cuda")
+    L.luffy_combine(dev(y_rep, tdt), dev(rep_row, torch.int32), dev(slot_pos, torch.int32),
+                    dev(gate, torch.float32), y)
+    got = y.double().cpu().numpy()
+    ref = O.combine(y_rep, rep_row, slot_pos, gate.astype(np.float64))
+    assert np.all(got[:7] == 0.0), "tokens without a kept slot must be zero"
+    # per element: bf16 rounding of an fp32 sum (2^-9 relative) or the fp32
+    # sum of at most two products
+    scale = sum(np.abs(gate[:, j:j + 1].astype(np.float64) *
+                       np.where(slot_pos[:, j:j + 1] >= 0, y_rep[rep_row[np.maximum(slot_pos[:, j], 0)]], 0.0))
+                for j in range(k))
+    rtol = 2.0 ** -8 if dtype == "bf16" else 1e-6
+    bad = np.abs(got - ref) > rtol * scale + 1e-30
+    assert not bad.any(), f"{bad.sum()} elements out of tolerance, first at {np.argwhere(bad)[0]}"
 
 
 def test_graph_replay_matches_eager():

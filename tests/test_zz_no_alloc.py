@@ -58,8 +58,8 @@ def assert_same(a, b):
 def test_noalloc_route_matches_route_twice():
     import paper_2411_15419_amd as L
     from tests.layer_runner import upload
-    big = G.make_inputs("c5", seed=0, T=65536, d=256, d_ff=64, weights=False)   # 64-token gate blocks, drops
-    small = G.make_inputs("c2", seed=1, T=3000, d=256, d_ff=64, n_centres=128, weights=False)  # 32-token blocks
+    big = G.make_inputs("c5", seed=0, T=65536, d=256, d_ff=64, weights=False)   # 1 MiB of slot counts, drops
+    small = G.make_inputs("c2", seed=1, T=3000, d=256, d_ff=64, n_centres=128, weights=False)
     devs = [upload(big), upload(small)]
     refs = [to_host(route_call(inp, dv, noalloc=False)) for inp, dv in zip((big, small), devs)]
     # two no-alloc calls in a row, the second on the smaller batch
@@ -70,7 +70,7 @@ def test_noalloc_route_matches_route_twice():
         outs.append(route_call(inp, dv, noalloc=True))
     for ref, out in zip(refs, outs):
         assert_same(ref, to_host(out))
-    assert L.load_library().luffy_route_noalloc_max_bytes() == 1 << 20
+    assert L.load_library().luffy_route_noalloc_max_bytes() == 4 << 20
 
 
 def test_noalloc_route_rejects_oversized_batch():
