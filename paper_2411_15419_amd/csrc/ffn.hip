@@ -245,6 +245,30 @@ struct FfnTiles {
     }
     return best;
   }
+  // Split plan of the second product: tiles [0, full) run whole, the `tail`
+  // tiles after them run as S parts each (items full + u, u < tail * S, are
+  // part u % S of tile full + u / S; partial slot u).  With fewer tiles than
+  // blocks every tile is a tail tile and S comes from parts().  With more,
+  // the whole rounds stay whole and only the tiles left over for the last,
+  // partial round are split, into the most parts (at most 4, at least 4
+  // K-units each) that one and a half rounds of blocks take: their parts
+  // then fill the CUs that finish their whole tiles first instead of
+  // leaving them idle (376 tiles of K = 8192 on 256 CUs: the 120 left over
+  // in thirds, second product + reduction 358 -> 345 us; halves 350,
+  // quarters 346).
+  __device__ __forceinline__ void split_plan(int grid, int nk, int& full, int& tail, int& S) const {
+    if (tiles < grid) {
+      full = 0;
+      tail = tiles;
+      S = parts(grid, nk);
+      return;
+    }
+    full = tiles / grid * grid;
+    tail = tiles - full;
+    S = 1;
+    for (int sp = 2; sp <= 4; ++sp)
+      if (tail > 0 && 2 * tail * sp <= 3 * grid && nk / sp >= 4 && tail * sp <= kFfnMaxSlots) S = sp;
+  }
 };
 
 // Multiplies with only the first nq of the wave's Q blocks (wave-uniform
@@ -356,9 +380,12 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
   int& item_s = *reinterpret_cast<int*>(lds + kFfnLds);
   const FfnTiles map(rep_offsets, E, N);
   const int nk = K / kFfnKUnit;
-  const int S = FIRST ? 1 : map.parts(gridDim.x, nk);
-  const int total = map.tiles * S;
-  const int g = gridDim.x, rounds = total / g;
+  int full = map.tiles, ntail = 0, S = 1;
+  if (!FIRST) map.split_plan(gridDim.x, nk, full, ntail, S);
+  const int total = full + ntail * S;
+  // static rounds: whole tiles only when the tail is split (its parts go
+  // to the blocks that finish first), else every whole round of items
+  const int g = gridDim.x, rounds = (full > 0 && S > 1) ? full / g : total / g;
   const int vb = xcd_virtual_block();
   for (int round = 0;; ++round) {
     int tt;
@@ -374,13 +401,16 @@ __global__ __launch_bounds__(FfnGemm::THREADS) void ffn_kernel_bf16(
       tt = item_s;
       if (tt >= total) break;
     }
-    const int t = tt / S, part = tt - t * S;
+    // whole tile, or part `part` of S of a tail tile (partial slot u)
+    const int u = tt - full;
+    const int sp = u < 0 ? 1 : S;
+    const int t = u < 0 ? tt : full + u / S, part = u < 0 ? 0 : u - (u / S) * S;
     int e, row0, rows, n0, shape;
     map.decode(t, E, e, row0, rows, n0, shape);
     const uint16_t* We = W + static_cast<size_t>(e) * N * K;
     // K range of this part, in whole 64-wide units
-    const int k0 = (part * nk / S) * kFfnKUnit, k1 = ((part + 1) * nk / S) * kFfnKUnit;
-    float* slot = S > 1 ? split_slots + static_cast<size_t>(tt) * kFfnSlotFloats : nullptr;
+    const int k0 = (part * nk / sp) * kFfnKUnit, k1 = ((part + 1) * nk / sp) * kFfnKUnit;
+    float* slot = sp > 1 ? split_slots + static_cast<size_t>(u) * kFfnSlotFloats : nullptr;
     using GN = std::conditional_t<WT, FfnGemmT, FfnGemm>;
     using GW = std::conditional_t<WT, FfnGemmWideT, FfnGemmWide>;
     using GS = std::conditional_t<WT, FfnGemmSmallT, FfnGemmSmall>;
@@ -443,9 +473,9 @@ __device__ __forceinline__ void reduce_unit(const float* __restrict__ slots, int
                       pack_bf16x2(c[3].z, c[3].w));
 }
 
-// Sums the split parts of every output tile in part order and stores bf16.
-// Recomputes the same tile map and split count, so it does nothing when the
-// product was not split.  One thread per (w, fm, fn, lane) unit of a tile;
+// Sums the split parts of every split (tail) tile in part order and stores
+// bf16.  Recomputes the same tile map and split plan, so it does nothing
+// when the product was not split.  One thread per (w, fm, fn, lane) unit of a tile;
 // a tile gets the block count of the wide shape (the narrow shape leaves
 // its last blocks idle).
 constexpr int kReduceUnits = FfnGemmWide::NWAVES * FfnGemmWide::FM * FfnGemmWide::FN * 64;
@@ -457,14 +487,15 @@ __global__ __launch_bounds__(256) void ffn_split_reduce_kernel(const int32_t* __
                                                                uint16_t* __restrict__ out, int grid_parts) {
   constexpr int PER_TILE = kReduceUnits / 256;   // blocks per tile
   const FfnTiles map(rep_offsets, E, N);
-  const int S = map.parts(grid_parts, K / kFfnKUnit);
+  int full, ntail, S;
+  map.split_plan(grid_parts, K / kFfnKUnit, full, ntail, S);
   if (S == 1) return;
-  for (int b = blockIdx.x; b < map.tiles * PER_TILE; b += gridDim.x) {
-    const int t = b / PER_TILE;
-    const int q = ((b - t * PER_TILE) * 256 + threadIdx.x) >> 6;   // (w*FM + fm)*FN + fn
+  for (int b = blockIdx.x; b < ntail * PER_TILE; b += gridDim.x) {
+    const int tt = b / PER_TILE;                                    // tail tile
+    const int q = ((b - tt * PER_TILE) * 256 + threadIdx.x) >> 6;   // (w*FM + fm)*FN + fn
     int e, row0, rows, n0, shape;
-    map.decode(t, E, e, row0, rows, n0, shape);
-    const float* slots = split_slots + static_cast<size_t>(t) * S * kFfnSlotFloats;
+    map.decode(full + tt, E, e, row0, rows, n0, shape);
+    const float* slots = split_slots + static_cast<size_t>(tt) * S * kFfnSlotFloats;
     const bool narrow_unit = q < FfnGemm::NWAVES * FfnGemm::FM * FfnGemm::FN;
     const bool small_unit = q < FfnGemmSmall::NWAVES * FfnGemmSmall::FM * FfnGemmSmall::FN;
     if (S == 4) {

@@ -288,6 +288,44 @@ def test_expert_ffn_tile_shapes(d, d_ff):
             assert np.array_equal(first, got), "the split sum differs between calls"
 
 
+def test_expert_ffn_split_tail():
+    """More second-product tiles than blocks with a partial round left: 40
+    experts of 1, 60, 128, 129, 256, 257, 300 and 320 rows (every tile
+    shape) times 8 column tiles (d = 2048) make 320 tiles; on 256 CUs the
+    first 256 run whole and the 64 left over (the last 8 experts, every
+    shape again) run in 4 parts of 4 K-stages each (d_ff = 1024), finished
+    by the reduction.  Each output row within the bf16 tolerance of the
+    oracle; two calls bit-identical."""
+    import torch
+    import paper_2411_15419_amd as L
+    from tests.layer_runner import TOL, rel_err_rows
+    d, d_ff = 2048, 1024
+    sizes = [1, 60, 128, 129, 256, 257, 300, 320] * 5
+    print_case("expert_ffn_split_tail", d=d, d_ff=d_ff, E=len(sizes))
+    E, R = len(sizes), sum(sizes)
+    rng = np.random.default_rng(12)
+    x = _bf16(rng.standard_normal((R, d)))
+    w1 = _bf16(0.03 * rng.standard_normal((E, d_ff, d)))
+    w2 = _bf16(0.03 * rng.standard_normal((E, d, d_ff)))
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    dev = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    y = torch.empty(R, d, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(L.expert_ffn_workspace_size(R, E, d_ff, L.LUFFY_BF16), dtype=torch.uint8, device="cuda")
+    args = (dev(x), None, dev(offsets, torch.int32), dev(w1), dev(w2))
+    ref = O.expert_ffn(x, offsets, w1, w2, "gelu")
+    first = None
+    for call in range(2):
+        y.fill_(float("nan"))
+        L.luffy_expert_ffn(*args, "gelu", R, y, ws)
+        got = y.double().cpu().numpy()
+        err, _ = rel_err_rows(got, ref)
+        assert err.max() <= TOL["bf16"], f"call {call}: max row rel err {err.max():.3g}"
+        if first is None:
+            first = got
+        else:
+            assert np.array_equal(first, got), "the split sum differs between calls"
+
+
 @pytest.mark.parametrize("T,d,E,k", [(32768, 256, 24, 2), (32768, 2560, 24, 2), (70001, 2560, 24, 2),
                                      (66000, 1024, 40, 1), (5000, 3072, 48, 2), (80000, 2048, 64, 1)])
 def test_route_large_batch(T, d, E, k):
