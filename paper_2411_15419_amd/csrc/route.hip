@@ -44,6 +44,56 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
+// Float64 re-decision of one token's close call, by the whole wave: the two
+// largest exact logits x.w_e + b_e over the candidate experts cm, visited in
+// ascending e (the lower expert first among equal values).  Up to four
+// candidates at a time: the lane's 16-byte pieces of x are loaded once per
+// batch and every candidate's pieces of W are in flight together (the
+// latency of a close call, not its arithmetic, is what the launch waits
+// for; NC candidates a batch).  wpiece(e, c) returns the 8 weights of
+// expert e at columns c..c+7.
+// Each candidate's sum takes the same lane partition and butterfly as a
+// one-candidate loop, so the values do not depend on the batching.
+template <int NC, class WPiece>
+__device__ __forceinline__ int2 redecide_bf16_f64(const uint16_t* __restrict__ xr, WPiece wpiece,
+                                                  const float* __restrict__ bias, int d, uint64_t cm) {
+  const int lane = threadIdx.x & 63;
+  double b0 = -INFINITY, b1 = -INFINITY;
+  int j0 = 0, j1 = 0;
+  while (cm) {
+    int ec[NC];
+    int nc = 0;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) ec[j] = 0;
+    for (; nc < NC && cm; ++nc) {
+      ec[nc] = __ffsll(static_cast<long long>(cm)) - 1;
+      cm &= cm - 1;
+    }
+    double sacc[NC];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) sacc[j] = 0.0;
+    for (int c = lane * 8; c < d; c += 512) {
+      Pack16 xa, wa[NC];
+      xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
+#pragma unroll
+      for (int j = 0; j < NC; ++j) wa[j].u4 = j < nc ? wpiece(ec[j], c) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < NC; ++j)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          sacc[j] += static_cast<double>(bf16_to_f32(xa.h[u])) * static_cast<double>(bf16_to_f32(wa[j].h[u]));
+    }
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      if (j >= nc) break;
+      const double v = wave_sum_f64(sacc[j]) + static_cast<double>(bias ? bias[ec[j]] : 0.f);
+      if (v > b0) { b1 = b0; j1 = j0; b0 = v; j0 = ec[j]; }
+      else if (v > b1) { b1 = v; j1 = ec[j]; }
+    }
+  }
+  return make_int2(j0, j1);
+}
+
 // Epilogue of a gate chunk of TOK tokens starting at t0, once the logit of
 // token tl and expert e (bias included) is in LDS at lg[e * (TOK + 4) + tl]: top-k, gates, the float64
 // re-decision of close calls; then wave 0 ranks every slot among the chunk's
@@ -123,23 +173,20 @@ __device__ __forceinline__ void gate_select(const float* lg, const float* bias, 
       ambmask &= ambmask - 1;
       const uint64_t cm = static_cast<uint64_t>(__shfl(static_cast<long long>(cand), tl, 64));
       const size_t xt = static_cast<size_t>(t0 + min(16 * w + (tl >> 2), TOK - 1)) * d;
-      double b0 = -INFINITY, b1 = -INFINITY;
       int j0 = 0, j1 = 0;
-      for (int e = 0; e < E; ++e) {
-        if (!((cm >> e) & 1ull)) continue;
-        double s = 0.0;
-        if constexpr (BF16) {
-          const uint16_t* xr = static_cast<const uint16_t*>(xv) + xt;
-          const uint16_t* wr = static_cast<const uint16_t*>(wv) + static_cast<size_t>(e) * d;
-          for (int c = lane * 8; c < d; c += 512) {
-            Pack16 xa, wa;
-            xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
-            wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-              s += static_cast<double>(bf16_to_f32(xa.h[i])) * static_cast<double>(bf16_to_f32(wa.h[i]));
-          }
-        } else {
+      if constexpr (BF16) {
+        const uint16_t* W = static_cast<const uint16_t*>(wv);
+        const int2 jj = redecide_bf16_f64<4>(
+            static_cast<const uint16_t*>(xv) + xt,
+            [&](int e, int c) { return *reinterpret_cast<const uint4*>(W + static_cast<size_t>(e) * d + c); },
+            bias, d, cm);
+        j0 = jj.x;
+        j1 = jj.y;
+      } else {
+        double b0 = -INFINITY, b1 = -INFINITY;
+        for (int e = 0; e < E; ++e) {
+          if (!((cm >> e) & 1ull)) continue;
+          double s = 0.0;
           const float* xr = static_cast<const float*>(xv) + xt;
           const float* wr = static_cast<const float*>(wv) + static_cast<size_t>(e) * d;
           for (int c = lane * 4; c < d; c += 256) {
@@ -148,11 +195,11 @@ __device__ __forceinline__ void gate_select(const float* lg, const float* bias, 
             s += static_cast<double>(xa.x) * wa.x + static_cast<double>(xa.y) * wa.y +
                  static_cast<double>(xa.z) * wa.z + static_cast<double>(xa.w) * wa.w;
           }
+          s = wave_sum_f64(s);
+          s += static_cast<double>(bias[e]);
+          if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
+          else if (s > b1) { b1 = s; j1 = e; }
         }
-        s = wave_sum_f64(s);
-        s += static_cast<double>(bias[e]);
-        if (s > b0) { b1 = b0; j1 = j0; b0 = s; j0 = e; }
-        else if (s > b1) { b1 = s; j1 = e; }
       }
       if ((lane >> 2) == (tl >> 2)) { i0 = j0; i1 = j1; }
     }
@@ -385,6 +432,7 @@ constexpr int kGateLdsW = 128 * 1024;            // bytes of W held in LDS
 constexpr int kGateStreamWaves = 16;
 constexpr int kGateStreamTok = 16;               // tokens per chunk (one wave)
 constexpr int kGateStreamNB = 4;                 // K steps (of 32) per load batch
+constexpr int kGateStreamNC = 1;                 // close-call candidates a batch (no spills)
 
 inline bool gate_stream_ok(int dtype, int E, int d) {
   return dtype == LUFFY_BF16 && E <= kMaxExperts && static_cast<long long>(E) * d * 2 <= kGateLdsW && d % 64 == 0;
@@ -431,36 +479,6 @@ __device__ __forceinline__ float key_value(uint32_t key) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
 }
 __device__ __forceinline__ int key_expert(uint32_t key) { return 63 - static_cast<int>(key & 63u); }
-
-// Float64 re-decision of one token's close call (called by the whole wave;
-// rare): the
-// two largest of the exact logits over the candidate experts cm, in
-// expert order (the lower expert first among equals).
-__device__ __forceinline__ int2 redecide_f64(const uint16_t* __restrict__ xr,
-                                                       const uint16_t* __restrict__ W,
-                                                       const float* __restrict__ bias_g, int d, int E, uint64_t cm) {
-  const int lane = threadIdx.x & 63;
-  double b0 = -INFINITY, b1 = -INFINITY;
-  int j0 = 0, j1 = 0;
-  for (int e = 0; e < E; ++e) {
-    if (!((cm >> e) & 1ull)) continue;
-    double sacc = 0.0;
-    const uint16_t* wr = W + static_cast<size_t>(e) * d;
-    for (int c = lane * 8; c < d; c += 512) {
-      Pack16 xa, wa;
-      xa.u4 = *reinterpret_cast<const uint4*>(xr + c);
-      wa.u4 = *reinterpret_cast<const uint4*>(wr + c);
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        sacc += static_cast<double>(bf16_to_f32(xa.h[u])) * static_cast<double>(bf16_to_f32(wa.h[u]));
-    }
-    sacc = wave_sum_f64(sacc);
-    sacc += static_cast<double>(bias_g ? bias_g[e] : 0.f);
-    if (sacc > b0) { b1 = b0; j1 = j0; b0 = sacc; j0 = e; }
-    else if (sacc > b1) { b1 = sacc; j1 = e; }
-  }
-  return make_int2(j0, j1);
-}
 
 template <int NEB>
 __global__ __launch_bounds__(kGateStreamWaves * 64) void gate_stream_kernel(
@@ -583,7 +601,9 @@ __global__ __launch_bounds__(kGateStreamWaves * 64) void gate_stream_kernel(
           const uint64_t bl = __ballot(16 * j + m < E && acc[j][i] >= thr);
           cm |= ((bl >> (16 * qq)) & 0xFFFFull) << (16 * j);
         }
-        const int2 jj = redecide_f64(X + static_cast<size_t>(t0 + 4 * qq + i) * d, W, bias_g, d, E, cm);
+        const int2 jj = redecide_bf16_f64<kGateStreamNC>(
+            X + static_cast<size_t>(t0 + 4 * qq + i) * d,
+            [&](int e, int c) { return wl[e * cpr + ((c >> 3) ^ (e & 7))]; }, bias_g, d, cm);
         const int j0 = jj.x, j1 = jj.y;
         if (q == qq) { e0 = j0; e1 = j1; }
       }
