@@ -315,6 +315,50 @@ __device__ __forceinline__ void ffn_tile(const uint16_t* __restrict__ A, const i
   G::zero(acc);
   run_nq<G, G::FN>(__builtin_amdgcn_readfirstlane(nq), We + (G::PT ? static_cast<size_t>(k0) * N : k0), poff,
                    A + k0, qoff, k1 - k0, N - n0, rows, lds, acc, N);
+  if constexpr (ACT != kActDzGelu && ACT != kActDzSilu) {
+    if (!slot) {
+      // bf16 rows: lane l (< 32) holds columns 8g..8g+3 and lane l + 32
+      // columns 8g+4..8g+7 of a 32-column block of one token row; after one
+      // exchange the low lane stores columns 0..15 and the high lane 16..31,
+      // two 16-byte stores each
+      const int hi = lane >> 5;
+#pragma unroll
+      for (int fm = 0; fm < G::FM; ++fm) {
+#pragma unroll
+        for (int fn = 0; fn < G::FN; ++fn) {
+          const int ml = G::q_row(wn, fn) + (lane & 31);
+          const int nb = n0 + wm * G::WTM + 32 * fm;
+          if (ml >= rows || nb >= N) continue;
+          uint32_t pk[4][2];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float z[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              z[q] = acc[fm][fn][4 * g + q];
+              if constexpr (FIRST) z[q] = act_fast<ACT>(z[q]);
+            }
+            pk[g][0] = pack_bf16x2(z[0], z[1]);
+            pk[g][1] = pack_bf16x2(z[2], z[3]);
+          }
+          uint32_t snd[4] = {hi ? pk[0][0] : pk[2][0], hi ? pk[0][1] : pk[2][1], hi ? pk[1][0] : pk[3][0],
+                             hi ? pk[1][1] : pk[3][1]};
+          uint32_t rcv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) rcv[i] = static_cast<uint32_t>(__shfl_xor(static_cast<int>(snd[i]), 32, 64));
+          uint4* dst = reinterpret_cast<uint4*>(out + static_cast<size_t>(row0 + ml) * N + nb + 16 * hi);
+          if (hi == 0) {
+            dst[0] = make_uint4(pk[0][0], pk[0][1], rcv[0], rcv[1]);
+            dst[1] = make_uint4(pk[1][0], pk[1][1], rcv[2], rcv[3]);
+          } else {
+            dst[0] = make_uint4(rcv[0], rcv[1], pk[2][0], pk[2][1]);
+            dst[1] = make_uint4(rcv[2], rcv[3], pk[3][0], pk[3][1]);
+          }
+        }
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
