@@ -20,9 +20,9 @@
 //                        every position of a union of cliques).
 //   greedy_more_kernel   persistent pass with bounded coherent revisits of
 //                        positions still undecided (dependency chains).
-//   greedy_finish_kernel one workgroup per bucket repeats rounds until the
-//                        bucket is fully decided (only when the pass before
-//                        left a position undecided).
+//   greedy_finish_kernel one workgroup per bucket: a few rounds, then one
+//                        visit per position left in priority order (only
+//                        when the pass before left a position undecided).
 //   claim_kernel         every kept position not yet pushed offers itself to
 //                        its neighbours (64-bit atomic max of degree,
 //                        ~position): an absorbed position ends with its
@@ -1469,15 +1469,22 @@ __global__ __launch_bounds__(256) void greedy_more_kernel(
   }
 }
 
-// One workgroup per bucket: rounds until every position is decided.  The
-// undecided positions left by the grid rounds are gathered once into a list
-// in LDS (a coalesced pass over the bucket's states); each round then visits
-// only the listed positions, 16 lanes each (64 at a time), and keeps those
-// still undecided for the next round.  Each round decides at least the
-// highest-priority undecided position, so rounds <= the list's length; a
-// bucket with more undecided positions than the list holds takes the
-// original path, a pass over all its positions per round.
+// One workgroup per bucket decides what the grid rounds left.  The
+// undecided positions are gathered into a list in LDS (a coalesced pass over
+// the bucket's states); at most kFinishRounds rounds then visit only the
+// listed positions, 16 lanes each (64 at a time), keeping those still
+// undecided for the next round (a round decides at least the
+// highest-priority undecided position; on clustered data one or two rounds
+// decide all).  What is left after them (dependency chains, such as a path
+// of similar tokens) is sorted by priority (degree descending, position
+// ascending; a bitonic sort in LDS) and visited once each in that order by
+// one wave: every higher-priority neighbour of a position is decided by its
+// turn, so each visit decides its position, and the work is bounded by one
+// visit per position instead of one per position and round.  A bucket with
+// more undecided positions than the list holds first runs rounds over all
+// its positions until the rest fits the list.
 constexpr int kFinishList = 16384;
+constexpr int kFinishRounds = 16;
 
 __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
@@ -1491,24 +1498,35 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
   const int lo = offsets[e], n = offsets[e + 1] - lo, W = (n + 63) / 64;
   if (n == 0) return;
   const int tid = threadIdx.x;
-  if (tid < 2) cnt[tid] = 0;
-  __syncthreads();
-  for (int i = tid; i < n; i += 1024) {
-    if (load_flag(&state[lo + i]) == kStateUndecided) {
-      const int slot = atomicAdd(&cnt[0], 1);
-      if (slot < kFinishList) list[0][slot] = i;
-    }
-  }
-  __syncthreads();
-  int m = cnt[0];
-  if (m == 0) return;
   const uint64_t* rows = bitmask + bm_off[e];
-  if (m <= kFinishList) {
+  int m;
+  for (;;) {
+    if (tid < 2) cnt[tid] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += 1024) {
+      if (load_flag(&state[lo + i]) == kStateUndecided) {
+        const int slot = atomicAdd(&cnt[0], 1);
+        if (slot < kFinishList) list[0][slot] = i;
+      }
+    }
+    __syncthreads();
+    m = cnt[0];
+    if (m == 0) return;
+    if (m <= kFinishList) break;
+    // more than the list holds: a round over all positions, one wave each
+    const int wv = tid >> 6;
+    for (int pl = wv; pl < n; pl += 16) {
+      const int p = lo + pl;
+      if (load_flag(&state[p]) != kStateUndecided) continue;
+      greedy_visit<true, 64>(p, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
+    }
+    __syncthreads();
+  }
+  int cur = 0;
+  {
     const int grp = tid / kVisitLanes;
     constexpr int kGroups = 1024 / kVisitLanes;
-    int cur = 0;
-    const int m0 = m;
-    for (int it = 0; it <= m0 && m > 0; ++it) {
+    for (int it = 0; it < kFinishRounds && m > 0; ++it) {
       for (int idx = grp; idx < m; idx += kGroups) {
         const int pl = list[cur][idx];
         greedy_visit<true, kVisitLanes>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
@@ -1524,17 +1542,44 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
       m = cnt[cur];
       __syncthreads();
     }
-    return;
   }
-  const int wv = tid >> 6;
-  for (int it = 0; it <= n; ++it) {
-    int undecided = 0;
-    for (int pl = wv; pl < n; pl += 16) {
-      const int p = lo + pl;
-      if (load_flag(&state[p]) != kStateUndecided) continue;
-      if (greedy_visit<true, 64>(p, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state)) undecided = 1;
+  if (m == 0) return;
+  // sort the m positions left by priority: list[cur] positions, list[cur ^ 1]
+  // their degrees; padded to a power of two with entries after every real one
+  int* pos = list[cur];
+  int* dg = list[cur ^ 1];
+  int P = 1;
+  while (P < m) P <<= 1;
+  for (int i = tid; i < P; i += 1024) {
+    if (i < m) dg[i] = deg[lo + pos[i]];
+    else { pos[i] = 0x7fffffff; dg[i] = -1; }
+  }
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < P; i += 1024) {
+        const int l = i ^ j;
+        if (l > i) {
+          // a_first: entry i comes before entry l (higher degree, then lower position)
+          const bool a_first = dg[i] > dg[l] || (dg[i] == dg[l] && pos[i] < pos[l]);
+          const bool up = (i & k) == 0;
+          if (up != a_first) {
+            const int tp = pos[i], td = dg[i];
+            pos[i] = pos[l];
+            dg[i] = dg[l];
+            pos[l] = tp;
+            dg[l] = td;
+          }
+        }
+      }
+      __syncthreads();
     }
-    if (!__syncthreads_or(undecided)) break;
+  }
+  if (tid < 64) {
+    for (int idx = 0; idx < m; ++idx) {
+      const int pl = pos[idx];
+      greedy_visit<true, 64>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
+    }
   }
 }
 

@@ -161,9 +161,14 @@ def _path_inputs(n_tokens, d, shuffle, seed):
     return inp
 
 
-@pytest.mark.parametrize("shuffle", [False, True])
-def test_long_chain_needs_many_rounds(shuffle):
-    inp = _path_inputs(511, 512, shuffle, seed=6)
+@pytest.mark.parametrize("n,shuffle", [(511, False), (511, True), (4000, False), (4000, True)])
+def test_long_chain_needs_many_rounds(n, shuffle):
+    """Threshold graphs that are paths: a decision chain as long as the
+    bucket, which the grid rounds leave mostly undecided; the finishing
+    pass takes a few rounds and then visits the rest once each in priority
+    order (4000 positions: the sorted pass over a list of thousands)."""
+    print_case("path", n=n, shuffle=shuffle)
+    inp = _path_inputs(n, (n // 64 + 2) * 64, shuffle, seed=6)
     g = run_gpu(inp)
     o = run_oracle(inp)
     assert_route_equal(g, o)
