@@ -30,7 +30,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense MFMA (fp32: vector/matrix fp32 peak)
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0, "f32": 157.3}   # dense MFMA (fp32: vector/matrix fp32 peak)
 
 WORKLOAD_NAMES = {
     "c1": "tiny MoE layer fp32, T=512 d=256 E=4 top-1",
@@ -60,8 +60,12 @@ def kernel_work(name, cfg, counts, norms_from_route=True):
                     bytes_act=float(nbytes if nbytes_act is None else nbytes_act))
 
     if name == "gram":
+        # on the fp8 screen the rows it streams are fp8 (one byte a value)
         n = counts["bucket_sizes"]
-        return w(2.0 * d * sum(x * (x + 1) / 2 for x in n), S * d * b)
+        return w(2.0 * d * sum(x * (x + 1) / 2 for x in n), S * d * (1 if counts.get("screen") else b))
+    if name == "gram_quant":
+        # reads the bf16 rows, writes the fp8 rows and a factor per row
+        return w(0.0, T * d * b + T * d + 8 * T)
     if name in ("ffn1", "ffn2"):
         wb = used * d * dff * b
         return w(2.0 * R * d * dff, wb, wb + R * d * b + R * dff * b)
@@ -98,7 +102,8 @@ def roofline(name, cfg, counts, sec_per_launch, norms_from_route=True):
     other kernel by HBM.  `attainable` = min(MFMA peak, intensity x 8 TB/s)
     in the kernel's unit; `frac_attainable` = achieved / attainable."""
     wk = kernel_work(name, cfg, counts, norms_from_route)
-    mfma_peak = MFMA_PEAK_TFLOPS[cfg.dtype]
+    # the screened similarity kernel multiplies fp8
+    mfma_peak = MFMA_PEAK_TFLOPS["fp8" if name == "gram" and counts.get("screen") else cfg.dtype]
     ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     tflops = wk["flops"] / sec_per_launch / 1e12
     gbs = wk["bytes"] / sec_per_launch / 1e9
@@ -375,7 +380,9 @@ def measure_forward(name, thresholds, args, torch, np, G, L, with_cpu):
         off = b.offsets.cpu().numpy()
         ro = b.rep_offsets.cpu().numpy()
         counts = dict(S=int(off[-1]), R=int(ro[-1]), bucket_sizes=np.diff(off).tolist(),
-                      used_experts=int((np.diff(ro) > 0).sum()))
+                      used_experts=int((np.diff(ro) > 0).sum()),
+                      screen=L.similarity_screen_applies(cfg.T, cfg.d, cfg.E, cfg.k,
+                                                         L.LUFFY_BF16 if cfg.dtype == "bf16" else L.LUFFY_F32))
         rl = roofline(dominant, cfg, counts, dom_ms / dom_n / 1e3)
         wk = kernel_work(dominant, cfg, counts)
         rl.update(traffic=recorded_traffic(name, dominant),
@@ -503,6 +510,8 @@ def main():
     ap.add_argument("--threshold", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-screen", action="store_true",
+                    help="similarity on bf16 MFMA for every tile (the fp8 screen off)")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward of the layer (combine and expert FFN) instead of the forward")
@@ -527,6 +536,8 @@ def main():
         copy_calibration()
         return
     L.load_library()
+    if args.no_screen:
+        L.set_similarity_screen(False)
     torch.cuda.set_device(0)
     cfg = G.config(args.config)
     h = cfg.h if args.threshold is None else args.threshold
@@ -563,7 +574,11 @@ def main():
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "T": cfg.T,
                    "d_model": cfg.d, "E": cfg.E, "top_k": cfg.k, "d_ff": cfg.d_ff,
                    "act": cfg.act, "threshold": h, "capacity_factor": cfg.capacity_factor,
-                   "seed": args.seed},
+                   "seed": args.seed,
+                   "similarity": ("fp8 (E4M3) screen, undecided tiles recomputed in bf16"
+                                  if L.similarity_screen_applies(cfg.T, cfg.d, cfg.E, cfg.k,
+                                                                 L.LUFFY_BF16 if cfg.dtype == "bf16" else L.LUFFY_F32)
+                                  else cfg.dtype)},
         "condensation": head["condensation"],
         "roofline": head["roofline"],
         "kernels": head["kernels"],

@@ -179,6 +179,29 @@ int luffy_condense(const void* x, int T, int d, int dtype,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Similarity screen of luffy_condense (bf16 calls with d >= 2048, d a
+ * multiple of 128 and T*k >= 512*E; not luffy_condense_history).  The
+ * cosines of Sec. 5.1 are first estimated on fp8 (E4M3) copies of the rows,
+ * each scaled by a power of two, with a bound derived from every row's
+ * quantisation error: |c~ - c| <= rho_a + rho_b + rho_a*rho_b (plus room for
+ * float32 rounding), rho = |x - x^| / |x|.  A 256 x 256 tile whose every
+ * estimate lies outside that band around the threshold is decided by the
+ * estimates, which then agree with the exact comparison for every pair; any
+ * other tile is recomputed from the bf16 rows.  The outputs are the same
+ * with the screen on or off.  The workspace of such calls holds the fp8
+ * rows (T*d bytes).
+ *
+ * luffy_set_similarity_screen  on != 0 enables the screen (the default),
+ *                              0 disables it for later calls in this
+ *                              process; returns the previous setting.
+ * luffy_similarity_screen_applies
+ *                              1 if a luffy_condense call of this shape and
+ *                              dtype would take the screen now, else 0.
+ * ---------------------------------------------------------------------- */
+int luffy_set_similarity_screen(int on);
+int luffy_similarity_screen_applies(int T, int d, int E, int k, int dtype);
+
+/* ------------------------------------------------------------------------
  * luffy_condense_history - luffy_condense with the historical similarity of
  * Sec. 5.1 step 2, for a stack of MoE blocks over the same tokens.
  *

@@ -48,6 +48,8 @@ _SIGS = {
     "luffy_condense_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int, _c_int,
                                 _c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "luffy_set_similarity_screen": (_c_int, [_c_int]),
+    "luffy_similarity_screen_applies": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_history_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "luffy_condense_history_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int, _c_int]),
     "luffy_condense_history": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int,
@@ -133,6 +135,17 @@ def route_workspace_size(T: int, E: int, k: int) -> int:
 
 def condense_workspace_size(T: int, d: int, E: int, k: int, max_bucket: int) -> int:
     return load_library().luffy_condense_workspace_size(T, d, E, k, max_bucket)
+
+
+def set_similarity_screen(on: bool) -> bool:
+    """Enables or disables the fp8 similarity screen of luffy_condense
+    (luffy_set_similarity_screen); returns the previous setting."""
+    return bool(load_library().luffy_set_similarity_screen(1 if on else 0))
+
+
+def similarity_screen_applies(T: int, d: int, E: int, k: int, dtype: int = LUFFY_BF16) -> bool:
+    """Whether a condense call of this shape takes the fp8 screen now."""
+    return bool(load_library().luffy_similarity_screen_applies(int(T), int(d), int(E), int(k), int(dtype)))
 
 
 def expert_ffn_workspace_size(max_rows: int, E: int, d_ff: int, dtype: int) -> int:
@@ -301,7 +314,8 @@ def profile_read():
     return ms.value, n.value
 
 
-KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram", "greedy_round", "greedy_push", "greedy_more",
+KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram_quant", "gram", "gram_recheck", "greedy_round",
+           "greedy_push", "greedy_more",
            "greedy_finish", "claim", "rep_local", "rep_finalize", "gather", "ffn_queue", "ffn1", "ffn2",
            "ffn2_reduce", "combine")
 

@@ -39,6 +39,7 @@
 // each other's updates early without changing the result, and every round
 // decides at least the highest-priority undecided position.
 #include <algorithm>
+#include <atomic>
 
 #include "gemm_core.h"
 #include "luffy_common.h"
@@ -118,12 +119,14 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
                                                    int tile, long long cap_words, int32_t* __restrict__ tile_off,
                                                    long long* __restrict__ bm_off, int* __restrict__ err,
                                                    unsigned long long* __restrict__ stats, int* __restrict__ queue,
-                                                   int* __restrict__ left) {
+                                                   int* __restrict__ left, int* __restrict__ list_count) {
   if (blockIdx.x == 0 && threadIdx.x < 64)
     gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
   if (stats && blockIdx.x == 0 && threadIdx.x >= 64 && threadIdx.x < 68) stats[threadIdx.x - 64] = 0ull;
   if (queue && blockIdx.x == 0 && threadIdx.x >= 128 && threadIdx.x < 128 + kTileQueues) queue[threadIdx.x - 128] = 0;
   if (blockIdx.x == 0 && threadIdx.x == 192) *left = 0;
+  // the similarity screen's count of listed tiles
+  if (list_count && blockIdx.x == 0 && threadIdx.x == 200) *list_count = 0;
   // also clears the degree counters, walk states and claim keys of all S positions
   for (int p = blockIdx.x * 256 + threadIdx.x; p < S; p += gridDim.x * 256) {
     deg[p] = 0;
@@ -368,6 +371,78 @@ __device__ __forceinline__ uint32_t transpose32_bits(uint32_t x) {
   return transpose_step<1>(x, i);
 }
 
+// fp8 copy of the token rows for the similarity screen (Sec. 3's cosine,
+// estimated): row t is scaled by 2^e (the power of two that takes its
+// largest |x| into (224, 448], the E4M3 range; the scaling is exact),
+// rounded to E4M3 by the hardware conversion (values below the smallest
+// normal, 2^-6, are stored as 0, so no subnormal reaches the MFMA), and
+// its factor inv_norm[t] * 2^-e goes to qf[t].  rho[t] = |x - x^| / |x| is
+// taken from the decoded bytes, i.e. from the values the MFMA multiplies,
+// and enlarged by 2^-9 to cover the float32 sums.  Then for every pair,
+// with c~ = x^_a . x^_b / (|x_a| |x_b|):
+//   |c - c~| <= (|x^_a| |e_b| + |e_a| |x_b|) / (|x_a| |x_b|) <= rho_a + rho_b + rho_a rho_b.
+// One wave a row; d % 8 == 0.
+__global__ __launch_bounds__(256) void gram_quant_kernel(const uint16_t* __restrict__ x, int T, int d,
+                                                         const float* __restrict__ inv_norm, uint8_t* __restrict__ x8,
+                                                         float* __restrict__ qf, float* __restrict__ rho) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const uint16_t* row = x + static_cast<size_t>(t) * d;
+  float mx = 0.f;
+  for (int c = lane * 8; c < d; c += 512) {
+    Pack16 v;
+    v.u4 = *reinterpret_cast<const uint4*>(row + c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mx = fmaxf(mx, fabsf(bf16_to_f32(v.h[i])));
+  }
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  int e = 0;
+  if (mx > 0.f) {
+    int ex;
+    const float fr = frexpf(mx, &ex);   // mx = fr 2^ex, fr in [0.5, 1); 448 = 0.875 2^9
+    e = min(max(fr <= 0.875f ? 9 - ex : 8 - ex, -120), 120);
+  }
+  const float sc = ldexpf(1.f, e);
+  float se = 0.f, sx = 0.f;
+  uint8_t* out = x8 + static_cast<size_t>(t) * d;
+  for (int c = lane * 8; c < d; c += 512) {
+    Pack16 v;
+    v.u4 = *reinterpret_cast<const uint4*>(row + c);
+    float f[8], g[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      f[i] = bf16_to_f32(v.h[i]) * sc;
+      g[i] = fabsf(f[i]) < 0x1p-6f ? 0.f : f[i];
+    }
+    int lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[0], g[1], 0, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[2], g[3], lo, true);
+    int hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[4], g[5], 0, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[6], g[7], hi, true);
+    *reinterpret_cast<uint2*>(out + c) = make_uint2(static_cast<uint32_t>(lo), static_cast<uint32_t>(hi));
+    const float dq[8] = {__builtin_amdgcn_cvt_f32_fp8(lo, 0), __builtin_amdgcn_cvt_f32_fp8(lo, 1),
+                         __builtin_amdgcn_cvt_f32_fp8(lo, 2), __builtin_amdgcn_cvt_f32_fp8(lo, 3),
+                         __builtin_amdgcn_cvt_f32_fp8(hi, 0), __builtin_amdgcn_cvt_f32_fp8(hi, 1),
+                         __builtin_amdgcn_cvt_f32_fp8(hi, 2), __builtin_amdgcn_cvt_f32_fp8(hi, 3)};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float df = f[i] - dq[i];
+      se = fmaf(df, df, se);
+      sx = fmaf(f[i], f[i], sx);
+    }
+  }
+  se = wave_sum_f32(se);
+  sx = wave_sum_f32(sx);
+  if (lane == 0) {
+    qf[t] = ldexpf(inv_norm[t], -e);
+    rho[t] = sx > 0.f ? sqrtf(se / sx) * (1.f + 0x1p-9f) : 0.f;
+  }
+}
+
+// Modes of the bf16 similarity kernel: every tile on bf16 MFMA; every tile
+// on fp8 MFMA as a screen; the bf16 pass over the tiles the screen left.
+enum GramMode { kGramPlain = 0, kGramScreen = 1, kGramList = 2 };
+
 // Persistent over the upper-triangle tiles of every bucket.  The loop is
 // software-pipelined across tiles: the next tile's bucket lookup is loaded
 // before the current tile's K loop (nothing waits on it until the loop is
@@ -377,57 +452,88 @@ __device__ __forceinline__ uint32_t transpose32_bits(uint32_t x) {
 // compares, and its first DMA stages are issued before the rest of this
 // tile's epilogue, which therefore keeps its bit pieces outside the operand
 // ring.
+//
+// kGramScreen: X holds the fp8 rows (E4M3, rows of d_units 16-bit units),
+// inv_norm the per-row factors 2^-e / |x| (e: the row's power-of-two scale),
+// so the tile's values are estimates c~ of the cosines with |c~ - c| <= band
+// for every pair: band = 2 r + r^2 + 4e-3, r the largest rho (quantisation
+// error, see gram_quant_kernel) of the tile's rows, the constant room for
+// the float32 rounding of both passes.  A tile whose every value lies
+// outside (h - band, h + band) is decided exactly by c~ >= h: it is written
+// as in the bf16 pass.  Any other tile is appended to `list` (count in
+// list_count) and leaves its words and degrees to the kGramList pass, which
+// recomputes it from the bf16 rows.
+template <int MODE>
 __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
-    const uint16_t* __restrict__ X, int d, const int32_t* __restrict__ perm_token,
+    const uint16_t* __restrict__ X, int d_units, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg) {
-  using G = GramGemm;
+    const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg,
+    const float* __restrict__ rho, int* __restrict__ list, int* __restrict__ list_count) {
+  using G = std::conditional_t<MODE == kGramScreen, GemmBig64F8, GramGemm>;
+  static_assert(G::BM == kTile && G::BN == kTile && G::THREADS == GramGemm::THREADS, "similarity tile");
   constexpr int NI = 2 * kTile / G::THREADS;   // inverse norms staged per thread
   static_assert(G::FN % 2 == 0, "column blocks are transposed in pairs");
   // One LDS array: the operand ring, then the inverse norms of the tile's P
   // rows (0..kTile-1) and Q rows (kTile..), then the tile's adjacency
-  // pieces, dbits[row][32-column group] and tbits[column][32-row group].
-  // With separate LDS variables the compiler loses the alias scopes that
-  // tell a stage's fragment reads from the DMA into the other stage, and
-  // waits for each stage's DMA right after issuing it (no overlap).
+  // pieces, dbits[row][32-column group] and tbits[column][32-row group],
+  // then the screen's flag.  With separate LDS variables the compiler loses
+  // the alias scopes that tell a stage's fragment reads from the DMA into
+  // the other stage, and waits for each stage's DMA right after issuing it
+  // (no overlap).
   constexpr int kInvOff = G::LDS_BYTES, kBitsOff = kInvOff + 2 * kTile * 4;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kBitsOff + 2 * kTile * (kTile / 32) * 4];
+  constexpr int kRhoOff = kBitsOff + 2 * kTile * (kTile / 32) * 4;
+  constexpr int kFlagOff = kRhoOff + (MODE == kGramScreen ? 2 * kTile * 4 : 0);
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kFlagOff + 16];
+  float* rho_ab = reinterpret_cast<float*>(lds + kRhoOff);   // the screen's rho of the P and Q rows
   float* inv_ab = reinterpret_cast<float*>(lds + kInvOff);
   uint32_t (*dbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kBitsOff);
   uint32_t (*tbits)[kTile / 32] = reinterpret_cast<uint32_t (*)[kTile / 32]>(lds + kBitsOff + kTile * (kTile / 32) * 4);
+  int* flag = reinterpret_cast<int*>(lds + kFlagOff);
   const float* inv_a = inv_ab;
   const float* inv_b = inv_ab + kTile;
   if (*err) return;
   const int w = G::wave();
   const int wm = G::wave_m(w), wn = G::wave_n(w);
-  const int total = tile_off[E];
-  int tile = xcd_virtual_block();
-  if (tile >= total) return;   // block-uniform, before any barrier
+  // items: tiles 0..total-1, or the listed ones
+  const int total = MODE == kGramList ? *list_count : tile_off[E];
+  auto tile_of = [&](int item) { return MODE == kGramList ? list[item] : item; };
+  int item = xcd_virtual_block();
+  if (item >= total) return;   // block-uniform, before any barrier
+  int tile = tile_of(item);
   TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
   int32_t ptok[G::LP], qtok[G::LQ], itok[NI];
   uint32_t poff[G::LP], qoff[G::LQ];
   gram_tile_tokens<G>(c, perm_token, ptok, qtok, itok);
 #pragma unroll
-  for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
+  for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d_units;
 #pragma unroll
-  for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
-  float inv[NI];
+  for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d_units;
+  float inv[NI], rh[NI];
 #pragma unroll
-  for (int u = 0; u < NI; ++u) inv[u] = gram_stage_inv(inv_norm, itok[u]);
-  G::Pipe pipe;
-  G::prefetch(X, poff, X, qoff, d, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, pipe);
+  for (int u = 0; u < NI; ++u) {
+    inv[u] = gram_stage_inv(inv_norm, itok[u]);
+    if constexpr (MODE == kGramScreen) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+  }
+  typename G::Pipe pipe;
+  G::prefetch(X, poff, X, qoff, d_units, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, pipe);
   for (;;) {
 #pragma unroll
     for (int u = 0; u < NI; ++u) inv_ab[opaque_tid() + u * G::THREADS] = inv[u];   // visible after the K loop's first barrier
-    const int next = tile + gridDim.x;
+    if constexpr (MODE == kGramScreen) {
+#pragma unroll
+      for (int u = 0; u < NI; ++u) rho_ab[opaque_tid() + u * G::THREADS] = rh[u];
+      if (opaque_tid() == 0) *flag = 0;   // likewise; every wave read the last tile's flag before the loop's barrier
+    }
+    const int nitem = item + gridDim.x;
+    const int next = nitem < total ? tile_of(nitem) : 0;
     int nto = 0, no0 = 0, no1 = 0;
-    if (next < total) bucket_lookup_loads(tile_off, offsets, E, nto, no0, no1);
-    G::Acc acc;
+    if (nitem < total) bucket_lookup_loads(tile_off, offsets, E, nto, no0, no1);
+    typename G::Acc acc;
     G::zero(acc);
     G::resume(pipe, lds, acc);   // ends with a barrier: the ring is free
     TileCoord cn = c;
-    if (next < total) {
+    if (nitem < total) {
       cn = decode_tile_grouped_from(next, nto, no0, no1, E);
       gram_tile_tokens<G>(cn, perm_token, ptok, qtok, itok);
     }
@@ -442,12 +548,25 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     // column pieces: the two column blocks of a wave are transposed
     // together, one per half-wave.  Edge test: dot * (1/|a|) * (1/|b|) >= h
     // (rows outside the bucket carry a NaN scale), never a token with
-    // itself.
+    // itself.  The screen also keeps the least |c~ - h| of the lane (a NaN
+    // value, which is no edge on either pass, does not count).
     // lane values recomputed from the opaque thread index: hoisted out of
     // the tile loop they would stay live across the K loop
     const int el = opaque_tid() & 63;
     const int l31 = el & 31, hi = el >> 5;
     const bool same_tile = c.ti == c.tj;
+    float dmin = __builtin_inff(), band = 0.f;
+    if constexpr (MODE == kGramScreen) {
+      // |c~ - c| <= rho_a + rho_b + rho_a rho_b over the tile's rows
+      float r = 0.f;
+#pragma unroll
+      for (int q = 0; q < 2 * kTile / 256; ++q) {
+        const float4 f = *reinterpret_cast<const float4*>(&rho_ab[256 * q + 4 * el]);
+        r = fmaxf(r, fmaxf(fmaxf(f.x, f.y), fmaxf(f.z, f.w)));
+      }
+      for (int o = 32; o >= 1; o >>= 1) r = fmaxf(r, __shfl_xor(r, o, 64));
+      band = 2.f * r + r * r + 4e-3f;
+    }
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
       const int abase = wm * G::WTM + 32 * fm;
@@ -471,10 +590,12 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
         float p = acc[fm][fn][15] * ia[15] * ib;
 #pragma unroll
         for (int v = 15; v >= 1; --v) {
+          if constexpr (MODE == kGramScreen) dmin = fminf(dmin, fabsf(p - h));
           float q;
           bits = shift_in_ge_next(bits, p, h, acc[fm][fn][v - 1], ia[v - 1], ib, q);
           p = q;
         }
+        if constexpr (MODE == kGramScreen) dmin = fminf(dmin, fabsf(p - h));
         bits = shift_in_ge_last(bits, p, h);
         // nibble k (accumulators 4k..4k+3) to bits 8k..8k+3, then this half's rows
         bits = (bits & 0xFFu) | ((bits & 0xFF00u) << 8);
@@ -494,51 +615,65 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
         dbits[abase + l31][(wn * G::WTN + 32 * (2 * p + hi)) >> 5] = rowbits;
       }
     }
+    if constexpr (MODE == kGramScreen) {
+      if (__ballot(dmin < band) != 0 && el == 0) *flag = 1;
+    }
     __builtin_amdgcn_sched_barrier(0);
-    if (next < total) {
+    if (nitem < total) {
 #pragma unroll
-      for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d;
+      for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d_units;
 #pragma unroll
-      for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d;
+      for (int j = 0; j < G::LQ; ++j) qoff[j] = static_cast<uint32_t>(qtok[j]) * d_units;
       // before the DMA: waiting for them then does not wait for the DMA
 #pragma unroll
-      for (int u = 0; u < NI; ++u) inv[u] = gram_stage_inv(inv_norm, itok[u]);
-      G::prefetch(X, poff, X, qoff, d, cn.n - cn.ti * kTile, cn.n - cn.tj * kTile, lds, pipe);
+      for (int u = 0; u < NI; ++u) {
+        inv[u] = gram_stage_inv(inv_norm, itok[u]);
+        if constexpr (MODE == kGramScreen) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+      }
+      G::prefetch(X, poff, X, qoff, d_units, cn.n - cn.ti * kTile, cn.n - cn.tj * kTile, lds, pipe);
     }
     // LDS-only barriers from here on: a full __syncthreads() would also wait
     // for the next tile's DMA
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's pieces are in LDS
     raw_barrier();
-    // degree: edges of each tile row (and, off the diagonal, of each mirrored row)
-    for (int i = opaque_tid(); i < 2 * kTile; i += G::THREADS) {
-      const bool mirror = i >= kTile;
-      const int rl = mirror ? i - kTile : i;
-      const uint32_t* pcs = mirror ? tbits[rl] : dbits[rl];
-      int cnt = 0;
-#pragma unroll
-      for (int g = 0; g < kTile / 32; ++g) cnt += __popc(pcs[g]);
-      const int r = (mirror ? c.tj : c.ti) * kTile + rl;
-      if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
+    bool decided = true;
+    if constexpr (MODE == kGramScreen) {
+      decided = *flag == 0;
+      if (!decided && opaque_tid() == 0) list[atomicAdd(list_count, 1)] = tile;
     }
-    // write the words: 4 per row of the tile, direct and (off-diagonal) mirrored
-    for (int i = opaque_tid(); i < kTile * 4; i += G::THREADS) {
-      const int rl = i >> 2, ww = i & 3;
-      const uint64_t dv = static_cast<uint64_t>(dbits[rl][2 * ww]) |
-                          (static_cast<uint64_t>(dbits[rl][2 * ww + 1]) << 32);
-      const int a = c.ti * kTile + rl, wd = 4 * c.tj + ww;
-      if (a < c.n && wd < c.W) bitmask[bm_off[c.e] + static_cast<long long>(a) * c.W + wd] = dv;
-      if (c.ti != c.tj) {
-        const uint64_t tv = static_cast<uint64_t>(tbits[rl][2 * ww]) |
-                            (static_cast<uint64_t>(tbits[rl][2 * ww + 1]) << 32);
-        const int bb = c.tj * kTile + rl, wt = 4 * c.ti + ww;
-        if (bb < c.n && wt < c.W) bitmask[bm_off[c.e] + static_cast<long long>(bb) * c.W + wt] = tv;
+    if (decided) {
+      // degree: edges of each tile row (and, off the diagonal, of each mirrored row)
+      for (int i = opaque_tid(); i < 2 * kTile; i += G::THREADS) {
+        const bool mirror = i >= kTile;
+        const int rl = mirror ? i - kTile : i;
+        const uint32_t* pcs = mirror ? tbits[rl] : dbits[rl];
+        int cnt = 0;
+#pragma unroll
+        for (int g = 0; g < kTile / 32; ++g) cnt += __popc(pcs[g]);
+        const int r = (mirror ? c.tj : c.ti) * kTile + rl;
+        if (cnt && r < c.n && (!mirror || c.ti != c.tj)) atomicAdd(&deg[c.lo + r], cnt);
+      }
+      // write the words: 4 per row of the tile, direct and (off-diagonal) mirrored
+      for (int i = opaque_tid(); i < kTile * 4; i += G::THREADS) {
+        const int rl = i >> 2, ww = i & 3;
+        const uint64_t dv = static_cast<uint64_t>(dbits[rl][2 * ww]) |
+                            (static_cast<uint64_t>(dbits[rl][2 * ww + 1]) << 32);
+        const int a = c.ti * kTile + rl, wd = 4 * c.tj + ww;
+        if (a < c.n && wd < c.W) bitmask[bm_off[c.e] + static_cast<long long>(a) * c.W + wd] = dv;
+        if (c.ti != c.tj) {
+          const uint64_t tv = static_cast<uint64_t>(tbits[rl][2 * ww]) |
+                              (static_cast<uint64_t>(tbits[rl][2 * ww + 1]) << 32);
+          const int bb = c.tj * kTile + rl, wt = 4 * c.ti + ww;
+          if (bb < c.n && wt < c.W) bitmask[bm_off[c.e] + static_cast<long long>(bb) * c.W + wt] = tv;
+        }
       }
     }
-    if (next >= total) break;
-    // every wave's reads of the pieces and of inv_ab are done before the
-    // next tile overwrites them
+    if (nitem >= total) break;
+    // every wave's reads of the pieces, of inv_ab, rho_ab and the flag are
+    // done before the next tile overwrites them
     __builtin_amdgcn_s_waitcnt(0xC07F);
     raw_barrier();
+    item = nitem;
     tile = next;
     c = cn;
   }
@@ -1752,9 +1887,36 @@ struct CondenseWs {
   int* left;                    // a position stayed undecided after the greedy rounds
   int32_t* colinfo = nullptr;   // previous positions of every slot of every position
   int* queue = nullptr;         // tile queues of the similarity kernel
+  // the fp8 screen (calls without history whose shape allows it): fp8 rows,
+  // row factors and quantisation errors, the tiles left to the bf16 pass
+  // and their count
+  uint8_t* x8 = nullptr;
+  float* qf = nullptr;
+  float* rho = nullptr;
+  int* list = nullptr;
+  int* list_count = nullptr;
 };
 
-CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool history = false) {
+// Process-wide switch of the fp8 similarity screen (on by default).
+std::atomic<int> g_gram_screen{1};
+
+// Shapes whose similarity call may take the fp8 screen: long products
+// (d >= 2048, whole 128-value fp8 stages) and buckets of MFMA-bound size
+// on average (T k / E >= 512); below that the extra pass over x costs
+// about what the screen saves.
+bool gram_screen_shape(int T, int d, int E, int k) {
+  return d >= 2048 && d % 128 == 0 && static_cast<long long>(T) * k >= 512ll * E;
+}
+
+// Upper bound of the number of similarity tiles: sum over buckets of
+// t_e (t_e + 1) / 2 with t_e = ceil(n_e / kTile) <= ceil(max_bucket / kTile)
+// and sum t_e <= S / kTile + E.
+long long gram_tile_bound(long long S, int E, int max_bucket) {
+  const long long tmax = (static_cast<long long>(max_bucket) + kTile - 1) / kTile;
+  return (S / kTile + E) * (tmax + 1) / 2 + 1;
+}
+
+CondenseWs carve_condense(Carver& c, int T, int d, int E, int k, int max_bucket, bool history = false) {
   CondenseWs w;
   const long long S = static_cast<long long>(T) * k;
   w.inv_norm = c.take<float>(T);
@@ -1775,6 +1937,12 @@ CondenseWs carve_condense(Carver& c, int T, int E, int k, int max_bucket, bool h
     w.stats = c.take<unsigned long long>(4);
     w.colinfo = c.take<int32_t>(static_cast<size_t>(S) * k);
     w.queue = c.take<int>(kTileQueues);
+  } else if (gram_screen_shape(T, d, E, k)) {
+    w.x8 = c.take<uint8_t>(static_cast<size_t>(T) * d);
+    w.qf = c.take<float>(T);
+    w.rho = c.take<float>(T);
+    w.list_count = c.take<int>(1);
+    w.list = c.take<int>(static_cast<size_t>(gram_tile_bound(S, E, max_bucket)));
   }
   return w;
 }
@@ -1828,7 +1996,7 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   {
     const int tile = bf16 ? kTile : kTileF32;
 #define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
-                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats, ws.queue, ws.left
+                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats, ws.queue, ws.left, ws.list_count
     if (bf16) {
       if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
       else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
@@ -1839,10 +2007,21 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
 #undef LUFFY_NORM_ARGS
   }
   if (!hc) {
-    if (bf16)
-      launch("gram", gram_kernel_bf16, persistent_grid(), GramGemm::THREADS, 0, s, static_cast<const uint16_t*>(x),
-             d, perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask,
-             ws.deg);
+    const uint16_t* xb = static_cast<const uint16_t*>(x);
+    if (bf16 && ws.x8 && g_gram_screen.load(std::memory_order_relaxed)) {
+      // fp8 screen over every tile, then the bf16 pass over the tiles it left
+      launch("gram_quant", gram_quant_kernel, (T + 3) / 4, 256, 0, s, xb, T, d, inv_norm_use, ws.x8, ws.qf,
+             ws.rho);
+      launch("gram", gram_kernel_bf16<kGramScreen>, persistent_grid(), GramGemm::THREADS, 0, s,
+             reinterpret_cast<const uint16_t*>(ws.x8), d / 2, perm_token, offsets, E, ws.qf, threshold, ws.tile_off,
+             ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.rho, ws.list, ws.list_count);
+      launch("gram_recheck", gram_kernel_bf16<kGramList>, persistent_grid(), GramGemm::THREADS, 0, s, xb, d,
+             perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg,
+             nullptr, ws.list, ws.list_count);
+    } else if (bf16)
+      launch("gram", gram_kernel_bf16<kGramPlain>, persistent_grid(), GramGemm::THREADS, 0, s, xb, d, perm_token,
+             offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg, nullptr,
+             nullptr, nullptr);
     else
       launch("gram", gram_kernel_f32, 2 * persistent_grid(), 256, 0, s, static_cast<const float*>(x), d, perm_token,
              offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg);
@@ -1924,10 +2103,9 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
 }  // namespace
 
 extern "C" size_t luffy_condense_workspace_size(int T, int d, int E, int k, int max_bucket) {
-  (void)d;
   if (T <= 0 || E <= 0 || k <= 0 || max_bucket < 0) return 0;
   Carver c(nullptr);
-  carve_condense(c, T, E, k, max_bucket);
+  carve_condense(c, T, d, E, k, max_bucket);
   return c.size();
 }
 
@@ -1945,10 +2123,17 @@ extern "C" int luffy_condense(const void* x, int T, int d, int dtype,
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "luffy_condense: workspace needs %zu bytes, 256-aligned", need);
   Carver c(workspace);
-  const CondenseWs ws = carve_condense(c, T, E, k, max_bucket);
+  const CondenseWs ws = carve_condense(c, T, d, E, k, max_bucket);
   condense_enqueue(x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold, rep_of_pos, rep_row,
                    rep_offsets, rep_token, x_rep, degree, inv_norm, ws, nullptr, static_cast<hipStream_t>(stream));
   return check_launch("luffy_condense");
+}
+
+extern "C" int luffy_set_similarity_screen(int on) { return g_gram_screen.exchange(on ? 1 : 0); }
+
+extern "C" int luffy_similarity_screen_applies(int T, int d, int E, int k, int dtype) {
+  return dtype == LUFFY_BF16 && T > 0 && E > 0 && k > 0 && gram_screen_shape(T, d, E, k) &&
+         g_gram_screen.load(std::memory_order_relaxed);
 }
 
 extern "C" size_t luffy_history_size(int T, int E, int k, int max_bucket) {
@@ -1959,10 +2144,9 @@ extern "C" size_t luffy_history_size(int T, int E, int k, int max_bucket) {
 }
 
 extern "C" size_t luffy_condense_history_workspace_size(int T, int d, int E, int k, int max_bucket) {
-  (void)d;
   if (T <= 0 || E <= 0 || k <= 0 || max_bucket < 0) return 0;
   Carver c(nullptr);
-  carve_condense(c, T, E, k, max_bucket, true);
+  carve_condense(c, T, d, E, k, max_bucket, true);
   return c.size();
 }
 
@@ -1989,7 +2173,7 @@ extern "C" int luffy_condense_history(const void* x, int T, int d, int dtype,
   if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(LUFFY_E_WORKSPACE, "%s: workspace needs %zu bytes, 256-aligned", fn, need);
   Carver c(workspace);
-  const CondenseWs ws = carve_condense(c, T, E, k, max_bucket, true);
+  const CondenseWs ws = carve_condense(c, T, d, E, k, max_bucket, true);
   HistCall hc{slot_pos, hist_in, hist_out, S1, S2, stats};
   condense_enqueue(x, T, d, dtype, perm_token, offsets, E, k, max_bucket, threshold, rep_of_pos, rep_row,
                    rep_offsets, rep_token, x_rep, degree, inv_norm, ws, &hc, static_cast<hipStream_t>(stream));

@@ -11,6 +11,8 @@
 // are dealt to the four SIMDs of a CU round-robin (wave w on SIMD w % 4).
 #pragma once
 
+#include <type_traits>
+
 #include "luffy_common.h"
 
 namespace luffy {
@@ -19,6 +21,16 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
 __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 32 fp8 (OCP E4M3) values a lane: one operand fragment of the 32 x 32 x 64
+// fp8 product.
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// v_mfma_scale_f32_32x32x64_f8f6f4 with both operands E4M3 (format 0) and
+// unit block scales (E8M0 exponent 127 = 2^0).
+__device__ __forceinline__ f32x16 mfma32x32x64_f8(i32x8 a, i32x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
 }
 
 // Workgroup barrier without the memory fences of __syncthreads(): the fence
@@ -71,8 +83,15 @@ __device__ __forceinline__ int opaque_tid() {
 // Result layout of acc[fm][fn][v] in lane l of wave w:
 //   P row  wave_m(w) * WTM + 32*fm + 8*(v/4) + 4*(l/32) + v%4
 //   Q row  q_row(wave_n(w), fn) + l%32
+//
+// F8: the operands are fp8 (E4M3) rows, handed to the core as rows of
+// 16-bit units (two values a unit: offsets, K and BK count units), so the
+// DMA is unchanged; a 64-unit stage holds 128 values of K, multiplied in
+// two steps of v_mfma_scale_f32_32x32x64_f8f6f4, whose fragments are two
+// 16-byte chunks of a row (lanes 0-31 chunks 4s and 4s+1 of step s, lanes
+// 32-63 chunks 4s+2 and 4s+3).  The accumulator layout is the same.
 template <int BM_, int BN_, int WM_, int WN_, bool MFAST_, bool QIL_, int BK_ = 64, int STAGES_ = 2,
-          bool PT_ = false, bool QT_ = false>
+          bool PT_ = false, bool QT_ = false, bool F8_ = false>
 struct GemmCore {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr bool QIL = QIL_;
@@ -93,7 +112,10 @@ struct GemmCore {
   static constexpr int ROW_BYTES = BK * 2;
   static constexpr int CPR = ROW_BYTES / 16;         // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;               // rows per DMA instruction
-  static constexpr int STEPS = BK / 16;              // MFMA K steps per stage
+  static constexpr bool F8 = F8_;
+  static_assert(!F8 || (BK == 64 && !PT && !QT), "fp8 operands: row-major, 64-unit stages");
+  static constexpr int STEPS = F8 ? BK / 32 : BK / 16;   // MFMA K steps per stage
+  static constexpr int READS = F8 ? 2 : 1;               // LDS reads per fragment
   static constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
   static constexpr int NWAVES = WM * WN;
@@ -224,9 +246,18 @@ struct GemmCore {
 
   // Fragments of one 16-wide K step (chunks 2*step and 2*step+1 of every
   // row: lanes 0-31 take the low chunk, lanes 32-63 the high one).
+  using Frag = std::conditional_t<F8, i32x8, bf16x8>;
   struct Frags {
-    bf16x8 a[FM], b[FN];
+    Frag a[FM], b[FN];
   };
+
+  // fp8 fragment: chunks c and c + 1 (byte offsets o0, o1) of a stage row
+  static __device__ __forceinline__ i32x8 read_f8(lds_ptr row, int o0, int o1) {
+    typedef int i32x4 __attribute__((ext_vector_type(4)));
+    const i32x4 lo = *reinterpret_cast<const __attribute__((address_space(3))) i32x4*>(row + o0);
+    const i32x4 hi = *reinterpret_cast<const __attribute__((address_space(3))) i32x4*>(row + o1);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
 
   // K step `step` of the stage at S, first NQ Q blocks.
   // One fragment of a K-major operand whose stage region starts at R (row
@@ -256,7 +287,14 @@ struct GemmCore {
   template <int NQ>
   static __device__ __forceinline__ void read_step(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
                                                    Frags& f) {
-    if constexpr (NQ > 0) {
+    if constexpr (NQ > 0 && F8) {
+      const int c0 = 4 * step + 2 * half;
+      const int o0 = (c0 ^ sw) * 16, o1 = ((c0 + 1) ^ sw) * 16;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) f.a[i] = read_f8(S + prow0 + 32 * i * ROW_BYTES, o0, o1);
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) f.b[j] = read_f8(S + qrow0 + QSTEP * j * ROW_BYTES, o0, o1);
+    } else if constexpr (NQ > 0) {
       const int pc = ((2 * step + half) ^ sw) * 16;
       if constexpr (PT) {
         const int wm = wave_m(wave());
@@ -286,7 +324,10 @@ struct GemmCore {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < NQ; ++j) acc[i][j] = mfma32x32x16(f.a[i], f.b[j], acc[i][j]);
+      for (int j = 0; j < NQ; ++j) {
+        if constexpr (F8) acc[i][j] = mfma32x32x64_f8(f.a[i], f.b[j], acc[i][j]);
+        else acc[i][j] = mfma32x32x16(f.a[i], f.b[j], acc[i][j]);
+      }
   }
 
   // Schedule of a step without buffer loads: the LDS reads of the next step
@@ -294,7 +335,7 @@ struct GemmCore {
   // next step starts.
   template <int NQ>
   static __device__ __forceinline__ void interleave_reads() {
-    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? FM + NQ : 0;
+    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? READS * (FM + NQ) : 0;
 #pragma unroll
     for (int i = 0; i < NMF; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -309,7 +350,7 @@ struct GemmCore {
   // latency is the longer one.
   template <int NQ>
   static __device__ __forceinline__ void interleave_loads() {
-    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? FM + NQ : 0, NVM = LOADS;
+    constexpr int NMF = FM * NQ, NDS = NQ > 0 ? READS * (FM + NQ) : 0, NVM = LOADS;
     constexpr int PV = NMF < NVM ? NMF : NVM;
     constexpr int PD = (NMF - PV) < NDS ? (NMF - PV) : NDS;
 #pragma unroll
@@ -414,10 +455,106 @@ struct GemmCore {
     resume<NQ>(p, lds_generic, acc);
   }
 
+  // fp8 step: the MFMAs of the fragments in f, while the fragments of step
+  // `step` of the stage at S are read into f: the B fragments into a
+  // second set first, then A fragment i as soon as the MFMAs that use it
+  // are issued.  Two sets of 32-byte fragments would not fit beside the
+  // accumulators.  READ = false: the MFMAs only.
+  template <int NQ, bool READ>
+  static __device__ __forceinline__ void mma_read_f8(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
+                                                     Frags& f, Acc& acc) {
+    const int c0 = 4 * step + 2 * half;
+    const int o0 = (c0 ^ sw) * 16, o1 = ((c0 + 1) ^ sw) * 16;
+    Frag nb[NQ > 0 ? NQ : 1];
+    if constexpr (READ) {
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) nb[j] = read_f8(S + qrow0 + QSTEP * j * ROW_BYTES, o0, o1);
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) acc[i][j] = mfma32x32x64_f8(f.a[i], f.b[j], acc[i][j]);
+      if constexpr (READ) f.a[i] = read_f8(S + prow0 + 32 * i * ROW_BYTES, o0, o1);
+    }
+    if constexpr (READ) {
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) f.b[j] = nb[j];
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * NQ, 0);   // DS reads of the B set
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NQ, 0);    // the MFMAs of A fragment i
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // its next-step reads
+      }
+    }
+  }
+
+  // resume() for fp8 operands: the same ring and barriers, one fragment set.
+  template <int NQ>
+  static __device__ __forceinline__ void resume_f8(const Pipe& p, uint8_t* lds_generic, Acc& acc) {
+    const lds_ptr lds = (lds_ptr)lds_generic;
+    const int lane = opaque_tid() & 63;
+    const int w = wave();
+    const int wm = wave_m(w), wn = wave_n(w);
+    const __amdgpu_buffer_rsrc_t prs = p.prs, qrs = p.qrs;
+    uint32_t goff[LOADS];
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) goff[j] = p.goff[j];
+    const int nk = p.nk;
+    const int pro = min(nk, STAGES);
+    wait_stages(pro - 1);
+    raw_barrier();
+    const int sw = swz(lane & 31);
+    const int prow0 = (wm * WTM + (lane & 31)) * ROW_BYTES;
+    const int qrow0 = (BM + q_row(wn, 0) + (lane & 31)) * ROW_BYTES;
+    const int half = lane >> 5;
+    Frags f;
+    read_step<NQ>(lds, prow0, qrow0, half, sw, 0, f);
+    int kt = 0, cb = 0;
+    // steady state: stage kt+STAGES exists
+    for (; kt + STAGES < nk; ++kt) {
+      const lds_ptr cur = lds + cb * STAGE_BYTES;
+      cb = cb + 1 == STAGES ? 0 : cb + 1;
+      const lds_ptr nxt = lds + cb * STAGE_BYTES;
+#pragma unroll
+      for (int st = 1; st < STEPS; ++st) {
+        __builtin_amdgcn_sched_barrier(0);
+        mma_read_f8<NQ, true>(cur, prow0, qrow0, half, sw, st, f, acc);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<(STAGES - 2) * LOADS>();   // stage kt+1 landed (this wave's part)
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): own reads of stage kt done
+      raw_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(prs, qrs, goff, kt + STAGES, cur, w);
+      mma_read_f8<NQ, true>(nxt, prow0, qrow0, half, sw, 0, f, acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // last stages: nothing more to issue; the reads that follow the very
+    // last step fetch unused values from a stage that is still intact
+    for (; kt < nk; ++kt) {
+      const lds_ptr cur = lds + cb * STAGE_BYTES;
+      cb = cb + 1 == STAGES ? 0 : cb + 1;
+#pragma unroll
+      for (int st = 1; st < STEPS; ++st) mma_read_f8<NQ, true>(cur, prow0, qrow0, half, sw, st, f, acc);
+      const bool more = kt + 1 < nk;
+      if (more) {
+        wait_stages(nk - 2 - kt);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        raw_barrier();
+      }
+      mma_read_f8<NQ, true>(more ? lds + cb * STAGE_BYTES : cur, prow0, qrow0, half, sw, 0, f, acc);
+    }
+    __syncthreads();
+  }
+
   // Second half of run(): waits for the prefetched stages and runs the K
   // loop; ends with a barrier after which the LDS may be reused.
   template <int NQ = FN>
   static __device__ __forceinline__ void resume(const Pipe& p, uint8_t* lds_generic, Acc& acc) {
+    if constexpr (F8) {
+      resume_f8<NQ>(p, lds_generic, acc);
+      return;
+    }
     const lds_ptr lds = (lds_ptr)lds_generic;
     const int lane = opaque_tid() & 63;
     const int w = wave();
@@ -474,6 +611,8 @@ struct GemmCore {
 
 // 256 x 256, 512 threads, wave tile 128 x 64, 64-wide stages.
 using GemmBig64 = GemmCore<256, 256, 2, 4, false, false>;
+// The same on fp8 rows: 128 values of K a stage.
+using GemmBig64F8 = GemmCore<256, 256, 2, 4, false, false, 64, 2, false, false, true>;
 // 256 x 256, 512 threads, wave tile 64 x 128 (SIMD s holds P rows
 // 64s..64s+63 of both Q halves), 64-wide stages.
 using GemmRagged64 = GemmCore<256, 256, 4, 2, true, false>;
