@@ -294,15 +294,23 @@ static_assert(GramGemm::BM == kTile && GramGemm::BN == kTile, "similarity tile")
 // of the tile's 2*kTile (P rows, then Q rows) goes to thread i % THREADS,
 // as its (i / THREADS)-th (-1 past the bucket).
 template <class G>
+// pad >= 0: rows past the bucket read row `pad` instead (a zero row, so
+// that every fetched row is defined).
 __device__ __forceinline__ void gram_tile_tokens(const TileCoord& c, const int32_t* __restrict__ perm_token,
                                                  int32_t (&ptok)[G::LP], int32_t (&qtok)[G::LQ],
-                                                 int32_t (&itok)[2 * kTile / G::THREADS]) {
+                                                 int32_t (&itok)[2 * kTile / G::THREADS], int pad = -1) {
   static_assert((2 * kTile) % G::THREADS == 0, "inverse norms per thread");
   const int32_t* pt = perm_token + c.lo;
 #pragma unroll
-  for (int j = 0; j < G::LP; ++j) ptok[j] = pt[min(c.ti * kTile + G::load_row(j), c.n - 1)];
+  for (int j = 0; j < G::LP; ++j) {
+    const int r = c.ti * kTile + G::load_row(j);
+    ptok[j] = pad >= 0 && r >= c.n ? pad : pt[min(r, c.n - 1)];
+  }
 #pragma unroll
-  for (int j = 0; j < G::LQ; ++j) qtok[j] = pt[min(c.tj * kTile + G::load_row(G::LP + j) - G::BM, c.n - 1)];
+  for (int j = 0; j < G::LQ; ++j) {
+    const int r = c.tj * kTile + G::load_row(G::LP + j) - G::BM;
+    qtok[j] = pad >= 0 && r >= c.n ? pad : pt[min(r, c.n - 1)];
+  }
 #pragma unroll
   for (int u = 0; u < 2 * kTile / G::THREADS; ++u) {
     const int i = static_cast<int>(threadIdx.x) + u * G::THREADS;
@@ -329,6 +337,21 @@ __device__ __forceinline__ uint32_t shift_in_ge_next(uint32_t bits, float p, flo
       "v_addc_co_u32 %0, vcc, %0, %0, vcc"
       : "+v"(bits), "=&v"(q)
       : "v"(p), "s"(h), "v"(a), "v"(b), "v"(c)
+      : "vcc");
+  return bits;
+}
+
+// bits * 2 + (p >= h) and m = min(m, |h - p|) (a NaN p shifts in 0 and
+// leaves m): the subtraction and the minimum fill the two wait states of
+// the VCC read.
+__device__ __forceinline__ uint32_t shift_in_ge_band(uint32_t bits, float p, float h, float& m) {
+  float dif;
+  asm("v_cmp_le_f32 vcc, %4, %3\n\t"
+      "v_sub_f32 %2, %4, %3\n\t"
+      "v_min_f32 %1, %1, |%2|\n\t"
+      "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+      : "+v"(bits), "+v"(m), "=&v"(dif)
+      : "v"(p), "s"(h)
       : "vcc");
   return bits;
 }
@@ -372,40 +395,32 @@ __device__ __forceinline__ uint32_t transpose32_bits(uint32_t x) {
 }
 
 // fp8 copy of the token rows for the similarity screen (Sec. 3's cosine,
-// estimated): row t is scaled by 2^e (the power of two that takes its
-// largest |x| into (224, 448], the E4M3 range; the scaling is exact),
-// rounded to E4M3 by the hardware conversion (values below the smallest
-// normal, 2^-6, are stored as 0, so no subnormal reaches the MFMA), and
-// its factor inv_norm[t] * 2^-e goes to qf[t].  rho[t] = |x - x^| / |x| is
-// taken from the decoded bytes, i.e. from the values the MFMA multiplies,
-// and enlarged by 2^-9 to cover the float32 sums.  Then for every pair,
-// with c~ = x^_a . x^_b / (|x_a| |x_b|):
-//   |c - c~| <= (|x^_a| |e_b| + |e_a| |x_b|) / (|x_a| |x_b|) <= rho_a + rho_b + rho_a rho_b.
-// One wave a row; d % 8 == 0.
+// estimated): row t is normalised and scaled by 2^8, x_n = x * inv_norm[t] *
+// 256 (|x_n| = 256 up to the rounding of the norm, every value within
+// +-256, inside the E4M3 range), rounded to E4M3 by the hardware conversion
+// (values below the smallest normal, 2^-6, stored as 0, so no subnormal
+// reaches the MFMA).  rho[t] = |x_n - x^| / |x_n| is taken from the decoded
+// bytes, i.e. from the values the MFMA multiplies, and enlarged by 2^-9 to
+// cover the float32 sums.  Then for every pair c~ = x^_a . x^_b / 2^16 (the
+// raw fp8 product scaled by a power of two) and the cosine c of the bf16
+// pass satisfy
+//   |c - c~| <= (|x^_a| |e_b| + |e_a| |x_b|) / (|x_a| |x_b|) <= rho_a + rho_b + rho_a rho_b
+// (e = x_n - x^, |x_n| = 256), up to float32 rounding.  Row T of x8 (the
+// pad row of partial tiles) is zero.  One wave a row; d % 8 == 0.
 __global__ __launch_bounds__(256) void gram_quant_kernel(const uint16_t* __restrict__ x, int T, int d,
                                                          const float* __restrict__ inv_norm, uint8_t* __restrict__ x8,
-                                                         float* __restrict__ qf, float* __restrict__ rho) {
+                                                         float* __restrict__ rho) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  const uint16_t* row = x + static_cast<size_t>(t) * d;
-  float mx = 0.f;
-  for (int c = lane * 8; c < d; c += 512) {
-    Pack16 v;
-    v.u4 = *reinterpret_cast<const uint4*>(row + c);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) mx = fmaxf(mx, fabsf(bf16_to_f32(v.h[i])));
-  }
-  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  int e = 0;
-  if (mx > 0.f) {
-    int ex;
-    const float fr = frexpf(mx, &ex);   // mx = fr 2^ex, fr in [0.5, 1); 448 = 0.875 2^9
-    e = min(max(fr <= 0.875f ? 9 - ex : 8 - ex, -120), 120);
-  }
-  const float sc = ldexpf(1.f, e);
-  float se = 0.f, sx = 0.f;
+  if (t > T) return;
   uint8_t* out = x8 + static_cast<size_t>(t) * d;
+  if (t == T) {
+    for (int c = lane * 8; c < d; c += 512) *reinterpret_cast<uint2*>(out + c) = make_uint2(0u, 0u);
+    return;
+  }
+  const uint16_t* row = x + static_cast<size_t>(t) * d;
+  const float sc = inv_norm[t] * 256.f;
+  float se = 0.f, sx = 0.f;
   for (int c = lane * 8; c < d; c += 512) {
     Pack16 v;
     v.u4 = *reinterpret_cast<const uint4*>(row + c);
@@ -433,10 +448,7 @@ __global__ __launch_bounds__(256) void gram_quant_kernel(const uint16_t* __restr
   }
   se = wave_sum_f32(se);
   sx = wave_sum_f32(sx);
-  if (lane == 0) {
-    qf[t] = ldexpf(inv_norm[t], -e);
-    rho[t] = sx > 0.f ? sqrtf(se / sx) * (1.f + 0x1p-9f) : 0.f;
-  }
+  if (lane == 0) rho[t] = sx > 0.f ? sqrtf(se / sx) * (1.f + 0x1p-9f) : 0.f;
 }
 
 // Modes of the bf16 similarity kernel: every tile on bf16 MFMA; every tile
@@ -453,23 +465,23 @@ enum GramMode { kGramPlain = 0, kGramScreen = 1, kGramList = 2 };
 // tile's epilogue, which therefore keeps its bit pieces outside the operand
 // ring.
 //
-// kGramScreen: X holds the fp8 rows (E4M3, rows of d_units 16-bit units),
-// inv_norm the per-row factors 2^-e / |x| (e: the row's power-of-two scale),
-// so the tile's values are estimates c~ of the cosines with |c~ - c| <= band
-// for every pair: band = 2 r + r^2 + 4e-3, r the largest rho (quantisation
-// error, see gram_quant_kernel) of the tile's rows, the constant room for
-// the float32 rounding of both passes.  A tile whose every value lies
-// outside (h - band, h + band) is decided exactly by c~ >= h: it is written
-// as in the bf16 pass.  Any other tile is appended to `list` (count in
-// list_count) and leaves its words and degrees to the kGramList pass, which
-// recomputes it from the bf16 rows.
+// kGramScreen (h > 0): X holds the fp8 rows (E4M3 unit rows scaled by 2^8,
+// rows of d_units 16-bit units; row T_pad is zero and stands in for the
+// rows past a bucket), so a tile's products are 2^16 c~, estimates of the
+// cosines with |c~ - c| <= band for every pair: band = 2 r + r^2 + 4e-3, r
+// the largest rho (quantisation error, see gram_quant_kernel) of the
+// tile's rows, the constant room for the float32 rounding of both passes.
+// A tile whose every value lies outside (h - band, h + band) is decided
+// exactly by c~ >= h: it is written as in the bf16 pass.  Any other tile is
+// appended to `list` (count in list_count) and leaves its words and degrees
+// to the kGramList pass, which recomputes it from the bf16 rows.
 template <int MODE>
 __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     const uint16_t* __restrict__ X, int d_units, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ offsets, int E, const float* __restrict__ inv_norm, float h,
     const int32_t* __restrict__ tile_off, const long long* __restrict__ bm_off,
     const int* __restrict__ err, uint64_t* __restrict__ bitmask, int32_t* __restrict__ deg,
-    const float* __restrict__ rho, int* __restrict__ list, int* __restrict__ list_count) {
+    const float* __restrict__ rho, int* __restrict__ list, int* __restrict__ list_count, int T_pad) {
   using G = std::conditional_t<MODE == kGramScreen, GemmBig64F8, GramGemm>;
   static_assert(G::BM == kTile && G::BN == kTile && G::THREADS == GramGemm::THREADS, "similarity tile");
   constexpr int NI = 2 * kTile / G::THREADS;   // inverse norms staged per thread
@@ -504,7 +516,10 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
   TileCoord c = decode_tile_grouped(tile, tile_off, offsets, E);
   int32_t ptok[G::LP], qtok[G::LQ], itok[NI];
   uint32_t poff[G::LP], qoff[G::LQ];
-  gram_tile_tokens<G>(c, perm_token, ptok, qtok, itok);
+  // the screen's rows past the bucket read the zero row T (x8 has T + 1)
+  constexpr bool SCR = MODE == kGramScreen;
+  const int pad = SCR ? T_pad : -1;
+  gram_tile_tokens<G>(c, perm_token, ptok, qtok, itok, pad);
 #pragma unroll
   for (int j = 0; j < G::LP; ++j) poff[j] = static_cast<uint32_t>(ptok[j]) * d_units;
 #pragma unroll
@@ -512,15 +527,17 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
   float inv[NI], rh[NI];
 #pragma unroll
   for (int u = 0; u < NI; ++u) {
-    inv[u] = gram_stage_inv(inv_norm, itok[u]);
-    if constexpr (MODE == kGramScreen) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+    if constexpr (SCR) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+    else inv[u] = gram_stage_inv(inv_norm, itok[u]);
   }
   typename G::Pipe pipe;
-  G::prefetch(X, poff, X, qoff, d_units, c.n - c.ti * kTile, c.n - c.tj * kTile, lds, pipe);
+  G::prefetch(X, poff, X, qoff, d_units, SCR ? kTile : c.n - c.ti * kTile, SCR ? kTile : c.n - c.tj * kTile, lds,
+              pipe);
   for (;;) {
+    if constexpr (!SCR) {
 #pragma unroll
-    for (int u = 0; u < NI; ++u) inv_ab[opaque_tid() + u * G::THREADS] = inv[u];   // visible after the K loop's first barrier
-    if constexpr (MODE == kGramScreen) {
+      for (int u = 0; u < NI; ++u) inv_ab[opaque_tid() + u * G::THREADS] = inv[u];   // visible after the K loop's first barrier
+    } else {
 #pragma unroll
       for (int u = 0; u < NI; ++u) rho_ab[opaque_tid() + u * G::THREADS] = rh[u];
       if (opaque_tid() == 0) *flag = 0;   // likewise; every wave read the last tile's flag before the loop's barrier
@@ -535,7 +552,7 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     TileCoord cn = c;
     if (nitem < total) {
       cn = decode_tile_grouped_from(next, nto, no0, no1, E);
-      gram_tile_tokens<G>(cn, perm_token, ptok, qtok, itok);
+      gram_tile_tokens<G>(cn, perm_token, ptok, qtok, itok, pad);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -548,8 +565,9 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
     // column pieces: the two column blocks of a wave are transposed
     // together, one per half-wave.  Edge test: dot * (1/|a|) * (1/|b|) >= h
     // (rows outside the bucket carry a NaN scale), never a token with
-    // itself.  The screen also keeps the least |c~ - h| of the lane (a NaN
-    // value, which is no edge on either pass, does not count).
+    // itself.  The screen tests its product against 2^16 h (its rows past
+    // the bucket are zero: no edge for h > 0) and also keeps the least
+    // |product - 2^16 h| of the lane.
     // lane values recomputed from the opaque thread index: hoisted out of
     // the tile loop they would stay live across the K loop
     const int el = opaque_tid() & 63;
@@ -565,38 +583,52 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
         r = fmaxf(r, fmaxf(fmaxf(f.x, f.y), fmaxf(f.z, f.w)));
       }
       for (int o = 32; o >= 1; o >>= 1) r = fmaxf(r, __shfl_xor(r, o, 64));
-      band = 2.f * r + r * r + 4e-3f;
+      band = (2.f * r + r * r + 4e-3f) * 65536.f;
     }
+    const float hs = h * 65536.f;   // the threshold in units of the screen's products (exact)
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
       const int abase = wm * G::WTM + 32 * fm;
       // this lane's 16 rows: abase + 8q + 4hi + r, as 4 runs of 4
       float ia[16];
+      if constexpr (!SCR) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 f = *reinterpret_cast<const float4*>(&inv_a[abase + 8 * q + 4 * hi]);
-        ia[4 * q] = f.x;
-        ia[4 * q + 1] = f.y;
-        ia[4 * q + 2] = f.z;
-        ia[4 * q + 3] = f.w;
+        for (int q = 0; q < 4; ++q) {
+          const float4 f = *reinterpret_cast<const float4*>(&inv_a[abase + 8 * q + 4 * hi]);
+          ia[4 * q] = f.x;
+          ia[4 * q + 1] = f.y;
+          ia[4 * q + 2] = f.z;
+          ia[4 * q + 3] = f.w;
+        }
       }
       uint32_t col[G::FN];
 #pragma unroll
       for (int fn = 0; fn < G::FN; ++fn) {
         const int bbase = wn * G::WTN + 32 * fn;
         const int bl = bbase + l31;
-        const float ib = inv_b[bl];
         uint32_t bits = 0;
-        float p = acc[fm][fn][15] * ia[15] * ib;
+        if constexpr (SCR) {
+          // raw fp8 products of unit rows scaled by 2^8: c~ = acc / 2^16;
+          // a token with itself is set to 0 (no edge for h > 0, and it
+          // stays out of the band; the word drops it below anyway)
+          if (same_tile && abase == bbase) {
 #pragma unroll
-        for (int v = 15; v >= 1; --v) {
-          if constexpr (MODE == kGramScreen) dmin = fminf(dmin, fabsf(p - h));
-          float q;
-          bits = shift_in_ge_next(bits, p, h, acc[fm][fn][v - 1], ia[v - 1], ib, q);
-          p = q;
+            for (int v = 0; v < 16; ++v)
+              if (8 * (v >> 2) + (v & 3) + 4 * hi == l31) acc[fm][fn][v] = 0.f;
+          }
+#pragma unroll
+          for (int v = 15; v >= 0; --v) bits = shift_in_ge_band(bits, acc[fm][fn][v], hs, dmin);
+        } else {
+          const float ib = inv_b[bl];
+          float p = acc[fm][fn][15] * ia[15] * ib;
+#pragma unroll
+          for (int v = 15; v >= 1; --v) {
+            float q;
+            bits = shift_in_ge_next(bits, p, h, acc[fm][fn][v - 1], ia[v - 1], ib, q);
+            p = q;
+          }
+          bits = shift_in_ge_last(bits, p, h);
         }
-        if constexpr (MODE == kGramScreen) dmin = fminf(dmin, fabsf(p - h));
-        bits = shift_in_ge_last(bits, p, h);
         // nibble k (accumulators 4k..4k+3) to bits 8k..8k+3, then this half's rows
         bits = (bits & 0xFFu) | ((bits & 0xFF00u) << 8);
         bits = (bits & 0x000F000Fu) | ((bits & 0x00F000F0u) << 4);
@@ -627,10 +659,11 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
       // before the DMA: waiting for them then does not wait for the DMA
 #pragma unroll
       for (int u = 0; u < NI; ++u) {
-        inv[u] = gram_stage_inv(inv_norm, itok[u]);
-        if constexpr (MODE == kGramScreen) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+        if constexpr (SCR) rh[u] = itok[u] >= 0 ? rho[itok[u]] : 0.f;
+        else inv[u] = gram_stage_inv(inv_norm, itok[u]);
       }
-      G::prefetch(X, poff, X, qoff, d_units, cn.n - cn.ti * kTile, cn.n - cn.tj * kTile, lds, pipe);
+      G::prefetch(X, poff, X, qoff, d_units, SCR ? kTile : cn.n - cn.ti * kTile, SCR ? kTile : cn.n - cn.tj * kTile,
+                  lds, pipe);
     }
     // LDS-only barriers from here on: a full __syncthreads() would also wait
     // for the next tile's DMA
@@ -1887,11 +1920,10 @@ struct CondenseWs {
   int* left;                    // a position stayed undecided after the greedy rounds
   int32_t* colinfo = nullptr;   // previous positions of every slot of every position
   int* queue = nullptr;         // tile queues of the similarity kernel
-  // the fp8 screen (calls without history whose shape allows it): fp8 rows,
-  // row factors and quantisation errors, the tiles left to the bf16 pass
-  // and their count
+  // the fp8 screen (calls without history whose shape allows it): fp8 rows
+  // (and a zero row), their quantisation errors, the tiles left to the bf16
+  // pass and their count
   uint8_t* x8 = nullptr;
-  float* qf = nullptr;
   float* rho = nullptr;
   int* list = nullptr;
   int* list_count = nullptr;
@@ -1938,8 +1970,7 @@ CondenseWs carve_condense(Carver& c, int T, int d, int E, int k, int max_bucket,
     w.colinfo = c.take<int32_t>(static_cast<size_t>(S) * k);
     w.queue = c.take<int>(kTileQueues);
   } else if (gram_screen_shape(T, d, E, k)) {
-    w.x8 = c.take<uint8_t>(static_cast<size_t>(T) * d);
-    w.qf = c.take<float>(T);
+    w.x8 = c.take<uint8_t>(static_cast<size_t>(T + 1) * d);
     w.rho = c.take<float>(T);
     w.list_count = c.take<int>(1);
     w.list = c.take<int>(static_cast<size_t>(gram_tile_bound(S, E, max_bucket)));
@@ -2008,20 +2039,19 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   }
   if (!hc) {
     const uint16_t* xb = static_cast<const uint16_t*>(x);
-    if (bf16 && ws.x8 && g_gram_screen.load(std::memory_order_relaxed)) {
+    if (bf16 && ws.x8 && threshold > 0.f && g_gram_screen.load(std::memory_order_relaxed)) {
       // fp8 screen over every tile, then the bf16 pass over the tiles it left
-      launch("gram_quant", gram_quant_kernel, (T + 3) / 4, 256, 0, s, xb, T, d, inv_norm_use, ws.x8, ws.qf,
-             ws.rho);
+      launch("gram_quant", gram_quant_kernel, (T + 4) / 4, 256, 0, s, xb, T, d, inv_norm_use, ws.x8, ws.rho);
       launch("gram", gram_kernel_bf16<kGramScreen>, persistent_grid(), GramGemm::THREADS, 0, s,
-             reinterpret_cast<const uint16_t*>(ws.x8), d / 2, perm_token, offsets, E, ws.qf, threshold, ws.tile_off,
-             ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.rho, ws.list, ws.list_count);
+             reinterpret_cast<const uint16_t*>(ws.x8), d / 2, perm_token, offsets, E, nullptr, threshold,
+             ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.rho, ws.list, ws.list_count, T);
       launch("gram_recheck", gram_kernel_bf16<kGramList>, persistent_grid(), GramGemm::THREADS, 0, s, xb, d,
              perm_token, offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-             nullptr, ws.list, ws.list_count);
+             nullptr, ws.list, ws.list_count, T);
     } else if (bf16)
       launch("gram", gram_kernel_bf16<kGramPlain>, persistent_grid(), GramGemm::THREADS, 0, s, xb, d, perm_token,
              offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg, nullptr,
-             nullptr, nullptr);
+             nullptr, nullptr, T);
     else
       launch("gram", gram_kernel_f32, 2 * persistent_grid(), 256, 0, s, static_cast<const float*>(x), d, perm_token,
              offsets, E, inv_norm_use, threshold, ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg);
