@@ -460,7 +460,9 @@ struct GemmCore {
   // second set first, then A fragment i as soon as the MFMAs that use it
   // are issued.  Two sets of 32-byte fragments would not fit beside the
   // accumulators.  READ = false: the MFMAs only.
-  template <int NQ, bool READ>
+  // NV: DMA instructions issued just before (the stage after the barrier),
+  // spread one after each MFMA.
+  template <int NQ, bool READ, int NV = 0>
   static __device__ __forceinline__ void mma_read_f8(lds_ptr S, int prow0, int qrow0, int half, int sw, int step,
                                                      Frags& f, Acc& acc) {
     const int c0 = 4 * step + 2 * half;
@@ -479,12 +481,20 @@ struct GemmCore {
     if constexpr (READ) {
 #pragma unroll
       for (int j = 0; j < NQ; ++j) f.b[j] = nb[j];
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * NQ, 0);   // DS reads of the B set
+      // MFMAs of A fragment i (each followed by one DMA while any is left),
+      // then its next-step reads, then one B fragment of the next step
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, NQ, 0);    // the MFMAs of A fragment i
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // its next-step reads
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (i * NQ + j < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        if (i < NQ) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       }
+      constexpr int REST = NV > FM * NQ ? NV - FM * NQ : 0;
+      if constexpr (REST > 0) __builtin_amdgcn_sched_group_barrier(0x020, REST, 0);
     }
   }
 
@@ -526,7 +536,7 @@ struct GemmCore {
       raw_barrier();
       __builtin_amdgcn_sched_barrier(0);
       issue(prs, qrs, goff, kt + STAGES, cur, w);
-      mma_read_f8<NQ, true>(nxt, prow0, qrow0, half, sw, 0, f, acc);
+      mma_read_f8<NQ, true, LOADS>(nxt, prow0, qrow0, half, sw, 0, f, acc);
       __builtin_amdgcn_sched_barrier(0);
     }
     // last stages: nothing more to issue; the reads that follow the very
