@@ -63,9 +63,7 @@ def kernel_work(name, cfg, counts, norms_from_route=True):
         # on the fp8 screen the rows it streams are fp8 (one byte a value)
         n = counts["bucket_sizes"]
         return w(2.0 * d * sum(x * (x + 1) / 2 for x in n), S * d * (1 if counts.get("screen") else b))
-    if name == "gram_quant":
-        # reads the bf16 rows, writes the fp8 rows and a factor per row
-        return w(0.0, T * d * b + T * d + 8 * T)
+
     if name in ("ffn1", "ffn2"):
         wb = used * d * dff * b
         return w(2.0 * R * d * dff, wb, wb + R * d * b + R * dff * b)
@@ -73,8 +71,12 @@ def kernel_work(name, cfg, counts, norms_from_route=True):
         return w(2.0 * T * d * E, T * d * b + E * d * b + 12 * T * k)
     if name == "norm":
         # with the norms from the gate pass it only clears the per-position
-        # state (degree, walk state, claim key: 16 bytes a position)
-        return w(0.0, 16 * S) if norms_from_route else w(2.0 * T * d, T * d * b + 16 * S)
+        # state (degree, walk state, claim key: 16 bytes a position); with the
+        # fp8 similarity screen it also reads the rows and writes their fp8
+        # copies and quantisation errors
+        screen = bool(counts.get("screen"))
+        nbytes = 16 * S + (T * d * b if screen or not norms_from_route else 0) + (T * d + 4 * T if screen else 0)
+        return w(0.0 if norms_from_route else 2.0 * T * d, nbytes)
     if name == "combine":
         return w(2.0 * S * d, R * d * b + 8 * T * k + T * d * b, R * d * b + 12 * T * k + T * d * b)
     if name == "gather":

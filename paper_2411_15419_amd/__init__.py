@@ -314,7 +314,7 @@ def profile_read():
     return ms.value, n.value
 
 
-KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram_quant", "gram", "gram_recheck", "greedy_round",
+KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram", "gram_recheck", "greedy_round",
            "greedy_push", "greedy_more",
            "greedy_finish", "claim", "rep_local", "rep_finalize", "gather", "ffn_queue", "ffn1", "ffn2",
            "ffn2_reduce", "combine")

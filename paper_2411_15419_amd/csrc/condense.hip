@@ -108,9 +108,65 @@ __device__ __forceinline__ void gram_layout(const int32_t* __restrict__ offsets,
   }
 }
 
+// fp8 copy of the token rows for the similarity screen (Sec. 3's cosine,
+// estimated): row t is normalised and scaled by 2^8, x_n = x * inv_norm[t] *
+// 256 (|x_n| = 256 up to the rounding of the norm, every value within
+// +-256, inside the E4M3 range), rounded to E4M3 by the hardware conversion
+// (values below the smallest normal, 2^-6, stored as 0, so no subnormal
+// reaches the MFMA).  rho[t] = |x_n - x^| / |x_n| is taken from the decoded
+// bytes, i.e. from the values the MFMA multiplies, and enlarged by 2^-9 to
+// cover the float32 sums.  Then for every pair c~ = x^_a . x^_b / 2^16 (the
+// raw fp8 product scaled by a power of two) and the cosine c of the bf16
+// pass satisfy
+//   |c - c~| <= (|x^_a| |e_b| + |e_a| |x_b|) / (|x_a| |x_b|) <= rho_a + rho_b + rho_a rho_b
+// (e = x_n - x^, |x_n| = 256), up to float32 rounding.  Row T of x8 (the
+// pad row of partial tiles) is zero.  One wave a row (norm_kernel's QUANT
+// pass); d % 8 == 0.
+__device__ __forceinline__ void gram_quant_row(const uint16_t* __restrict__ x, int T, int d, int t, float inv,
+                                               uint8_t* __restrict__ x8, float* __restrict__ rho) {
+  const int lane = threadIdx.x & 63;
+  uint8_t* out = x8 + static_cast<size_t>(t) * d;
+  if (t == T) {
+    for (int c = lane * 8; c < d; c += 512) *reinterpret_cast<uint2*>(out + c) = make_uint2(0u, 0u);
+    return;
+  }
+  const uint16_t* row = x + static_cast<size_t>(t) * d;
+  const float sc = inv * 256.f;
+  float se = 0.f, sx = 0.f;
+  for (int c = lane * 8; c < d; c += 512) {
+    Pack16 v;
+    v.u4 = *reinterpret_cast<const uint4*>(row + c);
+    float f[8], g[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      f[i] = bf16_to_f32(v.h[i]) * sc;
+      g[i] = fabsf(f[i]) < 0x1p-6f ? 0.f : f[i];
+    }
+    int lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[0], g[1], 0, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[2], g[3], lo, true);
+    int hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[4], g[5], 0, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[6], g[7], hi, true);
+    *reinterpret_cast<uint2*>(out + c) = make_uint2(static_cast<uint32_t>(lo), static_cast<uint32_t>(hi));
+    const float dq[8] = {__builtin_amdgcn_cvt_f32_fp8(lo, 0), __builtin_amdgcn_cvt_f32_fp8(lo, 1),
+                         __builtin_amdgcn_cvt_f32_fp8(lo, 2), __builtin_amdgcn_cvt_f32_fp8(lo, 3),
+                         __builtin_amdgcn_cvt_f32_fp8(hi, 0), __builtin_amdgcn_cvt_f32_fp8(hi, 1),
+                         __builtin_amdgcn_cvt_f32_fp8(hi, 2), __builtin_amdgcn_cvt_f32_fp8(hi, 3)};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float df = f[i] - dq[i];
+      se = fmaf(df, df, se);
+      sx = fmaf(f[i], f[i], sx);
+    }
+  }
+  se = wave_sum_f32(se);
+  sx = wave_sum_f32(sx);
+  if (lane == 0) rho[t] = sx > 0.f ? sqrtf(se / sx) * (1.f + 0x1p-9f) : 0.f;
+}
+
 // NORMS = false: the norms were computed by the caller (luffy_route); only
-// the clearing and the layout run.
-template <bool BF16, bool NORMS>
+// the clearing and the layout run.  QUANT (bf16): also the similarity
+// screen's fp8 rows (gram_quant_row; rows 0..T, T the zero pad row).
+template <bool BF16, bool NORMS, bool QUANT = false>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, int T, int d,
                                                    float* __restrict__ inv_norm, int S,
                                                    int32_t* __restrict__ deg, int32_t* __restrict__ state,
@@ -119,7 +175,8 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
                                                    int tile, long long cap_words, int32_t* __restrict__ tile_off,
                                                    long long* __restrict__ bm_off, int* __restrict__ err,
                                                    unsigned long long* __restrict__ stats, int* __restrict__ queue,
-                                                   int* __restrict__ left, int* __restrict__ list_count) {
+                                                   int* __restrict__ left, int* __restrict__ list_count,
+                                                   uint8_t* __restrict__ x8, float* __restrict__ rho) {
   if (blockIdx.x == 0 && threadIdx.x < 64)
     gram_layout(offsets, E, max_bucket, tile, cap_words, tile_off, bm_off, err);
   if (stats && blockIdx.x == 0 && threadIdx.x >= 64 && threadIdx.x < 68) stats[threadIdx.x - 64] = 0ull;
@@ -133,9 +190,18 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
     state[p] = 0;
     claim[p] = 0ull;
   }
-  if constexpr (!NORMS) return;
+  if constexpr (!NORMS && !QUANT) return;
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if constexpr (QUANT) {
+    static_assert(BF16, "fp8 rows of bf16 tokens");
+    if (t == T) gram_quant_row(static_cast<const uint16_t*>(xv), T, d, t, 0.f, x8, rho);
+    if (t >= T) return;
+    if constexpr (!NORMS) {
+      gram_quant_row(static_cast<const uint16_t*>(xv), T, d, t, inv_norm[t], x8, rho);
+      return;
+    }
+  }
   if (t >= T) return;
   float s = 0.f;
   if constexpr (BF16) {
@@ -160,7 +226,9 @@ __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ xv, 
     }
   }
   s = wave_sum_f32(s);
-  if (lane == 0) inv_norm[t] = s > 0.f ? 1.0f / sqrtf(s) : 0.f;
+  const float inv = s > 0.f ? 1.0f / sqrtf(s) : 0.f;
+  if (lane == 0) inv_norm[t] = inv;
+  if constexpr (QUANT) gram_quant_row(static_cast<const uint16_t*>(xv), T, d, t, inv, x8, rho);
 }
 
 struct TileCoord {
@@ -394,63 +462,6 @@ __device__ __forceinline__ uint32_t transpose32_bits(uint32_t x) {
   return transpose_step<1>(x, i);
 }
 
-// fp8 copy of the token rows for the similarity screen (Sec. 3's cosine,
-// estimated): row t is normalised and scaled by 2^8, x_n = x * inv_norm[t] *
-// 256 (|x_n| = 256 up to the rounding of the norm, every value within
-// +-256, inside the E4M3 range), rounded to E4M3 by the hardware conversion
-// (values below the smallest normal, 2^-6, stored as 0, so no subnormal
-// reaches the MFMA).  rho[t] = |x_n - x^| / |x_n| is taken from the decoded
-// bytes, i.e. from the values the MFMA multiplies, and enlarged by 2^-9 to
-// cover the float32 sums.  Then for every pair c~ = x^_a . x^_b / 2^16 (the
-// raw fp8 product scaled by a power of two) and the cosine c of the bf16
-// pass satisfy
-//   |c - c~| <= (|x^_a| |e_b| + |e_a| |x_b|) / (|x_a| |x_b|) <= rho_a + rho_b + rho_a rho_b
-// (e = x_n - x^, |x_n| = 256), up to float32 rounding.  Row T of x8 (the
-// pad row of partial tiles) is zero.  One wave a row; d % 8 == 0.
-__global__ __launch_bounds__(256) void gram_quant_kernel(const uint16_t* __restrict__ x, int T, int d,
-                                                         const float* __restrict__ inv_norm, uint8_t* __restrict__ x8,
-                                                         float* __restrict__ rho) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t > T) return;
-  uint8_t* out = x8 + static_cast<size_t>(t) * d;
-  if (t == T) {
-    for (int c = lane * 8; c < d; c += 512) *reinterpret_cast<uint2*>(out + c) = make_uint2(0u, 0u);
-    return;
-  }
-  const uint16_t* row = x + static_cast<size_t>(t) * d;
-  const float sc = inv_norm[t] * 256.f;
-  float se = 0.f, sx = 0.f;
-  for (int c = lane * 8; c < d; c += 512) {
-    Pack16 v;
-    v.u4 = *reinterpret_cast<const uint4*>(row + c);
-    float f[8], g[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      f[i] = bf16_to_f32(v.h[i]) * sc;
-      g[i] = fabsf(f[i]) < 0x1p-6f ? 0.f : f[i];
-    }
-    int lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[0], g[1], 0, false);
-    lo = __builtin_amdgcn_cvt_pk_fp8_f32(g[2], g[3], lo, true);
-    int hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[4], g[5], 0, false);
-    hi = __builtin_amdgcn_cvt_pk_fp8_f32(g[6], g[7], hi, true);
-    *reinterpret_cast<uint2*>(out + c) = make_uint2(static_cast<uint32_t>(lo), static_cast<uint32_t>(hi));
-    const float dq[8] = {__builtin_amdgcn_cvt_f32_fp8(lo, 0), __builtin_amdgcn_cvt_f32_fp8(lo, 1),
-                         __builtin_amdgcn_cvt_f32_fp8(lo, 2), __builtin_amdgcn_cvt_f32_fp8(lo, 3),
-                         __builtin_amdgcn_cvt_f32_fp8(hi, 0), __builtin_amdgcn_cvt_f32_fp8(hi, 1),
-                         __builtin_amdgcn_cvt_f32_fp8(hi, 2), __builtin_amdgcn_cvt_f32_fp8(hi, 3)};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float df = f[i] - dq[i];
-      se = fmaf(df, df, se);
-      sx = fmaf(f[i], f[i], sx);
-    }
-  }
-  se = wave_sum_f32(se);
-  sx = wave_sum_f32(sx);
-  if (lane == 0) rho[t] = sx > 0.f ? sqrtf(se / sx) * (1.f + 0x1p-9f) : 0.f;
-}
-
 // Modes of the bf16 similarity kernel: every tile on bf16 MFMA; every tile
 // on fp8 MFMA as a screen; the bf16 pass over the tiles the screen left.
 enum GramMode { kGramPlain = 0, kGramScreen = 1, kGramList = 2 };
@@ -469,7 +480,7 @@ enum GramMode { kGramPlain = 0, kGramScreen = 1, kGramList = 2 };
 // rows of d_units 16-bit units; row T_pad is zero and stands in for the
 // rows past a bucket), so a tile's products are 2^16 c~, estimates of the
 // cosines with |c~ - c| <= band for every pair: band = 2 r + r^2 + 4e-3, r
-// the largest rho (quantisation error, see gram_quant_kernel) of the
+// the largest rho (quantisation error, see gram_quant_row) of the
 // tile's rows, the constant room for the float32 rounding of both passes.
 // A tile whose every value lies outside (h - band, h + band) is decided
 // exactly by c~ >= h: it is written as in the bf16 pass.  Any other tile is
@@ -2023,12 +2034,19 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   unsigned long long* stats = hc ? (hc->stats ? hc->stats : ws.stats) : nullptr;
   // norms from the caller when given (the gate pass already read x)
   const float* inv_norm_use = inv_norm ? inv_norm : ws.inv_norm;
-  const int norm_blocks = inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
+  // the fp8 similarity screen: its rows are written by the norm pass
+  const bool screen = !hc && bf16 && ws.x8 && threshold > 0.f && g_gram_screen.load(std::memory_order_relaxed);
+  const int norm_blocks = screen ? std::max((S + 255) / 256, (T + 4) / 4)
+                                 : inv_norm ? std::max(1, (S + 255) / 256) : (T + 3) / 4;
   {
     const int tile = bf16 ? kTile : kTileF32;
-#define LUFFY_NORM_ARGS x, T, d, ws.inv_norm, S, ws.deg, ws.state, ws.claim, offsets, E, max_bucket, tile, \
-                        ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats, ws.queue, ws.left, ws.list_count
-    if (bf16) {
+#define LUFFY_NORM_ARGS x, T, d, inv_norm ? const_cast<float*>(inv_norm) : ws.inv_norm, S, ws.deg, ws.state, ws.claim, \
+                        offsets, E, max_bucket, tile, ws.cap_words, ws.tile_off, ws.bm_off, ws.err, stats, ws.queue,   \
+                        ws.left, ws.list_count, ws.x8, ws.rho
+    if (bf16 && screen) {
+      if (inv_norm) launch("norm", norm_kernel<true, false, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+      else launch("norm", norm_kernel<true, true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
+    } else if (bf16) {
       if (inv_norm) launch("norm", norm_kernel<true, false>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
       else launch("norm", norm_kernel<true, true>, norm_blocks, 256, 0, s, LUFFY_NORM_ARGS);
     } else {
@@ -2039,9 +2057,8 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   }
   if (!hc) {
     const uint16_t* xb = static_cast<const uint16_t*>(x);
-    if (bf16 && ws.x8 && threshold > 0.f && g_gram_screen.load(std::memory_order_relaxed)) {
+    if (screen) {
       // fp8 screen over every tile, then the bf16 pass over the tiles it left
-      launch("gram_quant", gram_quant_kernel, (T + 4) / 4, 256, 0, s, xb, T, d, inv_norm_use, ws.x8, ws.rho);
       launch("gram", gram_kernel_bf16<kGramScreen>, persistent_grid(), GramGemm::THREADS, 0, s,
              reinterpret_cast<const uint16_t*>(ws.x8), d / 2, perm_token, offsets, E, nullptr, threshold,
              ws.tile_off, ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.rho, ws.list, ws.list_count, T);

@@ -27,13 +27,13 @@ def _need_gpu():
     L.load_library()
 
 
-def _run(inp, screen, h=None, dev=None):
+def _run(inp, screen, h=None, dev=None, norms_from_route=True):
     import paper_2411_15419_amd as L
     prev = L.set_similarity_screen(screen)
     try:
         cfg = inp.cfg
         assert L.similarity_screen_applies(cfg.T, cfg.d, cfg.E, cfg.k) == screen
-        return run_gpu(inp, h=h, with_ffn=False, dev=dev)
+        return run_gpu(inp, h=h, with_ffn=False, dev=dev, norms_from_route=norms_from_route)
     finally:
         L.set_similarity_screen(prev)
 
@@ -100,3 +100,13 @@ def test_screen_repeat_calls_identical():
         inp = _near_threshold_inputs(T, 2048, 0.9, 7)
         dev = upload(inp)
         _assert_same(_run(inp, True, h=0.9, dev=dev), _run(inp, False, h=0.9, dev=dev))
+
+
+def test_screen_norms_computed_by_condense():
+    """The screen's fp8 rows written by the norm pass that also computes the
+    norms (no norms from the route call)."""
+    inp = _near_threshold_inputs(3000, 2048, 0.9, 3)
+    dev = upload(inp)
+    on = _run(inp, True, h=0.9, dev=dev, norms_from_route=False)
+    off = _run(inp, False, h=0.9, dev=dev, norms_from_route=False)
+    _assert_same(on, off)
