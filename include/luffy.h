@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUFFY_ABI_VERSION 5
+#define LUFFY_ABI_VERSION 6
 
 typedef enum {
   LUFFY_OK = 0,

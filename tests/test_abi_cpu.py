@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.luffy_abi_version() == 5
+    assert lib.luffy_abi_version() == 6
     assert lib.luffy_status_string(0) == b"ok"
     assert lib.luffy_status_string(-3).startswith(b"workspace")
 
