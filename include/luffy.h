@@ -138,7 +138,8 @@ int luffy_capacity(int T, int k, int E, double capacity_factor);
  *
  * Inside each bucket, positions a != b are joined when the cosine of their
  * embeddings is >= threshold (pairs in different buckets are never
- * compared).  A token with a zero embedding joins nothing.  The degree of a
+ * compared).  A token with a zero embedding has cosine 0 with every token
+ * (so it joins nothing for threshold > 0).  The degree of a
  * position is its number of edges.  Positions are then visited by
  * descending degree (lower position first on ties): a position not yet
  * decided becomes a representative and absorbs every undecided direct
