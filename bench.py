@@ -466,8 +466,8 @@ def measure_history(name, args, torch, np, G, L):
             us, gram_us = timed(lambda: b1.condense(xs[1], hist_in=b0.record))
             _, gather_us = timed(lambda: b1.condense(xs[1], hist_in=b0.record), "hist_gather")
             breakdown = {}
-            for kname in ("hist_cols", "norm", "hist_header", "greedy_round", "greedy_push", "greedy_more",
-                          "greedy_finish", "claim", "rep_local", "rep_finalize"):
+            for kname in ("hist_cols", "norm", "hist_header", "greedy_round", "greedy_more", "greedy_finish",
+                          "rep_local", "rep_finalize"):
                 breakdown[kname] = round(timed(lambda: b1.condense(xs[1], hist_in=b0.record), kname)[1], 1)
             st = b1.hist_stats.cpu().numpy().tolist()
             same = bool(torch.equal(b1.buf.rep_offsets, plain.buf.rep_offsets))

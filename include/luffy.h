@@ -370,10 +370,10 @@ int luffy_adaptive_threshold(double l_ini, double l_prev, double* h_out);
  * on the stream it runs on; NULL or "" turns this off.  luffy_profile_read
  * waits for the recorded events and returns the summed kernel time in
  * milliseconds and the number of launches since the previous read.
- * Kernel names: gate, slot_scan, slot_scatter, norm, gram, hist_cols,
- * hist_gather, hist_header, greedy_round, greedy_push, greedy_more,
- * greedy_finish, claim, rep_local, rep_finalize, gather, ffn_queue, ffn1,
- * ffn2, ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
+ * Kernel names: gate, slot_scan, slot_scatter, norm, gram, gram_recheck,
+ * hist_cols, hist_gather, hist_header, greedy_round, greedy_more,
+ * greedy_finish, rep_local, rep_finalize, gather, ffn_queue, ffn1, ffn2,
+ * ffn2_reduce, combine; backward: cbwd_group, cbwd_rows, cbwd_gate,
  * bwd_z, bwd_act, bwd_da, bwd_dx, bwd_dx_reduce, bwd_gather, bwd_dw2,
  * bwd_dw1.
  * ---------------------------------------------------------------------- */

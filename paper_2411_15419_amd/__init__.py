@@ -315,8 +315,7 @@ def profile_read():
 
 
 KERNELS = ("gate", "slot_scan", "slot_scatter", "norm", "gram", "gram_recheck", "greedy_round",
-           "greedy_push", "greedy_more",
-           "greedy_finish", "claim", "rep_local", "rep_finalize", "gather", "ffn_queue", "ffn1", "ffn2",
+           "greedy_more", "greedy_finish", "rep_local", "rep_finalize", "gather", "ffn_queue", "ffn1", "ffn2",
            "ffn2_reduce", "combine")
 
 

@@ -14,19 +14,17 @@
 //   greedy_round_kernel  first round of the parallel form of the greedy
 //                        walk, 16 lanes per position: keeps every position
 //                        with no undecided neighbour of higher priority.
-//   greedy_push_kernel   second round, from the kept side: each position
-//                        kept so far absorbs its neighbours and makes its
-//                        claims on them (with the first round, this decides
-//                        every position of a union of cliques).
+//                        A position is claimed by its neighbours as soon
+//                        as it is kept, in every pass: it absorbs them and
+//                        offers itself (64-bit atomic max of degree,
+//                        ~position), so an absorbed position ends with its
+//                        first-visited kept neighbour.  On a union of
+//                        cliques this round decides every position.
 //   greedy_more_kernel   persistent pass with bounded coherent revisits of
 //                        positions still undecided (dependency chains).
 //   greedy_finish_kernel one workgroup per bucket: a few rounds, then one
 //                        visit per position left in priority order (only
 //                        when the pass before left a position undecided).
-//   claim_kernel         every kept position not yet pushed offers itself to
-//                        its neighbours (64-bit atomic max of degree,
-//                        ~position): an absorbed position ends with its
-//                        first-visited kept neighbour.
 //   rep_local_kernel, rep_finalize_kernel  representative rows by a two-pass
 //                        scan: rep_row, rep_token, rep_offsets.
 //   gather_kernel        optional copy of the representative rows.
@@ -47,8 +45,6 @@
 namespace luffy {
 namespace {
 
-// claim word of a kept position whose claims the push round has made
-constexpr unsigned long long kClaimPushed = ~0ull;
 constexpr int kGreedyPasses = 32;   // visits of a blocked position in the round after the grid rounds
 constexpr int kTile = 256;      // similarity tile of the bf16 path (GramGemm)
 constexpr int kTileF32 = 64;    // similarity tile of the fp32 path
@@ -1508,9 +1504,46 @@ __device__ __forceinline__ void greedy_scan(int b0, int p, int dp, int lo, int n
   }
 }
 
+// A kept position q offers itself to every neighbour, as soon as it is
+// kept: it marks the neighbour absorbed (a neighbour of a kept position is
+// never kept, so it ends absorbed) and keeps in claim[b] the largest key
+// (degree << 32 | ~position), i.e. the neighbour's first kept neighbour in
+// walk order.  The maximum does not depend on when each kept position makes
+// its claims, so every pass that keeps a position claims for it at once and
+// no pass over the kept rows is needed afterwards.  The GW lanes of q's group
+// share the row, four words a lane at a time.
+template <int GW>
+__device__ __forceinline__ void greedy_claim(int q, int dq, int lo, int n, int W,
+                                             const uint64_t* __restrict__ row, int32_t* state,
+                                             unsigned long long* __restrict__ claim) {
+  const int gl = threadIdx.x & (GW - 1);
+  const unsigned long long key = (static_cast<unsigned long long>(dq) << 32) |
+                                 static_cast<unsigned int>(~static_cast<unsigned int>(q));
+  constexpr int U = 4;
+  for (int wd0 = gl; wd0 < W; wd0 += U * GW) {
+    uint64_t wv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) wv[u] = wd0 + GW * u < W ? row[wd0 + GW * u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint64_t bits = wv[u];
+      const int cbase = (wd0 + GW * u) * 64;
+      while (bits) {
+        const int b = __ffsll(static_cast<long long>(bits)) - 1;
+        bits &= bits - 1;
+        if (cbase + b < n) {
+          store_flag(&state[lo + cbase + b], kStateAbsorbed);
+          atomicMax(&claim[lo + cbase + b], key);
+        }
+      }
+    }
+  }
+}
+
 // Visit of undecided position p by a GW-lane group: kept if no neighbour is
-// kept or undecided with higher priority, absorbed if a neighbour is kept,
-// else left undecided (returns true).  The row is scanned in chunks and the
+// kept or undecided with higher priority (it then claims its neighbours at
+// once), absorbed if a neighbour is kept, else left undecided (returns
+// true).  The row is scanned in chunks and the
 // group stops at its first kept or blocking neighbour: the first chunk has
 // 4 words a lane (most rows stop there), later ones 8, so that a row
 // scanned to its end (every neighbour of lower priority) takes half the
@@ -1518,7 +1551,8 @@ __device__ __forceinline__ void greedy_scan(int b0, int p, int dp, int lo, int n
 template <bool FRESH, int GW>
 __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
                                              const uint64_t* __restrict__ row,
-                                             const int32_t* __restrict__ deg, int32_t* state) {
+                                             const int32_t* __restrict__ deg, int32_t* state,
+                                             unsigned long long* __restrict__ claim) {
   const int lane = threadIdx.x & 63;
   const int gl = lane & (GW - 1);
   const int gshift = lane & ~(GW - 1);
@@ -1536,6 +1570,7 @@ __device__ __forceinline__ bool greedy_visit(int p, int lo, int n, int W,
   }
   if (!any_blocked) {
     if (gl == 0) store_flag(&state[p], kStateKept);
+    greedy_claim<GW>(p, dp, lo, n, W, row, state, claim);
     return false;
   }
   return true;
@@ -1551,11 +1586,13 @@ __device__ __forceinline__ void load_offsets(const int32_t* __restrict__ offsets
 }
 
 // The first round over all positions (16 lanes each); also publishes the
-// degrees.
+// degrees.  On a union of cliques it decides every position: the first
+// member of each clique in walk order is kept and claims the others.
 __global__ __launch_bounds__(256) void greedy_round_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int32_t* __restrict__ degree_out) {
+    const int32_t* __restrict__ deg, int32_t* state, unsigned long long* __restrict__ claim,
+    int32_t* __restrict__ degree_out) {
   __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
   load_offsets(offsets, E, soff);
@@ -1563,58 +1600,13 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
   const int gl = threadIdx.x & (kVisitLanes - 1);
   if (p >= soff[E]) return;
   if (degree_out && gl == 0) degree_out[p] = deg[p];
-  // every state starts undecided and only p's own visit writes state[p] in
-  // this round: it need not be read
+  // every state starts undecided and is written in this round only by p's
+  // own visit or as absorbed by a kept neighbour's claims; p's visit can
+  // then only find it absorbed again or leave it, so it is not read
   const int e = bucket_of(soff, E, p);
   const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
   greedy_visit<false, kVisitLanes>(p, lo, n, W, bitmask + bm_off[e] + static_cast<long long>(p - lo) * W, deg,
-                                   state);
-}
-
-// Second round, pushed from the kept side.  Every position kept by the
-// first round marks each neighbour absorbed (kept positions are never
-// adjacent, so a neighbour of one is absorbed or undecided, and absorbed
-// for good) and offers itself as the neighbour's representative, as
-// claim_kernel does; its own claim word (unused for a kept position) then
-// tells claim_kernel to skip it.  Only kept rows are read, each once,
-// instead of every undecided row and then the kept rows again for the
-// claims.  Positions left undecided (no kept neighbour yet) go to the
-// passes after it.
-__global__ __launch_bounds__(256) void greedy_push_kernel(
-    const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, unsigned long long* __restrict__ claim) {
-  __shared__ int soff[kMaxExperts + 1];
-  if (*err) return;
-  load_offsets(offsets, E, soff);
-  const int q = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
-  const int gl = threadIdx.x & (kVisitLanes - 1);
-  if (q >= soff[E] || state[q] != kStateKept) return;
-  const int e = bucket_of(soff, E, q);
-  const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
-  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
-  const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
-                                 static_cast<unsigned int>(~static_cast<unsigned int>(q));
-  constexpr int U = 8;
-  for (int wd0 = gl; wd0 < W; wd0 += U * kVisitLanes) {
-    uint64_t wv[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) wv[u] = wd0 + kVisitLanes * u < W ? row[wd0 + kVisitLanes * u] : 0ull;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      uint64_t bits = wv[u];
-      const int cbase = (wd0 + kVisitLanes * u) * 64;
-      while (bits) {
-        const int b = __ffsll(static_cast<long long>(bits)) - 1;
-        bits &= bits - 1;
-        if (cbase + b < n) {
-          state[lo + cbase + b] = kStateAbsorbed;
-          atomicMax(&claim[lo + cbase + b], key);
-        }
-      }
-    }
-  }
-  if (gl == 0) claim[q] = kClaimPushed;
+                                   state, claim);
 }
 
 // The round after the grid rounds: a persistent grid, 16 lanes per
@@ -1627,7 +1619,8 @@ __global__ __launch_bounds__(256) void greedy_push_kernel(
 __global__ __launch_bounds__(256) void greedy_more_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, int* __restrict__ left) {
+    const int32_t* __restrict__ deg, int32_t* state, unsigned long long* __restrict__ claim,
+    int* __restrict__ left) {
   __shared__ int soff[kMaxExperts + 1];
   if (*err) return;
   load_offsets(offsets, E, soff);
@@ -1639,10 +1632,10 @@ __global__ __launch_bounds__(256) void greedy_more_kernel(
     const int e = bucket_of(soff, E, p);
     const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
     const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
-    bool still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+    bool still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
     for (int pass = 1; still && pass < kGreedyPasses; ++pass) {
       __builtin_amdgcn_s_sleep(32);
-      still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state);
+      still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
     }
     if (still && gl == 0) store_flag(&left[0], 1);
   }
@@ -1668,7 +1661,8 @@ constexpr int kFinishRounds = 16;
 __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
     const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, int32_t* state, const int* __restrict__ left) {
+    const int32_t* __restrict__ deg, int32_t* state, unsigned long long* __restrict__ claim,
+    const int* __restrict__ left) {
   __shared__ int list[2][kFinishList];
   __shared__ int cnt[2];
   if (*err) return;
@@ -1697,7 +1691,7 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     for (int pl = wv; pl < n; pl += 16) {
       const int p = lo + pl;
       if (load_flag(&state[p]) != kStateUndecided) continue;
-      greedy_visit<true, 64>(p, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
+      greedy_visit<true, 64>(p, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state, claim);
     }
     __syncthreads();
   }
@@ -1708,7 +1702,8 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
     for (int it = 0; it < kFinishRounds && m > 0; ++it) {
       for (int idx = grp; idx < m; idx += kGroups) {
         const int pl = list[cur][idx];
-        greedy_visit<true, kVisitLanes>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
+        greedy_visit<true, kVisitLanes>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state,
+                                        claim);
       }
       if (tid == 0) cnt[cur ^ 1] = 0;
       __syncthreads();
@@ -1757,44 +1752,7 @@ __global__ __launch_bounds__(1024) void greedy_finish_kernel(
   if (tid < 64) {
     for (int idx = 0; idx < m; ++idx) {
       const int pl = pos[idx];
-      greedy_visit<true, 64>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state);
-    }
-  }
-}
-
-// Each kept position offers itself to every neighbour: claim[b] keeps the
-// largest key (degree << 32 | ~position), i.e. the neighbour's first kept
-// neighbour in walk order.  Only kept positions scan their rows (16 lanes
-// each).
-__global__ __launch_bounds__(256) void claim_kernel(
-    const int32_t* __restrict__ offsets, int E, const long long* __restrict__ bm_off,
-    const int* __restrict__ err, const uint64_t* __restrict__ bitmask,
-    const int32_t* __restrict__ deg, const int32_t* __restrict__ state,
-    unsigned long long* __restrict__ claim) {
-  __shared__ int soff[kMaxExperts + 1];
-  if (*err) return;
-  load_offsets(offsets, E, soff);
-  const int q = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes);
-  const int gl = threadIdx.x & (kVisitLanes - 1);
-  if (q >= soff[E] || state[q] != kStateKept || claim[q] == kClaimPushed) return;
-  const int e = bucket_of(soff, E, q);
-  const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
-  const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(q - lo) * W;
-  const unsigned long long key = (static_cast<unsigned long long>(deg[q]) << 32) |
-                                 static_cast<unsigned int>(~static_cast<unsigned int>(q));
-  for (int wd0 = gl; wd0 < W; wd0 += 4 * kVisitLanes) {
-    uint64_t wv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = wd0 + kVisitLanes * u < W ? row[wd0 + kVisitLanes * u] : 0ull;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      uint64_t bits = wv[u];
-      const int cbase = (wd0 + kVisitLanes * u) * 64;
-      while (bits) {
-        const int b = __ffsll(static_cast<long long>(bits)) - 1;
-        bits &= bits - 1;
-        if (cbase + b < n) atomicMax(&claim[lo + cbase + b], key);
-      }
+      greedy_visit<true, 64>(lo + pl, lo, n, W, rows + static_cast<long long>(pl) * W, deg, state, claim);
     }
   }
 }
@@ -2127,15 +2085,11 @@ void condense_enqueue(const void* x, int T, int d, int dtype, const int32_t* per
   const int wave_blocks = (S + 3) / 4;
   const int visit_blocks = (S + kVisitPerBlock - 1) / kVisitPerBlock;
   launch("greedy_round", greedy_round_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-         ws.deg, ws.state, degree);
-  launch("greedy_push", greedy_push_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask,
-         ws.deg, ws.state, ws.claim);
+         ws.deg, ws.state, ws.claim, degree);
   launch("greedy_more", greedy_more_kernel, std::min(visit_blocks, persistent_grid()), 256, 0, s, offsets, E,
-         ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, ws.left);
+         ws.bm_off, ws.err, ws.bitmask, ws.deg, ws.state, ws.claim, ws.left);
   launch("greedy_finish", greedy_finish_kernel, E, 1024, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-         ws.state, ws.left);
-  launch("claim", claim_kernel, visit_blocks, 256, 0, s, offsets, E, ws.bm_off, ws.err, ws.bitmask, ws.deg,
-         ws.state, ws.claim);
+         ws.state, ws.claim, ws.left);
   const int pos_blocks = (S + 1023) / 1024;
   launch("rep_local", rep_local_kernel, pos_blocks, 1024, 0, s, offsets, E, ws.err, ws.state, ws.claim, rep_of_pos,
          ws.local, ws.bsum, S);
