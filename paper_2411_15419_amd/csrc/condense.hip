@@ -1610,8 +1610,9 @@ __global__ __launch_bounds__(256) void greedy_round_kernel(
 }
 
 // The round after the grid rounds: a persistent grid, 16 lanes per
-// position, that passes over every position (those already decided cost a
-// state read) and revisits a blocked one a bounded number of times, reading
+// position, that passes over every position (each group reads the states of
+// 16 consecutive positions with one load; decided ones cost nothing more)
+// and revisits a blocked one a bounded number of times, reading
 // the states coherently, so a dependency chain of length L resolves in
 // about L visits inside one launch instead of L launches (graphs whose
 // chains the grid rounds leave unfinished).  left[0] records that a
@@ -1625,19 +1626,28 @@ __global__ __launch_bounds__(256) void greedy_more_kernel(
   if (*err) return;
   load_offsets(offsets, E, soff);
   const int gl = threadIdx.x & (kVisitLanes - 1);
+  const int gshift = threadIdx.x & 63 & ~(kVisitLanes - 1);
   const int S = soff[E];
-  for (int p = blockIdx.x * kVisitPerBlock + (threadIdx.x / kVisitLanes); p < S;
-       p += gridDim.x * kVisitPerBlock) {
-    if (load_flag(&state[p]) != kStateUndecided) continue;
-    const int e = bucket_of(soff, E, p);
-    const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
-    const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
-    bool still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
-    for (int pass = 1; still && pass < kGreedyPasses; ++pass) {
-      __builtin_amdgcn_s_sleep(32);
-      still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
+  // a group reads the states of kVisitLanes consecutive positions with one
+  // load and visits the undecided ones among them (most are decided by now)
+  for (int base = (blockIdx.x * kVisitPerBlock + static_cast<int>(threadIdx.x) / kVisitLanes) * kVisitLanes;
+       base < S; base += gridDim.x * kVisitPerBlock * kVisitLanes) {
+    const int pq = base + gl;
+    const bool und = pq < S && load_flag(&state[pq]) == kStateUndecided;
+    uint32_t m = static_cast<uint32_t>((__ballot(und) >> gshift) & ((1ull << kVisitLanes) - 1));
+    while (m) {
+      const int p = base + __ffs(m) - 1;
+      m &= m - 1;
+      const int e = bucket_of(soff, E, p);
+      const int lo = soff[e], n = soff[e + 1] - lo, W = (n + 63) / 64;
+      const uint64_t* row = bitmask + bm_off[e] + static_cast<long long>(p - lo) * W;
+      bool still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
+      for (int pass = 1; still && pass < kGreedyPasses; ++pass) {
+        __builtin_amdgcn_s_sleep(32);
+        still = greedy_visit<true, kVisitLanes>(p, lo, n, W, row, deg, state, claim);
+      }
+      if (still && gl == 0) store_flag(&left[0], 1);
     }
-    if (still && gl == 0) store_flag(&left[0], 1);
   }
 }
 
