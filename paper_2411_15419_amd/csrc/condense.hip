@@ -623,8 +623,18 @@ __global__ __launch_bounds__(GramGemm::THREADS) void gram_kernel_bf16(
             for (int v = 0; v < 16; ++v)
               if (8 * (v >> 2) + (v & 3) + 4 * hi == l31) acc[fm][fn][v] = 0.f;
           }
+          // a 32 x 32 block without an edge (every product below 2^16 h,
+          // the common case) needs only its largest product: no bits, and
+          // its least distance to 2^16 h is 2^16 h minus that product
+          float mx = acc[fm][fn][0];
 #pragma unroll
-          for (int v = 15; v >= 0; --v) bits = shift_in_ge_band(bits, acc[fm][fn][v], hs, dmin);
+          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, acc[fm][fn][v]);
+          if (__ballot(mx >= hs) == 0) {
+            dmin = fminf(dmin, hs - mx);
+          } else {
+#pragma unroll
+            for (int v = 15; v >= 0; --v) bits = shift_in_ge_band(bits, acc[fm][fn][v], hs, dmin);
+          }
         } else {
           const float ib = inv_b[bl];
           float p = acc[fm][fn][15] * ia[15] * ib;
