@@ -110,3 +110,21 @@ def test_screen_norms_computed_by_condense():
     on = _run(inp, True, h=0.9, dev=dev, norms_from_route=False)
     off = _run(inp, False, h=0.9, dev=dev, norms_from_route=False)
     _assert_same(on, off)
+
+
+@pytest.mark.parametrize("h", [0.02, 0.999])
+def test_screen_extreme_thresholds(h):
+    """Thresholds at the ends of the range: near 0 the rows past a bucket
+    (zero products) and many cross-centre cosines fall inside the band, near
+    1 the same-centre cosines (about 0.9996) do, so many tiles go back to the
+    bf16 pass; the outputs still equal the all-bf16 call bit for bit.  (The
+    oracle is not compared here: at these thresholds some float64 cosines
+    lie within float32 rounding of h, which is the all-bf16 path's own
+    precision, not the screen's.)"""
+    inp = G.make_inputs("c3", seed=4, weights=False, T=3000, E=4, n_centres=300)
+    print(f"[case] extreme threshold h={h}", flush=True)
+    dev = upload(inp)
+    on = _run(inp, True, h=h, dev=dev)
+    off = _run(inp, False, h=h, dev=dev)
+    _assert_same(on, off)
+    assert on["degree"].max() > 0
